@@ -1,0 +1,116 @@
+"""Workload table and the seeded input generator.
+
+Draw order (numpy PCG64 `default_rng(seed)`, float32 standard normals, each a full array
+in [B, T, H, ...] row-major order): q, k, v, the log-gate pre-activation x_a, the level
+weight pre-activation x_l, and (delta-rule workloads only) the beta pre-activation x_b.
+
+Transforms by distribution name:
+  "unit"     q, k ~ N/sqrt(d_k), v ~ N/sqrt(d_v), log alpha = -softplus(x_a),     lambda = softplus(x_l)
+  "shifted"  q, k ~ N/sqrt(d_k), v ~ N(0,1),      log alpha = -softplus(x_a + 2), lambda = softplus(x_l)
+  "gdn"      q ~ N/sqrt(d_k), k = x/|x| per (b,t,h), v ~ N(0,1), beta = sigmoid(x_b),
+             log alpha = -softplus(x_a + 2), lambda = softplus(x_l)
+  "slow"     as "unit" but log alpha = -softplus(x_a - 6) (about -0.0025: every level matters)
+  "nodecay"  as "unit" but log alpha = 0 (alpha = 1)
+q, k, v are then rounded to the storage dtype (bf16 round-to-nearest-even via torch on the
+CPU, or kept float32); log alpha, lambda and beta are always float32.
+"""
+
+from dataclasses import dataclass, replace
+import math
+
+import numpy as np
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    variant: str      # "mamba2" or "gdn"
+    dtype: str        # "f32" or "bf16": storage dtype of q, k, v and o
+    B: int
+    H: int
+    T: int
+    dk: int
+    dv: int
+    C: int
+    seed: int
+    dist: str
+
+    @property
+    def levels(self) -> int:
+        # ceil(log2 T) + 1, the level count of lambda's last axis
+        return 1 if self.T == 1 else (self.T - 1).bit_length() + 1
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+WORKLOADS = {
+    w.name: w for w in [
+        Workload("ll_mamba2_f32_T64", "mamba2", "f32", 1, 1, 64, 16, 16, 16, 0, "unit"),
+        Workload("ll_mamba2_bf16_T2048", "mamba2", "bf16", 2, 8, 2048, 64, 64, 64, 2, "shifted"),
+        Workload("ll_mamba2_bf16_T8192", "mamba2", "bf16", 4, 32, 8192, 128, 64, 64, 3, "unit"),
+        Workload("ll_mamba2_bf16_T65536", "mamba2", "bf16", 1, 16, 65536, 128, 128, 64, 4, "unit"),
+        Workload("ll_gdn_bf16_T8192", "gdn", "bf16", 2, 16, 8192, 128, 128, 64, 5, "gdn"),
+    ]
+}
+
+
+def _softplus(x):
+    return np.logaddexp(0.0, x)
+
+
+def to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Round float values to the storage dtype and return them as float32 numpy
+    (bf16 values are exactly representable in float32)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if dtype == "f32":
+        return x
+    if dtype == "bf16":
+        import torch
+        return torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    raise ValueError(dtype)
+
+
+def generate(w: Workload, T: int = None, heads=None):
+    """Inputs for workload w as a dict of float32 numpy arrays.
+
+    `T` optionally truncates the sequence (a prefix is an exact sub-problem because the
+    method is causal); `heads` optionally keeps a subset of heads.  Both are applied after
+    drawing, so a truncated draw is a prefix of the full one."""
+    rng = np.random.default_rng(w.seed)
+    B, TT, H, dk, dv = w.B, w.T, w.H, w.dk, w.dv
+    L = w.levels
+    q = rng.standard_normal((B, TT, H, dk), dtype=np.float32)
+    k = rng.standard_normal((B, TT, H, dk), dtype=np.float32)
+    v = rng.standard_normal((B, TT, H, dv), dtype=np.float32)
+    xa = rng.standard_normal((B, TT, H), dtype=np.float32)
+    xl = rng.standard_normal((B, TT, H, L), dtype=np.float32)
+    xb = rng.standard_normal((B, TT, H), dtype=np.float32) if w.variant == "gdn" else None
+
+    q = q / np.float32(math.sqrt(dk))
+    if w.dist == "gdn":
+        k = k / np.linalg.norm(k.astype(np.float64), axis=-1, keepdims=True).astype(np.float32)
+    else:
+        k = k / np.float32(math.sqrt(dk))
+    if w.dist in ("unit", "slow", "nodecay"):
+        v = v / np.float32(math.sqrt(dv))
+    shift = {"unit": 0.0, "shifted": 2.0, "gdn": 2.0, "slow": -6.0, "nodecay": None}[w.dist]
+    if shift is None:
+        log_alpha = np.zeros((B, TT, H), dtype=np.float32)
+    else:
+        log_alpha = (-_softplus(xa.astype(np.float64) + shift)).astype(np.float32)
+    lam = _softplus(xl.astype(np.float64)).astype(np.float32)
+    out = dict(q=to_storage(q, w.dtype), k=to_storage(k, w.dtype), v=to_storage(v, w.dtype),
+               log_alpha=log_alpha, lam=lam)
+    if xb is not None:
+        out["beta"] = (1.0 / (1.0 + np.exp(-xb.astype(np.float64)))).astype(np.float32)
+    if T is not None or heads is not None:
+        T = TT if T is None else T
+        hs = slice(None) if heads is None else heads
+        Lt = 1 if T == 1 else (T - 1).bit_length() + 1
+        for key in out:
+            a = out[key][:, :T][:, :, hs]
+            if key == "lam":
+                a = a[..., :Lt]
+            out[key] = np.ascontiguousarray(a)
+    return out
