@@ -1,0 +1,117 @@
+/*
+ * libloglinear — chunkwise-parallel forward pass of log-linear attention on AMD MI355X (gfx950).
+ *
+ * Method: Guo et al., "Log-Linear Attention".  The library computes, per batch b and head h,
+ *
+ *     O = (Q K^T  (.)  M^S  (.)  M^H) V                        log-linear Mamba-2      (Sec. 3.4)
+ *     O = (A  (.)  M^S  (.)  M^H) V,
+ *         A = (Q K^T (.) L)(I + diag(beta)(K K^T (.) (L - I)))^{-1} diag(beta)
+ *                                                              log-linear Gated DeltaNet (Sec. 3.4)
+ *
+ * where M^S[t,s] = prod_{k=s+1..t} alpha_k is the gated (semiseparable) decay mask (Eq. 2),
+ * M^H[t,s] = lambda_t^(l(t,s)) is the Fenwick-tree hierarchical mask (Eq. 4) with l(t,s) the
+ * Fenwick level of position s seen from t (Sec. 3.1), and L is the lower-triangular ones matrix.
+ * It uses the chunkwise algorithm of Sec. 3.3 (Eq. 5): a dense C x C intra-chunk stage and
+ * O(log(T/C)) inter-chunk levels.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Layout.   All tensors are dense, row-major, in device memory:
+ *             q, k         [B, T, H, d_k]
+ *             v, o         [B, T, H, d_v]
+ *             log_alpha    [B, T, H]         (float32, log of alpha_t; the caller keeps it <= 0)
+ *             beta         [B, T, H]         (float32, GDN only)
+ *             lambda       [B, T, H, L]      (float32, L = ll_num_levels(T); the caller keeps it >= 0)
+ *           q, k, v and o share one storage dtype (ll_dtype); gates, beta and lambda are float32.
+ *           NaN or Inf in any input propagates to o; values are not checked.
+ * Shapes.   B, H >= 1; T >= 1 and T % C == 0; C a power of two; (dtype, C, d_k, d_v) must be one of
+ *           the compiled kernel shapes (ll_supported).
+ * Ownership. Every pointer is caller-owned device memory.  The library allocates nothing, keeps no
+ *           pointer after the call returns, and enqueues all work on `stream` (a hipStream_t passed
+ *           as void*, NULL = the default stream).  Calls return before the work finishes: the caller
+ *           keeps all buffers alive and unmodified until the stream reaches this point.
+ * Workspace. Device scratch of at least ll_workspace_size(...) bytes, 256-byte aligned, owned by the
+ *           caller; its contents on entry are irrelevant.  Calls sharing a workspace must be ordered.
+ * Errors.   Argument checks run on the host before any launch; on error nothing is enqueued.
+ *           A failed launch returns LL_ERR_HIP.  No exceptions cross the ABI.  Thread-safe: no
+ *           mutable global state.
+ */
+#ifndef LIBLOGLINEAR_H
+#define LIBLOGLINEAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LL_OK = 0,
+  LL_ERR_NULL_ARG = 1,     /* a required pointer is NULL                                        */
+  LL_ERR_BAD_SHAPE = 2,    /* B, T or H < 1, T % C != 0, C not a power of two, or d_k/d_v < 1   */
+  LL_ERR_UNSUPPORTED = 3,  /* no compiled kernel for (dtype, C, d_k, d_v), or an unknown dtype  */
+  LL_ERR_WORKSPACE = 4,    /* workspace smaller than ll_workspace_size(...) or misaligned       */
+  LL_ERR_HIP = 5           /* the HIP runtime reported an error when launching                   */
+} ll_status;
+
+typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
+
+typedef enum { LL_MAMBA2 = 0, LL_GDN = 1 } ll_variant;
+
+/* Number of Fenwick levels L for a sequence of length T (Sec. 3.1): one more than the largest
+ * level l(t,s) over all 0 <= s <= t < T, i.e. ceil(log2 T) + 1 for T >= 2 and 1 for T = 1.
+ * Returns -1 for T < 1.  Pure host function. */
+int32_t ll_num_levels(int64_t T);
+
+/* 1 if a kernel is compiled for this (variant, dtype, C, d_k, d_v), else 0.  Pure host function. */
+int32_t ll_supported(int32_t variant, int32_t dtype, int64_t C, int64_t d_k, int64_t d_v);
+
+/* Bytes of workspace the forward call needs for these arguments; `has_lambda` = 0 sizes the
+ * lambda == NULL path.  Returns 0 if the arguments are invalid.  Pure host function. */
+size_t ll_workspace_size(int32_t variant, int32_t dtype, int64_t B, int64_t T, int64_t H,
+                         int64_t d_k, int64_t d_v, int64_t C, int32_t has_lambda);
+
+/* Log-linear Mamba-2 forward, O = (Q K^T (.) M^S (.) M^H) V (Sec. 3.4; chunkwise algorithm
+ * Sec. 3.3, Eq. 5).  lambda == NULL runs the same kernels with all level weights equal to 1,
+ * which is exactly Mamba-2 / gated linear attention (Eq. 2) with a single running state
+ * between chunks.  Arguments as in the conventions above; o is written in full. */
+ll_status ll_mamba2_fwd(const void* q, const void* k, const void* v, const float* log_alpha,
+                        const float* lambda, void* o, int64_t B, int64_t T, int64_t H,
+                        int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Same computation as ll_mamba2_fwd, for measurement: records a HIP event on `stream` before
+ * each of the three kernel stages and after the last, waits for the stream to reach the final
+ * event (this call is synchronous), and writes the stages' durations in milliseconds to the host
+ * array stage_ms[3]: [0] chunk states, [1] level scan, [2] chunk outputs (intra-chunk and
+ * inter-chunk terms).  stage_ms == NULL returns LL_ERR_NULL_ARG. */
+ll_status ll_mamba2_fwd_timed(const void* q, const void* k, const void* v, const float* log_alpha,
+                              const float* lambda, void* o, int64_t B, int64_t T, int64_t H,
+                              int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                              void* workspace, size_t workspace_bytes, void* stream, float* stage_ms);
+
+/* Log-linear Gated DeltaNet forward (Sec. 3.4), with the delta-rule transition
+ * alpha_t (I - beta_t k_t k_t^T) applied chunkwise through a WY (UT) representation.
+ * beta is required; lambda == NULL gives plain Gated DeltaNet.  Returns LL_ERR_UNSUPPORTED
+ * for shapes without a compiled kernel. */
+ll_status ll_gdn_fwd(const void* q, const void* k, const void* v, const float* log_alpha,
+                     const float* beta, const float* lambda, void* o, int64_t B, int64_t T,
+                     int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Debug: writes out[t*T + s] = the Fenwick level l(t,s) that the forward kernels assign to the
+ * pair (t, s) for chunk size C (Sec. 3.1; the intra/inter split of Eq. 5), and -1 for s > t.
+ * `out` is device memory of T*T bytes.  Computed on the GPU by the same device functions the
+ * forward kernels use to pick masks and source groups.  Requires T % C == 0, C a power of two,
+ * 1 <= T <= 16384. */
+ll_status ll_debug_level_map(int64_t T, int64_t C, int8_t* out, void* stream);
+
+/* Static, human-readable name of a status code. */
+const char* ll_status_string(ll_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBLOGLINEAR_H */

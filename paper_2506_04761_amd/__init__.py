@@ -1,0 +1,10 @@
+"""libloglinear: log-linear attention forward (Guo et al., "Log-Linear Attention") on MI355X.
+
+The computation lives in the HIP library libloglinear.so (C ABI: include/libloglinear.h);
+this package is its Python binding.
+"""
+
+from ._lib import (  # noqa: F401
+    LL_BF16, LL_F32, LL_GDN, LL_MAMBA2, LLError, lib, ll_debug_level_map, ll_gdn_fwd,
+    ll_mamba2_fwd, ll_mamba2_fwd_timed, ll_num_levels, ll_status_string, ll_supported, ll_workspace_size,
+)

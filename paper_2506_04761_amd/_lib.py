@@ -1,0 +1,176 @@
+"""ctypes binding of libloglinear.so (the C ABI declared in include/libloglinear.h).
+
+Argument marshalling only: tensors are passed as raw device pointers plus sizes, and every step
+of the computation runs in the library's HIP kernels.  PyTorch supplies device memory and the
+current stream.  If the shared library is missing this module raises at import: there is no
+fallback implementation.
+"""
+
+import ctypes
+import os
+
+# PyTorch ships its own HIP runtime under the same soname as ROCm's (libamdhip64.so.7).  Load it
+# first so this library binds to the runtime that owns torch's device memory and streams.
+import torch  # noqa: F401
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libloglinear.so")
+
+LL_OK, LL_ERR_NULL_ARG, LL_ERR_BAD_SHAPE, LL_ERR_UNSUPPORTED, LL_ERR_WORKSPACE, LL_ERR_HIP = range(6)
+LL_F32, LL_BF16 = 0, 1
+LL_MAMBA2, LL_GDN = 0, 1
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build it with `python paper_2506_04761_amd/build.py` "
+        "(libloglinear has no non-HIP implementation)")
+
+lib = ctypes.CDLL(LIB_PATH)
+
+_i64, _i32, _vp, _sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+
+lib.ll_num_levels.argtypes = [_i64]
+lib.ll_num_levels.restype = _i32
+lib.ll_supported.argtypes = [_i32, _i32, _i64, _i64, _i64]
+lib.ll_supported.restype = _i32
+lib.ll_workspace_size.argtypes = [_i32, _i32, _i64, _i64, _i64, _i64, _i64, _i64, _i32]
+lib.ll_workspace_size.restype = _sz
+lib.ll_mamba2_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _sz, _vp]
+lib.ll_mamba2_fwd.restype = _i32
+lib.ll_mamba2_fwd_timed.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp,
+                                     _sz, _vp, ctypes.POINTER(ctypes.c_float)]
+lib.ll_mamba2_fwd_timed.restype = _i32
+lib.ll_gdn_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _sz, _vp]
+lib.ll_gdn_fwd.restype = _i32
+lib.ll_debug_level_map.argtypes = [_i64, _i64, _vp, _vp]
+lib.ll_debug_level_map.restype = _i32
+lib.ll_status_string.argtypes = [_i32]
+lib.ll_status_string.restype = ctypes.c_char_p
+
+
+class LLError(RuntimeError):
+    def __init__(self, status: int):
+        self.status = status
+        super().__init__(lib.ll_status_string(status).decode())
+
+
+def ll_num_levels(T: int) -> int:
+    return lib.ll_num_levels(T)
+
+
+def ll_supported(variant: int, dtype: int, C: int, d_k: int, d_v: int) -> bool:
+    return bool(lib.ll_supported(variant, dtype, C, d_k, d_v))
+
+
+def ll_workspace_size(variant, dtype, B, T, H, d_k, d_v, C, has_lambda) -> int:
+    return lib.ll_workspace_size(variant, dtype, B, T, H, d_k, d_v, C, int(bool(has_lambda)))
+
+
+def ll_status_string(status: int) -> str:
+    return lib.ll_status_string(status).decode()
+
+
+# ----------------------------------------------------------------------- torch-facing wrappers
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return LL_F32
+    if t.dtype == torch.bfloat16:
+        return LL_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; q, k, v must be float32 or bfloat16")
+
+
+def _check(t, name, dtype=None, shape=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _prepare(variant, q, k, v, log_alpha, beta, lam, C, out, workspace):
+    torch = _torch()
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    _check(q, "q")
+    _check(k, "k", q.dtype, (B, T, H, dk))
+    _check(v, "v", q.dtype, (B, T, H, dv))
+    _check(log_alpha, "log_alpha", torch.float32, (B, T, H))
+    if beta is not None:
+        _check(beta, "beta", torch.float32, (B, T, H))
+    L = ll_num_levels(T)
+    if lam is not None:
+        _check(lam, "lambda", torch.float32, (B, T, H, L))
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, T, H, dv), dtype=q.dtype, device=q.device)
+    _check(out, "out", q.dtype, (B, T, H, dv))
+    need = ll_workspace_size(variant, code, B, T, H, dk, dv, C, lam is not None)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _check(workspace, "workspace", torch.uint8)
+    return (B, T, H, dk, dv, code), out, workspace
+
+
+def ll_mamba2_fwd(q, k, v, log_alpha, lam, C, out=None, workspace=None, stream=None):
+    """Log-linear Mamba-2 forward on device tensors laid out [B, T, H, d]; `lam` may be None
+    (all level weights 1, i.e. Mamba-2).  Returns `out`.  Work is enqueued on `stream`
+    (default: torch's current stream) and is not synchronised."""
+    (B, T, H, dk, dv, code), out, ws = _prepare(LL_MAMBA2, q, k, v, log_alpha, None, lam, C, out, workspace)
+    st = lib.ll_mamba2_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(lam), _ptr(out),
+                           B, T, H, dk, dv, C, code, _ptr(ws), ws.numel(), _stream(stream))
+    if st != LL_OK:
+        raise LLError(st)
+    return out
+
+
+def ll_mamba2_fwd_timed(q, k, v, log_alpha, lam, C, out=None, workspace=None, stream=None):
+    """As ll_mamba2_fwd, but synchronous: returns (out, [chunk_state_ms, level_scan_ms,
+    chunk_out_ms]) measured with HIP events recorded on the stream between the stages."""
+    (B, T, H, dk, dv, code), out, ws = _prepare(LL_MAMBA2, q, k, v, log_alpha, None, lam, C, out, workspace)
+    ms = (ctypes.c_float * 3)()
+    st = lib.ll_mamba2_fwd_timed(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(lam), _ptr(out),
+                                 B, T, H, dk, dv, C, code, _ptr(ws), ws.numel(), _stream(stream), ms)
+    if st != LL_OK:
+        raise LLError(st)
+    return out, [float(x) for x in ms]
+
+
+def ll_gdn_fwd(q, k, v, log_alpha, beta, lam, C, out=None, workspace=None, stream=None):
+    """Log-linear Gated DeltaNet forward; as ll_mamba2_fwd plus `beta` [B, T, H] float32."""
+    (B, T, H, dk, dv, code), out, ws = _prepare(LL_GDN, q, k, v, log_alpha, beta, lam, C, out, workspace)
+    st = lib.ll_gdn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(beta), _ptr(lam), _ptr(out),
+                        B, T, H, dk, dv, C, code, _ptr(ws), ws.numel(), _stream(stream))
+    if st != LL_OK:
+        raise LLError(st)
+    return out
+
+
+def ll_debug_level_map(T, C, stream=None):
+    """The level map the kernels use, as a [T, T] int8 device tensor (-1 above the diagonal)."""
+    torch = _torch()
+    out = torch.empty((T, T), dtype=torch.int8, device="cuda")
+    st = lib.ll_debug_level_map(T, C, _ptr(out), _stream(stream))
+    if st != LL_OK:
+        raise LLError(st)
+    return out

@@ -1,0 +1,101 @@
+// Device-side building blocks shared by the libloglinear kernels (gfx950 / CDNA4).
+//
+//  * MFMA traits: one 16x16 output tile per instruction, bf16 (16x16x32) or fp32 (16x16x4).
+//    Operand convention used everywhere: lane l supplies row (A) or column (B) l & 15, and the
+//    KPL consecutive k values starting at (l >> 4) * KPL of the current k step.  A contraction
+//    only needs A and B to agree on which k each (lane group, slot) carries, so the same
+//    convention serves every operand loaded from memory.  The 16x16 fp32 result tile is held
+//    as lane l: column l & 15, rows 4 * (l >> 4) + r for r = 0..3.
+//  * Fenwick level functions (Sec. 3.1 footnote): l(t, s) = bit length of t XOR s for s <= t,
+//    and the chunk-level source group a chunk reads at each inter-chunk level (Sec. 3.3, Eq. 5).
+//  * A wave-wide inclusive prefix sum for the chunk-local cumulative log-gates (Eq. 2).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ll {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <typename T>
+struct Mfma;
+
+template <>
+struct Mfma<__bf16> {
+  static constexpr int KSTEP = 32;  // k per instruction
+  static constexpr int KPL = 8;     // k values per lane
+  typedef bf16x8 frag;
+  __device__ static inline f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline frag load(const __bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
+};
+
+template <>
+struct Mfma<float> {
+  static constexpr int KSTEP = 4;
+  static constexpr int KPL = 1;
+  typedef float frag;
+  __device__ static inline f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline frag load(const float* p) { return *p; }
+};
+
+// 16-byte vector of storage elements, for coalesced global <-> LDS copies.
+template <typename T>
+struct Vec16 {
+  static constexpr int N = 16 / sizeof(T);
+  typedef T type __attribute__((ext_vector_type(16 / sizeof(T))));
+};
+
+__device__ inline float to_f32(float x) { return x; }
+__device__ inline float to_f32(__bf16 x) { return static_cast<float>(x); }
+template <typename T>
+__device__ inline T from_f32(float x) { return static_cast<T>(x); }
+
+// ----------------------------------------------------------------------------------- levels
+
+// Bit length of x (0 for x == 0).
+__device__ __host__ inline int bitlen(uint32_t x) { return x ? 32 - __builtin_clz(x) : 0; }
+
+// Level of key position s seen from query position t, both inside one power-of-two-aligned
+// chunk and given as chunk-local indices (i = t mod C, j = s mod C, j <= i).  Because the
+// chunk start is a multiple of C, the global XOR equals the local one.
+__device__ __host__ inline int level_local(int i, int j) { return bitlen(uint32_t(i ^ j)); }
+
+// Chunk-level source group (Sec. 3.3): chunk z reads an inter-chunk term at chunk level
+// j >= 1 (token level log2(C) + j) iff bit j-1 of z is set; the keys then come from the chunk
+// range [first, first + 2^(j-1)) with first = ((z >> (j-1)) - 1) << (j-1), the 2^(j-1)-chunk
+// block immediately before z's own aligned block.
+__device__ __host__ inline bool reads_level(int64_t z, int j) { return (z >> (j - 1)) & 1; }
+__device__ __host__ inline int64_t source_first(int64_t z, int j) { return ((z >> (j - 1)) - 1) << (j - 1); }
+
+// Storage slot of the level-j summary of the source group that starts at chunk `first`
+// (first is a multiple of 2^j): summaries of level j follow those of levels 1..j-1, each
+// level holding ceil(N / 2^j) slots.
+__device__ __host__ inline int64_t node_slot(int64_t N, int j, int64_t first) {
+  int64_t off = 0;
+  for (int jj = 1; jj < j; ++jj) off += (N + (int64_t(1) << jj) - 1) >> jj;
+  return off + (first >> j);
+}
+
+// ----------------------------------------------------------------------------- wave helpers
+
+// Inclusive prefix sum across the 64 lanes of a wave (Hillis-Steele over DPP/permute).
+__device__ inline float wave_inclusive_scan(float x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    float y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+}  // namespace ll

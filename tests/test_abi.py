@@ -1,0 +1,99 @@
+"""Host-only checks of the C ABI: the library loads, exports every declared entry point, its
+pure host functions agree with the oracle, and every argument check returns its status before
+anything is launched (these calls pass dummy, never-dereferenced pointers)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import fenwick
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "libloglinear.h")
+
+ll = pytest.importorskip("paper_2506_04761_amd", reason="libloglinear.so not built")
+lib = ll.lib
+
+FAKE = ctypes.c_void_p(4096)  # non-null, 256-aligned, never dereferenced by a failing check
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ll_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert {"ll_mamba2_fwd", "ll_gdn_fwd", "ll_num_levels", "ll_workspace_size",
+            "ll_debug_level_map", "ll_status_string", "ll_supported"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_num_levels_matches_oracle():
+    for T in list(range(1, 700)) + [2048, 8192, 65536]:
+        assert ll.ll_num_levels(T) == fenwick.num_levels(T)
+    assert ll.ll_num_levels(2 ** 20) == 21
+    assert ll.ll_num_levels(0) == -1
+
+
+def test_supported_shapes_cover_the_workloads():
+    assert ll.ll_supported(ll.LL_MAMBA2, ll.LL_F32, 16, 16, 16)
+    assert ll.ll_supported(ll.LL_MAMBA2, ll.LL_BF16, 64, 64, 64)
+    assert ll.ll_supported(ll.LL_MAMBA2, ll.LL_BF16, 64, 128, 64)
+    assert ll.ll_supported(ll.LL_MAMBA2, ll.LL_BF16, 64, 128, 128)
+    assert not ll.ll_supported(ll.LL_MAMBA2, ll.LL_BF16, 64, 96, 128)
+    assert not ll.ll_supported(ll.LL_MAMBA2, 7, 64, 128, 128)
+
+
+def test_workspace_size():
+    ws = ll.ll_workspace_size(ll.LL_MAMBA2, ll.LL_BF16, 1, 65536, 16, 128, 128, 64, 1)
+    assert ws > 0 and ws % 256 == 0
+    assert ll.ll_workspace_size(ll.LL_MAMBA2, ll.LL_BF16, 1, 65536, 16, 128, 128, 64, 0) > 0
+    assert ll.ll_workspace_size(ll.LL_MAMBA2, ll.LL_BF16, 1, 100, 16, 128, 128, 64, 1) == 0  # T % C
+    assert ll.ll_workspace_size(ll.LL_MAMBA2, ll.LL_BF16, 1, 192, 16, 128, 128, 48, 1) == 0  # C not 2^k
+    assert ll.ll_workspace_size(ll.LL_MAMBA2, ll.LL_BF16, 0, 64, 1, 128, 128, 64, 1) == 0
+    assert ll.ll_workspace_size(ll.LL_MAMBA2, 9, 1, 64, 1, 128, 128, 64, 1) == 0
+
+
+def _m2(q=FAKE, k=FAKE, v=FAKE, la=FAKE, lam=FAKE, o=FAKE, B=1, T=128, H=2, dk=64, dv=64, C=64,
+        dtype=1, ws=FAKE, wsb=1 << 40):
+    return lib.ll_mamba2_fwd(q, k, v, la, lam, o, B, T, H, dk, dv, C, dtype, ws, wsb, None)
+
+
+def test_mamba2_argument_checks_return_before_launch():
+    assert _m2(q=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _m2(la=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _m2(o=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _m2(ws=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _m2(T=100) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _m2(C=48, T=96) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _m2(B=0) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _m2(H=0) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _m2(dk=96) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _m2(dtype=5) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _m2(C=32, T=128) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _m2(wsb=1000) == ll._lib.LL_ERR_WORKSPACE
+    assert _m2(ws=ctypes.c_void_p(4096 + 8)) == ll._lib.LL_ERR_WORKSPACE
+
+
+def test_gdn_argument_checks_return_before_launch():
+    def g(beta=FAKE, T=128, ws=FAKE, wsb=1 << 40, dk=128, dv=128):
+        return lib.ll_gdn_fwd(FAKE, FAKE, FAKE, FAKE, beta, FAKE, FAKE, 1, T, 2, dk, dv, 64, 1, ws, wsb, None)
+    assert g(beta=None) == ll._lib.LL_ERR_NULL_ARG
+    assert g(T=100) == ll._lib.LL_ERR_BAD_SHAPE
+    assert g(dk=96) == ll._lib.LL_ERR_UNSUPPORTED
+
+
+def test_debug_level_map_checks():
+    assert lib.ll_debug_level_map(64, 16, None, None) == ll._lib.LL_ERR_NULL_ARG
+    assert lib.ll_debug_level_map(60, 16, FAKE, None) == ll._lib.LL_ERR_BAD_SHAPE
+    assert lib.ll_debug_level_map(1 << 15, 16, FAKE, None) == ll._lib.LL_ERR_UNSUPPORTED
+
+
+def test_status_strings():
+    for s in range(6):
+        assert ll.ll_status_string(s).startswith("LL_")
