@@ -7,7 +7,8 @@
 
 namespace {
 
-constexpr int kMaxL = 24;  // lambda levels the kernels stage (T <= 2^23)
+constexpr int kMaxL = 24;          // lambda levels the kernels stage (T <= 2^23)
+constexpr int64_t kMaxTiles = 8192; // tiles of 4C tokens per sequence (the gap tree lives in LDS)
 
 inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 inline bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
@@ -15,14 +16,6 @@ inline int bitlen64(uint64_t x) { return x ? 64 - __builtin_clzll(x) : 0; }
 inline int64_t elem_size(int32_t dtype) { return dtype == LL_BF16 ? 2 : 4; }
 
 int32_t levels_of(int64_t T) { return T < 1 ? -1 : (T == 1 ? 1 : bitlen64(uint64_t(T - 1)) + 1); }
-int inter_levels(int64_t N) { return N <= 1 ? 0 : bitlen64(uint64_t(N - 1)); }
-
-int64_t nodes_per_bh(int64_t N, int J, bool has_lambda) {
-  if (!has_lambda) return N;
-  int64_t n = 0;
-  for (int j = 1; j <= J; ++j) n += (N + (int64_t(1) << j) - 1) >> j;
-  return n;
-}
 
 const ll::KernelEntry* find_mamba2(int32_t dtype, int64_t C, int64_t dk, int64_t dv) {
   int n = 0;
@@ -35,21 +28,6 @@ const ll::KernelEntry* find_mamba2(int32_t dtype, int64_t C, int64_t dk, int64_t
 ll_status check_shape(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C) {
   if (B < 1 || T < 1 || H < 1 || dk < 1 || dv < 1 || !is_pow2(C) || T % C != 0) return LL_ERR_BAD_SHAPE;
   return LL_OK;
-}
-
-// Byte offsets of the workspace regions; returns the total size.
-int64_t layout(int32_t dtype, int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, bool has_lambda,
-               int64_t off[4], int64_t* npb) {
-  const int64_t N = T / C;
-  const int J = inter_levels(N);
-  const int64_t BH = B * H, SZ = dk * dv;
-  *npb = nodes_per_bh(N, J, has_lambda);
-  int64_t cur = 0;
-  off[0] = cur; cur += align256(BH * N * 4);                               // tot2
-  off[1] = cur; cur += align256(has_lambda ? BH * N * (J > 0 ? J : 1) * 4 : 0);  // gaps2
-  off[2] = cur; cur += align256(BH * N * SZ * 4);                          // states
-  off[3] = cur; cur += align256(BH * (*npb) * SZ * elem_size(dtype));      // nodes
-  return cur;
 }
 
 }  // namespace
@@ -68,8 +46,7 @@ size_t ll_workspace_size(int32_t variant, int32_t dtype, int64_t B, int64_t T, i
   if (check_shape(B, T, H, d_k, d_v, C) != LL_OK) return 0;
   if (dtype != LL_F32 && dtype != LL_BF16) return 0;
   if (variant != LL_MAMBA2 && variant != LL_GDN) return 0;
-  int64_t off[4], npb;
-  return (size_t)layout(dtype, B, T, H, d_k, d_v, C, has_lambda != 0, off, &npb);
+  return (size_t)ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), has_lambda != 0, nullptr);
 }
 
 const char* ll_status_string(ll_status s) {
@@ -97,9 +74,8 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   const ll::KernelEntry* e = find_mamba2(dtype, C, d_k, d_v);
   if (!e) return LL_ERR_UNSUPPORTED;
   const int L = levels_of(T);
-  if (L > kMaxL || T / C > int64_t(0x7fffffff) || H > 65535 || B > 65535) return LL_ERR_UNSUPPORTED;
-  int64_t off[4], npb;
-  const int64_t need = layout(dtype, B, T, H, d_k, d_v, C, lambda != nullptr, off, &npb);
+  if (L > kMaxL || (T + 4 * C - 1) / (4 * C) > kMaxTiles || H > 65535 || B > 65535) return LL_ERR_UNSUPPORTED;
+  const int64_t need = ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), lambda != nullptr, nullptr);
   if (!workspace) return LL_ERR_NULL_ARG;
   if ((int64_t)workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
 
@@ -107,13 +83,7 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   a.q = q; a.k = k; a.v = v; a.log_alpha = log_alpha; a.lambda = lambda; a.o = o;
   a.B = B; a.T = T; a.H = H; a.dk = d_k; a.dv = d_v; a.C = C;
   a.L = L;
-  a.J = inter_levels(T / C);
-  char* base = static_cast<char*>(workspace);
-  a.ws.tot2 = reinterpret_cast<float*>(base + off[0]);
-  a.ws.gaps2 = reinterpret_cast<float*>(base + off[1]);
-  a.ws.states = reinterpret_cast<float*>(base + off[2]);
-  a.ws.nodes = base + off[3];
-  a.ws.nodes_per_bh = npb;
+  a.workspace = workspace;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (!stage_ms) {
     hipError_t err = e->launch(a, hs, nullptr);
@@ -168,8 +138,7 @@ ll_status ll_debug_level_map(int64_t T, int64_t C, int8_t* out, void* stream) {
   if (!out) return LL_ERR_NULL_ARG;
   if (T < 1 || !is_pow2(C) || T % C != 0) return LL_ERR_BAD_SHAPE;
   if (T > 16384) return LL_ERR_UNSUPPORTED;
-  const int log2C = bitlen64(uint64_t(C)) - 1;
-  hipError_t err = ll::launch_debug_level_map(T, int(C), log2C, inter_levels(T / C), out, static_cast<hipStream_t>(stream));
+  hipError_t err = ll::launch_debug_level_map(T, C, out, static_cast<hipStream_t>(stream));
   return err == hipSuccess ? LL_OK : LL_ERR_HIP;
 }
 

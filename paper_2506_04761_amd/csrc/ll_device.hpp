@@ -22,6 +22,10 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// 2^x with the hardware v_exp_f32 (arguments here are always <= 0; results below the normal
+// range may flush to zero, which only drops terms already negligible against the others).
+__device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 template <typename T>
 struct Mfma;
 

@@ -8,14 +8,18 @@
 
 namespace ll {
 
-// Workspace regions, carved by the C ABI from the caller's buffer (all device pointers).
-struct Workspace {
-  float* tot2 = nullptr;      // [B*H][N]          chunk totals of log2-domain gates
-  float* gaps2 = nullptr;     // [B*H][N][J]       log2 decay from a source group's end to a reader
-  float* states = nullptr;    // [B*H][N][d_v*d_k] chunk states, fp32, layout [p][n]
-  void* nodes = nullptr;      // [B*H][nodes_per_bh][d_v*d_k] level summaries (storage dtype)
-  int64_t nodes_per_bh = 0;
+// Byte offsets of the workspace regions of one forward call (see mamba2_workspace).
+struct WsLayout {
+  int64_t N = 0;       // tiles per sequence
+  int J = 0;           // inter-tile levels
+  int64_t n1 = 0, n2 = 0, nb = 0, nup = 0;  // per-(b,h) summary slots: levels 1, 2, 3 (blocks), >= 4
+  int64_t tot2 = 0, gaps2 = 0, lvl1 = 0, lvl2 = 0, blocks = 0, upper = 0, tiles = 0, running = 0;
+  int64_t total = 0;
 };
+
+// Workspace layout of ll_mamba2_fwd; returns the total byte count.
+int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, int64_t esize,
+                         bool has_lambda, WsLayout* lay);
 
 struct Mamba2Args {
   const void* q;
@@ -25,9 +29,8 @@ struct Mamba2Args {
   const float* lambda;  // may be null
   void* o;
   int64_t B, T, H, dk, dv, C;
-  int L;  // Fenwick levels of T
-  int J;  // inter-chunk levels
-  Workspace ws;
+  int L;                // Fenwick levels of T
+  void* workspace;      // at least mamba2_workspace(...) bytes, 256-byte aligned
 };
 
 typedef hipError_t (*Mamba2Launch)(const Mamba2Args&, hipStream_t, hipEvent_t* /* null or 4 events */);
@@ -40,6 +43,6 @@ struct KernelEntry {
 };
 
 const KernelEntry* mamba2_table(int* n);
-hipError_t launch_debug_level_map(int64_t T, int C, int log2C, int J, int8_t* out, hipStream_t st);
+hipError_t launch_debug_level_map(int64_t T, int64_t C, int8_t* out, hipStream_t st);
 
 }  // namespace ll

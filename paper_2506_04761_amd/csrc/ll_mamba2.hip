@@ -1,20 +1,28 @@
 // Log-linear Mamba-2 forward: O = (Q K^T (.) M^S (.) M^H) V  (Sec. 3.4), computed with the
-// chunkwise algorithm of Sec. 3.3 (Eq. 5) in three kernels:
+// chunkwise algorithm of Sec. 3.3 (Eq. 5), organised for gfx950 in tiles of R = 4C tokens.
 //
-//   chunk_state  per chunk z: chunk-local cumulative log-gate cl, total tot_z, and the chunk
-//                state S_z = sum_t exp(tot_z - cl_t) v_t k_t^T  (d_v x d_k, MFMA, K = C tokens).
-//   level_scan   per (b, h), elementwise over state entries, sequential over chunks: the
-//                summary of every source group each inter-chunk level reads (decayed to the
-//                group end), plus the decay gap from a group's end to each reader chunk.
-//                With lambda == NULL: the single running state entering every chunk.
-//   chunk_out    per chunk: the intra-chunk C x C masked contraction (the block-diagonal D of
-//                Eq. 5) and, for every set bit j-1 of the chunk index, the lambda-weighted
-//                inter-chunk term  lambda_t^(log2 C + j) exp(cl_t + gap) q_t^T U_j  (the
-//                masked Q S update of the chunkwise algorithm, App. C Alg. 1).
+// The hierarchical mask splits at the tile boundary exactly as Eq. 5 splits it at the chunk
+// boundary: pairs (t, s) inside one aligned tile have levels 0..log2 R and are computed densely
+// (the chunk-diagonal blocks D of Eq. 5 plus the two lowest inter-chunk levels, as one causal
+// R x R masked contraction on MFMA); pairs in different tiles have level log2 R + j, where j is
+// the bit length of (tile(t) XOR tile(s)), and are computed from summaries of whole source
+// groups of tiles (the masked Q S products of the chunkwise algorithm, App. C Alg. 1).
+//
+// Three kernels:
+//   block_state  per block of 4 tiles: the tile states S_u = sum_t exp(tot_u - cl_t) v_t k_t^T
+//                (MFMA, K = R tokens), folded on chip into the summaries the first three
+//                tile levels read: S_u of even tiles (level 1), the pair summary of tiles 0-1
+//                (level 2) and the whole-block summary (level 3, and the input of the scan).
+//   block_scan   per (b, h), elementwise over state entries, sequential over blocks: the
+//                summaries of the source groups of levels >= 4, and the decay gaps from each
+//                group's end to the tiles that read it.  With lambda == NULL: the single running
+//                state entering every tile.
+//   tile_out     per tile: the causal R x R masked contraction and, for every set bit j-1 of
+//                the tile index, the lambda-weighted term  lambda_t^(log2 R + j) exp(cl_t + gap) q_t^T U_j.
 //
 // Decays are kept in the log2 domain (gates pre-multiplied by log2 e) and every exp2 argument
-// is <= 0: chunk-local cumulative sums and exact range sums of chunk totals, never differences
-// of sequence-long prefix sums.
+// is <= 0: tile-local cumulative sums and exact range sums of tile totals, never differences of
+// sequence-long prefix sums.
 #include <type_traits>
 
 #include "ll_device.hpp"
@@ -22,351 +30,688 @@
 
 namespace ll {
 
+constexpr int kTileChunks = 4;    // chunks per tile
+constexpr int kBlockTiles = 4;    // tiles per block_state workgroup
+constexpr int kKB = 64;           // keys staged in LDS at a time
+constexpr int kMaxLevels = 24;    // Fenwick levels handled (T <= 2^23)
+
+// Device view of the summaries (all in the storage dtype, layout [p][n] = d_v x d_k).
+template <typename T>
+struct Nodes {
+  T* lvl1;       // [BH][ceil(N/2)]  tile states of even tiles
+  T* lvl2;       // [BH][ceil(N/4)]  pair summaries of tiles 4b, 4b+1
+  T* blocks;     // [BH][NB]         block summaries (4 tiles)
+  T* upper;      // [BH][nup]        levels >= 4
+  int64_t n1, n2, nb, nup;  // per-(b,h) slot counts
+  // Summary of the level-j source group that starts at tile f (f a multiple of 2^j).
+  __device__ __host__ T* at(int64_t bh, int64_t N, int j, int64_t f, int SZ) const {
+    if (j == 1) return lvl1 + (bh * n1 + (f >> 1)) * SZ;
+    if (j == 2) return lvl2 + (bh * n2 + (f >> 2)) * SZ;
+    if (j == 3) return blocks + (bh * nb + (f >> 2)) * SZ;
+    int64_t off = 0;
+    for (int jj = 4; jj < j; ++jj) off += (N + (int64_t(1) << jj) - 1) >> jj;
+    return upper + (bh * nup + off + (f >> j)) * SZ;
+  }
+};
+
+// Tile-local inclusive cumulative sum of log2 gates for the R rows of a tile (rows >= nrow get
+// a zero gate), computed by the first 4 waves of the workgroup (R/4 <= 64 rows each) into cl_s[R].
+// Starts and ends with a barrier.
+template <int R>
+__device__ inline void tile_cumsum(const float* __restrict__ log_alpha, int64_t row0, int nrow, int H, int h,
+                                   float* cl_s, float* wsum_s) {
+  constexpr int RPW = R / 4;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = wave * RPW + lane;
+  const bool mine = wave < 4 && lane < RPW;  // waves beyond the first four only take the barriers
+  float la = (mine && r < nrow) ? log_alpha[(row0 + r) * H + h] * kLog2e : 0.f;
+  float cl = wave_inclusive_scan(la);
+  __syncthreads();
+  if (wave < 4 && lane == 63) wsum_s[wave] = cl;
+  __syncthreads();
+  float base = 0.f;
+  for (int w = 0; w < wave && w < 4; ++w) base += wsum_s[w];
+  if (mine) cl_s[r] = base + cl;
+  __syncthreads();
+}
+
+// Register staging of one 64-row block of a [rows, H, D] tensor, loaded with 16-byte vectors by
+// the NT threads of the workgroup; rows at or beyond `nrow` read as zero.
+// D is the width loaded (elements per row) and LDROW the row length of the tensor in memory.
+//  * RowBlock:  thread-unit = (row, 16-byte column group); stored row-major (store_rows).
+//  * ColBlock:  thread-unit = (pair of rows 2t, 2t+1, 16-byte column group), 32 pairs fastest, so
+//               the transposed store writes one 4-byte word (bf16) or 8-byte pair (fp32) per
+//               column, and the 32 lanes of a half-wave hit 32 consecutive LDS words.
+template <typename T, int D, int NT, int LDROW = D>
+struct RowBlock {
+  static constexpr int VEC = Vec16<T>::N;
+  static constexpr int PER_ROW = D / VEC;
+  static constexpr int TOTAL = kKB * PER_ROW;
+  static constexpr int LOADS = (TOTAL + NT - 1) / NT;
+  typename Vec16<T>::type x[LOADS];
+  __device__ inline void load(const T* __restrict__ src, int64_t row0, int r0, int nrow, int H, int h) {
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int idx = threadIdx.x + NT * i;
+      const int t = idx / PER_ROW, d0 = (idx % PER_ROW) * VEC;
+      x[i] = typename Vec16<T>::type{};
+      if (idx < TOTAL && r0 + t < nrow)
+        x[i] = *reinterpret_cast<const typename Vec16<T>::type*>(src + ((row0 + r0 + t) * H + h) * LDROW + d0);
+    }
+  }
+  __device__ inline void store_rows(T* dst, int ld) const {
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int idx = threadIdx.x + NT * i;
+      const int t = idx / PER_ROW, d0 = (idx % PER_ROW) * VEC;
+      if (idx < TOTAL) *reinterpret_cast<typename Vec16<T>::type*>(&dst[t * ld + d0]) = x[i];
+    }
+  }
+};
+
+template <typename T, int D, int NT, int LDROW = D>
+struct ColBlock {
+  static constexpr int VEC = Vec16<T>::N;
+  static constexpr int GROUPS = D / VEC;
+  static constexpr int TOTAL = (kKB / 2) * GROUPS;
+  static constexpr int UNITS = (TOTAL + NT - 1) / NT;
+  typename Vec16<T>::type x0[UNITS], x1[UNITS];
+  __device__ inline void load(const T* __restrict__ src, int64_t row0, int r0, int nrow, int H, int h) {
+#pragma unroll
+    for (int i = 0; i < UNITS; ++i) {
+      const int idx = threadIdx.x + NT * i;
+      const int t = 2 * (idx % (kKB / 2)), d0 = (idx / (kKB / 2)) * VEC;
+      x0[i] = typename Vec16<T>::type{};
+      x1[i] = typename Vec16<T>::type{};
+      if (idx < TOTAL && r0 + t < nrow)
+        x0[i] = *reinterpret_cast<const typename Vec16<T>::type*>(src + ((row0 + r0 + t) * H + h) * LDROW + d0);
+      if (idx < TOTAL && r0 + t + 1 < nrow)
+        x1[i] = *reinterpret_cast<const typename Vec16<T>::type*>(src + ((row0 + r0 + t + 1) * H + h) * LDROW + d0);
+    }
+  }
+  // dst[d * ld + t] = x[t][d] * scale[t] (scale only if SCALE); ld must be even
+  template <bool SCALE>
+  __device__ inline void store_cols(T* dst, int ld, const float* scale) const {
+    typedef T T2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+    for (int i = 0; i < UNITS; ++i) {
+      const int idx = threadIdx.x + NT * i;
+      if (idx >= TOTAL) continue;
+      const int t = 2 * (idx % (kKB / 2)), d0 = (idx / (kKB / 2)) * VEC;
+      const float s0 = SCALE ? scale[t] : 1.f, s1 = SCALE ? scale[t + 1] : 1.f;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        T2 w;
+        w[0] = SCALE ? from_f32<T>(to_f32(x0[i][e]) * s0) : x0[i][e];
+        w[1] = SCALE ? from_f32<T>(to_f32(x1[i][e]) * s1) : x1[i][e];
+        *reinterpret_cast<T2*>(&dst[(d0 + e) * ld + t]) = w;
+      }
+    }
+  }
+};
+
 // ---------------------------------------------------------------------------------------------
-// Kernel 1: chunk states.  One workgroup (4 waves) per (chunk, head, batch).
+// Kernel 1: block states.  One workgroup (4 waves) per (block of 4 tiles, head, batch).  The K/V
+// rows of the next 64-row step are loaded into registers while the current step's MFMAs run.
 // ---------------------------------------------------------------------------------------------
-template <typename T, int C, int DK, int DV>
-__global__ __launch_bounds__(256) void k_chunk_state(const T* __restrict__ k, const T* __restrict__ v,
-                                                     const float* __restrict__ log_alpha,
-                                                     float* __restrict__ states, float* __restrict__ tot2_out,
+constexpr int kStateThreads = 512;  // block_state workgroup: 8 waves
+
+template <typename T, int C, int DK, int DV, bool HAS_LAMBDA>
+__global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restrict__ k, const T* __restrict__ v,
+                                                     const float* __restrict__ log_alpha, Nodes<T> nodes,
+                                                     T* __restrict__ tiles, float* __restrict__ tot2_out,
                                                      int64_t Tlen, int H) {
   using M = Mfma<T>;
+  constexpr int R = kTileChunks * C;
   constexpr int VEC = Vec16<T>::N;
-  constexpr int PAD = VEC;          // keeps 16-lane row accesses on distinct LDS banks
-  constexpr int LDT = C + PAD;      // row stride of the transposed tiles (elements)
-  __shared__ T vt_s[DV * LDT];      // V^T  [p][t]
-  __shared__ T kt_s[DK * LDT];      // (decay * K)^T  [n][t]
-  __shared__ float dec_s[C];
-
-  const int z = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t N = Tlen / C;
-  const int64_t tok0 = (int64_t)b * Tlen + (int64_t)z * C;  // first token row of the chunk
-
-  if (wave == 0) {
-    float la = lane < C ? log_alpha[(tok0 + lane) * H + h] * kLog2e : 0.f;
-    float cl = wave_inclusive_scan(la);
-    float tot = __shfl(cl, C - 1, 64);
-    if (lane < C) dec_s[lane] = exp2f(tot - cl);
-    if (lane == 0) tot2_out[((int64_t)b * H + h) * N + z] = tot;
-  }
-  __syncthreads();
-
-  // Stage V^T and (dec * K)^T.
-  for (int idx = tid; idx < C * DV / VEC; idx += 256) {
-    const int t = idx / (DV / VEC), d0 = (idx % (DV / VEC)) * VEC;
-    typename Vec16<T>::type x = *reinterpret_cast<const typename Vec16<T>::type*>(v + ((tok0 + t) * H + h) * DV + d0);
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) vt_s[(d0 + e) * LDT + t] = x[e];
-  }
-  for (int idx = tid; idx < C * DK / VEC; idx += 256) {
-    const int t = idx / (DK / VEC), d0 = (idx % (DK / VEC)) * VEC;
-    typename Vec16<T>::type x = *reinterpret_cast<const typename Vec16<T>::type*>(k + ((tok0 + t) * H + h) * DK + d0);
-    const float dt = dec_s[t];
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) kt_s[(d0 + e) * LDT + t] = from_f32<T>(to_f32(x[e]) * dt);
-  }
-  __syncthreads();
-
-  // S^T[p][n] = sum_t V^T[p][t] (dec K)^T[n][t]:  M = p, N = n, K = t.
+  constexpr int LDT = kKB + VEC;
   constexpr int MT = DV / 16, NT = DK / 16;
-  float* out = states + (((int64_t)b * H + h) * N + z) * (int64_t)(DV * DK);
-  const int r16 = lane & 15, g = lane >> 4;
-  for (int tile = wave; tile < MT * NT; tile += 4) {
-    const int mt = tile / NT, nt = tile % NT;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  constexpr int NW = kStateThreads / 64;
+  constexpr int WM = MT >= 2 ? 2 : 1;                            // waves along p
+  constexpr int WN = (NW / WM) < NT ? (NW / WM) : NT;            // waves along n
+  constexpr int TM = MT / WM, TN = NT / WN;                      // 16x16 tiles per wave
+  constexpr int SZ = DK * DV;
+  constexpr int STEPS = R / kKB;                                 // 64-row steps per tile
+  __shared__ T vt_s[DV * LDT];
+  __shared__ T kt_s[DK * LDT];
+  __shared__ float cl_s[R];
+  __shared__ float dec_s[R];
+  __shared__ float wsum_s[4];
+
+  const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
+  const int64_t N = (Tlen + R - 1) / R;  // tiles
+  const int64_t bh = (int64_t)b * H + h;
+  const bool active = wave < WM * WN;
+  const int wm = wave / WN, wn = wave % WN;
+  const int64_t u0 = (int64_t)blk * kBlockTiles;
+  const int ntile = (int)((N - u0) < kBlockTiles ? (N - u0) : kBlockTiles);
+
+  ColBlock<T, DK, kStateThreads> kr;
+  ColBlock<T, DV, kStateThreads> vr;
+  auto nrow_of = [&](int64_t u) { return (int)((Tlen - u * R) < R ? (Tlen - u * R) : R); };
+  kr.load(k, (int64_t)b * Tlen + u0 * R, 0, nrow_of(u0), H, h);
+  vr.load(v, (int64_t)b * Tlen + u0 * R, 0, nrow_of(u0), H, h);
+
+  f32x4 run[TM][TN];
 #pragma unroll
-    for (int ks = 0; ks < C / M::KSTEP; ++ks) {
-      const int k0 = ks * M::KSTEP + g * M::KPL;
-      acc = M::mma(M::load(&vt_s[(mt * 16 + r16) * LDT + k0]), M::load(&kt_s[(nt * 16 + r16) * LDT + k0]), acc);
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int jn = 0; jn < TN; ++jn) run[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int a = 0; a < ntile; ++a) {
+    const int64_t u = u0 + a;
+    const int64_t row0 = (int64_t)b * Tlen + u * R;
+    const int nrow = nrow_of(u);
+    tile_cumsum<R>(log_alpha, row0, nrow, H, h, cl_s, wsum_s);
+    const float tot = cl_s[R - 1];
+    for (int r = tid; r < R; r += kStateThreads) dec_s[r] = r < nrow ? fast_exp2(tot - cl_s[r]) : 0.f;
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < TN; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int kb = 0; kb < STEPS; ++kb) {
+      __syncthreads();  // previous step's readers done; dec_s visible
+      vr.template store_cols<false>(vt_s, LDT, nullptr);
+      kr.template store_cols<true>(kt_s, LDT, dec_s + kb * kKB);
+      __syncthreads();
+      // prefetch the next step (next 64 rows of this tile, or the first rows of the next tile)
+      if (kb + 1 < STEPS) {
+        kr.load(k, row0, (kb + 1) * kKB, nrow, H, h);
+        vr.load(v, row0, (kb + 1) * kKB, nrow, H, h);
+      } else if (a + 1 < ntile) {
+        kr.load(k, row0 + R, 0, nrow_of(u + 1), H, h);
+        vr.load(v, row0 + R, 0, nrow_of(u + 1), H, h);
+      }
+      if (active) {
+#pragma unroll
+        for (int ks = 0; ks < kKB / M::KSTEP; ++ks) {
+          const int k0 = ks * M::KSTEP + g * M::KPL;
+          typename M::frag bf[TN];
+#pragma unroll
+          for (int jn = 0; jn < TN; ++jn) bf[jn] = M::load(&kt_s[((wn * TN + jn) * 16 + r16) * LDT + k0]);
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            const typename M::frag af = M::load(&vt_s[((wm * TM + i) * 16 + r16) * LDT + k0]);
+#pragma unroll
+            for (int jn = 0; jn < TN; ++jn) acc[i][jn] = M::mma(af, bf[jn], acc[i][jn]);
+          }
+        }
+      }
+    }
+
+    if (tid == 0) tot2_out[bh * N + u] = tot;
+    if (!active) continue;
+    // Fold the tile state into the block's summaries and store the ones readers need.
+    T* dst0 = nullptr;
+    T* dst1 = nullptr;
+    if constexpr (HAS_LAMBDA) {
+      const float e = exp2f(tot);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int jn = 0; jn < TN; ++jn) run[i][jn] = run[i][jn] * e + acc[i][jn];
+      if ((a & 1) == 0) dst0 = nodes.at(bh, N, 1, u, SZ);                // even tile: its own state
+      if (a == 1) dst1 = nodes.at(bh, N, 2, u - 1, SZ);                  // pair summary, tiles 0-1
+      if (a == kBlockTiles - 1) dst1 = nodes.at(bh, N, 3, u - 3, SZ);    // block summary
+    } else {
+      dst0 = tiles + (bh * N + u) * SZ;
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) out[(int64_t)(mt * 16 + 4 * g + r) * DK + nt * 16 + r16] = acc[r];
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < TN; ++jn)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int p = (wm * TM + i) * 16 + 4 * g + r, n = (wn * TN + jn) * 16 + r16;
+          if (dst0) dst0[p * DK + n] = from_f32<T>(acc[i][jn][r]);
+          if (dst1) dst1[p * DK + n] = from_f32<T>(run[i][jn][r]);
+        }
   }
 }
 
 // ---------------------------------------------------------------------------------------------
-// Kernel 2: level scan.  Elementwise over the d_v*d_k state entries (4 per thread), sequential
-// over the chunks of one (b, h).
+// Kernel 2: block scan.  grid.x = element blocks + 1; the extra workgroup computes the gaps.
 //
-// Level j (group size 2^(j-1) chunks): the source groups are the even-indexed groups; inside
-// one, acc_j <- exp2(tot_z) acc_j + S_z, reset at the group start; at the group end the
-// summary (all chunk states decayed to the group end) is stored if some chunk reads it.
-// gap_j(z) = sum of tot over the chunks of z's own aligned 2^(j-1)-block that precede z.
+// Summaries (elementwise over the d_v*d_k state entries, 2 per thread, sequential over the
+// blocks of one (b, h)): tile level j >= 4 is block level jb = j - 2 (groups of 2^(jb-1) blocks).
+// The source groups are the even-indexed groups; inside one, acc <- exp2(block total) acc +
+// block summary, reset at the group start; the summary is stored at the group end.
+// lambda == NULL: the running state entering tile u, R_0 = 0, R_{u+1} = exp2(tot_u) R_u + S_u.
+//
+// Gaps: gap_j(u) = sum of tile totals over the tiles of u's own aligned 2^(j-1)-tile block that
+// precede u.  That range is the union, over the set bits k <= j-2 of u, of the aligned 2^k-tile
+// blocks ending where the next one starts, so gap_j(u) = gap_(j-1)(u) + [bit j-2 of u] *
+// (sum of tot over the 2^(j-2)-block with index (u >> (j-2)) - 1): a sum over exact ranges,
+// built from a tree of block sums in LDS.
 // ---------------------------------------------------------------------------------------------
-constexpr int kMaxLevels = 24;  // inter-chunk levels: supports T/C up to 2^24
+constexpr int kMaxGapTiles = 8192;  // tiles per sequence the gap tree holds (T <= 8192 R)
+constexpr int kScanUnroll = 8;      // summary loads in flight per thread
 
-template <typename TN>
-__global__ __launch_bounds__(256) void k_level_scan(const float* __restrict__ states,
-                                                    const float* __restrict__ tot2, TN* __restrict__ nodes,
+template <typename T>
+__global__ __launch_bounds__(256) void k_block_scan(Nodes<T> nodes, const T* __restrict__ tiles,
+                                                    T* __restrict__ running, const float* __restrict__ tot2,
                                                     float* __restrict__ gaps2, int64_t N, int J, int SZ,
-                                                    int64_t nodes_per_bh, int has_lambda) {
+                                                    int has_lambda) {
+  typedef T T2 __attribute__((ext_vector_type(2)));
   const int64_t bh = blockIdx.y;
-  const int e0 = (blockIdx.x * 256 + threadIdx.x) * 4;
+  const int tid = threadIdx.x;
   const float* tot = tot2 + bh * N;
+  const int64_t NB = (N + kBlockTiles - 1) / kBlockTiles;
 
-  if (blockIdx.x == 0 && threadIdx.x == 0 && has_lambda) {
-    float gsum[kMaxLevels];
-#pragma unroll
-    for (int j = 0; j < kMaxLevels; ++j) gsum[j] = 0.f;
-    for (int64_t z = 0; z < N; ++z) {
-      const float tz = tot[z];
-#pragma unroll
-      for (int j = 1; j <= kMaxLevels; ++j) {
-        if (j <= J) {
-          if ((z & ((int64_t(1) << (j - 1)) - 1)) == 0) gsum[j - 1] = 0.f;
-          gaps2[(bh * N + z) * J + (j - 1)] = gsum[j - 1];
-          gsum[j - 1] += tz;
-        }
-      }
+  if (blockIdx.x == gridDim.x - 1) {
+    __shared__ float bs[2 * kMaxGapTiles];
+    if (!has_lambda || J == 0) return;
+    for (int64_t u = tid; u < N; u += 256) bs[u] = tot[u];
+    __syncthreads();
+    int64_t off_prev = 0, off = N;
+    for (int k = 1; k < J; ++k) {
+      const int64_t len = N >> k;
+      for (int64_t m = tid; m < len; m += 256) bs[off + m] = bs[off_prev + 2 * m] + bs[off_prev + 2 * m + 1];
+      __syncthreads();
+      off_prev = off;
+      off += len;
     }
-  }
-  if (e0 >= SZ) return;
-
-  const float* src = states + bh * N * SZ + e0;
-  TN* dst = nodes + bh * nodes_per_bh * SZ + e0;
-  if (!has_lambda) {
-    f32x4 run = {0.f, 0.f, 0.f, 0.f};
-    for (int64_t z = 0; z < N; ++z) {
-      const f32x4 s = *reinterpret_cast<const f32x4*>(src + z * SZ);
-      const float e = exp2f(tot[z]);
-#pragma unroll
-      for (int c = 0; c < 4; ++c) dst[z * SZ + c] = from_f32<TN>(run[c]);
-      run = run * e + s;
+    for (int64_t u = tid; u < N; u += 256) {
+      float gsum = 0.f;
+      int64_t ok = 0;  // offset of the level-(j-2) block sums
+      for (int j = 1; j <= J; ++j) {
+        if (j >= 2) {
+          const int k = j - 2;
+          if ((u >> k) & 1) gsum += bs[ok + (u >> k) - 1];
+          ok += N >> k;
+        }
+        gaps2[(bh * N + u) * J + (j - 1)] = gsum;
+      }
     }
     return;
   }
-  f32x4 acc[kMaxLevels];
+
+  const int e0 = (blockIdx.x * 256 + tid) * 2;
+  if (e0 >= SZ) return;
+
+  if (!has_lambda) {
+    const T* src = tiles + bh * N * SZ + e0;
+    T* dst = running + bh * N * SZ + e0;
+    float r0 = 0.f, r1 = 0.f;
+    for (int64_t u0 = 0; u0 < N; u0 += kScanUnroll) {
+      T2 sv[kScanUnroll];
 #pragma unroll
-  for (int j = 0; j < kMaxLevels; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  f32x4 s_next = *reinterpret_cast<const f32x4*>(src);
-  for (int64_t z = 0; z < N; ++z) {
-    const f32x4 s = s_next;
-    if (z + 1 < N) s_next = *reinterpret_cast<const f32x4*>(src + (z + 1) * SZ);
-    const float e = exp2f(tot[z]);
+      for (int i = 0; i < kScanUnroll; ++i)
+        if (u0 + i < N) sv[i] = *reinterpret_cast<const T2*>(src + (u0 + i) * SZ);
 #pragma unroll
-    for (int j = 1; j <= kMaxLevels; ++j) {
-      const int64_t m = z >> (j - 1);
-      if (j > J || (m & 1)) continue;                       // beyond the top level, or z reads
-      const int64_t mask = (int64_t(1) << (j - 1)) - 1;
-      if ((z & mask) == 0) acc[j - 1] = s;                   // group start
-      else acc[j - 1] = acc[j - 1] * e + s;
-      if (((z + 1) & mask) == 0 && ((m + 1) << (j - 1)) < N) {  // group end with a reader
-        TN* d = dst + node_slot(N, j, m << (j - 1)) * SZ;
+      for (int i = 0; i < kScanUnroll; ++i) {
+        if (u0 + i >= N) break;
+        T2 out;
+        out[0] = from_f32<T>(r0);
+        out[1] = from_f32<T>(r1);
+        *reinterpret_cast<T2*>(dst + (u0 + i) * SZ) = out;
+        const float e = exp2f(tot[u0 + i]);
+        r0 = r0 * e + to_f32(sv[i][0]);
+        r1 = r1 * e + to_f32(sv[i][1]);
+      }
+    }
+    return;
+  }
+  if (J < 4) return;
+  float a0[kMaxLevels], a1[kMaxLevels];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) d[c] = from_f32<TN>(acc[j - 1][c]);
+  for (int j = 0; j < kMaxLevels; ++j) a0[j] = a1[j] = 0.f;
+  for (int64_t bl0 = 0; bl0 < NB; bl0 += kScanUnroll) {
+    T2 sv[kScanUnroll];
+#pragma unroll
+    for (int i = 0; i < kScanUnroll; ++i)
+      if (bl0 + i < NB) sv[i] = *reinterpret_cast<const T2*>(nodes.at(bh, N, 3, (bl0 + i) * kBlockTiles, SZ) + e0);
+#pragma unroll
+    for (int i = 0; i < kScanUnroll; ++i) {
+      const int64_t bl = bl0 + i;
+      if (bl >= NB) break;
+      float tb = 0.f;
+      for (int a = 0; a < kBlockTiles; ++a)
+        if (bl * kBlockTiles + a < N) tb += tot[bl * kBlockTiles + a];
+      const float e = exp2f(tb);
+      const float s0 = to_f32(sv[i][0]), s1 = to_f32(sv[i][1]);
+#pragma unroll
+      for (int j = 4; j <= kMaxLevels; ++j) {
+        const int jb = j - 2;
+        const int64_t m = bl >> (jb - 1);
+        if (j > J || (m & 1)) continue;
+        const int64_t mask = (int64_t(1) << (jb - 1)) - 1;
+        if ((bl & mask) == 0) {
+          a0[j - 1] = s0;
+          a1[j - 1] = s1;
+        } else {
+          a0[j - 1] = a0[j - 1] * e + s0;
+          a1[j - 1] = a1[j - 1] * e + s1;
+        }
+        const int64_t first_tile = (m << (jb - 1)) * kBlockTiles;
+        if (((bl + 1) & mask) == 0 && first_tile + (int64_t(1) << (j - 1)) < N) {
+          T2 out;
+          out[0] = from_f32<T>(a0[j - 1]);
+          out[1] = from_f32<T>(a1[j - 1]);
+          *reinterpret_cast<T2*>(nodes.at(bh, N, j, first_tile, SZ) + e0) = out;
+        }
       }
     }
   }
 }
 
 // ---------------------------------------------------------------------------------------------
-// Kernel 3: chunk outputs.  One wave per (chunk, head, batch).
+// Kernel 3: tile outputs.  RS workgroups (4 waves each) per (tile, head, batch).
 //
-// Orientation: the wave builds O^T (d_v x C) so that the query index is the MFMA column:
-//   S^T = K Q^T        (keys x queries, K = d_k),  masked in registers,
-//   O^T += V^T P^T     (P^T in the result layout of S^T is directly a B operand once its k
-//                       slots are matched by loading V^T at the same keys),
-//   O^T += w (.) U^T Q^T  per inter-chunk level, w = per-query weight (a column scale).
+// Work split: the R tile rows form R/16 groups of 16.  Each wave owns GPW groups, chosen so that
+// every wave does the same share of the causal triangle: with one workgroup per tile, wave w
+// owns groups w, w+4, ...; with two (R = 256), the groups pair up as (x, 15 - x), each pair
+// costing 17 key tiles, and the eight pairs are dealt to the two workgroups.
+// Orientation: the waves build O^T (d_v x rows) so that the query index is the MFMA column:
+//   S^T = K Q^T per 16x16 tile (K = d_k), masked in registers with
+//         lambda_i^(bitlen(i XOR j)) * exp2(cl_i - cl_j) for j <= i (tile-local i, j);
+//   O^T += V^T P^T (P^T in the result layout of S^T is directly a B operand once V^T is
+//         loaded at the same keys);
+//   O^T += w (.) U^T Q^T for every inter-tile level (w = per-query weight, a column scale).
+// The next 64-key block of K/V, and the next level's summary, are loaded into registers while
+// the current one is being used.
 // ---------------------------------------------------------------------------------------------
-template <typename T, int C, int DK, int DV, bool HAS_LAMBDA>
-__global__ __launch_bounds__(64) void k_chunk_out(const T* __restrict__ q, const T* __restrict__ k,
-                                                  const T* __restrict__ v, const float* __restrict__ log_alpha,
-                                                  const float* __restrict__ lam, const T* __restrict__ nodes,
-                                                  const float* __restrict__ gaps2, T* __restrict__ o,
-                                                  int64_t Tlen, int H, int L, int J, int64_t nodes_per_bh) {
-  using M = Mfma<T>;
-  constexpr int VEC = Vec16<T>::N;
-  constexpr int LDK = DK + VEC;   // K row stride (elements)
-  constexpr int LDV = C + VEC;    // V^T row stride (elements)
-  constexpr int LDL = 24;         // lambda row stride in LDS (>= L for every supported T)
-  constexpr int QT = C / 16, MT = DV / 16, KS = DK / M::KSTEP;
-  constexpr int LOG2C = (C == 16) ? 4 : (C == 32) ? 5 : (C == 64) ? 6 : 7;
-  __shared__ T k_s[C * LDK];
-  __shared__ T vt_s[DV * LDV];
-  __shared__ float cl_s[C];
-  __shared__ float lam_s[HAS_LAMBDA ? C * LDL : 1];
-
-  const int z = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int lane = threadIdx.x, r16 = lane & 15, g = lane >> 4;
-  const int64_t N = Tlen / C;
-  const int64_t bh = (int64_t)b * H + h;
-  const int64_t tok0 = (int64_t)b * Tlen + (int64_t)z * C;
-
-  {
-    float la = lane < C ? log_alpha[(tok0 + lane) * H + h] * kLog2e : 0.f;
-    float cl = wave_inclusive_scan(la);
-    if (lane < C) cl_s[lane] = cl;
-  }
-  if constexpr (HAS_LAMBDA) {
-    for (int idx = lane; idx < C * L; idx += 64) {
-      const int t = idx / L, l = idx % L;
-      lam_s[t * LDL + l] = lam[((tok0 + t) * H + h) * L + l];
+template <int R>
+struct RowMap {
+  static constexpr int RS = R >= 256 ? 2 : 1;   // workgroups per tile
+  static constexpr int GPW = R / (64 * RS);     // 16-row groups per wave
+  __device__ static inline int group(int c, int wave, int s) {
+    if constexpr (RS == 1) {
+      return wave + 4 * s;
+    } else {
+      // pairs (x, 15 - x); x in {0,3,4,7} -> workgroup 0, x in {1,2,5,6} -> workgroup 1
+      const int x = (c == 0) ? ((wave & 1) ? 4 * (wave >> 1) + 3 : 4 * (wave >> 1))
+                             : ((wave & 1) ? 4 * (wave >> 1) + 2 : 4 * (wave >> 1) + 1);
+      return s == 0 ? x : (R / 16 - 1) - x;
     }
   }
-  for (int idx = lane; idx < C * DK / VEC; idx += 64) {
-    const int t = idx / (DK / VEC), d0 = (idx % (DK / VEC)) * VEC;
-    *reinterpret_cast<typename Vec16<T>::type*>(&k_s[t * LDK + d0]) =
-        *reinterpret_cast<const typename Vec16<T>::type*>(k + ((tok0 + t) * H + h) * DK + d0);
-  }
-  for (int idx = lane; idx < C * DV / VEC; idx += 64) {
-    const int t = idx / (DV / VEC), d0 = (idx % (DV / VEC)) * VEC;
-    typename Vec16<T>::type x = *reinterpret_cast<const typename Vec16<T>::type*>(v + ((tok0 + t) * H + h) * DV + d0);
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) vt_s[(d0 + e) * LDV + t] = x[e];
-  }
+};
 
-  // Q^T fragments (B operand), kept in registers for the whole chunk.
-  typename M::frag qf[QT][KS];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qf[qt][ks] = M::load(q + ((tok0 + qt * 16 + r16) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
-  __syncthreads();
+template <typename T, int C, int DK, int DV, bool HAS_LAMBDA>
+__global__ __launch_bounds__(256, 2) void k_tile_out(const T* __restrict__ q, const T* __restrict__ k,
+                                                     const T* __restrict__ v, const float* __restrict__ log_alpha,
+                                                     const float* __restrict__ lam, Nodes<T> nodes,
+                                                     const T* __restrict__ running, const float* __restrict__ gaps2,
+                                                     T* __restrict__ o, int64_t Tlen, int H, int L, int J) {
+  using M = Mfma<T>;
+  typedef typename Vec16<T>::type V16;
+  constexpr int R = kTileChunks * C;
+  constexpr int LOG2R = (R == 64) ? 6 : (R == 128) ? 7 : (R == 256) ? 8 : 9;
+  constexpr int VEC = Vec16<T>::N;
+  constexpr int LDK = DK + VEC;     // K and U row stride (elements)
+  constexpr int LDV = kKB + VEC;    // V^T row stride (elements)
+  using RM = RowMap<R>;
+  constexpr int GPW = RM::GPW;
+  constexpr int ROWS = 64 * GPW;    // rows of this workgroup
+  constexpr int MT = DV / 16, KS = DK / M::KSTEP;
+  constexpr int SZ = DK * DV;
+  constexpr int KV_ELEMS = kKB * LDK + DV * LDV;
+  constexpr int U_ELEMS = DV * LDK;
+  constexpr int ULOADS = (SZ / VEC + 255) / 256;
+  __shared__ T buf_s[KV_ELEMS > U_ELEMS ? KV_ELEMS : U_ELEMS];
+  __shared__ float cl_s[R];
+  __shared__ float wsum_s[4];
+  __shared__ float lam_s[HAS_LAMBDA ? ROWS * kMaxLevels : 1];  // rows in slot order: (wave, s, r16)
+  __shared__ float kdec_s[R];
+  T* k_s = buf_s;
+  T* vt_s = buf_s + kKB * LDK;
+  T* u_s = buf_s;
 
-  f32x4 oacc[MT][QT];
+  const int u = blockIdx.x / RM::RS, c = blockIdx.x % RM::RS, h = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
+  const int64_t N = (Tlen + R - 1) / R;
+  const int64_t bh = (int64_t)b * H + h;
+  const int64_t row0 = (int64_t)b * Tlen + (int64_t)u * R;
+  const int nrow = (int)((Tlen - (int64_t)u * R) < R ? (Tlen - (int64_t)u * R) : R);
+  const int nkb = (nrow + kKB - 1) / kKB;
+  int grp[GPW];
+  int gmax = 0;
+#pragma unroll
+  for (int s = 0; s < GPW; ++s) {
+    grp[s] = RM::group(c, wave, s);
+    gmax = grp[s] > gmax ? grp[s] : gmax;
+  }
+  const int nkb_w = (16 * gmax + 15) / kKB + 1;  // key blocks this wave's rows reach
+
+  RowBlock<T, DK, 256> kr;
+  ColBlock<T, DV, 256> vr;
+  kr.load(k, row0, 0, nrow, H, h);
+  vr.load(v, row0, 0, nrow, H, h);
+
+  if constexpr (HAS_LAMBDA) {
+    // one row of lambda per thread (slot order), all loads issued before the LDS stores
+    if (tid < ROWS) {
+      const int ws = tid / (16 * GPW), ss = (tid / 16) % GPW;
+      const int row = 16 * RM::group(c, ws, ss) + (tid & 15);
+      if (row < nrow) {
+        float lv[kMaxLevels];
+#pragma unroll
+        for (int l = 0; l < kMaxLevels; ++l)
+          if (l < L) lv[l] = lam[((row0 + row) * H + h) * L + l];
+#pragma unroll
+        for (int l = 0; l < kMaxLevels; ++l)
+          if (l < L) lam_s[tid * L + l] = lv[l];
+      }
+    }
+  }
+  tile_cumsum<R>(log_alpha, row0, nrow, H, h, cl_s, wsum_s);
+  // key-side decay to the end of each 16-key tile: kdec[j] = exp2(cl[j | 15] - cl[j])
+  for (int r = tid; r < R; r += 256) kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
+
+  // Q^T fragments (B operand) for this wave's row groups, kept in registers.
+  typename M::frag qf[GPW][KS];
+#pragma unroll
+  for (int s = 0; s < GPW; ++s) {
+    const int row = 16 * grp[s] + r16;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (row < nrow) qf[s][ks] = M::load(q + ((row0 + row) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
+      else qf[s][ks] = typename M::frag{};
+    }
+  }
+  // lambda row of slot s of this lane in lam_s
+  auto lrow = [&](int s) { return (wave * GPW + s) * 16 + r16; };
+
+  f32x4 oacc[MT][GPW];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) oacc[mt][qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < GPW; ++s) oacc[mt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // ---- intra-chunk stage: D of Eq. 5
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    const int i = qt * 16 + r16;      // this lane's query (chunk-local)
-    const float cli = cl_s[i];
-    f32x4 p[QT];
-#pragma unroll
-    for (int kt = 0; kt <= qt; ++kt) {
-      f32x4 s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        s = M::mma(M::load(&k_s[(kt * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]), qf[qt][ks], s);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int j = kt * 16 + 4 * g + r;  // key (chunk-local)
-        float w = 0.f;
-        if (j <= i) {
-          w = exp2f(cli - cl_s[j]);
-          if constexpr (HAS_LAMBDA) w *= lam_s[i * LDL + level_local(i, j)];
-        }
-        p[kt][r] = s[r] * w;
-      }
+  // ---- intra-tile: causal R x R masked contraction, one 64-key block at a time
+  for (int kb = 0; kb < nkb; ++kb) {
+    __syncthreads();  // previous block's readers are done (and cl/lambda staging on entry)
+    kr.store_rows(k_s, LDK);
+    vr.template store_cols<false>(vt_s, LDV, nullptr);
+    __syncthreads();
+    if (kb + 1 < nkb) {
+      kr.load(k, row0, (kb + 1) * kKB, nrow, H, h);
+      vr.load(v, row0, (kb + 1) * kKB, nrow, H, h);
     }
+    if (kb >= nkb_w) continue;
+    // key sub-steps: 32 keys (bf16, two 16-key tiles) or 16 keys (fp32)
+    constexpr int KT_PER = (M::KPL == 8) ? 2 : 1;
 #pragma unroll
-    for (int kt = qt + 1; kt < QT; ++kt) p[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    if constexpr (M::KPL == 8) {
-      // bf16: one k step = 32 keys = key tiles (2 ks, 2 ks + 1); slots 0-3 <- tile 2 ks rows
-      // 4g..4g+3, slots 4-7 <- tile 2 ks + 1 rows 4g..4g+3.
+    for (int st = 0; st < 4 / KT_PER; ++st) {
+      const int KT0 = 4 * kb + st * KT_PER;  // first 16-key tile of the sub-step (tile-local)
+      if (KT0 > gmax) break;                  // no row group of this wave reaches these keys
+      f32x4 p[KT_PER][GPW];
 #pragma unroll
-      for (int ks = 0; ks < (QT + 1) / 2; ++ks) {
-        if (2 * ks > qt) break;
-        typename M::frag bp;
+      for (int hh = 0; hh < KT_PER; ++hh) {
+        const int kt = st * KT_PER + hh, KT = KT0 + hh;
+        typename M::frag kf[KS];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          bp[r] = from_f32<T>(p[2 * ks][r]);
-          bp[4 + r] = (2 * ks + 1 < QT) ? from_f32<T>(p[2 * ks + 1][r]) : from_f32<T>(0.f);
+        for (int ks = 0; ks < KS; ++ks) kf[ks] = M::load(&k_s[(kt * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]);
+#pragma unroll
+        for (int s = 0; s < GPW; ++s) {
+          const int gi = grp[s];
+          p[hh][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (KT > gi || 16 * gi >= nrow) continue;
+          f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) sacc = M::mma(kf[ks], qf[s][ks], sacc);
+          const int i = 16 * gi + r16;
+          const float cli = cl_s[i];
+          if (KT < gi) {
+            // off-diagonal 16x16 tile: one level for the whole tile (4 + bitlen(gi ^ KT)) and the
+            // decay split at the tile's last key: exp2(cl_i - cl_end) * exp2(cl_end - cl_j)
+            float qs = fast_exp2(cli - cl_s[16 * KT + 15]);
+            if constexpr (HAS_LAMBDA) qs *= lam_s[lrow(s) * L + level_local(16 * gi, 16 * KT)];
+            const f32x4 kd = *reinterpret_cast<const f32x4*>(&kdec_s[16 * KT + 4 * g]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) p[hh][s][r] = sacc[r] * qs * kd[r];
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int j = 16 * KT + 4 * g + r;
+              float w = 0.f;
+              if (j <= i) {
+                w = fast_exp2(cli - cl_s[j]);
+                if constexpr (HAS_LAMBDA) w *= lam_s[lrow(s) * L + level_local(i, j)];
+              }
+              p[hh][s][r] = sacc[r] * w;
+            }
+          }
         }
+      }
+      if constexpr (M::KPL == 8) {
+        // slots 0-3 <- key tile KT0 rows 4g..4g+3, slots 4-7 <- key tile KT0+1 rows 4g..4g+3;
+        // V^T is read at the same keys.
+        typename M::frag bp[GPW];
+#pragma unroll
+        for (int s = 0; s < GPW; ++s)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            bp[s][r] = from_f32<T>(p[0][s][r]);
+            bp[s][4 + r] = from_f32<T>(p[1][s][r]);
+          }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-          const T* row = &vt_s[(mt * 16 + r16) * LDV + ks * 32 + 4 * g];
+          const T* row = &vt_s[(mt * 16 + r16) * LDV + st * 32 + 4 * g];
           const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row);
           const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 16);
           const typename M::frag a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          oacc[mt][qt] = M::mma(a, bp, oacc[mt][qt]);
-        }
-      }
-    } else {
-      // fp32: one k step = 4 keys {kt*16 + 4g + r : g}, i.e. slot r of every lane group.
 #pragma unroll
-      for (int kt = 0; kt <= qt; ++kt)
+          for (int s = 0; s < GPW; ++s)
+            if (KT0 <= grp[s]) oacc[mt][s] = M::mma(a, bp[s], oacc[mt][s]);
+        }
+      } else {
+        // fp32: one k step = 4 keys {16 kt + 4g + r : g}, i.e. slot r of every lane group.
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-            oacc[mt][qt] = M::mma(vt_s[(mt * 16 + r16) * LDV + kt * 16 + 4 * g + r], p[kt][r], oacc[mt][qt]);
-    }
-  }
-
-  // ---- inter-chunk stage
-  if constexpr (HAS_LAMBDA) {
-    for (int j = 1; j <= J; ++j) {
-      if (!reads_level(z, j)) continue;
-      const T* U = nodes + (bh * nodes_per_bh + node_slot(N, j, source_first(z, j))) * (int64_t)(DV * DK);
-      const float gap = gaps2[(bh * N + z) * J + (j - 1)];
-      float w[QT];
+          for (int mt = 0; mt < MT; ++mt) {
+            const T a = vt_s[(mt * 16 + r16) * LDV + st * 16 + 4 * g + r];
 #pragma unroll
-      for (int qt = 0; qt < QT; ++qt) {
-        const int i = qt * 16 + r16;
-        w[qt] = lam_s[i * LDL + LOG2C + j] * exp2f(cl_s[i] + gap);
-      }
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        f32x4 tmp[QT];
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) tmp[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const typename M::frag a = M::load(U + (mt * 16 + r16) * DK + ks * M::KSTEP + g * M::KPL);
-#pragma unroll
-          for (int qt = 0; qt < QT; ++qt) tmp[qt] = M::mma(a, qf[qt][ks], tmp[qt]);
-        }
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) oacc[mt][qt] += w[qt] * tmp[qt];
-      }
-    }
-  } else {
-    if (z > 0) {
-      const T* U = nodes + (bh * nodes_per_bh + z) * (int64_t)(DV * DK);
-      float w[QT];
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) w[qt] = exp2f(cl_s[qt * 16 + r16]);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        f32x4 tmp[QT];
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) tmp[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const typename M::frag a = M::load(U + (mt * 16 + r16) * DK + ks * M::KSTEP + g * M::KPL);
-#pragma unroll
-          for (int qt = 0; qt < QT; ++qt) tmp[qt] = M::mma(a, qf[qt][ks], tmp[qt]);
-        }
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) oacc[mt][qt] += w[qt] * tmp[qt];
+            for (int s = 0; s < GPW; ++s)
+              if (KT0 <= grp[s]) oacc[mt][s] = M::mma(a, p[0][s][r], oacc[mt][s]);
+          }
       }
     }
   }
 
-  // ---- store O: lane holds query qt*16 + r16, d_v entries mt*16 + 4g .. +3
+  // ---- inter-tile levels (set bits of u), the next level's summary prefetched into registers
+  auto level_src = [&](int j, float* gap) -> const T* {
+    if constexpr (HAS_LAMBDA) {
+      *gap = gaps2[(bh * N + u) * J + (j - 1)];
+      return nodes.at(bh, N, j, source_first(u, j), SZ);
+    } else {
+      *gap = 0.f;
+      return running + (bh * N + u) * SZ;
+    }
+  };
+  auto next_level = [&](int j) {
+    if constexpr (HAS_LAMBDA) {
+      for (++j; j <= J; ++j)
+        if (reads_level(u, j)) return j;
+      return 0;
+    } else {
+      return (j == 0 && u > 0) ? 1 : 0;
+    }
+  };
+  V16 ur[ULOADS];
+  auto load_u = [&](const T* U) {
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    T* orow = o + ((tok0 + qt * 16 + r16) * H + h) * DV + 4 * g;
+    for (int i = 0; i < ULOADS; ++i) {
+      const int idx = tid + 256 * i;
+      if (idx < SZ / VEC) ur[i] = *reinterpret_cast<const V16*>(U + idx * VEC);
+    }
+  };
+  int j = next_level(0);
+  float gap = 0.f;
+  if (j) load_u(level_src(j, &gap));
+  while (j) {
+    __syncthreads();  // LDS buffer free
+#pragma unroll
+    for (int i = 0; i < ULOADS; ++i) {
+      const int idx = tid + 256 * i;
+      if (idx < SZ / VEC) {
+        const int p = idx / (DK / VEC), n0 = (idx % (DK / VEC)) * VEC;
+        *reinterpret_cast<V16*>(&u_s[p * LDK + n0]) = ur[i];
+      }
+    }
+    __syncthreads();
+    const int jn = next_level(j);
+    float gap_n = 0.f;
+    if (jn) load_u(level_src(jn, &gap_n));
+    float w[GPW];
+#pragma unroll
+    for (int s = 0; s < GPW; ++s) {
+      const int i = 16 * grp[s] + r16;
+      w[s] = fast_exp2(cl_s[i] + gap);
+      if constexpr (HAS_LAMBDA) w[s] *= (i < nrow) ? lam_s[lrow(s) * L + LOG2R + j] : 0.f;
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      f32x4 tmp[GPW];
+#pragma unroll
+      for (int s = 0; s < GPW; ++s) tmp[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const typename M::frag a = M::load(&u_s[(mt * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]);
+#pragma unroll
+        for (int s = 0; s < GPW; ++s) tmp[s] = M::mma(a, qf[s][ks], tmp[s]);
+      }
+#pragma unroll
+      for (int s = 0; s < GPW; ++s) oacc[mt][s] += w[s] * tmp[s];
+    }
+    j = jn;
+    gap = gap_n;
+  }
+
+  // ---- store O: lane holds row 16 grp[s] + r16, d_v entries 16 mt + 4g .. +3
+#pragma unroll
+  for (int s = 0; s < GPW; ++s) {
+    const int row = 16 * grp[s] + r16;
+    if (row >= nrow) continue;
+    T* orow = o + ((row0 + row) * H + h) * DV + 4 * g;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) orow[mt * 16 + r] = from_f32<T>(oacc[mt][qt][r]);
+      for (int r = 0; r < 4; ++r) orow[mt * 16 + r] = from_f32<T>(oacc[mt][s][r]);
   }
 }
 
 // ---------------------------------------------------------------------------------------------
-// Debug level map: the level each (t, s) pair receives from the device functions above.
+// Debug level map: the level each (t, s) pair receives from the device functions the kernels use.
 // ---------------------------------------------------------------------------------------------
-__global__ void k_debug_level_map(int64_t Tlen, int C, int log2C, int J, int8_t* out) {
+__global__ void k_debug_level_map(int64_t Tlen, int R, int log2R, int J, int8_t* out) {
   const int64_t t = blockIdx.x;
   for (int64_t s = threadIdx.x; s < Tlen; s += blockDim.x) {
     int lev = -1;
     if (s <= t) {
-      const int64_t zt = t / C, zs = s / C;
-      if (zt == zs) {
-        lev = level_local(int(t % C), int(s % C));
+      const int64_t ut = t / R, us = s / R;
+      if (ut == us) {
+        lev = level_local(int(t % R), int(s % R));
       } else {
         lev = -2;  // no source group claims the pair: a bug
         for (int j = 1; j <= J; ++j)
-          if (reads_level(zt, j) && zs >= source_first(zt, j) && zs < source_first(zt, j) + (int64_t(1) << (j - 1)))
-            lev = log2C + j;
+          if (reads_level(ut, j) && us >= source_first(ut, j) && us < source_first(ut, j) + (int64_t(1) << (j - 1)))
+            lev = log2R + j;
       }
     }
     out[t * Tlen + s] = (int8_t)lev;
@@ -374,37 +719,105 @@ __global__ void k_debug_level_map(int64_t Tlen, int C, int log2C, int J, int8_t*
 }
 
 // ---------------------------------------------------------------------------------------------
-// Host-side launchers
+// Host side
 // ---------------------------------------------------------------------------------------------
+static int bitlen_h(uint64_t x) { return x ? 64 - __builtin_clzll(x) : 0; }
+
+int64_t tiles_of(int64_t T, int64_t C) { return (T + kTileChunks * C - 1) / (kTileChunks * C); }
+
+int tile_levels(int64_t T, int64_t C) {
+  const int64_t N = tiles_of(T, C);
+  return N <= 1 ? 0 : bitlen_h(uint64_t(N - 1));
+}
+
+int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, int64_t esize,
+                         bool has_lambda, WsLayout* lay) {
+  const int64_t N = tiles_of(T, C);
+  const int J = tile_levels(T, C);
+  const int64_t BH = B * H, SZ = dk * dv;
+  auto al = [](int64_t x) { return (x + 255) & ~int64_t(255); };
+  WsLayout w{};
+  w.N = N;
+  w.J = J;
+  w.n1 = (N + 1) / 2;
+  w.n2 = (N + 3) / 4;
+  w.nb = (N + kBlockTiles - 1) / kBlockTiles;
+  w.nup = 0;
+  for (int j = 4; j <= J; ++j) w.nup += (N + (int64_t(1) << j) - 1) >> j;
+  int64_t cur = 0;
+  w.tot2 = cur; cur += al(BH * N * 4);
+  if (has_lambda) {
+    w.gaps2 = cur; cur += al(BH * N * (J > 0 ? J : 1) * 4);
+    w.lvl1 = cur; cur += al(BH * w.n1 * SZ * esize);
+    w.lvl2 = cur; cur += al(BH * w.n2 * SZ * esize);
+    w.blocks = cur; cur += al(BH * w.nb * SZ * esize);
+    w.upper = cur; cur += al(BH * (w.nup > 0 ? w.nup : 1) * SZ * esize);
+  } else {
+    w.tiles = cur; cur += al(BH * N * SZ * esize);
+    w.running = cur; cur += al(BH * N * SZ * esize);
+  }
+  w.total = cur;
+  if (lay) *lay = w;
+  return cur;
+}
+
 // Enqueues the three stages on `st`.  With `ev` non-null, ev[i] is recorded before stage i
 // and ev[3] after the last one (used by the timed entry point).
 template <typename T, int C, int DK, int DV>
 hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
-  const int64_t N = a.T / C;
-  const int SZ = DK * DV;
-  dim3 grid((unsigned)N, (unsigned)a.H, (unsigned)a.B);
+  constexpr int SZ = DK * DV;
+  WsLayout w;
+  mamba2_workspace(a.B, a.T, a.H, DK, DV, C, sizeof(T), a.lambda != nullptr, &w);
+  char* base = static_cast<char*>(a.workspace);
+  float* tot2 = reinterpret_cast<float*>(base + w.tot2);
+  Nodes<T> nodes{};
+  T* tiles = nullptr;
+  T* running = nullptr;
+  float* gaps2 = nullptr;
+  if (a.lambda) {
+    gaps2 = reinterpret_cast<float*>(base + w.gaps2);
+    nodes.lvl1 = reinterpret_cast<T*>(base + w.lvl1);
+    nodes.lvl2 = reinterpret_cast<T*>(base + w.lvl2);
+    nodes.blocks = reinterpret_cast<T*>(base + w.blocks);
+    nodes.upper = reinterpret_cast<T*>(base + w.upper);
+    nodes.n1 = w.n1;
+    nodes.n2 = w.n2;
+    nodes.nb = w.nb;
+    nodes.nup = w.nup;
+  } else {
+    tiles = reinterpret_cast<T*>(base + w.tiles);
+    running = reinterpret_cast<T*>(base + w.running);
+  }
+  const dim3 gblk((unsigned)w.nb, (unsigned)a.H, (unsigned)a.B);
+  const dim3 gscan((unsigned)((SZ / 2 + 255) / 256 + 1), (unsigned)(a.B * a.H));
+  const dim3 gtile((unsigned)(w.N * RowMap<kTileChunks * C>::RS), (unsigned)a.H, (unsigned)a.B);
   if (ev) (void)hipEventRecord(ev[0], st);
-  hipLaunchKernelGGL((k_chunk_state<T, C, DK, DV>), grid, dim3(256), 0, st, (const T*)a.k, (const T*)a.v,
-                     a.log_alpha, a.ws.states, a.ws.tot2, a.T, (int)a.H);
+  if (a.lambda)
+    hipLaunchKernelGGL((k_block_state<T, C, DK, DV, true>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
+                       a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H);
+  else
+    hipLaunchKernelGGL((k_block_state<T, C, DK, DV, false>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
+                       a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H);
   if (ev) (void)hipEventRecord(ev[1], st);
-  dim3 grid2((unsigned)((SZ / 4 + 255) / 256), (unsigned)(a.B * a.H));
-  hipLaunchKernelGGL((k_level_scan<T>), grid2, dim3(256), 0, st, a.ws.states, a.ws.tot2, (T*)a.ws.nodes,
-                     a.ws.gaps2, N, a.J, SZ, a.ws.nodes_per_bh, a.lambda != nullptr ? 1 : 0);
+  hipLaunchKernelGGL((k_block_scan<T>), gscan, dim3(256), 0, st, nodes, (const T*)tiles, running, (const float*)tot2,
+                     gaps2, w.N, w.J, SZ, a.lambda != nullptr ? 1 : 0);
   if (ev) (void)hipEventRecord(ev[2], st);
   if (a.lambda)
-    hipLaunchKernelGGL((k_chunk_out<T, C, DK, DV, true>), grid, dim3(64), 0, st, (const T*)a.q, (const T*)a.k,
-                       (const T*)a.v, a.log_alpha, a.lambda, (const T*)a.ws.nodes, a.ws.gaps2, (T*)a.o, a.T,
-                       (int)a.H, a.L, a.J, a.ws.nodes_per_bh);
+    hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, true>), gtile, dim3(256), 0, st, (const T*)a.q, (const T*)a.k,
+                       (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (const float*)gaps2,
+                       (T*)a.o, a.T, (int)a.H, a.L, w.J);
   else
-    hipLaunchKernelGGL((k_chunk_out<T, C, DK, DV, false>), grid, dim3(64), 0, st, (const T*)a.q, (const T*)a.k,
-                       (const T*)a.v, a.log_alpha, a.lambda, (const T*)a.ws.nodes, a.ws.gaps2, (T*)a.o, a.T,
-                       (int)a.H, a.L, a.J, a.ws.nodes_per_bh);
+    hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, false>), gtile, dim3(256), 0, st, (const T*)a.q, (const T*)a.k,
+                       (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (const float*)gaps2,
+                       (T*)a.o, a.T, (int)a.H, a.L, w.J);
   if (ev) (void)hipEventRecord(ev[3], st);
   return hipGetLastError();
 }
 
-hipError_t launch_debug_level_map(int64_t T, int C, int log2C, int J, int8_t* out, hipStream_t st) {
-  hipLaunchKernelGGL(k_debug_level_map, dim3((unsigned)T), dim3(256), 0, st, T, C, log2C, J, out);
+hipError_t launch_debug_level_map(int64_t T, int64_t C, int8_t* out, hipStream_t st) {
+  const int R = kTileChunks * (int)C;
+  hipLaunchKernelGGL(k_debug_level_map, dim3((unsigned)T), dim3(256), 0, st, T, R, bitlen_h(uint64_t(R)) - 1,
+                     tile_levels(T, C), out);
   return hipGetLastError();
 }
 
