@@ -101,6 +101,8 @@ def main():
     ap.add_argument("--workload", default="ll_mamba2_bf16_T65536")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="also run a plain device-to-device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the operator's "
@@ -195,6 +197,15 @@ def main():
         "roofline": {"kernel": names[dom], "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak, "traffic": None},
     }
+    if args.copy_mib:
+        # A plain copy kernel of known size: its FETCH_SIZE / WRITE_SIZE counters calibrate the
+        # HBM traffic that the same counters report for the kernels above.
+        src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)

@@ -89,6 +89,19 @@ __device__ __host__ inline int64_t node_slot(int64_t N, int j, int64_t first) {
   return off + (first >> j);
 }
 
+// ------------------------------------------------------------------------- dispatch order
+
+// MI355X has 8 XCDs, each with its own L2, and hands out workgroups round-robin over them.
+// Remapping the dispatch index this way gives each XCD one contiguous range of logical work
+// items, so neighbours in logical order (the two halves of a tile, consecutive tiles of one
+// head that share summaries) run on the same XCD and share its L2.
+constexpr int kXcds = 8;
+__device__ inline int64_t xcd_remap(int64_t id, int64_t total) {
+  const int64_t q = total / kXcds, rem = total % kXcds;
+  const int64_t xcd = id % kXcds, slot = id / kXcds;
+  return xcd * q + (xcd < rem ? xcd : rem) + slot;
+}
+
 // ----------------------------------------------------------------------------- wave helpers
 
 // Inclusive prefix sum across the 64 lanes of a wave (Hillis-Steele over DPP/permute).

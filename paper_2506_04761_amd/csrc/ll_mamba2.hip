@@ -178,10 +178,13 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
   __shared__ float dec_s[R];
   __shared__ float wsum_s[4];
 
-  const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
   const int64_t N = (Tlen + R - 1) / R;  // tiles
-  const int64_t bh = (int64_t)b * H + h;
+  const int64_t NB = (N + kBlockTiles - 1) / kBlockTiles;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // logical order (b, h, blk)
+  const int blk = (int)(work % NB);
+  const int64_t bh = work / NB;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
   const bool active = wave < WM * WN;
   const int wm = wave / WN, wn = wave % WN;
   const int64_t u0 = (int64_t)blk * kBlockTiles;
@@ -418,25 +421,28 @@ __global__ __launch_bounds__(256) void k_block_scan(Nodes<T> nodes, const T* __r
 template <int R>
 struct RowMap {
   static constexpr int RS = R >= 256 ? 2 : 1;   // workgroups per tile
-  static constexpr int GPW = R / (64 * RS);     // 16-row groups per wave
-  __device__ static inline int group(int c, int wave, int s) {
+  static constexpr int NW = R / 16 / RS;        // waves per workgroup: one 16-row group each
+  static constexpr int NT = 64 * NW;            // threads per workgroup
+  // 16-row group owned by `wave` of workgroup c
+  __device__ static inline int group(int c, int wave) {
     if constexpr (RS == 1) {
-      return wave + 4 * s;
+      return wave;
     } else {
-      // pairs (x, 15 - x); x in {0,3,4,7} -> workgroup 0, x in {1,2,5,6} -> workgroup 1
-      const int x = (c == 0) ? ((wave & 1) ? 4 * (wave >> 1) + 3 : 4 * (wave >> 1))
-                             : ((wave & 1) ? 4 * (wave >> 1) + 2 : 4 * (wave >> 1) + 1);
-      return s == 0 ? x : (R / 16 - 1) - x;
+      // pairs (x, 15 - x); x in {0,3,4,7} -> workgroup 0, x in {1,2,5,6} -> workgroup 1;
+      // waves 0-3 take x, waves 4-7 take 15 - x
+      const int w4 = wave & 3;
+      const int x = (c == 0) ? ((w4 & 1) ? 4 * (w4 >> 1) + 3 : 4 * (w4 >> 1))
+                             : ((w4 & 1) ? 4 * (w4 >> 1) + 2 : 4 * (w4 >> 1) + 1);
+      return wave < 4 ? x : (R / 16 - 1) - x;
     }
   }
 };
 
 template <typename T, int C, int DK, int DV, bool HAS_LAMBDA>
-__global__ __launch_bounds__(256, 2) void k_tile_out(const T* __restrict__ q, const T* __restrict__ k,
-                                                     const T* __restrict__ v, const float* __restrict__ log_alpha,
-                                                     const float* __restrict__ lam, Nodes<T> nodes,
-                                                     const T* __restrict__ running, const float* __restrict__ gaps2,
-                                                     T* __restrict__ o, int64_t Tlen, int H, int L, int J) {
+__global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ log_alpha,
+    const float* __restrict__ lam, Nodes<T> nodes, const T* __restrict__ running, const float* __restrict__ gaps2,
+    T* __restrict__ o, int64_t Tlen, int H, int L, int J) {
   using M = Mfma<T>;
   typedef typename Vec16<T>::type V16;
   constexpr int R = kTileChunks * C;
@@ -445,82 +451,75 @@ __global__ __launch_bounds__(256, 2) void k_tile_out(const T* __restrict__ q, co
   constexpr int LDK = DK + VEC;     // K and U row stride (elements)
   constexpr int LDV = kKB + VEC;    // V^T row stride (elements)
   using RM = RowMap<R>;
-  constexpr int GPW = RM::GPW;
-  constexpr int ROWS = 64 * GPW;    // rows of this workgroup
+  constexpr int NT = RM::NT;
+  constexpr int ROWS = 16 * RM::NW; // rows of this workgroup
   constexpr int MT = DV / 16, KS = DK / M::KSTEP;
   constexpr int SZ = DK * DV;
   constexpr int KV_ELEMS = kKB * LDK + DV * LDV;
   constexpr int U_ELEMS = DV * LDK;
-  constexpr int ULOADS = (SZ / VEC + 255) / 256;
+  constexpr int ULOADS = (SZ / VEC + NT - 1) / NT;
   __shared__ T buf_s[KV_ELEMS > U_ELEMS ? KV_ELEMS : U_ELEMS];
   __shared__ float cl_s[R];
   __shared__ float wsum_s[4];
-  __shared__ float lam_s[HAS_LAMBDA ? ROWS * kMaxLevels : 1];  // rows in slot order: (wave, s, r16)
+  __shared__ float lam_s[HAS_LAMBDA ? ROWS * kMaxLevels : 1];  // row 16 * wave + r16 of this workgroup
   __shared__ float kdec_s[R];
   T* k_s = buf_s;
   T* vt_s = buf_s + kKB * LDK;
   T* u_s = buf_s;
 
-  const int u = blockIdx.x / RM::RS, c = blockIdx.x % RM::RS, h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
   const int64_t N = (Tlen + R - 1) / R;
-  const int64_t bh = (int64_t)b * H + h;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // logical order (b, h, u, c)
+  const int c = (int)(work % RM::RS);
+  const int u = (int)((work / RM::RS) % N);
+  const int64_t bh = work / (RM::RS * N);
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
   const int64_t row0 = (int64_t)b * Tlen + (int64_t)u * R;
   const int nrow = (int)((Tlen - (int64_t)u * R) < R ? (Tlen - (int64_t)u * R) : R);
   const int nkb = (nrow + kKB - 1) / kKB;
-  int grp[GPW];
-  int gmax = 0;
-#pragma unroll
-  for (int s = 0; s < GPW; ++s) {
-    grp[s] = RM::group(c, wave, s);
-    gmax = grp[s] > gmax ? grp[s] : gmax;
-  }
-  const int nkb_w = (16 * gmax + 15) / kKB + 1;  // key blocks this wave's rows reach
+  const int gi = RM::group(c, wave);             // this wave's 16-row group
+  const int i = 16 * gi + r16;                   // this lane's row (tile-local)
+  const int nkb_w = (16 * gi + 15) / kKB + 1;    // key blocks this wave's rows reach
 
-  RowBlock<T, DK, 256> kr;
-  ColBlock<T, DV, 256> vr;
+  RowBlock<T, DK, NT> kr;
+  ColBlock<T, DV, NT> vr;
   kr.load(k, row0, 0, nrow, H, h);
   vr.load(v, row0, 0, nrow, H, h);
 
+  // Q^T fragments (B operand) of this lane's row, kept in registers.
+  typename M::frag qf[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    if (i < nrow) qf[ks] = M::load(q + ((row0 + i) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
+    else qf[ks] = typename M::frag{};
+  }
   if constexpr (HAS_LAMBDA) {
-    // one row of lambda per thread (slot order), all loads issued before the LDS stores
+    // one row of lambda per thread of the first ROWS threads, loads issued before the stores
     if (tid < ROWS) {
-      const int ws = tid / (16 * GPW), ss = (tid / 16) % GPW;
-      const int row = 16 * RM::group(c, ws, ss) + (tid & 15);
+      const int row = 16 * RM::group(c, tid >> 4) + (tid & 15);
       if (row < nrow) {
-        float lv[kMaxLevels];
+        const float* src = lam + ((row0 + row) * H + h) * L;
 #pragma unroll
-        for (int l = 0; l < kMaxLevels; ++l)
-          if (l < L) lv[l] = lam[((row0 + row) * H + h) * L + l];
+        for (int l0 = 0; l0 < kMaxLevels; l0 += kMaxLevels / 3) {  // three batches of loads
+          float lv[kMaxLevels / 3];
 #pragma unroll
-        for (int l = 0; l < kMaxLevels; ++l)
-          if (l < L) lam_s[tid * L + l] = lv[l];
+          for (int l = 0; l < kMaxLevels / 3; ++l)
+            if (l0 + l < L) lv[l] = src[l0 + l];
+#pragma unroll
+          for (int l = 0; l < kMaxLevels / 3; ++l)
+            if (l0 + l < L) lam_s[tid * L + l0 + l] = lv[l];
+        }
       }
     }
   }
   tile_cumsum<R>(log_alpha, row0, nrow, H, h, cl_s, wsum_s);
   // key-side decay to the end of each 16-key tile: kdec[j] = exp2(cl[j | 15] - cl[j])
-  for (int r = tid; r < R; r += 256) kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
+  for (int r = tid; r < R; r += NT) kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
+  const float* lrow = &lam_s[(16 * wave + r16) * L];  // this lane's lambda row
 
-  // Q^T fragments (B operand) for this wave's row groups, kept in registers.
-  typename M::frag qf[GPW][KS];
+  f32x4 oacc[MT];
 #pragma unroll
-  for (int s = 0; s < GPW; ++s) {
-    const int row = 16 * grp[s] + r16;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (row < nrow) qf[s][ks] = M::load(q + ((row0 + row) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
-      else qf[s][ks] = typename M::frag{};
-    }
-  }
-  // lambda row of slot s of this lane in lam_s
-  auto lrow = [&](int s) { return (wave * GPW + s) * 16 + r16; };
-
-  f32x4 oacc[MT][GPW];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int s = 0; s < GPW; ++s) oacc[mt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int mt = 0; mt < MT; ++mt) oacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // ---- intra-tile: causal R x R masked contraction, one 64-key block at a time
   for (int kb = 0; kb < nkb; ++kb) {
@@ -532,84 +531,69 @@ __global__ __launch_bounds__(256, 2) void k_tile_out(const T* __restrict__ q, co
       kr.load(k, row0, (kb + 1) * kKB, nrow, H, h);
       vr.load(v, row0, (kb + 1) * kKB, nrow, H, h);
     }
-    if (kb >= nkb_w) continue;
+    if (kb >= nkb_w || 16 * gi >= nrow) continue;
+    const float cli = cl_s[i];
     // key sub-steps: 32 keys (bf16, two 16-key tiles) or 16 keys (fp32)
     constexpr int KT_PER = (M::KPL == 8) ? 2 : 1;
 #pragma unroll
     for (int st = 0; st < 4 / KT_PER; ++st) {
       const int KT0 = 4 * kb + st * KT_PER;  // first 16-key tile of the sub-step (tile-local)
-      if (KT0 > gmax) break;                  // no row group of this wave reaches these keys
-      f32x4 p[KT_PER][GPW];
+      if (KT0 > gi) break;
+      f32x4 p[KT_PER];
 #pragma unroll
       for (int hh = 0; hh < KT_PER; ++hh) {
         const int kt = st * KT_PER + hh, KT = KT0 + hh;
-        typename M::frag kf[KS];
+        p[hh] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (KT > gi) continue;
+        f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) kf[ks] = M::load(&k_s[(kt * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]);
+        for (int ks = 0; ks < KS; ++ks)
+          sacc = M::mma(M::load(&k_s[(kt * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]), qf[ks], sacc);
+        if (KT < gi) {
+          // off-diagonal 16x16 tile: one level for the whole tile (4 + bitlen(gi ^ KT)) and the
+          // decay split at the tile's last key: exp2(cl_i - cl_end) * exp2(cl_end - cl_j)
+          float qs = fast_exp2(cli - cl_s[16 * KT + 15]);
+          if constexpr (HAS_LAMBDA) qs *= lrow[level_local(16 * gi, 16 * KT)];
+          const f32x4 kd = *reinterpret_cast<const f32x4*>(&kdec_s[16 * KT + 4 * g]);
 #pragma unroll
-        for (int s = 0; s < GPW; ++s) {
-          const int gi = grp[s];
-          p[hh][s] = f32x4{0.f, 0.f, 0.f, 0.f};
-          if (KT > gi || 16 * gi >= nrow) continue;
-          f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+          for (int r = 0; r < 4; ++r) p[hh][r] = sacc[r] * qs * kd[r];
+        } else {
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) sacc = M::mma(kf[ks], qf[s][ks], sacc);
-          const int i = 16 * gi + r16;
-          const float cli = cl_s[i];
-          if (KT < gi) {
-            // off-diagonal 16x16 tile: one level for the whole tile (4 + bitlen(gi ^ KT)) and the
-            // decay split at the tile's last key: exp2(cl_i - cl_end) * exp2(cl_end - cl_j)
-            float qs = fast_exp2(cli - cl_s[16 * KT + 15]);
-            if constexpr (HAS_LAMBDA) qs *= lam_s[lrow(s) * L + level_local(16 * gi, 16 * KT)];
-            const f32x4 kd = *reinterpret_cast<const f32x4*>(&kdec_s[16 * KT + 4 * g]);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) p[hh][s][r] = sacc[r] * qs * kd[r];
-          } else {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int j = 16 * KT + 4 * g + r;
-              float w = 0.f;
-              if (j <= i) {
-                w = fast_exp2(cli - cl_s[j]);
-                if constexpr (HAS_LAMBDA) w *= lam_s[lrow(s) * L + level_local(i, j)];
-              }
-              p[hh][s][r] = sacc[r] * w;
+          for (int r = 0; r < 4; ++r) {
+            const int j = 16 * KT + 4 * g + r;
+            float w = 0.f;
+            if (j <= i) {
+              w = fast_exp2(cli - cl_s[j]);
+              if constexpr (HAS_LAMBDA) w *= lrow[level_local(i, j)];
             }
+            p[hh][r] = sacc[r] * w;
           }
         }
       }
       if constexpr (M::KPL == 8) {
         // slots 0-3 <- key tile KT0 rows 4g..4g+3, slots 4-7 <- key tile KT0+1 rows 4g..4g+3;
         // V^T is read at the same keys.
-        typename M::frag bp[GPW];
+        typename M::frag bp;
 #pragma unroll
-        for (int s = 0; s < GPW; ++s)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            bp[s][r] = from_f32<T>(p[0][s][r]);
-            bp[s][4 + r] = from_f32<T>(p[1][s][r]);
-          }
+        for (int r = 0; r < 4; ++r) {
+          bp[r] = from_f32<T>(p[0][r]);
+          bp[4 + r] = from_f32<T>(p[1][r]);
+        }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
           const T* row = &vt_s[(mt * 16 + r16) * LDV + st * 32 + 4 * g];
           const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row);
           const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 16);
           const typename M::frag a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-#pragma unroll
-          for (int s = 0; s < GPW; ++s)
-            if (KT0 <= grp[s]) oacc[mt][s] = M::mma(a, bp[s], oacc[mt][s]);
+          oacc[mt] = M::mma(a, bp, oacc[mt]);
         }
       } else {
         // fp32: one k step = 4 keys {16 kt + 4g + r : g}, i.e. slot r of every lane group.
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            const T a = vt_s[(mt * 16 + r16) * LDV + st * 16 + 4 * g + r];
-#pragma unroll
-            for (int s = 0; s < GPW; ++s)
-              if (KT0 <= grp[s]) oacc[mt][s] = M::mma(a, p[0][s][r], oacc[mt][s]);
-          }
+          for (int mt = 0; mt < MT; ++mt)
+            oacc[mt] = M::mma(vt_s[(mt * 16 + r16) * LDV + st * 16 + 4 * g + r], p[0][r], oacc[mt]);
       }
     }
   }
@@ -636,9 +620,9 @@ __global__ __launch_bounds__(256, 2) void k_tile_out(const T* __restrict__ q, co
   V16 ur[ULOADS];
   auto load_u = [&](const T* U) {
 #pragma unroll
-    for (int i = 0; i < ULOADS; ++i) {
-      const int idx = tid + 256 * i;
-      if (idx < SZ / VEC) ur[i] = *reinterpret_cast<const V16*>(U + idx * VEC);
+    for (int e = 0; e < ULOADS; ++e) {
+      const int idx = tid + NT * e;
+      if (idx < SZ / VEC) ur[e] = *reinterpret_cast<const V16*>(U + idx * VEC);
     }
   };
   int j = next_level(0);
@@ -647,52 +631,38 @@ __global__ __launch_bounds__(256, 2) void k_tile_out(const T* __restrict__ q, co
   while (j) {
     __syncthreads();  // LDS buffer free
 #pragma unroll
-    for (int i = 0; i < ULOADS; ++i) {
-      const int idx = tid + 256 * i;
+    for (int e = 0; e < ULOADS; ++e) {
+      const int idx = tid + NT * e;
       if (idx < SZ / VEC) {
         const int p = idx / (DK / VEC), n0 = (idx % (DK / VEC)) * VEC;
-        *reinterpret_cast<V16*>(&u_s[p * LDK + n0]) = ur[i];
+        *reinterpret_cast<V16*>(&u_s[p * LDK + n0]) = ur[e];
       }
     }
     __syncthreads();
     const int jn = next_level(j);
     float gap_n = 0.f;
     if (jn) load_u(level_src(jn, &gap_n));
-    float w[GPW];
-#pragma unroll
-    for (int s = 0; s < GPW; ++s) {
-      const int i = 16 * grp[s] + r16;
-      w[s] = fast_exp2(cl_s[i] + gap);
-      if constexpr (HAS_LAMBDA) w[s] *= (i < nrow) ? lam_s[lrow(s) * L + LOG2R + j] : 0.f;
-    }
+    float w = fast_exp2(cl_s[i] + gap);
+    if constexpr (HAS_LAMBDA) w *= (i < nrow) ? lrow[LOG2R + j] : 0.f;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      f32x4 tmp[GPW];
+      f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < GPW; ++s) tmp[s] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const typename M::frag a = M::load(&u_s[(mt * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]);
-#pragma unroll
-        for (int s = 0; s < GPW; ++s) tmp[s] = M::mma(a, qf[s][ks], tmp[s]);
-      }
-#pragma unroll
-      for (int s = 0; s < GPW; ++s) oacc[mt][s] += w[s] * tmp[s];
+      for (int ks = 0; ks < KS; ++ks)
+        tmp = M::mma(M::load(&u_s[(mt * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]), qf[ks], tmp);
+      oacc[mt] += w * tmp;
     }
     j = jn;
     gap = gap_n;
   }
 
-  // ---- store O: lane holds row 16 grp[s] + r16, d_v entries 16 mt + 4g .. +3
-#pragma unroll
-  for (int s = 0; s < GPW; ++s) {
-    const int row = 16 * grp[s] + r16;
-    if (row >= nrow) continue;
-    T* orow = o + ((row0 + row) * H + h) * DV + 4 * g;
+  // ---- store O: lane holds row i, d_v entries 16 mt + 4g .. +3
+  if (i < nrow) {
+    T* orow = o + ((row0 + i) * H + h) * DV + 4 * g;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) orow[mt * 16 + r] = from_f32<T>(oacc[mt][s][r]);
+      for (int r = 0; r < 4; ++r) orow[mt * 16 + r] = from_f32<T>(oacc[mt][r]);
   }
 }
 
@@ -788,9 +758,9 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
     tiles = reinterpret_cast<T*>(base + w.tiles);
     running = reinterpret_cast<T*>(base + w.running);
   }
-  const dim3 gblk((unsigned)w.nb, (unsigned)a.H, (unsigned)a.B);
+  const dim3 gblk((unsigned)(w.nb * a.H * a.B));
   const dim3 gscan((unsigned)((SZ / 2 + 255) / 256 + 1), (unsigned)(a.B * a.H));
-  const dim3 gtile((unsigned)(w.N * RowMap<kTileChunks * C>::RS), (unsigned)a.H, (unsigned)a.B);
+  const dim3 gtile((unsigned)(w.N * RowMap<kTileChunks * C>::RS * a.H * a.B));
   if (ev) (void)hipEventRecord(ev[0], st);
   if (a.lambda)
     hipLaunchKernelGGL((k_block_state<T, C, DK, DV, true>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
@@ -803,11 +773,11 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
                      gaps2, w.N, w.J, SZ, a.lambda != nullptr ? 1 : 0);
   if (ev) (void)hipEventRecord(ev[2], st);
   if (a.lambda)
-    hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, true>), gtile, dim3(256), 0, st, (const T*)a.q, (const T*)a.k,
+    hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, true>), gtile, dim3(RowMap<kTileChunks * C>::NT), 0, st, (const T*)a.q, (const T*)a.k,
                        (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (const float*)gaps2,
                        (T*)a.o, a.T, (int)a.H, a.L, w.J);
   else
-    hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, false>), gtile, dim3(256), 0, st, (const T*)a.q, (const T*)a.k,
+    hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, false>), gtile, dim3(RowMap<kTileChunks * C>::NT), 0, st, (const T*)a.q, (const T*)a.k,
                        (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (const float*)gaps2,
                        (T*)a.o, a.T, (int)a.H, a.L, w.J);
   if (ev) (void)hipEventRecord(ev[3], st);
