@@ -25,6 +25,15 @@ const ll::KernelEntry* find_mamba2(int32_t dtype, int64_t C, int64_t dk, int64_t
   return nullptr;
 }
 
+const ll::GdnEntry* find_gdn(int32_t dtype, int64_t C, int64_t dk, int64_t dv) {
+  if (dtype != LL_BF16) return nullptr;
+  int n = 0;
+  const ll::GdnEntry* t = ll::gdn_table(&n);
+  for (int i = 0; i < n; ++i)
+    if (t[i].C == C && t[i].dk == dk && t[i].dv == dv) return &t[i];
+  return nullptr;
+}
+
 ll_status check_shape(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C) {
   if (B < 1 || T < 1 || H < 1 || dk < 1 || dv < 1 || !is_pow2(C) || T % C != 0) return LL_ERR_BAD_SHAPE;
   return LL_OK;
@@ -38,6 +47,7 @@ int32_t ll_num_levels(int64_t T) { return levels_of(T); }
 
 int32_t ll_supported(int32_t variant, int32_t dtype, int64_t C, int64_t d_k, int64_t d_v) {
   if (variant == LL_MAMBA2) return find_mamba2(dtype, C, d_k, d_v) ? 1 : 0;
+  if (variant == LL_GDN) return find_gdn(dtype, C, d_k, d_v) ? 1 : 0;
   return 0;
 }
 
@@ -45,8 +55,10 @@ size_t ll_workspace_size(int32_t variant, int32_t dtype, int64_t B, int64_t T, i
                          int64_t C, int32_t has_lambda) {
   if (check_shape(B, T, H, d_k, d_v, C) != LL_OK) return 0;
   if (dtype != LL_F32 && dtype != LL_BF16) return 0;
-  if (variant != LL_MAMBA2 && variant != LL_GDN) return 0;
-  return (size_t)ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), has_lambda != 0, nullptr);
+  if (variant == LL_MAMBA2)
+    return (size_t)ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), has_lambda != 0, nullptr);
+  if (variant == LL_GDN) return (size_t)ll::gdn_workspace(B, T, H, d_k, d_v, C, nullptr);
+  return 0;
 }
 
 const char* ll_status_string(ll_status s) {
@@ -128,12 +140,26 @@ ll_status ll_mamba2_fwd_timed(const void* q, const void* k, const void* v, const
 ll_status ll_gdn_fwd(const void* q, const void* k, const void* v, const float* log_alpha, const float* beta,
                      const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C,
                      int32_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
-  (void)lambda; (void)workspace; (void)workspace_bytes; (void)stream;
   if (!q || !k || !v || !log_alpha || !beta || !o) return LL_ERR_NULL_ARG;
   ll_status st = check_shape(B, T, H, d_k, d_v, C);
   if (st != LL_OK) return st;
-  (void)dtype;
-  return LL_ERR_UNSUPPORTED;
+  const ll::GdnEntry* e = find_gdn(dtype, C, d_k, d_v);
+  if (!e) return LL_ERR_UNSUPPORTED;
+  const int64_t N = T / C;
+  const int J = N <= 1 ? 0 : bitlen64(uint64_t(N - 1));
+  const int L = levels_of(T);
+  if (J > ll::kGdnMaxLevels || L > kMaxL || H > 65535 || B > 65535 || B * H * N >= (int64_t(1) << 31))
+    return LL_ERR_UNSUPPORTED;
+  const int64_t need = ll::gdn_workspace(B, T, H, d_k, d_v, C, nullptr);
+  if (!workspace) return LL_ERR_NULL_ARG;
+  if ((int64_t)workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
+  ll::GdnArgs a;
+  a.q = q; a.k = k; a.v = v; a.log_alpha = log_alpha; a.beta = beta; a.lambda = lambda; a.o = o;
+  a.B = B; a.T = T; a.H = H; a.dk = d_k; a.dv = d_v; a.C = C;
+  a.L = L;
+  a.workspace = workspace;
+  hipError_t err = e->launch(a, static_cast<hipStream_t>(stream));
+  return err == hipSuccess ? LL_OK : LL_ERR_HIP;
 }
 
 ll_status ll_debug_level_map(int64_t T, int64_t C, int8_t* out, void* stream) {

@@ -1,0 +1,457 @@
+// Log-linear Gated DeltaNet forward (Sec. 3.4): O = (A (.) M^S (.) M^H) V with
+// A = (Q K^T (.) L)(I + diag(beta)(K K^T (.) (L - I)))^{-1} diag(beta), i.e. the recurrence
+// S_t = alpha_t S_{t-1} (I - beta_t k_t k_t^T) + beta_t v_t k_t^T read out per Fenwick level.
+//
+// Chunkwise form (chunks of C tokens; local rows t, s; gamma_t = exp(cl_t) with cl the
+// chunk-local inclusive cumulative log-gate; Gamma[t,s] = gamma_t / gamma_s for s <= t):
+//   T_G   = (I + diag(beta)(K K^T (.) Gamma (.) (L - I)))^{-1} diag(beta)   (unit-lower solve)
+//   W     = T_G diag(gamma) K,   U = T_G V                                   (WY / UT form)
+//   P_G   = Q K^T (.) Gamma (.) L
+//   intra : O_c = ((P_G T_G) (.) M^H_c) V       -- the chunk's own block of A, level-masked
+//   Qc    = diag(gamma) Q - P_G W               -- query seen through the chunk's transitions
+//   state : S_end^T = P_z S_start^T + H_z,  P_z = gamma_C I - K~^T W,  H_z = K~^T U,
+//           K~ = diag(exp(tot - cl)) K
+// An earlier state S (d_v x d_k) reaches row t of the chunk as S q~_t (q~_t = row t of Qc).
+// Inter-chunk levels (Sec. 3.3 with the delta-rule transition): per chunk level j the state
+// R_j (d_k x d_v) restarts at every chunk z with z % 2^j == 0, absorbs H_z in the source half
+// (bit j-1 of z clear) and propagates through P_z everywhere; a chunk with bit j-1 set adds
+// lambda_t^(log2 C + j) q~_t^T R_j to its rows, with R_j taken at the chunk's start.
+//
+// Kernels: gdn_chunk (per chunk: the WY solve in fp32 and all chunk-local products on MFMA,
+// bf16 operands with fp32 accumulation) and gdn_scan (per (b, h, 16 d_v columns): every level's
+// state slice in registers, P_z / Q~ streamed through LDS once per chunk).
+#include <type_traits>
+
+#include "ll_device.hpp"
+#include "ll_launch.hpp"
+
+namespace ll {
+
+namespace gdn {
+
+constexpr int kMaxJ = 16;      // inter-chunk levels handled by the scan (T <= C * 2^16)
+constexpr int kSlice = 16;     // d_v columns per scan workgroup
+constexpr int kScanWaves = 8;  // waves per scan workgroup
+typedef __bf16 bf;
+
+// C = A B over 16x16 output tiles, A [M][K] row-major (lda), Bt = B^T [N][K] row-major (ldb), both
+// bf16 in LDS; tiles dealt round-robin to the 4 waves; epi(mt, nt, acc) consumes each tile
+// (lane holds column 16 nt + (lane & 15), rows 16 mt + 4 (lane >> 4) + r).
+template <int M, int N, int K, typename Epi>
+__device__ inline void gemm_lds(const bf* A, int lda, const bf* Bt, int ldb, Epi epi) {
+  using MF = Mfma<bf>;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
+  constexpr int MT = M / 16, NT = N / 16;
+  for (int tile = wave; tile < MT * NT; tile += 4) {
+    const int mt = tile / NT, nt = tile % NT;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < K / MF::KSTEP; ++ks) {
+      const int k0 = ks * MF::KSTEP + g * MF::KPL;
+      acc = MF::mma(MF::load(&A[(mt * 16 + r16) * lda + k0]), MF::load(&Bt[(nt * 16 + r16) * ldb + k0]), acc);
+    }
+    epi(mt, nt, acc);
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Kernel 1: per-chunk WY solve and chunk-local products.  One workgroup (4 waves) per chunk.
+// Outputs (workspace, per chunk): Qc [C][DK] bf16, P_z [DK][DK] bf16, H_z [DK][DV] bf16,
+// intra-chunk output [C][DV] fp32.
+// ---------------------------------------------------------------------------------------------
+template <int C, int DK, int DV, bool HAS_LAMBDA>
+__global__ __launch_bounds__(256) void k_gdn_chunk(const bf* __restrict__ q, const bf* __restrict__ k,
+                                                   const bf* __restrict__ v, const float* __restrict__ log_alpha,
+                                                   const float* __restrict__ beta, const float* __restrict__ lam,
+                                                   bf* __restrict__ qc_out, bf* __restrict__ pz_out,
+                                                   bf* __restrict__ hz_out, float* __restrict__ oin_out,
+                                                   int64_t Tlen, int H, int L) {
+  static_assert(C == 64, "the forward substitution maps one lane of wave 0 to each of the C columns");
+  constexpr int LOG2C = 6;
+  constexpr int PD = 8;                 // row padding (elements)
+  constexpr int LDD = DK + PD;          // rows of length d_k
+  constexpr int LDC = C + PD;           // rows of length C
+  constexpr int VEC = 8;
+  // region 1: phase A/B (K, Q row-major, fp32 L) reused in phase C/D (W^T, U^T, masked P)
+  constexpr int R1A = 2 * C * LDD * 2 + C * (C + 1) * 4;
+  constexpr int R1B = (DK * LDC + DV * LDC + C * LDC) * 2;
+  constexpr int R1 = R1A > R1B ? R1A : R1B;
+  __shared__ __attribute__((aligned(16))) char r1[R1];
+  __shared__ bf kgt_s[DK * LDC];   // (gamma K)^T
+  __shared__ bf kdt_s[DK * LDC];   // (decay-to-end K)^T
+  __shared__ bf vt_s[DV * LDC];    // V^T
+  __shared__ bf pg_s[C * LDC];     // P_G
+  __shared__ bf z_s[C * LDC];      // T_G
+  __shared__ bf zt_s[C * LDC];     // T_G^T
+  __shared__ float cl_s[C], gm_s[C], dc_s[C], bt_s[C];
+  __shared__ float lam_s[HAS_LAMBDA ? C * (LOG2C + 1) : 1];
+  bf* k_s = reinterpret_cast<bf*>(r1);
+  bf* q_s = k_s + C * LDD;
+  float* l_s = reinterpret_cast<float*>(r1 + 2 * C * LDD * 2);
+  bf* wt_s = reinterpret_cast<bf*>(r1);
+  bf* ut_s = wt_s + DK * LDC;
+  bf* ph_s = ut_s + DV * LDC;
+
+  const int64_t N = Tlen / C;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // (b, h, z)
+  const int64_t z = work % N;
+  const int64_t bh = work / N;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
+  const int64_t tok0 = (int64_t)b * Tlen + z * C;
+  const int64_t cidx = bh * N + z;
+
+  // ---- phase A: gates, staging, K K^T and Q K^T
+  if (wave == 0) {
+    const float la = lane < C ? log_alpha[(tok0 + lane) * H + h] * kLog2e : 0.f;
+    const float cl = wave_inclusive_scan(la);
+    const float tot = __shfl(cl, C - 1, 64);
+    if (lane < C) {
+      cl_s[lane] = cl;
+      gm_s[lane] = fast_exp2(cl);
+      dc_s[lane] = fast_exp2(tot - cl);
+      bt_s[lane] = beta[(tok0 + lane) * H + h];
+    }
+  }
+  if constexpr (HAS_LAMBDA) {
+    for (int idx = tid; idx < C * (LOG2C + 1); idx += 256) {
+      const int t = idx / (LOG2C + 1), l = idx % (LOG2C + 1);
+      lam_s[idx] = lam[((tok0 + t) * H + h) * L + l];
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < C * DK / VEC; idx += 256) {
+    const int t = idx / (DK / VEC), d0 = (idx % (DK / VEC)) * VEC;
+    const bf16x8 kv = *reinterpret_cast<const bf16x8*>(k + ((tok0 + t) * H + h) * DK + d0);
+    const bf16x8 qv = *reinterpret_cast<const bf16x8*>(q + ((tok0 + t) * H + h) * DK + d0);
+    *reinterpret_cast<bf16x8*>(&k_s[t * LDD + d0]) = kv;
+    *reinterpret_cast<bf16x8*>(&q_s[t * LDD + d0]) = qv;
+    const float gt = gm_s[t], dt = dc_s[t];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const float x = static_cast<float>(kv[e]);
+      kgt_s[(d0 + e) * LDC + t] = static_cast<bf>(x * gt);
+      kdt_s[(d0 + e) * LDC + t] = static_cast<bf>(x * dt);
+    }
+  }
+  for (int idx = tid; idx < C * DV / VEC; idx += 256) {
+    const int t = idx / (DV / VEC), d0 = (idx % (DV / VEC)) * VEC;
+    const bf16x8 vv = *reinterpret_cast<const bf16x8*>(v + ((tok0 + t) * H + h) * DV + d0);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) vt_s[(d0 + e) * LDC + t] = vv[e];
+  }
+  __syncthreads();
+  // L[t][s] = beta_t (k_t . k_s) Gamma[t,s] for s < t (fp32);  P_G[t][s] = (q_t . k_s) Gamma[t,s], s <= t
+  gemm_lds<C, C, DK>(k_s, LDD, k_s, LDD, [&](int mt, int nt, f32x4 acc) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = mt * 16 + 4 * g + r, s = nt * 16 + r16;
+      l_s[t * (C + 1) + s] = s < t ? bt_s[t] * acc[r] * fast_exp2(cl_s[t] - cl_s[s]) : 0.f;
+    }
+  });
+  gemm_lds<C, C, DK>(q_s, LDD, k_s, LDD, [&](int mt, int nt, f32x4 acc) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = mt * 16 + 4 * g + r, s = nt * 16 + r16;
+      pg_s[t * LDC + s] = static_cast<bf>(s <= t ? acc[r] * fast_exp2(cl_s[t] - cl_s[s]) : 0.f);
+    }
+  });
+  __syncthreads();
+
+  // ---- phase B: X = (I + L)^{-1} by forward substitution, lane c = column c (wave 0);
+  //      T_G = X diag(beta): z_s[t][c] and zt_s[c][t]
+  if (wave == 0) {
+    const int c = lane;
+    float x[C];
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+      float acc = (i == c) ? 1.f : 0.f;
+#pragma unroll
+      for (int j = 0; j < i; ++j) acc -= l_s[i * (C + 1) + j] * x[j];
+      x[i] = (i < c) ? 0.f : acc;
+    }
+    const float bc = bt_s[c];
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+      const bf zv = static_cast<bf>(x[i] * bc);
+      z_s[i * LDC + c] = zv;
+      zt_s[c * LDC + i] = zv;
+    }
+  }
+  __syncthreads();
+
+  // ---- phase C: W = T_G (gamma K), U = T_G V (stored transposed), A_c = P_G T_G masked by M^H
+  gemm_lds<C, DK, C>(z_s, LDC, kgt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+    bf16x4 w4;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) w4[r] = static_cast<bf>(acc[r]);
+    *reinterpret_cast<bf16x4*>(&wt_s[(nt * 16 + r16) * LDC + mt * 16 + 4 * g]) = w4;
+  });
+  gemm_lds<C, DV, C>(z_s, LDC, vt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+    bf16x4 u4;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) u4[r] = static_cast<bf>(acc[r]);
+    *reinterpret_cast<bf16x4*>(&ut_s[(nt * 16 + r16) * LDC + mt * 16 + 4 * g]) = u4;
+  });
+  gemm_lds<C, C, C>(pg_s, LDC, zt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = mt * 16 + 4 * g + r, s = nt * 16 + r16;
+      float w = s <= t ? acc[r] : 0.f;
+      if constexpr (HAS_LAMBDA) w *= lam_s[t * (LOG2C + 1) + level_local(t, s)];
+      ph_s[t * LDC + s] = static_cast<bf>(w);
+    }
+  });
+  __syncthreads();
+
+  // ---- phase D: intra output, corrected queries, transition and chunk state
+  float* oin = oin_out + cidx * (C * DV);
+  gemm_lds<C, DV, C>(ph_s, LDC, vt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) oin[(mt * 16 + 4 * g + r) * DV + nt * 16 + r16] = acc[r];
+  });
+  bf* qc = qc_out + cidx * (C * DK);
+  gemm_lds<C, DK, C>(pg_s, LDC, wt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = mt * 16 + 4 * g + r, d = nt * 16 + r16;
+      const float qv = static_cast<float>(q[((tok0 + t) * H + h) * DK + d]);
+      qc[t * DK + d] = static_cast<bf>(gm_s[t] * qv - acc[r]);
+    }
+  });
+  bf* pz = pz_out + cidx * (DK * DK);
+  const float gC = gm_s[C - 1];
+  gemm_lds<DK, DK, C>(kdt_s, LDC, wt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int d = mt * 16 + 4 * g + r, e = nt * 16 + r16;
+      pz[d * DK + e] = static_cast<bf>((d == e ? gC : 0.f) - acc[r]);
+    }
+  });
+  bf* hz = hz_out + cidx * (DK * DV);
+  gemm_lds<DK, DV, C>(kdt_s, LDC, ut_s, LDC, [&](int mt, int nt, f32x4 acc) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) hz[(mt * 16 + 4 * g + r) * DV + nt * 16 + r16] = static_cast<bf>(acc[r]);
+  });
+}
+
+// ---------------------------------------------------------------------------------------------
+// Kernel 2: level scan.  One workgroup (8 waves) per (b, h, 16 d_v columns), sequential over
+// the chunks.  Wave w owns levels w+1 and w+9; each level state R_j (d_k x 16, fp32)
+// lives in registers in the MFMA result layout (lane: column = lane & 15, rows 16 mt + 4g + r).
+// lambda == NULL: one state, read by every chunk, absorbing every chunk (wave 0).
+// ---------------------------------------------------------------------------------------------
+template <int C, int DK, int DV, bool HAS_LAMBDA>
+__global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __restrict__ lam, const bf* __restrict__ qc_in,
+                                                  const bf* __restrict__ pz_in, const bf* __restrict__ hz_in,
+                                                  const float* __restrict__ oin_in, bf* __restrict__ o,
+                                                  int64_t Tlen, int H, int L, int J) {
+  using MF = Mfma<bf>;
+  constexpr int LOG2C = (C == 16) ? 4 : (C == 32) ? 5 : 6;
+  constexpr int PD = 8;
+  constexpr int LDD = DK + PD;
+  constexpr int MTD = DK / 16;          // 16-row tiles of a state
+  constexpr int MTC = C / 16;           // 16-row tiles of a chunk
+  constexpr int KS = DK / 32;           // k steps over d_k
+  constexpr int NSL = DV / kSlice;
+  constexpr int LPW = HAS_LAMBDA ? kMaxJ / kScanWaves : 1;  // level slots per wave
+  constexpr int NT = 64 * kScanWaves;
+  __shared__ bf pz_s[DK * LDD];
+  __shared__ bf qc_s[C * LDD];
+  __shared__ float part_s[kScanWaves * C * kSlice];
+  __shared__ float lw_s[HAS_LAMBDA ? C * kMaxJ : 1];
+
+  const int64_t N = Tlen / C;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // (b, h, slice)
+  const int sl = (int)(work % NSL);
+  const int64_t bh = work / NSL;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
+  const int p0 = sl * kSlice;
+
+  f32x4 R[LPW][MTD];
+#pragma unroll
+  for (int m = 0; m < LPW; ++m)
+#pragma unroll
+    for (int mt = 0; mt < MTD; ++mt) R[m][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int64_t z = 0; z < N; ++z) {
+    const int64_t cidx = bh * N + z;
+    const int64_t tok0 = (int64_t)b * Tlen + z * C;
+    __syncthreads();
+    {
+      const bf* src = pz_in + cidx * (DK * DK);
+      for (int idx = tid; idx < DK * DK / 8; idx += NT) {
+        const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
+        *reinterpret_cast<bf16x8*>(&pz_s[r * LDD + c0]) = *reinterpret_cast<const bf16x8*>(src + r * DK + c0);
+      }
+      const bf* qs = qc_in + cidx * (C * DK);
+      for (int idx = tid; idx < C * DK / 8; idx += NT) {
+        const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
+        *reinterpret_cast<bf16x8*>(&qc_s[r * LDD + c0]) = *reinterpret_cast<const bf16x8*>(qs + r * DK + c0);
+      }
+      if constexpr (HAS_LAMBDA) {
+        for (int idx = tid; idx < C * J; idx += NT) {
+          const int t = idx / J, jj = idx % J;
+          lw_s[t * kMaxJ + jj] = lam[((tok0 + t) * H + h) * L + LOG2C + 1 + jj];
+        }
+      }
+    }
+    __syncthreads();
+
+    f32x4 out[MTC];
+#pragma unroll
+    for (int mt = 0; mt < MTC; ++mt) out[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // this lane's entries of H_z (rows 16 mt + 4g + r, column p0 + r16)
+    f32x4 hzv[MTD];
+    {
+      const bf* hs = hz_in + cidx * (DK * DV) + p0 + r16;
+#pragma unroll
+      for (int mt = 0; mt < MTD; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) hzv[mt][r] = static_cast<float>(hs[(mt * 16 + 4 * g + r) * DV]);
+    }
+
+#pragma unroll
+    for (int m = 0; m < LPW; ++m) {
+      int j;
+      bool reader, source, restart;
+      if constexpr (HAS_LAMBDA) {
+        j = wave + 1 + kScanWaves * m;
+        if (j > J) continue;
+        reader = (z >> (j - 1)) & 1;
+        source = !reader;
+        restart = (z & ((int64_t(1) << j) - 1)) == 0;
+      } else {
+        if (wave != 0) continue;
+        j = 0;
+        reader = z > 0;
+        source = true;
+        restart = z == 0;
+      }
+      // B fragments of R_j (k slots: rows 4g..4g+3 of tiles 2ks and 2ks+1)
+      bf16x8 rb[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          rb[ks][r] = static_cast<bf>(R[m][2 * ks][r]);
+          rb[ks][4 + r] = static_cast<bf>(R[m][2 * ks + 1][r]);
+        }
+      if (reader) {
+#pragma unroll
+        for (int mt = 0; mt < MTC; ++mt) {
+          f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            const bf* row = &qc_s[(mt * 16 + r16) * LDD + ks * 32 + 4 * g];
+            const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row);
+            const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 16);
+            tmp = MF::mma(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), rb[ks], tmp);
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = mt * 16 + 4 * g + r;
+            const float wgt = HAS_LAMBDA ? lw_s[t * kMaxJ + (j - 1)] : 1.f;
+            out[mt][r] += wgt * tmp[r];
+          }
+        }
+      }
+      if (restart) {
+#pragma unroll
+        for (int mt = 0; mt < MTD; ++mt) R[m][mt] = hzv[mt];
+      } else {
+#pragma unroll
+        for (int mt = 0; mt < MTD; ++mt) {
+          f32x4 acc = source ? hzv[mt] : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            const bf* row = &pz_s[(mt * 16 + r16) * LDD + ks * 32 + 4 * g];
+            const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row);
+            const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 16);
+            acc = MF::mma(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), rb[ks], acc);
+          }
+          R[m][mt] = acc;
+        }
+      }
+    }
+
+    // combine the waves' contributions with the intra-chunk output
+#pragma unroll
+    for (int mt = 0; mt < MTC; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) part_s[(wave * C + mt * 16 + 4 * g + r) * kSlice + r16] = out[mt][r];
+    __syncthreads();
+    const float* oin = oin_in + cidx * (C * DV);
+    for (int idx = tid; idx < C * kSlice; idx += NT) {
+      const int t = idx / kSlice, p = idx % kSlice;
+      float acc = oin[t * DV + p0 + p];
+#pragma unroll
+      for (int w = 0; w < kScanWaves; ++w) acc += part_s[(w * C + t) * kSlice + p];
+      o[((tok0 + t) * H + h) * DV + p0 + p] = static_cast<bf>(acc);
+    }
+  }
+}
+
+}  // namespace gdn
+
+// ---------------------------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------------------------
+int64_t gdn_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, GdnLayout* lay) {
+  const int64_t N = T / C, BHN = B * H * N;
+  auto al = [](int64_t x) { return (x + 255) & ~int64_t(255); };
+  GdnLayout w{};
+  int64_t cur = 0;
+  w.qc = cur; cur += al(BHN * C * dk * 2);
+  w.pz = cur; cur += al(BHN * dk * dk * 2);
+  w.hz = cur; cur += al(BHN * dk * dv * 2);
+  w.oin = cur; cur += al(BHN * C * dv * 4);
+  w.total = cur;
+  if (lay) *lay = w;
+  return cur;
+}
+
+template <int C, int DK, int DV>
+hipError_t launch_gdn(const GdnArgs& a, hipStream_t st) {
+  GdnLayout w;
+  gdn_workspace(a.B, a.T, a.H, DK, DV, C, &w);
+  char* base = static_cast<char*>(a.workspace);
+  __bf16* qc = reinterpret_cast<__bf16*>(base + w.qc);
+  __bf16* pz = reinterpret_cast<__bf16*>(base + w.pz);
+  __bf16* hz = reinterpret_cast<__bf16*>(base + w.hz);
+  float* oin = reinterpret_cast<float*>(base + w.oin);
+  const int64_t N = a.T / C;
+  const int J = N <= 1 ? 0 : 64 - __builtin_clzll(uint64_t(N - 1));
+  const dim3 g1((unsigned)(a.B * a.H * N)), g2((unsigned)(a.B * a.H * (DV / gdn::kSlice)));
+  const __bf16* q = static_cast<const __bf16*>(a.q);
+  const __bf16* k = static_cast<const __bf16*>(a.k);
+  const __bf16* v = static_cast<const __bf16*>(a.v);
+  __bf16* o = static_cast<__bf16*>(a.o);
+  if (a.lambda) {
+    hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, true>), g1, dim3(256), 0, st, q, k, v, a.log_alpha, a.beta,
+                       a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L);
+    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, true>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz, hz, oin, o, a.T,
+                       (int)a.H, a.L, J);
+  } else {
+    hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, false>), g1, dim3(256), 0, st, q, k, v, a.log_alpha, a.beta,
+                       a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L);
+    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, false>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz, hz, oin, o, a.T,
+                       (int)a.H, a.L, J);
+  }
+  return hipGetLastError();
+}
+
+#define LL_GDN_SHAPES(X) \
+  X(64, 64, 64)          \
+  X(64, 128, 128)
+
+const GdnEntry* gdn_table(int* n) {
+#define LL_ENTRY(C, DK, DV) {C, DK, DV, &launch_gdn<C, DK, DV>},
+  static const GdnEntry table[] = {LL_GDN_SHAPES(LL_ENTRY)};
+#undef LL_ENTRY
+  *n = sizeof(table) / sizeof(table[0]);
+  return table;
+}
+
+}  // namespace ll

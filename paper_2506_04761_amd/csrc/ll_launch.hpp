@@ -43,6 +43,32 @@ struct KernelEntry {
 };
 
 const KernelEntry* mamba2_table(int* n);
+
+// Gated DeltaNet: per-chunk buffers carved from the workspace (byte offsets).
+struct GdnLayout {
+  int64_t qc = 0, pz = 0, hz = 0, oin = 0, total = 0;
+};
+int64_t gdn_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, GdnLayout* lay);
+
+struct GdnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const float* log_alpha;
+  const float* beta;
+  const float* lambda;  // may be null
+  void* o;
+  int64_t B, T, H, dk, dv, C;
+  int L;
+  void* workspace;
+};
+typedef hipError_t (*GdnLaunch)(const GdnArgs&, hipStream_t);
+struct GdnEntry {
+  int C, dk, dv;
+  GdnLaunch launch;
+};
+const GdnEntry* gdn_table(int* n);
+constexpr int kGdnMaxLevels = 16;  // inter-chunk levels of the GDN scan
 hipError_t launch_debug_level_map(int64_t T, int64_t C, int8_t* out, hipStream_t st);
 
 }  // namespace ll

@@ -11,6 +11,7 @@ Transforms by distribution name:
              log alpha = -softplus(x_a + 2), lambda = softplus(x_l)
   "slow"     as "unit" but log alpha = -softplus(x_a - 6) (about -0.0025: every level matters)
   "nodecay"  as "unit" but log alpha = 0 (alpha = 1)
+  "gdn_slow", "gdn_nodecay"  as "gdn" with the "slow" / "nodecay" gates
 q, k, v are then rounded to the storage dtype (bf16 round-to-nearest-even via torch on the
 CPU, or kept float32); log alpha, lambda and beta are always float32.
 """
@@ -88,13 +89,14 @@ def generate(w: Workload, T: int = None, heads=None):
     xb = rng.standard_normal((B, TT, H), dtype=np.float32) if w.variant == "gdn" else None
 
     q = q / np.float32(math.sqrt(dk))
-    if w.dist == "gdn":
+    if w.dist.startswith("gdn"):
         k = k / np.linalg.norm(k.astype(np.float64), axis=-1, keepdims=True).astype(np.float32)
     else:
         k = k / np.float32(math.sqrt(dk))
     if w.dist in ("unit", "slow", "nodecay"):
         v = v / np.float32(math.sqrt(dv))
-    shift = {"unit": 0.0, "shifted": 2.0, "gdn": 2.0, "slow": -6.0, "nodecay": None}[w.dist]
+    shift = {"unit": 0.0, "shifted": 2.0, "gdn": 2.0, "slow": -6.0, "nodecay": None,
+             "gdn_slow": -6.0, "gdn_nodecay": None}[w.dist]
     if shift is None:
         log_alpha = np.zeros((B, TT, H), dtype=np.float32)
     else:

@@ -35,3 +35,13 @@ def run_mamba2(inp, dtype, C, with_lambda=True, out=None, workspace=None):
 
 def rel_err(got, ref):
     return float(np.max(np.abs(got - ref)) / max(float(np.max(np.abs(ref))), 1e-30))
+
+
+def run_gdn(inp, C, with_lambda=True, out=None, workspace=None):
+    import torch
+    import paper_2506_04761_amd as ll
+    d = device_inputs(inp, "bf16")
+    o = ll.ll_gdn_fwd(d["q"], d["k"], d["v"], d["log_alpha"], d["beta"], d["lam"] if with_lambda else None, C,
+                      out=out, workspace=workspace)
+    torch.cuda.synchronize()
+    return o.float().cpu().numpy().astype(np.float64)

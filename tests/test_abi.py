@@ -86,6 +86,8 @@ def test_gdn_argument_checks_return_before_launch():
     assert g(beta=None) == ll._lib.LL_ERR_NULL_ARG
     assert g(T=100) == ll._lib.LL_ERR_BAD_SHAPE
     assert g(dk=96) == ll._lib.LL_ERR_UNSUPPORTED
+    assert ll.ll_supported(ll.LL_GDN, ll.LL_BF16, 64, 128, 128)
+    assert not ll.ll_supported(ll.LL_GDN, ll.LL_F32, 64, 128, 128)
 
 
 def test_debug_level_map_checks():
