@@ -51,6 +51,29 @@ struct Mfma<float> {
   __device__ static inline frag load(const float* p) { return *p; }
 };
 
+// Transposing LDS read (ds_read_b64_tr_b16, gfx950).  Within each group of 16 lanes, lane j
+// supplies the address of four consecutive 16-bit elements e_j[0..3]; lane i receives
+// { e_(i/4 + 4k)[i % 4] : k = 0..3 }.  Supplying, from lane j of the group, row (base + j/4)
+// and column (c0 + 4 (j % 4)) of a row-major matrix therefore hands lane i column c0 + i of
+// rows base .. base + 3: a 4 x 16 block read as 16 columns, i.e. an MFMA operand fragment whose
+// k slots run down the rows.
+__device__ inline bf16x4 lds_read_tr(const __bf16* p) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+  return __builtin_bit_cast(bf16x4, r);
+}
+
+// bf16 MFMA operand fragment (8 k slots) taken down the rows of a row-major bf16 matrix in LDS:
+// lane (g = lane / 16, i = lane % 16) gets column col0 + i at rows row0 + 4g + {0..3} (slots
+// 0-3) and row0 + 16 + 4g + {0..3} (slots 4-7).  `ld` is the row stride in elements.
+__device__ inline bf16x8 frag_down_rows(const __bf16* m, int ld, int row0, int col0) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+  const __bf16* p = m + (row0 + 4 * g + (i >> 2)) * ld + col0 + 4 * (i & 3);
+  const bf16x4 lo = lds_read_tr(p);
+  const bf16x4 hi = lds_read_tr(p + 16 * ld);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 // 16-byte vector of storage elements, for coalesced global <-> LDS copies.
 template <typename T>
 struct Vec16 {

@@ -107,6 +107,20 @@ struct RowBlock {
       if (idx < TOTAL) *reinterpret_cast<typename Vec16<T>::type*>(&dst[t * ld + d0]) = x[i];
     }
   }
+  // row-major copy with a per-row scale: dst[t * ld + d] = x[t][d] * scale[t]
+  __device__ inline void store_rows_scaled(T* dst, int ld, const float* scale) const {
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int idx = threadIdx.x + NT * i;
+      const int t = idx / PER_ROW, d0 = (idx % PER_ROW) * VEC;
+      if (idx >= TOTAL) continue;
+      const float sc = scale[t];
+      typename Vec16<T>::type y;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) y[e] = from_f32<T>(to_f32(x[i][e]) * sc);
+      *reinterpret_cast<typename Vec16<T>::type*>(&dst[t * ld + d0]) = y;
+    }
+  }
 };
 
 template <typename T, int D, int NT, int LDROW = D>
@@ -163,8 +177,8 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
                                                      int64_t Tlen, int H) {
   using M = Mfma<T>;
   constexpr int R = kTileChunks * C;
-  constexpr int VEC = Vec16<T>::N;
-  constexpr int LDT = kKB + VEC;
+  constexpr int LDV = DV + 16;   // row strides of the row-major V and (decay * K) tiles
+  constexpr int LDK = DK + 16;
   constexpr int MT = DV / 16, NT = DK / 16;
   constexpr int NW = kStateThreads / 64;
   constexpr int WM = MT >= 2 ? 2 : 1;                            // waves along p
@@ -172,8 +186,8 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
   constexpr int TM = MT / WM, TN = NT / WN;                      // 16x16 tiles per wave
   constexpr int SZ = DK * DV;
   constexpr int STEPS = R / kKB;                                 // 64-row steps per tile
-  __shared__ T vt_s[DV * LDT];
-  __shared__ T kt_s[DK * LDT];
+  __shared__ T v_s[kKB * LDV];   // V rows of the current 64-row step
+  __shared__ T k_s[kKB * LDK];   // decay * K rows
   __shared__ float cl_s[R];
   __shared__ float dec_s[R];
   __shared__ float wsum_s[4];
@@ -190,8 +204,8 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
   const int64_t u0 = (int64_t)blk * kBlockTiles;
   const int ntile = (int)((N - u0) < kBlockTiles ? (N - u0) : kBlockTiles);
 
-  ColBlock<T, DK, kStateThreads> kr;
-  ColBlock<T, DV, kStateThreads> vr;
+  RowBlock<T, DK, kStateThreads> kr;
+  RowBlock<T, DV, kStateThreads> vr;
   auto nrow_of = [&](int64_t u) { return (int)((Tlen - u * R) < R ? (Tlen - u * R) : R); };
   kr.load(k, (int64_t)b * Tlen + u0 * R, 0, nrow_of(u0), H, h);
   vr.load(v, (int64_t)b * Tlen + u0 * R, 0, nrow_of(u0), H, h);
@@ -218,8 +232,8 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
 
     for (int kb = 0; kb < STEPS; ++kb) {
       __syncthreads();  // previous step's readers done; dec_s visible
-      vr.template store_cols<false>(vt_s, LDT, nullptr);
-      kr.template store_cols<true>(kt_s, LDT, dec_s + kb * kKB);
+      vr.store_rows(v_s, LDV);
+      kr.store_rows_scaled(k_s, LDK, dec_s + kb * kKB);
       __syncthreads();
       // prefetch the next step (next 64 rows of this tile, or the first rows of the next tile)
       if (kb + 1 < STEPS) {
@@ -230,15 +244,22 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
         vr.load(v, row0 + R, 0, nrow_of(u + 1), H, h);
       }
       if (active) {
+        // S^T[p][n] += sum_t V[t][p] (dK)[t][n]: both operands read down the token rows
 #pragma unroll
         for (int ks = 0; ks < kKB / M::KSTEP; ++ks) {
-          const int k0 = ks * M::KSTEP + g * M::KPL;
           typename M::frag bf[TN];
 #pragma unroll
-          for (int jn = 0; jn < TN; ++jn) bf[jn] = M::load(&kt_s[((wn * TN + jn) * 16 + r16) * LDT + k0]);
+          for (int jn = 0; jn < TN; ++jn) {
+            const int n0 = (wn * TN + jn) * 16;
+            if constexpr (M::KPL == 8) bf[jn] = frag_down_rows(k_s, LDK, ks * 32, n0);
+            else bf[jn] = k_s[(ks * 4 + g) * LDK + n0 + r16];
+          }
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
-            const typename M::frag af = M::load(&vt_s[((wm * TM + i) * 16 + r16) * LDT + k0]);
+            const int p0 = (wm * TM + i) * 16;
+            typename M::frag af;
+            if constexpr (M::KPL == 8) af = frag_down_rows(v_s, LDV, ks * 32, p0);
+            else af = v_s[(ks * 4 + g) * LDV + p0 + r16];
 #pragma unroll
             for (int jn = 0; jn < TN; ++jn) acc[i][jn] = M::mma(af, bf[jn], acc[i][jn]);
           }
@@ -449,13 +470,13 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
   constexpr int LOG2R = (R == 64) ? 6 : (R == 128) ? 7 : (R == 256) ? 8 : 9;
   constexpr int VEC = Vec16<T>::N;
   constexpr int LDK = DK + VEC;     // K and U row stride (elements)
-  constexpr int LDV = kKB + VEC;    // V^T row stride (elements)
+  constexpr int LDV = DV + 16;      // V row stride (elements)
   using RM = RowMap<R>;
   constexpr int NT = RM::NT;
   constexpr int ROWS = 16 * RM::NW; // rows of this workgroup
   constexpr int MT = DV / 16, KS = DK / M::KSTEP;
   constexpr int SZ = DK * DV;
-  constexpr int KV_ELEMS = kKB * LDK + DV * LDV;
+  constexpr int KV_ELEMS = kKB * LDK + kKB * LDV;
   constexpr int U_ELEMS = DV * LDK;
   constexpr int ULOADS = (SZ / VEC + NT - 1) / NT;
   __shared__ T buf_s[KV_ELEMS > U_ELEMS ? KV_ELEMS : U_ELEMS];
@@ -464,7 +485,7 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
   __shared__ float lam_s[HAS_LAMBDA ? ROWS * kMaxLevels : 1];  // row 16 * wave + r16 of this workgroup
   __shared__ float kdec_s[R];
   T* k_s = buf_s;
-  T* vt_s = buf_s + kKB * LDK;
+  T* v_s = buf_s + kKB * LDK;
   T* u_s = buf_s;
 
   const int64_t N = (Tlen + R - 1) / R;
@@ -482,7 +503,7 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
   const int nkb_w = (16 * gi + 15) / kKB + 1;    // key blocks this wave's rows reach
 
   RowBlock<T, DK, NT> kr;
-  ColBlock<T, DV, NT> vr;
+  RowBlock<T, DV, NT> vr;
   kr.load(k, row0, 0, nrow, H, h);
   vr.load(v, row0, 0, nrow, H, h);
 
@@ -525,7 +546,7 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
   for (int kb = 0; kb < nkb; ++kb) {
     __syncthreads();  // previous block's readers are done (and cl/lambda staging on entry)
     kr.store_rows(k_s, LDK);
-    vr.template store_cols<false>(vt_s, LDV, nullptr);
+    vr.store_rows(v_s, LDV);
     __syncthreads();
     if (kb + 1 < nkb) {
       kr.load(k, row0, (kb + 1) * kKB, nrow, H, h);
@@ -572,7 +593,7 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
       }
       if constexpr (M::KPL == 8) {
         // slots 0-3 <- key tile KT0 rows 4g..4g+3, slots 4-7 <- key tile KT0+1 rows 4g..4g+3;
-        // V^T is read at the same keys.
+        // the V^T fragment is read down the same key rows of the row-major V tile.
         typename M::frag bp;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -580,20 +601,14 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
           bp[4 + r] = from_f32<T>(p[1][r]);
         }
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const T* row = &vt_s[(mt * 16 + r16) * LDV + st * 32 + 4 * g];
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row);
-          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 16);
-          const typename M::frag a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          oacc[mt] = M::mma(a, bp, oacc[mt]);
-        }
+        for (int mt = 0; mt < MT; ++mt) oacc[mt] = M::mma(frag_down_rows(v_s, LDV, st * 32, mt * 16), bp, oacc[mt]);
       } else {
         // fp32: one k step = 4 keys {16 kt + 4g + r : g}, i.e. slot r of every lane group.
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
-            oacc[mt] = M::mma(vt_s[(mt * 16 + r16) * LDV + st * 16 + 4 * g + r], p[0][r], oacc[mt]);
+            oacc[mt] = M::mma(v_s[(st * 16 + 4 * g + r) * LDV + mt * 16 + r16], p[0][r], oacc[mt]);
       }
     }
   }
