@@ -58,13 +58,20 @@ struct Nodes {
 // a zero gate), computed by the first 4 waves of the workgroup (R/4 <= 64 rows each) into cl_s[R].
 // Starts and ends with a barrier.
 template <int R>
-__device__ inline void tile_cumsum(const float* __restrict__ log_alpha, int64_t row0, int nrow, int H, int h,
-                                   float* cl_s, float* wsum_s) {
+__device__ inline float tile_gate(const float* __restrict__ log_alpha, int64_t row0, int nrow, int H, int h) {
+  constexpr int RPW = R / 4;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = wave * RPW + lane;
+  return (wave < 4 && lane < RPW && r < nrow) ? log_alpha[(row0 + r) * H + h] * kLog2e : 0.f;
+}
+
+// Scan of the gates returned by tile_gate (which may be loaded well before the scan).
+template <int R>
+__device__ inline void tile_cumsum_of(float la, float* cl_s, float* wsum_s) {
   constexpr int RPW = R / 4;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = wave * RPW + lane;
   const bool mine = wave < 4 && lane < RPW;  // waves beyond the first four only take the barriers
-  float la = (mine && r < nrow) ? log_alpha[(row0 + r) * H + h] * kLog2e : 0.f;
   float cl = wave_inclusive_scan(la);
   __syncthreads();
   if (wave < 4 && lane == 63) wsum_s[wave] = cl;
@@ -73,6 +80,12 @@ __device__ inline void tile_cumsum(const float* __restrict__ log_alpha, int64_t 
   for (int w = 0; w < wave && w < 4; ++w) base += wsum_s[w];
   if (mine) cl_s[r] = base + cl;
   __syncthreads();
+}
+
+template <int R>
+__device__ inline void tile_cumsum(const float* __restrict__ log_alpha, int64_t row0, int nrow, int H, int h,
+                                   float* cl_s, float* wsum_s) {
+  tile_cumsum_of<R>(tile_gate<R>(log_alpha, row0, nrow, H, h), cl_s, wsum_s);
 }
 
 // Register staging of one 64-row block of a [rows, H, D] tensor, loaded with 16-byte vectors by
@@ -312,7 +325,7 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
 // (sum of tot over the 2^(j-2)-block with index (u >> (j-2)) - 1): a sum over exact ranges,
 // built from a tree of block sums in LDS.
 // ---------------------------------------------------------------------------------------------
-constexpr int kMaxGapTiles = 8192;  // tiles per sequence the gap tree holds (T <= 8192 R)
+constexpr int kMaxGapTiles = 8192;  // tiles per sequence the scan stages in LDS (T <= 8192 R)
 constexpr int kScanUnroll = 8;      // summary loads in flight per thread
 
 template <typename T>
@@ -321,16 +334,19 @@ __global__ __launch_bounds__(256) void k_block_scan(Nodes<T> nodes, const T* __r
                                                     float* __restrict__ gaps2, int64_t N, int J, int SZ,
                                                     int has_lambda) {
   typedef T T2 __attribute__((ext_vector_type(2)));
+  extern __shared__ float dyn_s[];  // 2 N floats: tile totals, then sums over aligned blocks
   const int64_t bh = blockIdx.y;
   const int tid = threadIdx.x;
   const float* tot = tot2 + bh * N;
   const int64_t NB = (N + kBlockTiles - 1) / kBlockTiles;
+  float* tot_s = dyn_s;
+
+  for (int64_t u = tid; u < N; u += 256) tot_s[u] = tot[u];
+  __syncthreads();
 
   if (blockIdx.x == gridDim.x - 1) {
-    __shared__ float bs[2 * kMaxGapTiles];
     if (!has_lambda || J == 0) return;
-    for (int64_t u = tid; u < N; u += 256) bs[u] = tot[u];
-    __syncthreads();
+    float* bs = dyn_s;  // level k block sums follow level k-1's (level 0 = the tile totals)
     int64_t off_prev = 0, off = N;
     for (int k = 1; k < J; ++k) {
       const int64_t len = N >> k;
@@ -373,7 +389,7 @@ __global__ __launch_bounds__(256) void k_block_scan(Nodes<T> nodes, const T* __r
         out[0] = from_f32<T>(r0);
         out[1] = from_f32<T>(r1);
         *reinterpret_cast<T2*>(dst + (u0 + i) * SZ) = out;
-        const float e = exp2f(tot[u0 + i]);
+        const float e = fast_exp2(tot_s[u0 + i]);
         r0 = r0 * e + to_f32(sv[i][0]);
         r1 = r1 * e + to_f32(sv[i][1]);
       }
@@ -395,8 +411,8 @@ __global__ __launch_bounds__(256) void k_block_scan(Nodes<T> nodes, const T* __r
       if (bl >= NB) break;
       float tb = 0.f;
       for (int a = 0; a < kBlockTiles; ++a)
-        if (bl * kBlockTiles + a < N) tb += tot[bl * kBlockTiles + a];
-      const float e = exp2f(tb);
+        if (bl * kBlockTiles + a < N) tb += tot_s[bl * kBlockTiles + a];
+      const float e = fast_exp2(tb);
       const float s0 = to_f32(sv[i][0]), s1 = to_f32(sv[i][1]);
 #pragma unroll
       for (int j = 4; j <= kMaxLevels; ++j) {
@@ -506,6 +522,7 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
   RowBlock<T, DV, NT> vr;
   kr.load(k, row0, 0, nrow, H, h);
   vr.load(v, row0, 0, nrow, H, h);
+  const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);  // issued with the other loads
 
   // Q^T fragments (B operand) of this lane's row, kept in registers.
   typename M::frag qf[KS];
@@ -533,10 +550,41 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
       }
     }
   }
-  tile_cumsum<R>(log_alpha, row0, nrow, H, h, cl_s, wsum_s);
+  tile_cumsum_of<R>(la, cl_s, wsum_s);
   // key-side decay to the end of each 16-key tile: kdec[j] = exp2(cl[j | 15] - cl[j])
   for (int r = tid; r < R; r += NT) kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
   const float* lrow = &lam_s[(16 * wave + r16) * L];  // this lane's lambda row
+
+  // ---- summaries of the inter-tile levels (set bits of u); the first one is prefetched while
+  //      the last key block is being used, each next one while the current level is
+  auto level_src = [&](int j, float* gap) -> const T* {
+    if constexpr (HAS_LAMBDA) {
+      *gap = gaps2[(bh * N + u) * J + (j - 1)];
+      return nodes.at(bh, N, j, source_first(u, j), SZ);
+    } else {
+      *gap = 0.f;
+      return running + (bh * N + u) * SZ;
+    }
+  };
+  auto next_level = [&](int j) {
+    if constexpr (HAS_LAMBDA) {
+      for (++j; j <= J; ++j)
+        if (reads_level(u, j)) return j;
+      return 0;
+    } else {
+      return (j == 0 && u > 0) ? 1 : 0;
+    }
+  };
+  V16 ur[ULOADS];
+  auto load_u = [&](const T* U) {
+#pragma unroll
+    for (int e = 0; e < ULOADS; ++e) {
+      const int idx = tid + NT * e;
+      if (idx < SZ / VEC) ur[e] = *reinterpret_cast<const V16*>(U + idx * VEC);
+    }
+  };
+  int j = next_level(0);
+  float gap = 0.f;
 
   f32x4 oacc[MT];
 #pragma unroll
@@ -551,6 +599,8 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
     if (kb + 1 < nkb) {
       kr.load(k, row0, (kb + 1) * kKB, nrow, H, h);
       vr.load(v, row0, (kb + 1) * kKB, nrow, H, h);
+    } else if (HAS_LAMBDA && j) {
+      load_u(level_src(j, &gap));
     }
     if (kb >= nkb_w || 16 * gi >= nrow) continue;
     const float cli = cl_s[i];
@@ -613,36 +663,7 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
     }
   }
 
-  // ---- inter-tile levels (set bits of u), the next level's summary prefetched into registers
-  auto level_src = [&](int j, float* gap) -> const T* {
-    if constexpr (HAS_LAMBDA) {
-      *gap = gaps2[(bh * N + u) * J + (j - 1)];
-      return nodes.at(bh, N, j, source_first(u, j), SZ);
-    } else {
-      *gap = 0.f;
-      return running + (bh * N + u) * SZ;
-    }
-  };
-  auto next_level = [&](int j) {
-    if constexpr (HAS_LAMBDA) {
-      for (++j; j <= J; ++j)
-        if (reads_level(u, j)) return j;
-      return 0;
-    } else {
-      return (j == 0 && u > 0) ? 1 : 0;
-    }
-  };
-  V16 ur[ULOADS];
-  auto load_u = [&](const T* U) {
-#pragma unroll
-    for (int e = 0; e < ULOADS; ++e) {
-      const int idx = tid + NT * e;
-      if (idx < SZ / VEC) ur[e] = *reinterpret_cast<const V16*>(U + idx * VEC);
-    }
-  };
-  int j = next_level(0);
-  float gap = 0.f;
-  if (j) load_u(level_src(j, &gap));
+  if (!HAS_LAMBDA && j) load_u(level_src(j, &gap));
   while (j) {
     __syncthreads();  // LDS buffer free
 #pragma unroll
@@ -784,7 +805,8 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
     hipLaunchKernelGGL((k_block_state<T, C, DK, DV, false>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
                        a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H);
   if (ev) (void)hipEventRecord(ev[1], st);
-  hipLaunchKernelGGL((k_block_scan<T>), gscan, dim3(256), 0, st, nodes, (const T*)tiles, running, (const float*)tot2,
+  hipLaunchKernelGGL((k_block_scan<T>), gscan, dim3(256), 2 * w.N * sizeof(float), st, nodes, (const T*)tiles,
+                     running, (const float*)tot2,
                      gaps2, w.N, w.J, SZ, a.lambda != nullptr ? 1 : 0);
   if (ev) (void)hipEventRecord(ev[2], st);
   if (a.lambda)
