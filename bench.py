@@ -1,12 +1,13 @@
 """Benchmark: log-linear Mamba-2 chunkwise forward on one MI355X.
 
-One step = one ll_mamba2_fwd call over the whole workload (all three kernel stages: chunk
-states, level scan, chunk outputs), inputs already resident in HBM.  Default workload:
+One step = one ll_mamba2_fwd call over the whole workload (all three kernel stages: tile
+states, level scan, tile outputs), inputs already resident in HBM.  Default workload:
 B=1, H=16, T=65536, d_k=d_v=128, C=64, bf16 q/k/v with fp32 gates and lambda (17 levels).
 
 Prints ONE JSON line with throughput (tokens/s), TFLOP/s against the bf16 MFMA peak, the
-lambda == NULL (Mamba-2) run of the same library, per-stage HIP-event timings, the roofline of
-the dominant kernel and the float64 oracle timed on the host cores.
+lambda == NULL (Mamba-2) run of the same library, per-stage durations read from HIP events
+recorded between the stages of every timed step, the roofline of the dominant kernel and the
+float64 oracle timed on the host cores.
 
 FLOP convention (counted, not issued): log-linear Mamba-2
     F = B*H*T*[2C(d_k+d_v) + 2 d_k d_v + d_k d_v log2(T/C)]
@@ -44,19 +45,61 @@ def flops_mamba2(w):
     return w.B * w.H * w.T * (2 * w.C * (w.dk + w.dv) + 4 * w.dk * w.dv)
 
 
+STAGES = ["block_state", "block_scan", "tile_out"]
+KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_mamba2.hip", "paper_2506_04761_amd/csrc/ll_device.hpp"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tile_out_ll_mamba2_bf16_T65536_hbm_traffic.md")
+
+
 def stage_figures(w, has_lambda=True):
-    """Per-launch algorithmic work of each stage: (bound, amount, unit-name)."""
+    """Algorithmic work of one launch of each stage: (bound, amount).  FLOPs for the MFMA
+    stages under the convention above; bytes for the scan (HBM-bound, elementwise)."""
     es = 2 if w.dtype == "bf16" else 4
-    BHT = w.B * w.H * w.T
-    N = w.T // w.C
-    J = int(math.log2(N)) if N > 1 else 0
+    BH, BHT = w.B * w.H, w.B * w.H * w.T
     SZ = w.dk * w.dv
+    J_chunk = math.log2(w.T // w.C) if w.T > w.C else 0.0
     f_state = 2.0 * BHT * w.dk * w.dv
-    f_out = BHT * (2 * w.C * (w.dk + w.dv) + (w.dk * w.dv * J if has_lambda else 2 * w.dk * w.dv))
-    # level scan: chunk states read once (fp32), one summary per reader group written (storage dtype)
-    nodes = sum((N + (1 << j) - 1) >> j for j in range(1, J + 1)) if has_lambda else N
-    b_scan = w.B * w.H * (N * SZ * 4 + nodes * SZ * es + N * 4)
-    return {"chunk_state": ("mfma", f_state), "level_scan": ("hbm", b_scan), "chunk_out": ("mfma", f_out)}
+    f_out = BHT * (2 * w.C * (w.dk + w.dv) + (w.dk * w.dv * J_chunk if has_lambda else 2 * w.dk * w.dv))
+    R = 4 * w.C                              # tile = 4 chunks
+    N = -(-w.T // R)                         # tiles per sequence
+    NB = -(-N // 4)                          # 4-tile blocks
+    J = (N - 1).bit_length() if N > 1 else 0  # inter-tile levels
+    if has_lambda:
+        # read: block summaries, tile totals; write: summaries of levels >= 4, gaps (fp32, N x J)
+        nup = sum(-(-(N - (1 << (j - 1))) // (1 << j)) for j in range(4, J + 1) if N > (1 << (j - 1)))
+        b_scan = BH * ((NB + nup) * SZ * es + N * 4 + N * J * 4)
+    else:
+        # read: tile states, tile totals; write: running state entering each tile
+        b_scan = BH * (2 * N * SZ * es + N * 4)
+    return {"block_state": ("mfma", f_state), "block_scan": ("hbm", b_scan), "tile_out": ("mfma", f_out)}
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(workload):
+    """HBM bytes per tile_out launch from the committed counter summary (FETCH_SIZE and
+    WRITE_SIZE, calibrated against a plain copy), or None when there is none for this workload
+    or the kernel sources changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    rec = {}
+    with open(TRAFFIC_FILE) as fh:
+        for line in fh:
+            if line.startswith("- ") and ": " in line:
+                key, val = line[2:].split(": ", 1)
+                rec[key.strip()] = val.strip().strip("`")
+    if rec.get("workload") != workload or rec.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return float(rec["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def algorithmic_bytes(w):
@@ -132,7 +175,7 @@ def main():
     def run(lmb):
         ll.ll_mamba2_fwd(d["q"], d["k"], d["v"], la, lmb, w.C, out=out, workspace=ws, stream=stream)
 
-    def timed(lmb, K, W):
+    def timed_plain(lmb, K, W):
         for _ in range(W):
             run(lmb)
         torch.cuda.synchronize()
@@ -144,21 +187,33 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / K
 
-    print(f"[bench] {w.name}: warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
-    ms = timed(lam, args.steps, args.warmup)
-    ms_m2 = timed(None, args.steps, args.warmup)
-    print(f"[bench] log-linear {ms:.3f} ms/step, lambda=NULL {ms_m2:.3f} ms/step", file=sys.stderr, flush=True)
+    def timed_staged(K, W):
+        """K timed steps, each recording HIP events between its kernel stages on the launch
+        stream; returns (ms per step over the whole region, mean ms of each stage)."""
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(max(K, 1))]
+        for i in range(W):
+            ll.ll_mamba2_fwd_staged(d["q"], d["k"], d["v"], la, lam, w.C, evs[i % K], out=out, workspace=ws,
+                                    stream=stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(K):
+            ll.ll_mamba2_fwd_staged(d["q"], d["k"], d["v"], la, lam, w.C, evs[i], out=out, workspace=ws,
+                                    stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        st = np.array([[e[s].elapsed_time(e[s + 1]) for s in range(3)] for e in evs[:K]]).mean(axis=0)
+        return e0.elapsed_time(e1) / K, st
 
-    # per-stage durations (HIP events recorded between the stages, on the same stream)
-    stage_ms = np.zeros(3)
-    for _ in range(args.steps):
-        _, s = ll.ll_mamba2_fwd_timed(d["q"], d["k"], d["v"], la, lam, w.C, out=out, workspace=ws, stream=stream)
-        stage_ms += np.array(s)
-    stage_ms /= args.steps
-    names = ["chunk_state", "level_scan", "chunk_out"]
+    print(f"[bench] {w.name}: warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
+    ms, stage_ms = timed_staged(args.steps, args.warmup)
+    ms_m2 = timed_plain(None, args.steps, args.warmup)
+    print(f"[bench] log-linear {ms:.3f} ms/step (stages {', '.join(f'{x:.3f}' for x in stage_ms)}), "
+          f"lambda=NULL {ms_m2:.3f} ms/step", file=sys.stderr, flush=True)
+
     figs = stage_figures(w)
     dom = int(np.argmax(stage_ms))
-    bound, amount = figs[names[dom]]
+    bound, amount = figs[STAGES[dom]]
     if bound == "mfma":
         achieved = amount / (stage_ms[dom] * 1e-3) / 1e12
         peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS
@@ -166,6 +221,7 @@ def main():
     else:
         achieved = amount / (stage_ms[dom] * 1e-3) / 1e9
         peak, unit = PEAK_HBM_GBS, "GB/s"
+    traffic = recorded_traffic(w.name) if STAGES[dom] == "tile_out" else None
 
     F = flops_loglinear(w)
     tflops = F / (ms * 1e-3) / 1e12
@@ -193,9 +249,11 @@ def main():
         "mamba2_lambda_null": {"ms_per_step": ms_m2, "tokens_per_s": w.B * w.T / (ms_m2 * 1e-3),
                                "tflops": F2 / (ms_m2 * 1e-3) / 1e12},
         "log_factor_overhead": ms / ms_m2,
-        "stages_ms": dict(zip(names, [float(s) for s in stage_ms])),
-        "roofline": {"kernel": names[dom], "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
-                     "frac": achieved / peak, "traffic": None},
+        "stages_ms": dict(zip(STAGES, [float(x) for x in stage_ms])),
+        "roofline": {"kernel": STAGES[dom], "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+                     "frac": achieved / peak, "traffic": traffic,
+                     "algorithmic_per_launch": amount,
+                     "traffic_note": "HBM bytes per launch (FETCH_SIZE x 2 + WRITE_SIZE, copy-calibrated)"},
     }
     if args.copy_mib:
         # A plain copy kernel of known size: its FETCH_SIZE / WRITE_SIZE counters calibrate the

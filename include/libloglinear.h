@@ -81,15 +81,17 @@ ll_status ll_mamba2_fwd(const void* q, const void* k, const void* v, const float
                         int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                         void* workspace, size_t workspace_bytes, void* stream);
 
-/* Same computation as ll_mamba2_fwd, for measurement: records a HIP event on `stream` before
- * each of the three kernel stages and after the last, waits for the stream to reach the final
- * event (this call is synchronous), and writes the stages' durations in milliseconds to the host
- * array stage_ms[3]: [0] chunk states, [1] level scan, [2] chunk outputs (intra-chunk and
- * inter-chunk terms).  stage_ms == NULL returns LL_ERR_NULL_ARG. */
-ll_status ll_mamba2_fwd_timed(const void* q, const void* k, const void* v, const float* log_alpha,
-                              const float* lambda, void* o, int64_t B, int64_t T, int64_t H,
-                              int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
-                              void* workspace, size_t workspace_bytes, void* stream, float* stage_ms);
+/* Same computation as ll_mamba2_fwd, for measurement: also records the caller's HIP events
+ * (hipEvent_t handles passed as void*) on `stream`, events[i] right before kernel stage i and
+ * events[3] after the last stage, so that the caller can read each stage's duration with
+ * hipEventElapsedTime once the stream has passed them.  Stages: 0 tile states, 1 level scan,
+ * 2 tile outputs (intra-tile and inter-tile terms).  Asynchronous like ll_mamba2_fwd.  events
+ * == NULL or any events[i] == NULL returns LL_ERR_NULL_ARG; the events stay owned by the caller. */
+ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
+                               const float* lambda, void* o, int64_t B, int64_t T, int64_t H,
+                               int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                               void* workspace, size_t workspace_bytes, void* stream,
+                               void* const* events);
 
 /* Log-linear Gated DeltaNet forward (Sec. 3.4), with the delta-rule transition
  * alpha_t (I - beta_t k_t k_t^T) applied chunkwise through a WY (UT) representation.

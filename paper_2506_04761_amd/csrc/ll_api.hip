@@ -78,7 +78,7 @@ const char* ll_status_string(ll_status s) {
 namespace {
 ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
                       void* o, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
-                      void* workspace, size_t workspace_bytes, void* stream, float* stage_ms) {
+                      void* workspace, size_t workspace_bytes, void* stream, void* const* events) {
   if (!q || !k || !v || !log_alpha || !o) return LL_ERR_NULL_ARG;
   ll_status st = check_shape(B, T, H, d_k, d_v, C);
   if (st != LL_OK) return st;
@@ -99,22 +99,10 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   a.L = L;
   a.workspace = workspace;
   hipStream_t hs = static_cast<hipStream_t>(stream);
-  if (!stage_ms) {
-    hipError_t err = e->launch(a, hs, nullptr);
-    return err == hipSuccess ? LL_OK : LL_ERR_HIP;
-  }
   hipEvent_t ev[ll::kMamba2Stages + 1];
-  int made = 0;
-  hipError_t err = hipSuccess;
-  for (int i = 0; i <= ll::kMamba2Stages; ++i) {
-    err = hipEventCreate(&ev[i]);
-    if (err != hipSuccess) break;
-    ++made;
-  }
-  if (err == hipSuccess) err = e->launch(a, hs, ev);
-  if (err == hipSuccess) err = hipEventSynchronize(ev[ll::kMamba2Stages]);
-  for (int i = 0; i < ll::kMamba2Stages && err == hipSuccess; ++i) err = hipEventElapsedTime(&stage_ms[i], ev[i], ev[i + 1]);
-  for (int i = 0; i < made; ++i) (void)hipEventDestroy(ev[i]);
+  if (events)
+    for (int i = 0; i <= ll::kMamba2Stages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);
+  const hipError_t err = e->launch(a, hs, events ? ev : nullptr);
   return err == hipSuccess ? LL_OK : LL_ERR_HIP;
 }
 }  // namespace
@@ -128,13 +116,15 @@ ll_status ll_mamba2_fwd(const void* q, const void* k, const void* v, const float
                      nullptr);
 }
 
-ll_status ll_mamba2_fwd_timed(const void* q, const void* k, const void* v, const float* log_alpha,
-                              const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t d_k,
-                              int64_t d_v, int64_t C, int32_t dtype, void* workspace, size_t workspace_bytes,
-                              void* stream, float* stage_ms) {
-  if (!stage_ms) return LL_ERR_NULL_ARG;
+ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
+                               const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t d_k,
+                               int64_t d_v, int64_t C, int32_t dtype, void* workspace, size_t workspace_bytes,
+                               void* stream, void* const* events) {
+  if (!events) return LL_ERR_NULL_ARG;
+  for (int i = 0; i <= ll::kMamba2Stages; ++i)
+    if (!events[i]) return LL_ERR_NULL_ARG;
   return mamba2_impl(q, k, v, log_alpha, lambda, o, B, T, H, d_k, d_v, C, dtype, workspace, workspace_bytes, stream,
-                     stage_ms);
+                     events);
 }
 
 ll_status ll_gdn_fwd(const void* q, const void* k, const void* v, const float* log_alpha, const float* beta,

@@ -768,7 +768,7 @@ int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv
 }
 
 // Enqueues the three stages on `st`.  With `ev` non-null, ev[i] is recorded before stage i
-// and ev[3] after the last one (used by the timed entry point).
+// and ev[3] after the last one (used by the staged entry point).
 template <typename T, int C, int DK, int DV>
 hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
   constexpr int SZ = DK * DV;
