@@ -51,34 +51,67 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tile_out_ll_mamba2_bf16_T65536_hb
 
 
 def stage_figures(w, has_lambda=True):
-    """Algorithmic work of one launch of each stage: (bound, amount).  FLOPs for the MFMA
-    stages under the convention above; bytes for the scan (HBM-bound, elementwise)."""
+    """Algorithmic work of one launch of each stage: {stage: (flops, bytes)}.
+
+    FLOPs follow the convention above.  Bytes: block_state reads k, v and the log-gates and
+    writes the summaries it produces; block_scan reads block summaries and tile totals and writes
+    the upper-level summaries and gaps (lambda == NULL: tile states in, running states out);
+    tile_out reads q, k, v, the log-gates and lambda and writes o -- the path's algorithmic bytes.
+    Summary reads inside tile_out are implementation traffic (see the rocprofv3 counters)."""
     es = 2 if w.dtype == "bf16" else 4
     BH, BHT = w.B * w.H, w.B * w.H * w.T
     SZ = w.dk * w.dv
     J_chunk = math.log2(w.T // w.C) if w.T > w.C else 0.0
-    f_state = 2.0 * BHT * w.dk * w.dv
-    f_out = BHT * (2 * w.C * (w.dk + w.dv) + (w.dk * w.dv * J_chunk if has_lambda else 2 * w.dk * w.dv))
     R = 4 * w.C                              # tile = 4 chunks
     N = -(-w.T // R)                         # tiles per sequence
     NB = -(-N // 4)                          # 4-tile blocks
     J = (N - 1).bit_length() if N > 1 else 0  # inter-tile levels
+    L = w.levels if has_lambda else 0
+    f_state = 2.0 * BHT * w.dk * w.dv
+    f_out = BHT * (2 * w.C * (w.dk + w.dv) + (w.dk * w.dv * J_chunk if has_lambda else 2 * w.dk * w.dv))
     if has_lambda:
-        # read: block summaries, tile totals; write: summaries of levels >= 4, gaps (fp32, N x J)
+        n_state_out = (-(-N // 2) + -(-N // 4) + NB)  # even tile states, pair and block summaries
         nup = sum(-(-(N - (1 << (j - 1))) // (1 << j)) for j in range(4, J + 1) if N > (1 << (j - 1)))
         b_scan = BH * ((NB + nup) * SZ * es + N * 4 + N * J * 4)
     else:
-        # read: tile states, tile totals; write: running state entering each tile
+        n_state_out = N
         b_scan = BH * (2 * N * SZ * es + N * 4)
-    return {"block_state": ("mfma", f_state), "block_scan": ("hbm", b_scan), "tile_out": ("mfma", f_out)}
+    b_state = BHT * ((w.dk + w.dv) * es + 4) + BH * (n_state_out * SZ * es + N * 4)
+    b_out = BHT * ((2 * w.dk + 2 * w.dv) * es + 4 + L * 4)
+    return {"block_state": (f_state, b_state), "block_scan": (0.0, b_scan), "tile_out": (f_out, b_out)}
+
+
+def roofline(w, flops, nbytes, ms):
+    """Roofline position of one kernel launch: the bound is whichever of the MFMA time and the
+    HBM time of its algorithmic work is longer; both fractions are reported."""
+    peak_f = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS
+    t_f = flops / (peak_f * 1e12)
+    t_b = nbytes / (PEAK_HBM_GBS * 1e9)
+    tflops = flops / (ms * 1e-3) / 1e12
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    if t_f >= t_b:
+        r = {"bound": "mfma", "achieved": tflops, "peak": peak_f, "unit": "TFLOP/s"}
+    else:
+        r = {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    r["frac"] = r["achieved"] / r["peak"]
+    r["mfma_frac"] = tflops / peak_f
+    r["hbm_frac"] = gbs / PEAK_HBM_GBS
+    r["algorithmic_flops"] = flops
+    r["algorithmic_bytes"] = nbytes
+    return r
 
 
 def kernel_source_hash():
+    """Hash of the kernel sources with comments and blank lines removed (comment edits do not
+    change the kernel)."""
     import hashlib
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, f)) as fh:
+            for line in fh:
+                code = line.split("//", 1)[0].strip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 
@@ -110,9 +143,9 @@ def algorithmic_bytes(w):
 
 def cpu_baseline(w, budget_s):
     """Time the float64 oracle's per-level recurrent form on a prefix of the workload (all heads),
-    growing the prefix until one run takes at least `budget_s` / 4; report tokens/s."""
-    from oracle import mamba2
-    x = generate(w.with_(T=min(w.T, 4096)))
+    growing the prefix until one run takes at least `budget_s` / 2; report tokens/s."""
+    from oracle import gdn, mamba2
+    x = generate(w.with_(T=min(w.T, 16384)))
     L = w.levels
     lam_full = np.zeros(x["lam"].shape[:-1] + (L,), np.float32)
     lam_full[..., :x["lam"].shape[-1]] = x["lam"]
@@ -120,9 +153,13 @@ def cpu_baseline(w, budget_s):
     while True:
         sl = slice(0, T)
         t0, c0 = time.perf_counter(), time.process_time()
-        mamba2.recurrent(x["q"][:, sl], x["k"][:, sl], x["v"][:, sl], x["log_alpha"][:, sl], lam_full[:, sl])
+        if w.variant == "gdn":
+            gdn.recurrent(x["q"][:, sl], x["k"][:, sl], x["v"][:, sl], x["log_alpha"][:, sl], x["beta"][:, sl],
+                          lam_full[:, sl])
+        else:
+            mamba2.recurrent(x["q"][:, sl], x["k"][:, sl], x["v"][:, sl], x["log_alpha"][:, sl], lam_full[:, sl])
         wall, cpu = time.perf_counter() - t0, time.process_time() - c0
-        if wall >= budget_s / 4 or T >= x["q"].shape[1]:
+        if wall >= budget_s / 2 or T >= x["q"].shape[1]:
             break
         T *= 2
     return {
@@ -131,7 +168,8 @@ def cpu_baseline(w, budget_s):
         "cores": max(1, round(cpu / wall)),
         "host_cores_available": len(os.sched_getaffinity(0)),
         "kind": "oracle",
-        "sample": f"float64 per-level recurrent form (Sec. 3.2 states, Eq. 3 output), first {T} tokens of "
+        "sample": f"float64 per-level recurrent form (Sec. 3.2 states, Eq. 3 output, "
+                  f"{'gated delta rule' if w.variant == 'gdn' else 'scalar decay'}), first {T} tokens of "
                   f"all {w.H} heads, B={w.B}, {L} level states; {wall:.2f} s wall, {cpu:.2f} s CPU",
     }
 
@@ -156,7 +194,8 @@ def main():
     import paper_2506_04761_amd as ll
 
     w = WORKLOADS[args.workload]
-    assert w.variant == "mamba2"
+    if w.variant == "gdn":
+        return main_gdn(args, w, torch, ll)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
@@ -213,14 +252,7 @@ def main():
 
     figs = stage_figures(w)
     dom = int(np.argmax(stage_ms))
-    bound, amount = figs[STAGES[dom]]
-    if bound == "mfma":
-        achieved = amount / (stage_ms[dom] * 1e-3) / 1e12
-        peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS
-        unit = "TFLOP/s"
-    else:
-        achieved = amount / (stage_ms[dom] * 1e-3) / 1e9
-        peak, unit = PEAK_HBM_GBS, "GB/s"
+    roof = roofline(w, *figs[STAGES[dom]], stage_ms[dom])
     traffic = recorded_traffic(w.name) if STAGES[dom] == "tile_out" else None
 
     F = flops_loglinear(w)
@@ -250,10 +282,9 @@ def main():
                                "tflops": F2 / (ms_m2 * 1e-3) / 1e12},
         "log_factor_overhead": ms / ms_m2,
         "stages_ms": dict(zip(STAGES, [float(x) for x in stage_ms])),
-        "roofline": {"kernel": STAGES[dom], "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
-                     "frac": achieved / peak, "traffic": traffic,
-                     "algorithmic_per_launch": amount,
-                     "traffic_note": "HBM bytes per launch (FETCH_SIZE x 2 + WRITE_SIZE, copy-calibrated)"},
+        "roofline": {"kernel": STAGES[dom], **roof, "traffic": traffic,
+                     "traffic_note": "HBM bytes per launch from rocprofv3 FETCH_SIZE x 2 + WRITE_SIZE x 1 "
+                                     "(factors from a 1 GiB copy), null if the kernel changed since"},
     }
     if args.copy_mib:
         # A plain copy kernel of known size: its FETCH_SIZE / WRITE_SIZE counters calibrate the
@@ -264,6 +295,123 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if not args.no_cpu_baseline:
+        print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+# ------------------------------------------------------------------------- Gated DeltaNet
+
+def gdn_issued(w, has_lambda=True):
+    """MFMA FLOPs the two GDN kernels issue, counted from their loop structure, and the
+    algorithmic bytes of the whole call.
+    gdn_chunk, per chunk: K K^T, Q K^T (C x C x d_k), W = T_G (gamma K), Q~ correction (C x d_k x C),
+    U = T_G V, intra output (C x d_v x C), P_G T_G (C x C x C), P_z (d_k x d_k x C), H_z (d_k x d_v x C).
+    gdn_scan, per chunk and level j: propagation R_j <- P_z R_j (d_k x d_k x d_v) unless the level
+    restarts at this chunk, and the read-out q~^T R_j (C x d_k x d_v) if the chunk reads level j."""
+    C, dk, dv = w.C, w.dk, w.dv
+    N = w.T // C
+    J = (N - 1).bit_length() if N > 1 else 0
+    f_chunk = 2.0 * (3 * C * C * dk + C * C * dk + 2 * C * C * dv + C ** 3 + dk * dk * C + dk * dv * C)
+    f_scan = 0.0
+    for z in range(N):
+        levels = range(1, J + 1) if has_lambda else [0]
+        for j in levels:
+            reader = ((z >> (j - 1)) & 1) if j else z > 0
+            restart = (z & ((1 << j) - 1)) == 0 if j else z == 0
+            f_scan += (2.0 * C * dk * dv if reader else 0.0) + (0.0 if restart else 2.0 * dk * dk * dv)
+    BH = w.B * w.H
+    es = 2 if w.dtype == "bf16" else 4
+    L = w.levels if has_lambda else 0
+    nbytes = w.B * w.T * w.H * ((2 * dk + 2 * dv) * es + 8 + 4 * L)
+    return BH * N * f_chunk, BH * f_scan, nbytes
+
+
+def main_gdn(args, w, torch, ll):
+    """Log-linear Gated DeltaNet forward: same line format, issued-FLOP convention."""
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    x = generate(w)
+    d = {n: torch.from_numpy(x[n]).to(dev).to(torch.bfloat16).contiguous() for n in ("q", "k", "v")}
+    la = torch.from_numpy(x["log_alpha"]).to(dev)
+    beta = torch.from_numpy(x["beta"]).to(dev)
+    lam = torch.from_numpy(x["lam"]).to(dev)
+    del x
+    out = torch.empty((w.B, w.T, w.H, w.dv), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(ll.ll_workspace_size(ll.LL_GDN, ll.LL_BF16, w.B, w.T, w.H, w.dk, w.dv, w.C, 1),
+                     dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    K, W = args.steps, args.warmup
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+
+    def step(lmb, e=None):
+        if e is None:
+            ll.ll_gdn_fwd(d["q"], d["k"], d["v"], la, beta, lmb, w.C, out=out, workspace=ws, stream=stream)
+        else:
+            ll.ll_gdn_fwd_staged(d["q"], d["k"], d["v"], la, beta, lmb, w.C, e, out=out, workspace=ws,
+                                 stream=stream)
+
+    print(f"[bench] {w.name}: warmup {W}, steps {K}", file=sys.stderr, flush=True)
+    for i in range(W):
+        step(lam, evs[i % K])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(K):
+        step(lam, evs[i])
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    stage_ms = np.array([[e[s].elapsed_time(e[s + 1]) for s in range(2)] for e in evs]).mean(axis=0)
+    for _ in range(W):
+        step(None)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(K):
+        step(None)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_null = e0.elapsed_time(e1) / K
+    print(f"[bench] log-linear GDN {ms:.3f} ms/step (stages {stage_ms[0]:.3f}, {stage_ms[1]:.3f}), "
+          f"lambda=NULL {ms_null:.3f} ms/step", file=sys.stderr, flush=True)
+
+    f_chunk, f_scan, nbytes = gdn_issued(w)
+    names = ["gdn_chunk", "gdn_scan"]
+    dom = int(np.argmax(stage_ms))
+    # per-stage algorithmic bytes: the chunk kernel reads q, k, v, gates, beta and writes the
+    # per-chunk products (Q~, P_z, H_z bf16, intra output fp32); the scan reads those and lambda
+    # and writes o.
+    N = w.T // w.C
+    BHN = w.B * w.H * N
+    prod = BHN * (w.C * w.dk * 2 + w.dk * w.dk * 2 + w.dk * w.dv * 2 + w.C * w.dv * 4)
+    BTH = w.B * w.T * w.H
+    b_chunk = BTH * ((2 * w.dk + w.dv) * 2 + 8) + prod
+    b_scan = prod + BTH * (4 * w.levels + w.dv * 2)
+    figs = {"gdn_chunk": (f_chunk, b_chunk), "gdn_scan": (f_scan, b_scan)}
+    roof = roofline(w, *figs[names[dom]], stage_ms[dom])
+    F = f_chunk + f_scan
+    f_n, s_n, _ = gdn_issued(w, has_lambda=False)
+    res = {
+        "metric": "fwd tokens/sec + TFLOP/s (issued, % bf16 MFMA peak), log-linear Gated DeltaNet",
+        "value": w.B * w.T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "variant": "log-linear Gated DeltaNet", "B": w.B, "H": w.H, "T": w.T,
+                   "d_k": w.dk, "d_v": w.dv, "C": w.C, "levels": w.levels,
+                   "inputs": "bf16 q/k/v (k L2-normalised), fp32 log-gates, beta and lambda, seeded synthetic"},
+        "tflops_issued": F / (ms * 1e-3) / 1e12,
+        "mfma_peak_frac": F / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        "flop_convention": "MFMA FLOPs issued by gdn_chunk and gdn_scan (see gdn_issued)",
+        "hbm_GBps_algorithmic": nbytes / (ms * 1e-3) / 1e9,
+        "gdn_lambda_null": {"ms_per_step": ms_null, "tokens_per_s": w.B * w.T / (ms_null * 1e-3),
+                            "tflops_issued": (f_n + s_n) / (ms_null * 1e-3) / 1e12},
+        "log_factor_overhead": ms / ms_null,
+        "stages_ms": dict(zip(names, [float(v) for v in stage_ms])),
+        "roofline": {"kernel": names[dom], **roof, "traffic": None},
+    }
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)

@@ -102,6 +102,16 @@ ll_status ll_gdn_fwd(const void* q, const void* k, const void* v, const float* l
                      int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* Same computation as ll_gdn_fwd, for measurement: also records the caller's HIP events (as in
+ * ll_mamba2_fwd_staged) on `stream`: events[0] before the per-chunk kernel, events[1] between
+ * it and the level scan, events[2] after the scan.  Asynchronous.  events == NULL or any
+ * events[i] == NULL returns LL_ERR_NULL_ARG. */
+ll_status ll_gdn_fwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
+                            const float* beta, const float* lambda, void* o, int64_t B, int64_t T,
+                            int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                            void* workspace, size_t workspace_bytes, void* stream,
+                            void* const* events);
+
 /* Debug: writes out[t*T + s] = the Fenwick level l(t,s) that the forward kernels assign to the
  * pair (t, s) for chunk size C (Sec. 3.1; the intra/inter split of Eq. 5), and -1 for s > t.
  * `out` is device memory of T*T bytes.  Computed on the GPU by the same device functions the

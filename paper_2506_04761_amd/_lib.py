@@ -42,6 +42,9 @@ lib.ll_mamba2_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _
 lib.ll_mamba2_fwd_staged.restype = _i32
 lib.ll_gdn_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _sz, _vp]
 lib.ll_gdn_fwd.restype = _i32
+lib.ll_gdn_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _sz,
+                                   _vp, ctypes.POINTER(_vp)]
+lib.ll_gdn_fwd_staged.restype = _i32
 lib.ll_debug_level_map.argtypes = [_i64, _i64, _vp, _vp]
 lib.ll_debug_level_map.restype = _i32
 lib.ll_status_string.argtypes = [_i32]
@@ -144,20 +147,25 @@ def ll_mamba2_fwd(q, k, v, log_alpha, lam, C, out=None, workspace=None, stream=N
     return out
 
 
+def _event_handles(events, n, stream):
+    """HIP event handles of `n` torch.cuda.Event objects (created with enable_timing=True)."""
+    torch = _torch()
+    if len(events) != n:
+        raise ValueError(f"events must hold {n} torch.cuda.Event objects")
+    s = torch.cuda.current_stream() if stream is None else stream
+    for e in events:
+        if e.cuda_event == 0:  # torch creates the HIP event on its first record
+            e.record(s)
+    return (_vp * n)(*[e.cuda_event for e in events]), s
+
+
 def ll_mamba2_fwd_staged(q, k, v, log_alpha, lam, C, events, out=None, workspace=None, stream=None):
     """As ll_mamba2_fwd, and records the four torch.cuda.Event objects in `events` (created with
     enable_timing=True) on the stream around the three kernel stages: events[i] before stage i
     (tile states, level scan, tile outputs) and events[3] after the last.  Asynchronous; read
     the durations with events[i].elapsed_time(events[i + 1]) after synchronising."""
-    torch = _torch()
-    if len(events) != 4:
-        raise ValueError("events must hold 4 torch.cuda.Event objects")
-    s = torch.cuda.current_stream() if stream is None else stream
-    for e in events:
-        if e.cuda_event == 0:  # torch creates the HIP event on its first record
-            e.record(s)
+    handles, s = _event_handles(events, 4, stream)
     (B, T, H, dk, dv, code), out, ws = _prepare(LL_MAMBA2, q, k, v, log_alpha, None, lam, C, out, workspace)
-    handles = (_vp * 4)(*[e.cuda_event for e in events])
     st = lib.ll_mamba2_fwd_staged(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(lam), _ptr(out),
                                   B, T, H, dk, dv, C, code, _ptr(ws), ws.numel(), _stream(s), handles)
     if st != LL_OK:
@@ -170,6 +178,18 @@ def ll_gdn_fwd(q, k, v, log_alpha, beta, lam, C, out=None, workspace=None, strea
     (B, T, H, dk, dv, code), out, ws = _prepare(LL_GDN, q, k, v, log_alpha, beta, lam, C, out, workspace)
     st = lib.ll_gdn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(beta), _ptr(lam), _ptr(out),
                         B, T, H, dk, dv, C, code, _ptr(ws), ws.numel(), _stream(stream))
+    if st != LL_OK:
+        raise LLError(st)
+    return out
+
+
+def ll_gdn_fwd_staged(q, k, v, log_alpha, beta, lam, C, events, out=None, workspace=None, stream=None):
+    """As ll_gdn_fwd, recording three torch.cuda.Event objects around its two kernel stages
+    (per-chunk WY kernel, level scan); see ll_mamba2_fwd_staged."""
+    handles, s = _event_handles(events, 3, stream)
+    (B, T, H, dk, dv, code), out, ws = _prepare(LL_GDN, q, k, v, log_alpha, beta, lam, C, out, workspace)
+    st = lib.ll_gdn_fwd_staged(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(beta), _ptr(lam), _ptr(out),
+                               B, T, H, dk, dv, C, code, _ptr(ws), ws.numel(), _stream(s), handles)
     if st != LL_OK:
         raise LLError(st)
     return out

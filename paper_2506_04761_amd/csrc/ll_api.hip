@@ -105,6 +105,33 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   const hipError_t err = e->launch(a, hs, events ? ev : nullptr);
   return err == hipSuccess ? LL_OK : LL_ERR_HIP;
 }
+ll_status gdn_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* beta,
+                   const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C,
+                   int32_t dtype, void* workspace, size_t workspace_bytes, void* stream, void* const* events) {
+  if (!q || !k || !v || !log_alpha || !beta || !o) return LL_ERR_NULL_ARG;
+  ll_status st = check_shape(B, T, H, d_k, d_v, C);
+  if (st != LL_OK) return st;
+  const ll::GdnEntry* e = find_gdn(dtype, C, d_k, d_v);
+  if (!e) return LL_ERR_UNSUPPORTED;
+  const int64_t N = T / C;
+  const int J = N <= 1 ? 0 : bitlen64(uint64_t(N - 1));
+  const int L = levels_of(T);
+  if (J > ll::kGdnMaxLevels || L > kMaxL || H > 65535 || B > 65535 || B * H * N >= (int64_t(1) << 31))
+    return LL_ERR_UNSUPPORTED;
+  const int64_t need = ll::gdn_workspace(B, T, H, d_k, d_v, C, nullptr);
+  if (!workspace) return LL_ERR_NULL_ARG;
+  if ((int64_t)workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
+  ll::GdnArgs a;
+  a.q = q; a.k = k; a.v = v; a.log_alpha = log_alpha; a.beta = beta; a.lambda = lambda; a.o = o;
+  a.B = B; a.T = T; a.H = H; a.dk = d_k; a.dv = d_v; a.C = C;
+  a.L = L;
+  a.workspace = workspace;
+  hipEvent_t ev[ll::kGdnStages + 1];
+  if (events)
+    for (int i = 0; i <= ll::kGdnStages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);
+  const hipError_t err = e->launch(a, static_cast<hipStream_t>(stream), events ? ev : nullptr);
+  return err == hipSuccess ? LL_OK : LL_ERR_HIP;
+}
 }  // namespace
 
 extern "C" {
@@ -130,26 +157,19 @@ ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, cons
 ll_status ll_gdn_fwd(const void* q, const void* k, const void* v, const float* log_alpha, const float* beta,
                      const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C,
                      int32_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
-  if (!q || !k || !v || !log_alpha || !beta || !o) return LL_ERR_NULL_ARG;
-  ll_status st = check_shape(B, T, H, d_k, d_v, C);
-  if (st != LL_OK) return st;
-  const ll::GdnEntry* e = find_gdn(dtype, C, d_k, d_v);
-  if (!e) return LL_ERR_UNSUPPORTED;
-  const int64_t N = T / C;
-  const int J = N <= 1 ? 0 : bitlen64(uint64_t(N - 1));
-  const int L = levels_of(T);
-  if (J > ll::kGdnMaxLevels || L > kMaxL || H > 65535 || B > 65535 || B * H * N >= (int64_t(1) << 31))
-    return LL_ERR_UNSUPPORTED;
-  const int64_t need = ll::gdn_workspace(B, T, H, d_k, d_v, C, nullptr);
-  if (!workspace) return LL_ERR_NULL_ARG;
-  if ((int64_t)workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
-  ll::GdnArgs a;
-  a.q = q; a.k = k; a.v = v; a.log_alpha = log_alpha; a.beta = beta; a.lambda = lambda; a.o = o;
-  a.B = B; a.T = T; a.H = H; a.dk = d_k; a.dv = d_v; a.C = C;
-  a.L = L;
-  a.workspace = workspace;
-  hipError_t err = e->launch(a, static_cast<hipStream_t>(stream));
-  return err == hipSuccess ? LL_OK : LL_ERR_HIP;
+  return gdn_impl(q, k, v, log_alpha, beta, lambda, o, B, T, H, d_k, d_v, C, dtype, workspace, workspace_bytes, stream,
+                  nullptr);
+}
+
+ll_status ll_gdn_fwd_staged(const void* q, const void* k, const void* v, const float* log_alpha, const float* beta,
+                            const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v,
+                            int64_t C, int32_t dtype, void* workspace, size_t workspace_bytes, void* stream,
+                            void* const* events) {
+  if (!events) return LL_ERR_NULL_ARG;
+  for (int i = 0; i <= ll::kGdnStages; ++i)
+    if (!events[i]) return LL_ERR_NULL_ARG;
+  return gdn_impl(q, k, v, log_alpha, beta, lambda, o, B, T, H, d_k, d_v, C, dtype, workspace, workspace_bytes, stream,
+                  events);
 }
 
 ll_status ll_debug_level_map(int64_t T, int64_t C, int8_t* out, void* stream) {

@@ -7,8 +7,8 @@
 //    convention serves every operand loaded from memory.  The 16x16 fp32 result tile is held
 //    as lane l: column l & 15, rows 4 * (l >> 4) + r for r = 0..3.
 //  * Fenwick level functions (Sec. 3.1 footnote): l(t, s) = bit length of t XOR s for s <= t,
-//    and the chunk-level source group a chunk reads at each inter-chunk level (Sec. 3.3, Eq. 5).
-//  * A wave-wide inclusive prefix sum for the chunk-local cumulative log-gates (Eq. 2).
+//    and the source group a block of tokens reads at each level above it (Sec. 3.3, Eq. 5).
+//  * A wave-wide inclusive prefix sum for the block-local cumulative log-gates (Eq. 2).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -92,25 +92,17 @@ __device__ inline T from_f32(float x) { return static_cast<T>(x); }
 __device__ __host__ inline int bitlen(uint32_t x) { return x ? 32 - __builtin_clz(x) : 0; }
 
 // Level of key position s seen from query position t, both inside one power-of-two-aligned
-// chunk and given as chunk-local indices (i = t mod C, j = s mod C, j <= i).  Because the
-// chunk start is a multiple of C, the global XOR equals the local one.
+// block of P tokens and given as block-local indices (i = t mod P, j = s mod P, j <= i).
+// Because the block start is a multiple of P, the global XOR equals the local one.
 __device__ __host__ inline int level_local(int i, int j) { return bitlen(uint32_t(i ^ j)); }
 
-// Chunk-level source group (Sec. 3.3): chunk z reads an inter-chunk term at chunk level
-// j >= 1 (token level log2(C) + j) iff bit j-1 of z is set; the keys then come from the chunk
-// range [first, first + 2^(j-1)) with first = ((z >> (j-1)) - 1) << (j-1), the 2^(j-1)-chunk
-// block immediately before z's own aligned block.
+// Source group (Sec. 3.3, Eq. 5), for aligned blocks of P = 2^p tokens (chunks in the paper,
+// tiles of 4 chunks here): block z reads a term at block level j >= 1 (token level p + j) iff
+// bit j-1 of z is set; the keys then come from the block range [first, first + 2^(j-1)) with
+// first = ((z >> (j-1)) - 1) << (j-1), the 2^(j-1) blocks immediately before z's own aligned
+// 2^(j-1)-block.
 __device__ __host__ inline bool reads_level(int64_t z, int j) { return (z >> (j - 1)) & 1; }
 __device__ __host__ inline int64_t source_first(int64_t z, int j) { return ((z >> (j - 1)) - 1) << (j - 1); }
-
-// Storage slot of the level-j summary of the source group that starts at chunk `first`
-// (first is a multiple of 2^j): summaries of level j follow those of levels 1..j-1, each
-// level holding ceil(N / 2^j) slots.
-__device__ __host__ inline int64_t node_slot(int64_t N, int j, int64_t first) {
-  int64_t off = 0;
-  for (int jj = 1; jj < j; ++jj) off += (N + (int64_t(1) << jj) - 1) >> jj;
-  return off + (first >> j);
-}
 
 // ------------------------------------------------------------------------- dispatch order
 

@@ -412,8 +412,10 @@ int64_t gdn_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, i
   return cur;
 }
 
+// Enqueues the two stages on `st`.  With `ev` non-null, ev[0] is recorded before the chunk
+// kernel, ev[1] between the kernels and ev[2] after the scan (used by the staged entry point).
 template <int C, int DK, int DV>
-hipError_t launch_gdn(const GdnArgs& a, hipStream_t st) {
+hipError_t launch_gdn(const GdnArgs& a, hipStream_t st, hipEvent_t* ev) {
   GdnLayout w;
   gdn_workspace(a.B, a.T, a.H, DK, DV, C, &w);
   char* base = static_cast<char*>(a.workspace);
@@ -428,17 +430,21 @@ hipError_t launch_gdn(const GdnArgs& a, hipStream_t st) {
   const __bf16* k = static_cast<const __bf16*>(a.k);
   const __bf16* v = static_cast<const __bf16*>(a.v);
   __bf16* o = static_cast<__bf16*>(a.o);
-  if (a.lambda) {
+  if (ev) (void)hipEventRecord(ev[0], st);
+  if (a.lambda)
     hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, true>), g1, dim3(256), 0, st, q, k, v, a.log_alpha, a.beta,
                        a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L);
-    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, true>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz, hz, oin, o, a.T,
-                       (int)a.H, a.L, J);
-  } else {
+  else
     hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, false>), g1, dim3(256), 0, st, q, k, v, a.log_alpha, a.beta,
                        a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L);
-    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, false>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz, hz, oin, o, a.T,
-                       (int)a.H, a.L, J);
-  }
+  if (ev) (void)hipEventRecord(ev[1], st);
+  if (a.lambda)
+    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, true>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz, hz,
+                       oin, o, a.T, (int)a.H, a.L, J);
+  else
+    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, false>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz,
+                       hz, oin, o, a.T, (int)a.H, a.L, J);
+  if (ev) (void)hipEventRecord(ev[2], st);
   return hipGetLastError();
 }
 

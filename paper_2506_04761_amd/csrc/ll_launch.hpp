@@ -62,7 +62,8 @@ struct GdnArgs {
   int L;
   void* workspace;
 };
-typedef hipError_t (*GdnLaunch)(const GdnArgs&, hipStream_t);
+typedef hipError_t (*GdnLaunch)(const GdnArgs&, hipStream_t, hipEvent_t* /* null or 3 events */);
+constexpr int kGdnStages = 2;
 struct GdnEntry {
   int C, dk, dv;
   GdnLaunch launch;

@@ -89,12 +89,9 @@ __device__ inline void tile_cumsum(const float* __restrict__ log_alpha, int64_t 
 }
 
 // Register staging of one 64-row block of a [rows, H, D] tensor, loaded with 16-byte vectors by
-// the NT threads of the workgroup; rows at or beyond `nrow` read as zero.
-// D is the width loaded (elements per row) and LDROW the row length of the tensor in memory.
-//  * RowBlock:  thread-unit = (row, 16-byte column group); stored row-major (store_rows).
-//  * ColBlock:  thread-unit = (pair of rows 2t, 2t+1, 16-byte column group), 32 pairs fastest, so
-//               the transposed store writes one 4-byte word (bf16) or 8-byte pair (fp32) per
-//               column, and the 32 lanes of a half-wave hit 32 consecutive LDS words.
+// the NT threads of the workgroup (thread unit = one row's 16-byte column group, consecutive
+// threads along the row); rows at or beyond `nrow` read as zero.  D is the width loaded
+// (elements per row) and LDROW the row length of the tensor in memory.  Stored row-major.
 template <typename T, int D, int NT, int LDROW = D>
 struct RowBlock {
   static constexpr int VEC = Vec16<T>::N;
@@ -136,49 +133,8 @@ struct RowBlock {
   }
 };
 
-template <typename T, int D, int NT, int LDROW = D>
-struct ColBlock {
-  static constexpr int VEC = Vec16<T>::N;
-  static constexpr int GROUPS = D / VEC;
-  static constexpr int TOTAL = (kKB / 2) * GROUPS;
-  static constexpr int UNITS = (TOTAL + NT - 1) / NT;
-  typename Vec16<T>::type x0[UNITS], x1[UNITS];
-  __device__ inline void load(const T* __restrict__ src, int64_t row0, int r0, int nrow, int H, int h) {
-#pragma unroll
-    for (int i = 0; i < UNITS; ++i) {
-      const int idx = threadIdx.x + NT * i;
-      const int t = 2 * (idx % (kKB / 2)), d0 = (idx / (kKB / 2)) * VEC;
-      x0[i] = typename Vec16<T>::type{};
-      x1[i] = typename Vec16<T>::type{};
-      if (idx < TOTAL && r0 + t < nrow)
-        x0[i] = *reinterpret_cast<const typename Vec16<T>::type*>(src + ((row0 + r0 + t) * H + h) * LDROW + d0);
-      if (idx < TOTAL && r0 + t + 1 < nrow)
-        x1[i] = *reinterpret_cast<const typename Vec16<T>::type*>(src + ((row0 + r0 + t + 1) * H + h) * LDROW + d0);
-    }
-  }
-  // dst[d * ld + t] = x[t][d] * scale[t] (scale only if SCALE); ld must be even
-  template <bool SCALE>
-  __device__ inline void store_cols(T* dst, int ld, const float* scale) const {
-    typedef T T2 __attribute__((ext_vector_type(2)));
-#pragma unroll
-    for (int i = 0; i < UNITS; ++i) {
-      const int idx = threadIdx.x + NT * i;
-      if (idx >= TOTAL) continue;
-      const int t = 2 * (idx % (kKB / 2)), d0 = (idx / (kKB / 2)) * VEC;
-      const float s0 = SCALE ? scale[t] : 1.f, s1 = SCALE ? scale[t + 1] : 1.f;
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        T2 w;
-        w[0] = SCALE ? from_f32<T>(to_f32(x0[i][e]) * s0) : x0[i][e];
-        w[1] = SCALE ? from_f32<T>(to_f32(x1[i][e]) * s1) : x1[i][e];
-        *reinterpret_cast<T2*>(&dst[(d0 + e) * ld + t]) = w;
-      }
-    }
-  }
-};
-
 // ---------------------------------------------------------------------------------------------
-// Kernel 1: block states.  One workgroup (4 waves) per (block of 4 tiles, head, batch).  The K/V
+// Kernel 1: block states.  One workgroup (8 waves) per (block of 4 tiles, head, batch).  The K/V
 // rows of the next 64-row step are loaded into registers while the current step's MFMAs run.
 // ---------------------------------------------------------------------------------------------
 constexpr int kStateThreads = 512;  // block_state workgroup: 8 waves
@@ -440,12 +396,12 @@ __global__ __launch_bounds__(256) void k_block_scan(Nodes<T> nodes, const T* __r
 }
 
 // ---------------------------------------------------------------------------------------------
-// Kernel 3: tile outputs.  RS workgroups (4 waves each) per (tile, head, batch).
+// Kernel 3: tile outputs.  RS workgroups per (tile, head, batch), one wave per 16-row group.
 //
-// Work split: the R tile rows form R/16 groups of 16.  Each wave owns GPW groups, chosen so that
-// every wave does the same share of the causal triangle: with one workgroup per tile, wave w
-// owns groups w, w+4, ...; with two (R = 256), the groups pair up as (x, 15 - x), each pair
-// costing 17 key tiles, and the eight pairs are dealt to the two workgroups.
+// Work split: the R tile rows form R/16 groups of 16, one per wave.  With one workgroup per tile
+// (R <= 128) wave w owns group w; with two (R = 256, 8 waves each) the groups pair up as
+// (x, 15 - x), each pair costing 17 key tiles of the causal triangle, and the eight pairs are
+// dealt to the two workgroups so that both do the same work.
 // Orientation: the waves build O^T (d_v x rows) so that the query index is the MFMA column:
 //   S^T = K Q^T per 16x16 tile (K = d_k), masked in registers with
 //         lambda_i^(bitlen(i XOR j)) * exp2(cl_i - cl_j) for j <= i (tile-local i, j);
