@@ -62,7 +62,7 @@ def stage_figures(w, has_lambda=True):
     BH, BHT = w.B * w.H, w.B * w.H * w.T
     SZ = w.dk * w.dv
     J_chunk = math.log2(w.T // w.C) if w.T > w.C else 0.0
-    R = 4 * w.C                              # tile = 4 chunks
+    R = max(2 * w.C, 64)                     # tile rows
     N = -(-w.T // R)                         # tiles per sequence
     NB = -(-N // 4)                          # 4-tile blocks
     J = (N - 1).bit_length() if N > 1 else 0  # inter-tile levels

@@ -86,7 +86,7 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   const ll::KernelEntry* e = find_mamba2(dtype, C, d_k, d_v);
   if (!e) return LL_ERR_UNSUPPORTED;
   const int L = levels_of(T);
-  const int64_t tiles = (T + 4 * C - 1) / (4 * C);
+  const int64_t tiles = ll::tiles_of(T, C);
   if (L > kMaxL || tiles > kMaxTiles || H > 65535 || B > 65535 || tiles * 2 * H * B >= (int64_t(1) << 31))
     return LL_ERR_UNSUPPORTED;
   const int64_t need = ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), lambda != nullptr, nullptr);

@@ -17,6 +17,9 @@ struct WsLayout {
   int64_t total = 0;
 };
 
+// Tiles of one sequence of length T for chunk size C (the blocks the Mamba-2 kernels summarise).
+int64_t tiles_of(int64_t T, int64_t C);
+
 // Workspace layout of ll_mamba2_fwd; returns the total byte count.
 int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, int64_t esize,
                          bool has_lambda, WsLayout* lay);

@@ -30,7 +30,9 @@
 
 namespace ll {
 
-constexpr int kTileChunks = 4;    // chunks per tile
+// Tile rows R: two chunks (C >= 32), at least 64 tokens.  Levels up to log2 R are computed densely
+// inside a tile, the ones above from summaries of whole tiles.
+__host__ __device__ constexpr int tile_rows(int C) { return 2 * C >= 64 ? 2 * C : 64; }
 constexpr int kBlockTiles = 4;    // tiles per block_state workgroup
 constexpr int kKB = 64;           // keys staged in LDS at a time
 constexpr int kMaxLevels = 24;    // Fenwick levels handled (T <= 2^23)
@@ -145,7 +147,7 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
                                                      T* __restrict__ tiles, float* __restrict__ tot2_out,
                                                      int64_t Tlen, int H) {
   using M = Mfma<T>;
-  constexpr int R = kTileChunks * C;
+  constexpr int R = tile_rows(C);
   constexpr int LDV = DV + 16;   // row strides of the row-major V and (decay * K) tiles
   constexpr int LDK = DK + 16;
   constexpr int MT = DV / 16, NT = DK / 16;
@@ -432,13 +434,13 @@ struct RowMap {
 };
 
 template <typename T, int C, int DK, int DV, bool HAS_LAMBDA>
-__global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
+__global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ log_alpha,
     const float* __restrict__ lam, Nodes<T> nodes, const T* __restrict__ running, const float* __restrict__ gaps2,
     T* __restrict__ o, int64_t Tlen, int H, int L, int J) {
   using M = Mfma<T>;
   typedef typename Vec16<T>::type V16;
-  constexpr int R = kTileChunks * C;
+  constexpr int R = tile_rows(C);
   constexpr int LOG2R = (R == 64) ? 6 : (R == 128) ? 7 : (R == 256) ? 8 : 9;
   constexpr int VEC = Vec16<T>::N;
   constexpr int LDK = DK + VEC;     // K and U row stride (elements)
@@ -659,6 +661,334 @@ __global__ __launch_bounds__(RowMap<kTileChunks * C>::NT, 4) void k_tile_out(
 }
 
 // ---------------------------------------------------------------------------------------------
+// Kernel 3, bf16 tiles of R = 128 rows (C = 64): tile outputs with the tile's K and V resident
+// in LDS.  One workgroup of 4 waves per (tile, head, batch).
+//
+// Wave w owns the 16-row groups w and 7 - w (32 rows): each wave covers 9 of the 36 key tiles of
+// the causal triangle and 32 rows of every inter-tile level, and every K, V or summary fragment
+// it reads from LDS feeds two MFMAs (one per group).  Orientation as in k_tile_out (O^T built
+// with the query index as the MFMA column).
+//
+// K, V and the level summaries are copied straight from global memory into LDS
+// (global_load_lds_dwordx4: lane l of a wave instruction writes bytes 16 l .. 16 l + 15 of a 1 KiB
+// span), into row-major tiles whose 16-byte chunks are XOR-swizzled by row: chunk c of row r sits
+// at position c ^ (r mod chunks-per-row), so a fragment read down 16 consecutive rows touches 16
+// different chunk positions.  With the whole tile resident, the intra-tile phase runs without a
+// barrier; the inter-tile levels alternate between the K and V regions, the next level's summary
+// being copied in while the current one is used.
+// ---------------------------------------------------------------------------------------------
+constexpr int kFastRows = 128;
+constexpr int kFastThreads = 256;
+
+// Element offset of 16-byte chunk c of row r in a swizzled row-major bf16 tile of D columns.
+template <int D>
+__device__ inline int swz(int r, int c) {
+  return r * D + ((c ^ (r & (D / 8 - 1))) << 3);
+}
+
+// Copies ROWS rows of D bf16 elements (row r at src + r * stride) into the swizzled LDS tile
+// `dst` by direct global->LDS loads, one 1 KiB span per wave instruction, spans dealt to the NT/64
+// waves in turn.  Rows at or beyond `nrow` are filled from row nrow - 1 (callers never read
+// them).  The copy is complete once the issuing wave has waited for its vector-memory operations.
+template <int D, int ROWS, int NT>
+__device__ inline void lds_copy_rows(__bf16* dst, const __bf16* __restrict__ src, int64_t stride, int nrow) {
+  constexpr int CH = D / 8;      // chunks per row
+  constexpr int RPI = NT / CH;   // rows per pass of all waves
+  static_assert(NT % CH == 0 && RPI % CH == 0 && ROWS % RPI == 0, "whole rows per pass");
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int q0 = wave * 64 + lane;                     // chunk position in the first pass
+  const int r0 = q0 / CH, c = (q0 % CH) ^ (r0 & (CH - 1));  // the swizzle repeats every pass
+#pragma unroll
+  for (int it = 0; it < ROWS / RPI; ++it) {
+    const int r = r0 + it * RPI;
+    const int rs = r < nrow ? r : nrow - 1;
+    __builtin_amdgcn_global_load_lds(src + rs * stride + c * 8,
+                                     (__attribute__((address_space(3))) void*)(dst + (it * NT + wave * 64) * 8), 16, 0,
+                                     0);
+  }
+}
+
+// Copies lambda of the tile's rows into dst[r * kMaxLevels + l] (l < L; the other slots receive
+// copies of valid entries and are never read) by direct global->LDS loads of one float per lane.
+template <int ROWS, int NT>
+__device__ inline void lds_copy_lambda(float* dst, const float* __restrict__ lam, int64_t row0, int H, int h, int L,
+                                       int nrow) {
+  constexpr int TOTAL = ROWS * kMaxLevels;
+  static_assert(TOTAL % NT == 0, "whole passes");
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+#pragma unroll
+  for (int it = 0; it < TOTAL / NT; ++it) {
+    const int pos = it * NT + wave * 64 + lane;
+    const int r = pos / kMaxLevels, l = pos % kMaxLevels;
+    const int rs = r < nrow ? r : nrow - 1, ls = l < L ? l : L - 1;
+    __builtin_amdgcn_global_load_lds(lam + ((row0 + rs) * H + h) * L + ls,
+                                     (__attribute__((address_space(3))) void*)(dst + it * NT + wave * 64), 4, 0, 0);
+  }
+}
+
+// bf16 MFMA operand fragment down the rows of a swizzled tile (as frag_down_rows).
+template <int D>
+__device__ inline bf16x8 frag_down_rows_swz(const __bf16* m, int row0, int col0) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+  const int r = row0 + 4 * g + (i >> 2), col = col0 + 4 * (i & 3);
+  const bf16x4 lo = lds_read_tr(m + swz<D>(r, col >> 3) + (col & 7));
+  const bf16x4 hi = lds_read_tr(m + swz<D>(r + 16, col >> 3) + (col & 7));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// bf16 MFMA operand fragment along a row of a swizzled tile: row row0 + (lane % 16), the 8
+// elements starting at column 8 * chunk0 + 8 * (lane / 16).
+template <int D>
+__device__ inline bf16x8 frag_along_row_swz(const __bf16* m, int row0, int chunk0) {
+  const int lane = threadIdx.x & 63;
+  return *reinterpret_cast<const bf16x8*>(m + swz<D>(row0 + (lane & 15), chunk0 + (lane >> 4)));
+}
+
+// Waits for this wave's outstanding vector-memory operations (including direct-to-LDS loads).
+__device__ inline void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
+
+template <int DK, int DV, bool HAS_LAMBDA>
+__global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
+    const float* __restrict__ log_alpha, const float* __restrict__ lam, Nodes<__bf16> nodes,
+    const __bf16* __restrict__ running, const float* __restrict__ gaps2, __bf16* __restrict__ o, int64_t Tlen,
+    int H, int L, int J) {
+  using M = Mfma<__bf16>;
+  typedef __bf16 bf;
+  typedef typename M::frag frag;
+  constexpr int R = kFastRows, LOG2R = 7;
+  constexpr int NT = kFastThreads;
+  constexpr int MT = DV / 16, KS = DK / M::KSTEP, KC = M::KSTEP / 8;  // KC: 16-byte chunks per k step
+  constexpr int SZ = DK * DV;
+  static_assert(DK <= R && DV <= R, "a summary must fit in the K and in the V region");
+  __shared__ bf k_s[R * DK];
+  __shared__ bf v_s[R * DV];
+  __shared__ float lam_s[HAS_LAMBDA ? R * kMaxLevels : 1];
+  __shared__ float cl_s[R];
+  __shared__ float kdec_s[R];
+  __shared__ float wsum_s[4];
+
+  const int64_t N = (Tlen + R - 1) / R;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // logical order (b, h, u)
+  const int u = (int)(work % N);
+  const int64_t bh = work / N;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t row0 = (int64_t)b * Tlen + (int64_t)u * R;
+  const int nrow = (int)((Tlen - (int64_t)u * R) < R ? (Tlen - (int64_t)u * R) : R);
+  const int gA = wave, gB = 7 - wave;          // this wave's 16-row groups
+  const int iA = 16 * gA + r16, iB = 16 * gB + r16;
+  const bool liveB = 16 * gB < nrow;           // nrow is a multiple of C = 64
+
+  // ---- loads: gates first (needed first), then Q into registers, then K, V, lambda into LDS
+  const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);
+  frag qA[KS], qB[KS];
+  {
+    const int rA = iA < nrow ? iA : nrow - 1, rB = iB < nrow ? iB : nrow - 1;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      qA[ks] = M::load(q + ((row0 + rA) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
+      qB[ks] = M::load(q + ((row0 + rB) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
+    }
+  }
+  lds_copy_rows<DK, R, NT>(k_s, k + (row0 * H + h) * DK, (int64_t)H * DK, nrow);
+  lds_copy_rows<DV, R, NT>(v_s, v + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
+  if constexpr (HAS_LAMBDA) lds_copy_lambda<R, NT>(lam_s, lam, row0, H, h, L, nrow);
+  tile_cumsum_of<R>(la, cl_s, wsum_s);
+  for (int r = tid; r < R; r += NT) kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
+  wait_vmem();
+  __syncthreads();  // K, V, lambda, kdec visible
+  if (!liveB) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qB[ks] = frag{};  // rows past the end contribute nothing
+  }
+
+  // ---- intra-tile: causal 128 x 128 masked contraction, 32 keys per step, no barrier.  The
+  //      body is instantiated per wave (groups GA = wave, GB = 7 - wave known at compile time),
+  //      so that every skipped key tile and every mask case is resolved statically.
+  const float cliA = cl_s[iA], cliB = cl_s[iB];
+  const float* lrowA = &lam_s[HAS_LAMBDA ? iA * kMaxLevels : 0];
+  const float* lrowB = &lam_s[HAS_LAMBDA ? iB * kMaxLevels : 0];
+  f32x4 oA[MT], oB[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) oA[mt] = oB[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // weights of the diagonal 16 x 16 tile (keys 16 gi + 4g + r): decay and lambda of the level
+  // bitlen(r16 ^ (4g + r)); zero above the diagonal
+  auto diag_weights = [&](int gi, float cli, const float* lrow) {
+    f32x4 w;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int jl = 4 * g + r;
+      float x = fast_exp2(fminf(cli - cl_s[16 * gi + jl], 0.f));
+      if constexpr (HAS_LAMBDA) x *= lrow[bitlen(uint32_t(r16 ^ jl))];
+      w[r] = jl <= r16 ? x : 0.f;
+    }
+    return w;
+  };
+  // off-diagonal key tile KT < gi: one level for the whole tile, decay split at its last key
+  auto offdiag = [&](f32x4 sacc, int KT, int gi, float cli, const float* lrow) {
+    float qs = fast_exp2(cli - cl_s[16 * KT + 15]);
+    if constexpr (HAS_LAMBDA) qs *= lrow[4 + bitlen(uint32_t(gi ^ KT))];
+    const f32x4 kd = *reinterpret_cast<const f32x4*>(&kdec_s[16 * KT + 4 * g]);
+    f32x4 p;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) p[r] = sacc[r] * qs * kd[r];
+    return p;
+  };
+
+  auto intra = [&](auto wave_c) {
+    constexpr int GA = decltype(wave_c)::value, GB = 7 - GA;
+    const f32x4 wdA = diag_weights(GA, cliA, lrowA), wdB = diag_weights(GB, cliB, lrowB);
+    auto mask = [&](f32x4 sacc, auto kt_c, auto gi_c, float cli, const float* lrow, f32x4 wd) {
+      constexpr int KT = decltype(kt_c)::value, GI = decltype(gi_c)::value;
+      if constexpr (KT < GI) {
+        return offdiag(sacc, KT, GI, cli, lrow);
+      } else if constexpr (KT == GI) {
+        f32x4 p;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) p[r] = sacc[r] * wd[r];
+        return p;
+      } else {
+        return f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    };
+    auto step = [&](auto st_c) {
+      constexpr int ST = decltype(st_c)::value, KT0 = 2 * ST, KT1 = 2 * ST + 1;
+      constexpr bool B0 = KT0 <= GB, B1 = KT1 <= GB, A0 = KT0 <= GA, A1 = KT1 <= GA;
+      if constexpr (B0) {  // GB > GA: group B reaches every key tile group A does
+        f32x4 sA0 = {0.f, 0.f, 0.f, 0.f}, sA1 = sA0, sB0 = sA0, sB1 = sA0;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const frag k0 = frag_along_row_swz<DK>(k_s, 16 * KT0, ks * KC);
+          sB0 = M::mma(k0, qB[ks], sB0);
+          if constexpr (A0) sA0 = M::mma(k0, qA[ks], sA0);
+          if constexpr (B1) {
+            const frag k1 = frag_along_row_swz<DK>(k_s, 16 * KT1, ks * KC);
+            sB1 = M::mma(k1, qB[ks], sB1);
+            if constexpr (A1) sA1 = M::mma(k1, qA[ks], sA1);
+          }
+        }
+        // P^T fragments: slots 0-3 <- key tile KT0 rows 4g..4g+3, slots 4-7 <- key tile KT1
+        frag pA, pB;
+        {
+          using K0 = std::integral_constant<int, KT0>;
+          using K1 = std::integral_constant<int, KT1>;
+          using CA = std::integral_constant<int, GA>;
+          using CB = std::integral_constant<int, GB>;
+          const f32x4 m0 = mask(sB0, K0{}, CB{}, cliB, lrowB, wdB), m1 = mask(sB1, K1{}, CB{}, cliB, lrowB, wdB);
+          const f32x4 n0 = mask(sA0, K0{}, CA{}, cliA, lrowA, wdA), n1 = mask(sA1, K1{}, CA{}, cliA, lrowA, wdA);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            pB[r] = from_f32<bf>(m0[r]);
+            pB[4 + r] = from_f32<bf>(m1[r]);
+            pA[r] = from_f32<bf>(n0[r]);
+            pA[4 + r] = from_f32<bf>(n1[r]);
+          }
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const frag vf = frag_down_rows_swz<DV>(v_s, ST * 32, mt * 16);
+          oB[mt] = M::mma(vf, pB, oB[mt]);
+          if constexpr (A0) oA[mt] = M::mma(vf, pA, oA[mt]);
+        }
+      }
+    };
+    step(std::integral_constant<int, 0>{});
+    step(std::integral_constant<int, 1>{});
+    step(std::integral_constant<int, 2>{});
+    step(std::integral_constant<int, 3>{});
+  };
+  switch (wave) {
+    case 0: intra(std::integral_constant<int, 0>{}); break;
+    case 1: intra(std::integral_constant<int, 1>{}); break;
+    case 2: intra(std::integral_constant<int, 2>{}); break;
+    default: intra(std::integral_constant<int, 3>{}); break;
+  }
+
+  // ---- inter-tile levels (set bits of u): summaries alternate between the K and V regions
+  auto level_src = [&](int j, float* gap) -> const bf* {
+    if constexpr (HAS_LAMBDA) {
+      *gap = gaps2[(bh * N + u) * J + (j - 1)];
+      return nodes.at(bh, N, j, source_first(u, j), SZ);
+    } else {
+      *gap = 0.f;
+      return running + (bh * N + u) * SZ;
+    }
+  };
+  auto next_level = [&](int j) {
+    if constexpr (HAS_LAMBDA) {
+      for (++j; j <= J; ++j)
+        if (reads_level(u, j)) return j;
+      return 0;
+    } else {
+      return (j == 0 && u > 0) ? 1 : 0;
+    }
+  };
+  // One level from `cur` (already being copied in); the next level's summary goes to `nxt`.
+  auto level_step = [&](int& j, float& gap, const bf* cur, bf* nxt) {
+    wait_vmem();
+    __syncthreads();  // `cur` complete and visible; every wave is done with `nxt`
+    const int jn = next_level(j);
+    float gap_n = 0.f;
+    if (jn) lds_copy_rows<DK, DV, NT>(nxt, level_src(jn, &gap_n), DK, DV);
+    float wA = fast_exp2(cliA + gap), wB = fast_exp2(cliB + gap);
+    if constexpr (HAS_LAMBDA) {
+      wA *= lrowA[LOG2R + j];
+      wB *= lrowB[LOG2R + j];
+    }
+    // summary fragments read one 16-row block ahead of their use
+    frag uf[2][KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) uf[0][ks] = frag_along_row_swz<DK>(cur, 0, ks * KC);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      if (mt + 1 < MT) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) uf[(mt + 1) & 1][ks] = frag_along_row_swz<DK>(cur, 16 * (mt + 1), ks * KC);
+      }
+      f32x4 tA = {0.f, 0.f, 0.f, 0.f}, tB = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        tA = M::mma(uf[mt & 1][ks], qA[ks], tA);
+        tB = M::mma(uf[mt & 1][ks], qB[ks], tB);
+      }
+      oA[mt] += wA * tA;
+      oB[mt] += wB * tB;
+    }
+    j = jn;
+    gap = gap_n;
+  };
+
+  int j = next_level(0);
+  float gap = 0.f;
+  __syncthreads();  // every wave is done with K and V
+  if (j) lds_copy_rows<DK, DV, NT>(k_s, level_src(j, &gap), DK, DV);
+  while (j) {
+    level_step(j, gap, k_s, v_s);
+    if (!j) break;
+    level_step(j, gap, v_s, k_s);
+  }
+
+  // ---- store O: lane holds rows iA, iB, d_v entries 16 mt + 4g .. +3
+  auto store_rows = [&](const f32x4* acc, int i) {
+    bf* orow = o + ((row0 + i) * H + h) * DV + 4 * g;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      bf16x4 val;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) val[r] = from_f32<bf>(acc[mt][r]);
+      *reinterpret_cast<bf16x4*>(orow + mt * 16) = val;
+    }
+  };
+  if (iA < nrow) store_rows(oA, iA);
+  if (liveB) store_rows(oB, iB);
+}
+
+// ---------------------------------------------------------------------------------------------
 // Debug level map: the level each (t, s) pair receives from the device functions the kernels use.
 // ---------------------------------------------------------------------------------------------
 __global__ void k_debug_level_map(int64_t Tlen, int R, int log2R, int J, int8_t* out) {
@@ -685,7 +1015,7 @@ __global__ void k_debug_level_map(int64_t Tlen, int R, int log2R, int J, int8_t*
 // ---------------------------------------------------------------------------------------------
 static int bitlen_h(uint64_t x) { return x ? 64 - __builtin_clzll(x) : 0; }
 
-int64_t tiles_of(int64_t T, int64_t C) { return (T + kTileChunks * C - 1) / (kTileChunks * C); }
+int64_t tiles_of(int64_t T, int64_t C) { return (T + tile_rows((int)C) - 1) / tile_rows((int)C); }
 
 int tile_levels(int64_t T, int64_t C) {
   const int64_t N = tiles_of(T, C);
@@ -752,7 +1082,8 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
   }
   const dim3 gblk((unsigned)(w.nb * a.H * a.B));
   const dim3 gscan((unsigned)((SZ / 2 + 255) / 256 + 1), (unsigned)(a.B * a.H));
-  const dim3 gtile((unsigned)(w.N * RowMap<kTileChunks * C>::RS * a.H * a.B));
+  constexpr bool kFast = std::is_same<T, __bf16>::value && tile_rows(C) == kFastRows;
+  const dim3 gtile((unsigned)(w.N * (kFast ? 1 : RowMap<tile_rows(C)>::RS) * a.H * a.B));
   if (ev) (void)hipEventRecord(ev[0], st);
   if (a.lambda)
     hipLaunchKernelGGL((k_block_state<T, C, DK, DV, true>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
@@ -765,20 +1096,31 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
                      running, (const float*)tot2,
                      gaps2, w.N, w.J, SZ, a.lambda != nullptr ? 1 : 0);
   if (ev) (void)hipEventRecord(ev[2], st);
-  if (a.lambda)
-    hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, true>), gtile, dim3(RowMap<kTileChunks * C>::NT), 0, st, (const T*)a.q, (const T*)a.k,
-                       (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (const float*)gaps2,
-                       (T*)a.o, a.T, (int)a.H, a.L, w.J);
-  else
-    hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, false>), gtile, dim3(RowMap<kTileChunks * C>::NT), 0, st, (const T*)a.q, (const T*)a.k,
-                       (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (const float*)gaps2,
-                       (T*)a.o, a.T, (int)a.H, a.L, w.J);
+  if constexpr (kFast) {
+    if (a.lambda)
+      hipLaunchKernelGGL((k_tile_out_fast<DK, DV, true>), gtile, dim3(kFastThreads), 0, st, (const T*)a.q,
+                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running,
+                         (const float*)gaps2, (T*)a.o, a.T, (int)a.H, a.L, w.J);
+    else
+      hipLaunchKernelGGL((k_tile_out_fast<DK, DV, false>), gtile, dim3(kFastThreads), 0, st, (const T*)a.q,
+                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running,
+                         (const float*)gaps2, (T*)a.o, a.T, (int)a.H, a.L, w.J);
+  } else {
+    if (a.lambda)
+      hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, true>), gtile, dim3(RowMap<tile_rows(C)>::NT), 0, st, (const T*)a.q,
+                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running,
+                         (const float*)gaps2, (T*)a.o, a.T, (int)a.H, a.L, w.J);
+    else
+      hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, false>), gtile, dim3(RowMap<tile_rows(C)>::NT), 0, st, (const T*)a.q,
+                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running,
+                         (const float*)gaps2, (T*)a.o, a.T, (int)a.H, a.L, w.J);
+  }
   if (ev) (void)hipEventRecord(ev[3], st);
   return hipGetLastError();
 }
 
 hipError_t launch_debug_level_map(int64_t T, int64_t C, int8_t* out, hipStream_t st) {
-  const int R = kTileChunks * (int)C;
+  const int R = tile_rows((int)C);
   hipLaunchKernelGGL(k_debug_level_map, dim3((unsigned)T), dim3(256), 0, st, T, R, bitlen_h(uint64_t(R)) - 1,
                      tile_levels(T, C), out);
   return hipGetLastError();
