@@ -137,7 +137,9 @@ struct RowBlock {
 
 // ---------------------------------------------------------------------------------------------
 // Kernel 1: block states.  One workgroup (8 waves) per (block of 4 tiles, head, batch).  The K/V
-// rows of the next 64-row step are loaded into registers while the current step's MFMAs run.
+// rows of the 64-row steps are loaded into registers two steps ahead of their use (two register
+// buffers, across tile boundaries), the next tile's gates one tile ahead.  Finished summaries
+// are staged in LDS and written with 16-byte stores.
 // ---------------------------------------------------------------------------------------------
 constexpr int kStateThreads = 512;  // block_state workgroup: 8 waves
 
@@ -147,6 +149,7 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
                                                      T* __restrict__ tiles, float* __restrict__ tot2_out,
                                                      int64_t Tlen, int H) {
   using M = Mfma<T>;
+  typedef typename Vec16<T>::type V16;
   constexpr int R = tile_rows(C);
   constexpr int LDV = DV + 16;   // row strides of the row-major V and (decay * K) tiles
   constexpr int LDK = DK + 16;
@@ -156,9 +159,11 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
   constexpr int WN = (NW / WM) < NT ? (NW / WM) : NT;            // waves along n
   constexpr int TM = MT / WM, TN = NT / WN;                      // 16x16 tiles per wave
   constexpr int SZ = DK * DV;
+  constexpr int VEC = Vec16<T>::N;
   constexpr int STEPS = R / kKB;                                 // 64-row steps per tile
   __shared__ T v_s[kKB * LDV];   // V rows of the current 64-row step
   __shared__ T k_s[kKB * LDK];   // decay * K rows
+  __shared__ T out_s[2][SZ];     // summaries on their way out ([p][n], d_v x d_k)
   __shared__ float cl_s[R];
   __shared__ float dec_s[R];
   __shared__ float wsum_s[4];
@@ -169,92 +174,38 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
   const int blk = (int)(work % NB);
   const int64_t bh = work / NB;
   const int h = (int)(bh % H), b = (int)(bh / H);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool active = wave < WM * WN;
   const int wm = wave / WN, wn = wave % WN;
   const int64_t u0 = (int64_t)blk * kBlockTiles;
   const int ntile = (int)((N - u0) < kBlockTiles ? (N - u0) : kBlockTiles);
-
-  RowBlock<T, DK, kStateThreads> kr;
-  RowBlock<T, DV, kStateThreads> vr;
+  const int nsteps = ntile * STEPS;
   auto nrow_of = [&](int64_t u) { return (int)((Tlen - u * R) < R ? (Tlen - u * R) : R); };
-  kr.load(k, (int64_t)b * Tlen + u0 * R, 0, nrow_of(u0), H, h);
-  vr.load(v, (int64_t)b * Tlen + u0 * R, 0, nrow_of(u0), H, h);
+  auto tile_row0 = [&](int64_t u) { return (int64_t)b * Tlen + u * R; };
 
-  f32x4 run[TM][TN];
+  RowBlock<T, DK, kStateThreads> kr0, kr1;
+  RowBlock<T, DV, kStateThreads> vr0, vr1;
+  auto load_step = [&](int s, RowBlock<T, DK, kStateThreads>& kr, RowBlock<T, DV, kStateThreads>& vr) {
+    if (s >= nsteps) return;
+    const int64_t u = u0 + s / STEPS;
+    const int kb = s % STEPS;
+    kr.load(k, tile_row0(u), kb * kKB, nrow_of(u), H, h);
+    vr.load(v, tile_row0(u), kb * kKB, nrow_of(u), H, h);
+  };
+  float la_next = tile_gate<R>(log_alpha, tile_row0(u0), nrow_of(u0), H, h);
+  load_step(0, kr0, vr0);
+  load_step(1, kr1, vr1);
+
+  f32x4 run[TM][TN], acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int jn = 0; jn < TN; ++jn) run[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int jn = 0; jn < TN; ++jn) run[i][jn] = acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float tot = 0.f;
 
-  for (int a = 0; a < ntile; ++a) {
-    const int64_t u = u0 + a;
-    const int64_t row0 = (int64_t)b * Tlen + u * R;
-    const int nrow = nrow_of(u);
-    tile_cumsum<R>(log_alpha, row0, nrow, H, h, cl_s, wsum_s);
-    const float tot = cl_s[R - 1];
-    for (int r = tid; r < R; r += kStateThreads) dec_s[r] = r < nrow ? fast_exp2(tot - cl_s[r]) : 0.f;
-
-    f32x4 acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int jn = 0; jn < TN; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    for (int kb = 0; kb < STEPS; ++kb) {
-      __syncthreads();  // previous step's readers done; dec_s visible
-      vr.store_rows(v_s, LDV);
-      kr.store_rows_scaled(k_s, LDK, dec_s + kb * kKB);
-      __syncthreads();
-      // prefetch the next step (next 64 rows of this tile, or the first rows of the next tile)
-      if (kb + 1 < STEPS) {
-        kr.load(k, row0, (kb + 1) * kKB, nrow, H, h);
-        vr.load(v, row0, (kb + 1) * kKB, nrow, H, h);
-      } else if (a + 1 < ntile) {
-        kr.load(k, row0 + R, 0, nrow_of(u + 1), H, h);
-        vr.load(v, row0 + R, 0, nrow_of(u + 1), H, h);
-      }
-      if (active) {
-        // S^T[p][n] += sum_t V[t][p] (dK)[t][n]: both operands read down the token rows
-#pragma unroll
-        for (int ks = 0; ks < kKB / M::KSTEP; ++ks) {
-          typename M::frag bf[TN];
-#pragma unroll
-          for (int jn = 0; jn < TN; ++jn) {
-            const int n0 = (wn * TN + jn) * 16;
-            if constexpr (M::KPL == 8) bf[jn] = frag_down_rows(k_s, LDK, ks * 32, n0);
-            else bf[jn] = k_s[(ks * 4 + g) * LDK + n0 + r16];
-          }
-#pragma unroll
-          for (int i = 0; i < TM; ++i) {
-            const int p0 = (wm * TM + i) * 16;
-            typename M::frag af;
-            if constexpr (M::KPL == 8) af = frag_down_rows(v_s, LDV, ks * 32, p0);
-            else af = v_s[(ks * 4 + g) * LDV + p0 + r16];
-#pragma unroll
-            for (int jn = 0; jn < TN; ++jn) acc[i][jn] = M::mma(af, bf[jn], acc[i][jn]);
-          }
-        }
-      }
-    }
-
-    if (tid == 0) tot2_out[bh * N + u] = tot;
-    if (!active) continue;
-    // Fold the tile state into the block's summaries and store the ones readers need.
-    T* dst0 = nullptr;
-    T* dst1 = nullptr;
-    if constexpr (HAS_LAMBDA) {
-      const float e = exp2f(tot);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int jn = 0; jn < TN; ++jn) run[i][jn] = run[i][jn] * e + acc[i][jn];
-      if ((a & 1) == 0) dst0 = nodes.at(bh, N, 1, u, SZ);                // even tile: its own state
-      if (a == 1) dst1 = nodes.at(bh, N, 2, u - 1, SZ);                  // pair summary, tiles 0-1
-      if (a == kBlockTiles - 1) dst1 = nodes.at(bh, N, 3, u - 3, SZ);    // block summary
-    } else {
-      dst0 = tiles + (bh * N + u) * SZ;
-    }
+  // stage a summary (registers of the active waves) in out_s[slot]
+  auto stage = [&](int slot, const f32x4 (&x)[TM][TN]) {
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -262,9 +213,85 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int p = (wm * TM + i) * 16 + 4 * g + r, n = (wn * TN + jn) * 16 + r16;
-          if (dst0) dst0[p * DK + n] = from_f32<T>(acc[i][jn][r]);
-          if (dst1) dst1[p * DK + n] = from_f32<T>(run[i][jn][r]);
+          out_s[slot][p * DK + n] = from_f32<T>(x[i][jn][r]);
         }
+  };
+  auto flush = [&](int slot, T* dst) {
+    for (int idx = tid; idx < SZ / VEC; idx += kStateThreads)
+      *reinterpret_cast<V16*>(dst + idx * VEC) = *reinterpret_cast<const V16*>(&out_s[slot][idx * VEC]);
+  };
+
+  auto step = [&](int s, RowBlock<T, DK, kStateThreads>& kr, RowBlock<T, DV, kStateThreads>& vr) {
+    const int a = s / STEPS, kb = s % STEPS;
+    const int64_t u = u0 + a;
+    const int nrow = nrow_of(u);
+    if (kb == 0) {
+      tile_cumsum_of<R>(la_next, cl_s, wsum_s);  // starts and ends with a barrier
+      if (a + 1 < ntile) la_next = tile_gate<R>(log_alpha, tile_row0(u + 1), nrow_of(u + 1), H, h);
+      tot = cl_s[R - 1];
+      for (int r = tid; r < R; r += kStateThreads) dec_s[r] = r < nrow ? fast_exp2(tot - cl_s[r]) : 0.f;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int jn = 0; jn < TN; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    __syncthreads();  // previous step's readers done; dec_s visible
+    vr.store_rows(v_s, LDV);
+    kr.store_rows_scaled(k_s, LDK, dec_s + kb * kKB);
+    __syncthreads();
+    load_step(s + 2, kr, vr);
+    if (active) {
+      // S^T[p][n] += sum_t V[t][p] (dK)[t][n]: both operands read down the token rows
+#pragma unroll
+      for (int ks = 0; ks < kKB / M::KSTEP; ++ks) {
+        typename M::frag bf[TN];
+#pragma unroll
+        for (int jn = 0; jn < TN; ++jn) {
+          const int n0 = (wn * TN + jn) * 16;
+          if constexpr (M::KPL == 8) bf[jn] = frag_down_rows(k_s, LDK, ks * 32, n0);
+          else bf[jn] = k_s[(ks * 4 + g) * LDK + n0 + r16];
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int p0 = (wm * TM + i) * 16;
+          typename M::frag af;
+          if constexpr (M::KPL == 8) af = frag_down_rows(v_s, LDV, ks * 32, p0);
+          else af = v_s[(ks * 4 + g) * LDV + p0 + r16];
+#pragma unroll
+          for (int jn = 0; jn < TN; ++jn) acc[i][jn] = M::mma(af, bf[jn], acc[i][jn]);
+        }
+      }
+    }
+    if (kb == STEPS - 1) {
+      // tile done: fold it into the block's summaries and write the ones readers need
+      if (tid == 0) tot2_out[bh * N + u] = tot;
+      T* dst0 = nullptr;
+      T* dst1 = nullptr;
+      if constexpr (HAS_LAMBDA) {
+        const float e = fast_exp2(tot);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int jn = 0; jn < TN; ++jn) run[i][jn] = run[i][jn] * e + acc[i][jn];
+        if ((a & 1) == 0) dst0 = nodes.at(bh, N, 1, u, SZ);                // even tile: its own state
+        if (a == 1) dst1 = nodes.at(bh, N, 2, u - 1, SZ);                  // pair summary, tiles 0-1
+        if (a == kBlockTiles - 1) dst1 = nodes.at(bh, N, 3, u - 3, SZ);    // block summary
+      } else {
+        dst0 = tiles + (bh * N + u) * SZ;
+      }
+      if (active) {
+        if (dst0) stage(0, acc);
+        if (dst1) stage(1, run);
+      }
+      __syncthreads();
+      if (dst0) flush(0, dst0);
+      if (dst1) flush(1, dst1);
+    }
+  };
+
+  for (int s = 0; s < nsteps; s += 2) {
+    step(s, kr0, vr0);
+    if (s + 1 < nsteps) step(s + 1, kr1, vr1);
   }
 }
 
@@ -286,112 +313,146 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
 constexpr int kMaxGapTiles = 8192;  // tiles per sequence the scan stages in LDS (T <= 8192 R)
 constexpr int kScanUnroll = 8;      // summary loads in flight per thread
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_block_scan(Nodes<T> nodes, const T* __restrict__ tiles,
-                                                    T* __restrict__ running, const float* __restrict__ tot2,
-                                                    float* __restrict__ gaps2, int64_t N, int J, int SZ,
-                                                    int has_lambda) {
+// Gaps of every (tile, level) of one (b, h): one workgroup, block sums in LDS (see above).
+__device__ inline void scan_gaps(float* dyn_s, const float* __restrict__ tot, float* __restrict__ gaps, int64_t N,
+                                 int J) {
+  const int tid = threadIdx.x;
+  float* bs = dyn_s;  // level k block sums follow level k-1's (level 0 = the tile totals)
+  for (int64_t u = tid; u < N; u += 256) bs[u] = tot[u];
+  __syncthreads();
+  int64_t off_prev = 0, off = N;
+  for (int k = 1; k < J; ++k) {
+    const int64_t len = N >> k;
+    for (int64_t m = tid; m < len; m += 256) bs[off + m] = bs[off_prev + 2 * m] + bs[off_prev + 2 * m + 1];
+    __syncthreads();
+    off_prev = off;
+    off += len;
+  }
+  for (int64_t u = tid; u < N; u += 256) {
+    float gsum = 0.f;
+    int64_t ok = 0;  // offset of the level-(j-2) block sums
+    for (int j = 1; j <= J; ++j) {
+      if (j >= 2) {
+        const int k = j - 2;
+        if ((u >> k) & 1) gsum += bs[ok + (u >> k) - 1];
+        ok += N >> k;
+      }
+      gaps[u * J + (j - 1)] = gsum;
+    }
+  }
+}
+
+// lambda given: grid (element blocks of 512 + 1, B * H).  Each thread owns two state entries and
+// walks the blocks of its (b, h) in order, keeping one accumulator per level >= 4.  JMAX bounds
+// J at compile time so that the unrolled per-block level loop stays short.
+template <typename T, int JMAX>
+__global__ __launch_bounds__(256) void k_level_scan(Nodes<T> nodes, const float* __restrict__ tot2,
+                                                    float* __restrict__ gaps2, int64_t N, int J, int SZ) {
   typedef T T2 __attribute__((ext_vector_type(2)));
-  extern __shared__ float dyn_s[];  // 2 N floats: tile totals, then sums over aligned blocks
+  extern __shared__ float dyn_s[];  // gaps: 2 N floats; summaries: the NB block totals
   const int64_t bh = blockIdx.y;
   const int tid = threadIdx.x;
   const float* tot = tot2 + bh * N;
-  const int64_t NB = (N + kBlockTiles - 1) / kBlockTiles;
-  float* tot_s = dyn_s;
-
-  for (int64_t u = tid; u < N; u += 256) tot_s[u] = tot[u];
-  __syncthreads();
-
   if (blockIdx.x == gridDim.x - 1) {
-    if (!has_lambda || J == 0) return;
-    float* bs = dyn_s;  // level k block sums follow level k-1's (level 0 = the tile totals)
-    int64_t off_prev = 0, off = N;
-    for (int k = 1; k < J; ++k) {
-      const int64_t len = N >> k;
-      for (int64_t m = tid; m < len; m += 256) bs[off + m] = bs[off_prev + 2 * m] + bs[off_prev + 2 * m + 1];
-      __syncthreads();
-      off_prev = off;
-      off += len;
-    }
-    for (int64_t u = tid; u < N; u += 256) {
-      float gsum = 0.f;
-      int64_t ok = 0;  // offset of the level-(j-2) block sums
-      for (int j = 1; j <= J; ++j) {
-        if (j >= 2) {
-          const int k = j - 2;
-          if ((u >> k) & 1) gsum += bs[ok + (u >> k) - 1];
-          ok += N >> k;
-        }
-        gaps2[(bh * N + u) * J + (j - 1)] = gsum;
-      }
-    }
+    if (J > 0) scan_gaps(dyn_s, tot, gaps2 + bh * N * J, N, J);
     return;
   }
+  const int64_t NB = (N + kBlockTiles - 1) / kBlockTiles;
+  float* btot_s = dyn_s;
+  for (int64_t bl = tid; bl < NB; bl += 256) {
+    float t = 0.f;
+    for (int a = 0; a < kBlockTiles; ++a)
+      if (bl * kBlockTiles + a < N) t += tot[bl * kBlockTiles + a];
+    btot_s[bl] = t;
+  }
+  __syncthreads();
+  const int e0 = (blockIdx.x * 256 + tid) * 2;
+  if (J < 4 || e0 >= SZ) return;
 
+  // output slot base of each level: levels 4 .. j-1 come first, ceil(N / 2^jj) slots each
+  int64_t lvl_off[JMAX + 1];
+  {
+    int64_t off = 0;
+#pragma unroll
+    for (int j = 4; j <= JMAX; ++j) {
+      lvl_off[j] = off;
+      if (j <= J) off += (N + (int64_t(1) << j) - 1) >> j;
+    }
+  }
+  T* const up = nodes.upper + bh * nodes.nup * SZ + e0;
+  const T* const src = nodes.blocks + bh * nodes.nb * SZ + e0;
+  float a0[JMAX + 1], a1[JMAX + 1];
+#pragma unroll
+  for (int j = 0; j <= JMAX; ++j) a0[j] = a1[j] = 0.f;
+  for (int64_t bl0 = 0; bl0 < NB; bl0 += kScanUnroll) {
+    T2 sv[kScanUnroll];
+#pragma unroll
+    for (int i = 0; i < kScanUnroll; ++i) {
+      const int64_t bl = bl0 + i < NB ? bl0 + i : NB - 1;
+      sv[i] = *reinterpret_cast<const T2*>(src + bl * SZ);
+    }
+#pragma unroll
+    for (int i = 0; i < kScanUnroll; ++i) {
+      const int64_t bl = bl0 + i;
+      if (bl < NB) {
+        const float e = fast_exp2(btot_s[bl]);
+        const float s0 = to_f32(sv[i][0]), s1 = to_f32(sv[i][1]);
+#pragma unroll
+        for (int j = 4; j <= JMAX; ++j) {
+          // tile level j: source groups of 2^(j-3) blocks, the even-indexed ones
+          const int sh = j - 3;
+          const int64_t m = bl >> sh;
+          if (j <= J && !(m & 1)) {
+            const bool first = (bl & ((int64_t(1) << sh) - 1)) == 0;
+            a0[j] = first ? s0 : a0[j] * e + s0;
+            a1[j] = first ? s1 : a1[j] * e + s1;
+            const bool last = ((bl + 1) & ((int64_t(1) << sh) - 1)) == 0;
+            const int64_t first_tile = (m << sh) * kBlockTiles;
+            if (last && first_tile + (int64_t(1) << (j - 1)) < N) {
+              T2 out;
+              out[0] = from_f32<T>(a0[j]);
+              out[1] = from_f32<T>(a1[j]);
+              *reinterpret_cast<T2*>(up + (lvl_off[j] + (first_tile >> j)) * SZ) = out;
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
+// lambda == NULL: the running state entering each tile, R_0 = 0, R_(u+1) = exp2(tot_u) R_u + S_u.
+template <typename T>
+__global__ __launch_bounds__(256) void k_running_scan(const T* __restrict__ tiles, T* __restrict__ running,
+                                                      const float* __restrict__ tot2, int64_t N, int SZ) {
+  typedef T T2 __attribute__((ext_vector_type(2)));
+  extern __shared__ float dyn_s[];  // the N tile totals
+  const int64_t bh = blockIdx.y;
+  const int tid = threadIdx.x;
+  for (int64_t u = tid; u < N; u += 256) dyn_s[u] = tot2[bh * N + u];
+  __syncthreads();
   const int e0 = (blockIdx.x * 256 + tid) * 2;
   if (e0 >= SZ) return;
-
-  if (!has_lambda) {
-    const T* src = tiles + bh * N * SZ + e0;
-    T* dst = running + bh * N * SZ + e0;
-    float r0 = 0.f, r1 = 0.f;
-    for (int64_t u0 = 0; u0 < N; u0 += kScanUnroll) {
-      T2 sv[kScanUnroll];
+  const T* src = tiles + bh * N * SZ + e0;
+  T* dst = running + bh * N * SZ + e0;
+  float r0 = 0.f, r1 = 0.f;
+  for (int64_t u0 = 0; u0 < N; u0 += kScanUnroll) {
+    T2 sv[kScanUnroll];
 #pragma unroll
-      for (int i = 0; i < kScanUnroll; ++i)
-        if (u0 + i < N) sv[i] = *reinterpret_cast<const T2*>(src + (u0 + i) * SZ);
+    for (int i = 0; i < kScanUnroll; ++i) {
+      const int64_t u = u0 + i < N ? u0 + i : N - 1;
+      sv[i] = *reinterpret_cast<const T2*>(src + u * SZ);
+    }
 #pragma unroll
-      for (int i = 0; i < kScanUnroll; ++i) {
-        if (u0 + i >= N) break;
+    for (int i = 0; i < kScanUnroll; ++i) {
+      if (u0 + i < N) {
         T2 out;
         out[0] = from_f32<T>(r0);
         out[1] = from_f32<T>(r1);
         *reinterpret_cast<T2*>(dst + (u0 + i) * SZ) = out;
-        const float e = fast_exp2(tot_s[u0 + i]);
+        const float e = fast_exp2(dyn_s[u0 + i]);
         r0 = r0 * e + to_f32(sv[i][0]);
         r1 = r1 * e + to_f32(sv[i][1]);
-      }
-    }
-    return;
-  }
-  if (J < 4) return;
-  float a0[kMaxLevels], a1[kMaxLevels];
-#pragma unroll
-  for (int j = 0; j < kMaxLevels; ++j) a0[j] = a1[j] = 0.f;
-  for (int64_t bl0 = 0; bl0 < NB; bl0 += kScanUnroll) {
-    T2 sv[kScanUnroll];
-#pragma unroll
-    for (int i = 0; i < kScanUnroll; ++i)
-      if (bl0 + i < NB) sv[i] = *reinterpret_cast<const T2*>(nodes.at(bh, N, 3, (bl0 + i) * kBlockTiles, SZ) + e0);
-#pragma unroll
-    for (int i = 0; i < kScanUnroll; ++i) {
-      const int64_t bl = bl0 + i;
-      if (bl >= NB) break;
-      float tb = 0.f;
-      for (int a = 0; a < kBlockTiles; ++a)
-        if (bl * kBlockTiles + a < N) tb += tot_s[bl * kBlockTiles + a];
-      const float e = fast_exp2(tb);
-      const float s0 = to_f32(sv[i][0]), s1 = to_f32(sv[i][1]);
-#pragma unroll
-      for (int j = 4; j <= kMaxLevels; ++j) {
-        const int jb = j - 2;
-        const int64_t m = bl >> (jb - 1);
-        if (j > J || (m & 1)) continue;
-        const int64_t mask = (int64_t(1) << (jb - 1)) - 1;
-        if ((bl & mask) == 0) {
-          a0[j - 1] = s0;
-          a1[j - 1] = s1;
-        } else {
-          a0[j - 1] = a0[j - 1] * e + s0;
-          a1[j - 1] = a1[j - 1] * e + s1;
-        }
-        const int64_t first_tile = (m << (jb - 1)) * kBlockTiles;
-        if (((bl + 1) & mask) == 0 && first_tile + (int64_t(1) << (j - 1)) < N) {
-          T2 out;
-          out[0] = from_f32<T>(a0[j - 1]);
-          out[1] = from_f32<T>(a1[j - 1]);
-          *reinterpret_cast<T2*>(nodes.at(bh, N, j, first_tile, SZ) + e0) = out;
-        }
       }
     }
   }
@@ -1092,9 +1153,15 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
     hipLaunchKernelGGL((k_block_state<T, C, DK, DV, false>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
                        a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H);
   if (ev) (void)hipEventRecord(ev[1], st);
-  hipLaunchKernelGGL((k_block_scan<T>), gscan, dim3(256), 2 * w.N * sizeof(float), st, nodes, (const T*)tiles,
-                     running, (const float*)tot2,
-                     gaps2, w.N, w.J, SZ, a.lambda != nullptr ? 1 : 0);
+  if (a.lambda && w.J <= 12)
+    hipLaunchKernelGGL((k_level_scan<T, 12>), gscan, dim3(256), 2 * w.N * sizeof(float), st, nodes,
+                       (const float*)tot2, gaps2, w.N, w.J, SZ);
+  else if (a.lambda)
+    hipLaunchKernelGGL((k_level_scan<T, kMaxLevels>), gscan, dim3(256), 2 * w.N * sizeof(float), st, nodes,
+                       (const float*)tot2, gaps2, w.N, w.J, SZ);
+  else
+    hipLaunchKernelGGL((k_running_scan<T>), dim3(gscan.x - 1, gscan.y), dim3(256), w.N * sizeof(float), st,
+                       (const T*)tiles, running, (const float*)tot2, w.N, SZ);
   if (ev) (void)hipEventRecord(ev[2], st);
   if constexpr (kFast) {
     if (a.lambda)
