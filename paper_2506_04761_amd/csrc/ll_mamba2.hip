@@ -384,13 +384,15 @@ __global__ __launch_bounds__(256) void k_level_scan(Nodes<T> nodes, const float*
   float a0[JMAX + 1], a1[JMAX + 1];
 #pragma unroll
   for (int j = 0; j <= JMAX; ++j) a0[j] = a1[j] = 0.f;
-  for (int64_t bl0 = 0; bl0 < NB; bl0 += kScanUnroll) {
-    T2 sv[kScanUnroll];
+  // batches of kScanUnroll blocks; the next batch's loads are issued before the current one is used
+  auto load_batch = [&](int64_t bl0, T2 (&sv)[kScanUnroll]) {
 #pragma unroll
     for (int i = 0; i < kScanUnroll; ++i) {
       const int64_t bl = bl0 + i < NB ? bl0 + i : NB - 1;
       sv[i] = *reinterpret_cast<const T2*>(src + bl * SZ);
     }
+  };
+  auto use_batch = [&](int64_t bl0, const T2 (&sv)[kScanUnroll]) {
 #pragma unroll
     for (int i = 0; i < kScanUnroll; ++i) {
       const int64_t bl = bl0 + i;
@@ -418,6 +420,15 @@ __global__ __launch_bounds__(256) void k_level_scan(Nodes<T> nodes, const float*
         }
       }
     }
+  };
+  T2 sa[kScanUnroll], sb[kScanUnroll];
+  load_batch(0, sa);
+  for (int64_t bl0 = 0; bl0 < NB; bl0 += 2 * kScanUnroll) {
+    if (bl0 + kScanUnroll < NB) load_batch(bl0 + kScanUnroll, sb);
+    use_batch(bl0, sa);
+    if (bl0 + kScanUnroll >= NB) break;
+    if (bl0 + 2 * kScanUnroll < NB) load_batch(bl0 + 2 * kScanUnroll, sa);
+    use_batch(bl0 + kScanUnroll, sb);
   }
 }
 

@@ -60,6 +60,20 @@ def test_parity_ragged_chunk_counts(chunks, dk, dv):
     assert err <= TOL["bf16"], err
 
 
+@pytest.mark.parametrize("chunks", [5, 7])
+def test_parity_many_heads_short_blocks(chunks):
+    # more (b, h) blocks of 4 tiles than block_state has persistent workgroups, every one of
+    # them short (fewer than 4 tiles): the step pipeline crosses block boundaries with gaps
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=2, H=160, T=64 * chunks, dk=64, dv=64, seed=60 + chunks)
+    x = generate(w)
+    for with_lambda in (True, False):
+        lam = x["lam"] if with_lambda else np.ones_like(x["lam"])
+        ref = mamba2.quadratic(x["q"], x["k"], x["v"], x["log_alpha"], lam)
+        err = rel_err(run_mamba2(x, "bf16", 64, with_lambda=with_lambda), ref)
+        print(f"B=2 H=160 T={w.T} lambda={with_lambda}: rel err {err:.3e}")
+        assert err <= TOL["bf16"], err
+
+
 @pytest.mark.parametrize("T", [16, 48, 256, 1024])
 def test_parity_fp32_small_chunk(T):
     w = WORKLOADS["ll_mamba2_f32_T64"].with_(B=2, H=3, T=T, seed=T)
