@@ -104,6 +104,84 @@ __device__ __host__ inline int level_local(int i, int j) { return bitlen(uint32_
 __device__ __host__ inline bool reads_level(int64_t z, int j) { return (z >> (j - 1)) & 1; }
 __device__ __host__ inline int64_t source_first(int64_t z, int j) { return ((z >> (j - 1)) - 1) << (j - 1); }
 
+// ------------------------------------------------------------------ direct global -> LDS tiles
+//
+// Row-major bf16 tiles whose 16-byte chunks are XOR-swizzled by row (chunk c of row r sits at
+// position c ^ (r mod chunks-per-row)), filled by direct global->LDS loads
+// (global_load_lds_dwordx4: lane l of a wave instruction writes bytes 16 l .. 16 l + 15 of a
+// 1 KiB span).  A fragment read down 16 consecutive rows then touches 16 different positions.
+
+// Element offset of 16-byte chunk c of row r in a swizzled row-major bf16 tile of D columns.
+template <int D>
+__device__ inline int swz(int r, int c) {
+  return r * D + ((c ^ (r & (D / 8 - 1))) << 3);
+}
+
+// Copies ROWS rows of D bf16 elements (row r at src + r * stride) into the swizzled LDS tile
+// `dst` by direct global->LDS loads, one 1 KiB span per wave instruction, spans dealt to the NT/64
+// waves in turn.  Rows at or beyond `nrow` are filled from row nrow - 1 (callers never read
+// them).  The copy is complete once the issuing wave has waited for its vector-memory operations.
+template <int D, int ROWS, int NT>
+__device__ inline void lds_copy_rows(__bf16* dst, const __bf16* __restrict__ src, int64_t stride, int nrow) {
+  constexpr int CH = D / 8;      // chunks per row
+  constexpr int RPI = NT / CH;   // rows per pass of all waves
+  static_assert(NT % CH == 0 && RPI % CH == 0 && ROWS % RPI == 0, "whole rows per pass");
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int q0 = wave * 64 + lane;                     // chunk position in the first pass
+  const int r0 = q0 / CH, c = (q0 % CH) ^ (r0 & (CH - 1));  // the swizzle repeats every pass
+#pragma unroll
+  for (int it = 0; it < ROWS / RPI; ++it) {
+    const int r = r0 + it * RPI;
+    const int rs = r < nrow ? r : nrow - 1;
+    __builtin_amdgcn_global_load_lds(src + rs * stride + c * 8,
+                                     (__attribute__((address_space(3))) void*)(dst + (it * NT + wave * 64) * 8), 16, 0,
+                                     0);
+  }
+}
+
+// bf16 MFMA operand fragment down the rows of a swizzled tile (as frag_down_rows).
+template <int D>
+__device__ inline bf16x8 frag_down_rows_swz(const __bf16* m, int row0, int col0) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+  const int r = row0 + 4 * g + (i >> 2), col = col0 + 4 * (i & 3);
+  const bf16x4 lo = lds_read_tr(m + swz<D>(r, col >> 3) + (col & 7));
+  const bf16x4 hi = lds_read_tr(m + swz<D>(r + 16, col >> 3) + (col & 7));
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// bf16 MFMA operand fragment along a row of a swizzled tile: row row0 + (lane % 16), the 8
+// elements starting at column 8 * chunk0 + 8 * (lane / 16).
+template <int D>
+__device__ inline bf16x8 frag_along_row_swz(const __bf16* m, int row0, int chunk0) {
+  const int lane = threadIdx.x & 63;
+  return *reinterpret_cast<const bf16x8*>(m + swz<D>(row0 + (lane & 15), chunk0 + (lane >> 4)));
+}
+
+// Copies n 16-byte pieces (n a multiple of 64) into LDS, piece q to dst + 16 q bytes, from global
+// addresses src(q), by direct global->LDS loads; the NT/64 waves take 64 pieces in turn.
+template <int NT, typename Src>
+__device__ inline void lds_gather16(void* dst, int n, Src src) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  for (int s0 = wave * 64; s0 < n; s0 += NT)
+    __builtin_amdgcn_global_load_lds(src(s0 + lane),
+                                     (__attribute__((address_space(3))) void*)((char*)dst + s0 * 16), 16, 0, 0);
+}
+
+// As lds_gather16 for 4-byte pieces: piece q to dst + 4 q bytes.
+template <int NT, typename Src>
+__device__ inline void lds_gather4(void* dst, int n, Src src) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  for (int s0 = wave * 64; s0 < n; s0 += NT)
+    __builtin_amdgcn_global_load_lds(src(s0 + lane),
+                                     (__attribute__((address_space(3))) void*)((char*)dst + s0 * 4), 4, 0, 0);
+}
+
+// Waits for this wave's outstanding vector-memory operations (including direct-to-LDS loads).
+__device__ inline void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
+
 // ------------------------------------------------------------------------- dispatch order
 
 // MI355X has 8 XCDs, each with its own L2, and hands out workgroups round-robin over them.

@@ -240,6 +240,9 @@ __global__ __launch_bounds__(256) void k_gdn_chunk(const bf* __restrict__ q, con
 // the chunks.  Wave w owns levels w+1 and w+9; each level state R_j (d_k x 16, fp32)
 // lives in registers in the MFMA result layout (lane: column = lane & 15, rows 16 mt + 4g + r).
 // lambda == NULL: one state, read by every chunk, absorbing every chunk (wave 0).
+// Everything a chunk step reads (P_z, Q~, this slice of H_z and of the intra output, the level
+// weights) is copied into LDS by direct global->LDS loads one chunk ahead, into the other half of
+// double buffers.
 // ---------------------------------------------------------------------------------------------
 template <int C, int DK, int DV, bool HAS_LAMBDA>
 __global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __restrict__ lam, const bf* __restrict__ qc_in,
@@ -248,26 +251,49 @@ __global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __res
                                                   int64_t Tlen, int H, int L, int J) {
   using MF = Mfma<bf>;
   constexpr int LOG2C = (C == 16) ? 4 : (C == 32) ? 5 : 6;
-  constexpr int PD = 8;
-  constexpr int LDD = DK + PD;
   constexpr int MTD = DK / 16;          // 16-row tiles of a state
   constexpr int MTC = C / 16;           // 16-row tiles of a chunk
   constexpr int KS = DK / 32;           // k steps over d_k
   constexpr int NSL = DV / kSlice;
   constexpr int LPW = HAS_LAMBDA ? kMaxJ / kScanWaves : 1;  // level slots per wave
   constexpr int NT = 64 * kScanWaves;
-  __shared__ bf pz_s[DK * LDD];
-  __shared__ bf qc_s[C * LDD];
+  static_assert(kSlice == 16, "one 16-column slice: 2 bf16 / 4 fp32 chunks per row");
+  __shared__ bf pz_s[2][DK * DK];                    // swizzled
+  __shared__ bf qc_s[2][C * DK];                     // swizzled
+  __shared__ bf hz_s[2][DK * kSlice];                // [row][16]
+  __shared__ float oin_s[2][C * kSlice];             // [t][16]
+  __shared__ float lw_s[2][HAS_LAMBDA ? C * kMaxJ : 1];
   __shared__ float part_s[kScanWaves * C * kSlice];
-  __shared__ float lw_s[HAS_LAMBDA ? C * kMaxJ : 1];
 
   const int64_t N = Tlen / C;
   const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // (b, h, slice)
   const int sl = (int)(work % NSL);
   const int64_t bh = work / NSL;
   const int h = (int)(bh % H), b = (int)(bh / H);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int p0 = sl * kSlice;
+
+  // copies of chunk z into buffer half `buf`
+  auto fetch = [&](int64_t z, int buf) {
+    const int64_t cidx = bh * N + z;
+    const int64_t tok0 = (int64_t)b * Tlen + z * C;
+    lds_copy_rows<DK, DK, NT>(pz_s[buf], pz_in + cidx * (DK * DK), DK, DK);
+    lds_copy_rows<DK, C, NT>(qc_s[buf], qc_in + cidx * (C * DK), DK, C);
+    const bf* hs = hz_in + cidx * (DK * DV) + p0;
+    lds_gather16<NT>(hz_s[buf], DK * 2, [&](int q) { return hs + (q >> 1) * DV + (q & 1) * 8; });
+    const float* os = oin_in + cidx * (C * DV) + p0;
+    lds_gather16<NT>(oin_s[buf], C * 4, [&](int q) { return os + (q >> 2) * DV + (q & 3) * 4; });
+    if constexpr (HAS_LAMBDA) {
+      if (J > 0) {  // weights of levels LOG2C + 1 .. LOG2C + J (slots jj >= J repeat level J)
+        const float* ls = lam + (tok0 * H + h) * L + LOG2C + 1;
+        lds_gather4<NT>(lw_s[buf], C * kMaxJ, [&](int q) {
+          const int t = q / kMaxJ, jj = q % kMaxJ;
+          return ls + (int64_t)t * H * L + (jj < J ? jj : J - 1);
+        });
+      }
+    }
+  };
 
   f32x4 R[LPW][MTD];
 #pragma unroll
@@ -275,42 +301,33 @@ __global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __res
 #pragma unroll
     for (int mt = 0; mt < MTD; ++mt) R[m][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  fetch(0, 0);
   for (int64_t z = 0; z < N; ++z) {
-    const int64_t cidx = bh * N + z;
+    const int buf = (int)(z & 1);
     const int64_t tok0 = (int64_t)b * Tlen + z * C;
-    __syncthreads();
-    {
-      const bf* src = pz_in + cidx * (DK * DK);
-      for (int idx = tid; idx < DK * DK / 8; idx += NT) {
-        const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
-        *reinterpret_cast<bf16x8*>(&pz_s[r * LDD + c0]) = *reinterpret_cast<const bf16x8*>(src + r * DK + c0);
-      }
-      const bf* qs = qc_in + cidx * (C * DK);
-      for (int idx = tid; idx < C * DK / 8; idx += NT) {
-        const int r = idx / (DK / 8), c0 = (idx % (DK / 8)) * 8;
-        *reinterpret_cast<bf16x8*>(&qc_s[r * LDD + c0]) = *reinterpret_cast<const bf16x8*>(qs + r * DK + c0);
-      }
-      if constexpr (HAS_LAMBDA) {
-        for (int idx = tid; idx < C * J; idx += NT) {
-          const int t = idx / J, jj = idx % J;
-          lw_s[t * kMaxJ + jj] = lam[((tok0 + t) * H + h) * L + LOG2C + 1 + jj];
-        }
-      }
-    }
-    __syncthreads();
+    wait_vmem();
+    __syncthreads();  // chunk z in LDS; every wave is done with the other half
+    if (z + 1 < N) fetch(z + 1, buf ^ 1);
+    const bf* pzb = pz_s[buf];
+    const bf* qcb = qc_s[buf];
+    // A-operand fragment of a swizzled [rows][DK] tile: row, k slots 0-3 <- columns ks*32 + 4g..,
+    // slots 4-7 <- columns ks*32 + 16 + 4g.. (the layout of the R_j fragments below)
+    auto afrag = [&](const bf* m, int row, int ks) {
+      const int c0 = ks * 32 + 4 * g;
+      const bf16x4 lo = *reinterpret_cast<const bf16x4*>(m + swz<DK>(row, c0 >> 3) + (c0 & 7));
+      const bf16x4 hi = *reinterpret_cast<const bf16x4*>(m + swz<DK>(row, (c0 + 16) >> 3) + (c0 & 7));
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
 
     f32x4 out[MTC];
 #pragma unroll
     for (int mt = 0; mt < MTC; ++mt) out[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
     // this lane's entries of H_z (rows 16 mt + 4g + r, column p0 + r16)
     f32x4 hzv[MTD];
-    {
-      const bf* hs = hz_in + cidx * (DK * DV) + p0 + r16;
 #pragma unroll
-      for (int mt = 0; mt < MTD; ++mt)
+    for (int mt = 0; mt < MTD; ++mt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) hzv[mt][r] = static_cast<float>(hs[(mt * 16 + 4 * g + r) * DV]);
-    }
+      for (int r = 0; r < 4; ++r) hzv[mt][r] = static_cast<float>(hz_s[buf][(mt * 16 + 4 * g + r) * kSlice + r16]);
 
 #pragma unroll
     for (int m = 0; m < LPW; ++m) {
@@ -343,16 +360,11 @@ __global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __res
         for (int mt = 0; mt < MTC; ++mt) {
           f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            const bf* row = &qc_s[(mt * 16 + r16) * LDD + ks * 32 + 4 * g];
-            const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row);
-            const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 16);
-            tmp = MF::mma(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), rb[ks], tmp);
-          }
+          for (int ks = 0; ks < KS; ++ks) tmp = MF::mma(afrag(qcb, mt * 16 + r16, ks), rb[ks], tmp);
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = mt * 16 + 4 * g + r;
-            const float wgt = HAS_LAMBDA ? lw_s[t * kMaxJ + (j - 1)] : 1.f;
+            const float wgt = HAS_LAMBDA ? lw_s[buf][t * kMaxJ + (j - 1)] : 1.f;
             out[mt][r] += wgt * tmp[r];
           }
         }
@@ -365,12 +377,7 @@ __global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __res
         for (int mt = 0; mt < MTD; ++mt) {
           f32x4 acc = source ? hzv[mt] : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            const bf* row = &pz_s[(mt * 16 + r16) * LDD + ks * 32 + 4 * g];
-            const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row);
-            const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 16);
-            acc = MF::mma(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), rb[ks], acc);
-          }
+          for (int ks = 0; ks < KS; ++ks) acc = MF::mma(afrag(pzb, mt * 16 + r16, ks), rb[ks], acc);
           R[m][mt] = acc;
         }
       }
@@ -382,10 +389,9 @@ __global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __res
 #pragma unroll
       for (int r = 0; r < 4; ++r) part_s[(wave * C + mt * 16 + 4 * g + r) * kSlice + r16] = out[mt][r];
     __syncthreads();
-    const float* oin = oin_in + cidx * (C * DV);
     for (int idx = tid; idx < C * kSlice; idx += NT) {
       const int t = idx / kSlice, p = idx % kSlice;
-      float acc = oin[t * DV + p0 + p];
+      float acc = oin_s[buf][idx];
 #pragma unroll
       for (int w = 0; w < kScanWaves; ++w) acc += part_s[(w * C + t) * kSlice + p];
       o[((tok0 + t) * H + h) * DV + p0 + p] = static_cast<bf>(acc);

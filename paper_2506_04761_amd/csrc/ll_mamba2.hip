@@ -752,35 +752,6 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
 constexpr int kFastRows = 128;
 constexpr int kFastThreads = 256;
 
-// Element offset of 16-byte chunk c of row r in a swizzled row-major bf16 tile of D columns.
-template <int D>
-__device__ inline int swz(int r, int c) {
-  return r * D + ((c ^ (r & (D / 8 - 1))) << 3);
-}
-
-// Copies ROWS rows of D bf16 elements (row r at src + r * stride) into the swizzled LDS tile
-// `dst` by direct global->LDS loads, one 1 KiB span per wave instruction, spans dealt to the NT/64
-// waves in turn.  Rows at or beyond `nrow` are filled from row nrow - 1 (callers never read
-// them).  The copy is complete once the issuing wave has waited for its vector-memory operations.
-template <int D, int ROWS, int NT>
-__device__ inline void lds_copy_rows(__bf16* dst, const __bf16* __restrict__ src, int64_t stride, int nrow) {
-  constexpr int CH = D / 8;      // chunks per row
-  constexpr int RPI = NT / CH;   // rows per pass of all waves
-  static_assert(NT % CH == 0 && RPI % CH == 0 && ROWS % RPI == 0, "whole rows per pass");
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int q0 = wave * 64 + lane;                     // chunk position in the first pass
-  const int r0 = q0 / CH, c = (q0 % CH) ^ (r0 & (CH - 1));  // the swizzle repeats every pass
-#pragma unroll
-  for (int it = 0; it < ROWS / RPI; ++it) {
-    const int r = r0 + it * RPI;
-    const int rs = r < nrow ? r : nrow - 1;
-    __builtin_amdgcn_global_load_lds(src + rs * stride + c * 8,
-                                     (__attribute__((address_space(3))) void*)(dst + (it * NT + wave * 64) * 8), 16, 0,
-                                     0);
-  }
-}
-
 // Copies lambda of the tile's rows into dst[r * kMaxLevels + l] (l < L; the other slots receive
 // copies of valid entries and are never read) by direct global->LDS loads of one float per lane.
 template <int ROWS, int NT>
@@ -799,27 +770,6 @@ __device__ inline void lds_copy_lambda(float* dst, const float* __restrict__ lam
                                      (__attribute__((address_space(3))) void*)(dst + it * NT + wave * 64), 4, 0, 0);
   }
 }
-
-// bf16 MFMA operand fragment down the rows of a swizzled tile (as frag_down_rows).
-template <int D>
-__device__ inline bf16x8 frag_down_rows_swz(const __bf16* m, int row0, int col0) {
-  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
-  const int r = row0 + 4 * g + (i >> 2), col = col0 + 4 * (i & 3);
-  const bf16x4 lo = lds_read_tr(m + swz<D>(r, col >> 3) + (col & 7));
-  const bf16x4 hi = lds_read_tr(m + swz<D>(r + 16, col >> 3) + (col & 7));
-  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-
-// bf16 MFMA operand fragment along a row of a swizzled tile: row row0 + (lane % 16), the 8
-// elements starting at column 8 * chunk0 + 8 * (lane / 16).
-template <int D>
-__device__ inline bf16x8 frag_along_row_swz(const __bf16* m, int row0, int chunk0) {
-  const int lane = threadIdx.x & 63;
-  return *reinterpret_cast<const bf16x8*>(m + swz<D>(row0 + (lane & 15), chunk0 + (lane >> 4)));
-}
-
-// Waits for this wave's outstanding vector-memory operations (including direct-to-LDS loads).
-__device__ inline void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
 
 template <int DK, int DV, bool HAS_LAMBDA>
 __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
