@@ -149,25 +149,45 @@ __global__ __launch_bounds__(256) void k_gdn_chunk(const bf* __restrict__ q, con
       l_s[t * (C + 1) + s] = s < t ? bt_s[t] * acc[r] * fast_exp2(cl_s[t] - cl_s[s]) : 0.f;
     }
   });
-  gemm_lds<C, C, DK>(q_s, LDD, k_s, LDD, [&](int mt, int nt, f32x4 acc) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int t = mt * 16 + 4 * g + r, s = nt * 16 + r16;
-      pg_s[t * LDC + s] = static_cast<bf>(s <= t ? acc[r] * fast_exp2(cl_s[t] - cl_s[s]) : 0.f);
-    }
-  });
   __syncthreads();
 
-  // ---- phase B: X = (I + L)^{-1} by forward substitution, lane c = column c (wave 0);
-  //      T_G = X diag(beta): z_s[t][c] and zt_s[c][t]
-  if (wave == 0) {
+  // ---- phase B: X = (I + L)^{-1} by forward substitution, lane c = column c (wave 0), each
+  //      row's dot product split over four independent partial sums;
+  //      T_G = X diag(beta): z_s[t][c] and zt_s[c][t].  Meanwhile waves 1-3 form P_G.
+  if (wave != 0) {
+    // P_G[t][s] = (q_t . k_s) Gamma[t,s], s <= t, 16 x 16 tiles dealt to waves 1-3
+    using MF = Mfma<bf>;
+    constexpr int MT = C / 16;
+    for (int tile = wave - 1; tile < MT * MT; tile += 3) {
+      const int mt = tile / MT, nt = tile % MT;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < DK / MF::KSTEP; ++ks) {
+        const int k0 = ks * MF::KSTEP + g * MF::KPL;
+        acc = MF::mma(MF::load(&q_s[(mt * 16 + r16) * LDD + k0]), MF::load(&k_s[(nt * 16 + r16) * LDD + k0]), acc);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = mt * 16 + 4 * g + r, s = nt * 16 + r16;
+        pg_s[t * LDC + s] = static_cast<bf>(s <= t ? acc[r] * fast_exp2(cl_s[t] - cl_s[s]) : 0.f);
+      }
+    }
+  } else {
     const int c = lane;
     float x[C];
 #pragma unroll
     for (int i = 0; i < C; ++i) {
-      float acc = (i == c) ? 1.f : 0.f;
+      float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
 #pragma unroll
-      for (int j = 0; j < i; ++j) acc -= l_s[i * (C + 1) + j] * x[j];
+      for (int j = 0; j + 3 < i; j += 4) {
+        a0 += l_s[i * (C + 1) + j] * x[j];
+        a1 += l_s[i * (C + 1) + j + 1] * x[j + 1];
+        a2 += l_s[i * (C + 1) + j + 2] * x[j + 2];
+        a3 += l_s[i * (C + 1) + j + 3] * x[j + 3];
+      }
+#pragma unroll
+      for (int j = i & ~3; j < i; ++j) a0 += l_s[i * (C + 1) + j] * x[j];
+      const float acc = ((i == c) ? 1.f : 0.f) - ((a0 + a1) + (a2 + a3));
       x[i] = (i < c) ? 0.f : acc;
     }
     const float bc = bt_s[c];
