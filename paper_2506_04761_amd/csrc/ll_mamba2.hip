@@ -447,13 +447,15 @@ __global__ __launch_bounds__(256) void k_running_scan(const T* __restrict__ tile
   const T* src = tiles + bh * N * SZ + e0;
   T* dst = running + bh * N * SZ + e0;
   float r0 = 0.f, r1 = 0.f;
-  for (int64_t u0 = 0; u0 < N; u0 += kScanUnroll) {
-    T2 sv[kScanUnroll];
+  // batches of kScanUnroll tiles; the next batch's loads are issued before the current one is used
+  auto load_batch = [&](int64_t u0, T2 (&sv)[kScanUnroll]) {
 #pragma unroll
     for (int i = 0; i < kScanUnroll; ++i) {
       const int64_t u = u0 + i < N ? u0 + i : N - 1;
       sv[i] = *reinterpret_cast<const T2*>(src + u * SZ);
     }
+  };
+  auto use_batch = [&](int64_t u0, const T2 (&sv)[kScanUnroll]) {
 #pragma unroll
     for (int i = 0; i < kScanUnroll; ++i) {
       if (u0 + i < N) {
@@ -466,6 +468,15 @@ __global__ __launch_bounds__(256) void k_running_scan(const T* __restrict__ tile
         r1 = r1 * e + to_f32(sv[i][1]);
       }
     }
+  };
+  T2 sa[kScanUnroll], sb[kScanUnroll];
+  load_batch(0, sa);
+  for (int64_t u0 = 0; u0 < N; u0 += 2 * kScanUnroll) {
+    if (u0 + kScanUnroll < N) load_batch(u0 + kScanUnroll, sb);
+    use_batch(u0, sa);
+    if (u0 + kScanUnroll >= N) break;
+    if (u0 + 2 * kScanUnroll < N) load_batch(u0 + 2 * kScanUnroll, sa);
+    use_batch(u0 + kScanUnroll, sb);
   }
 }
 
