@@ -30,19 +30,20 @@ namespace ll {
 namespace gdn {
 
 constexpr int kMaxJ = 16;      // inter-chunk levels handled by the scan (T <= C * 2^16)
+constexpr int kChunkWaves = 8; // waves per gdn_chunk workgroup
 constexpr int kSlice = 16;     // d_v columns per scan workgroup
 constexpr int kScanWaves = 8;  // waves per scan workgroup
 typedef __bf16 bf;
 
 // C = A B over 16x16 output tiles, A [M][K] row-major (lda), Bt = B^T [N][K] row-major (ldb), both
-// bf16 in LDS; tiles dealt round-robin to the 4 waves; epi(mt, nt, acc) consumes each tile
+// bf16 in LDS; tiles dealt round-robin to the kChunkWaves waves; epi(mt, nt, acc) consumes each tile
 // (lane holds column 16 nt + (lane & 15), rows 16 mt + 4 (lane >> 4) + r).
 template <int M, int N, int K, typename Epi>
 __device__ inline void gemm_lds(const bf* A, int lda, const bf* Bt, int ldb, Epi epi) {
   using MF = Mfma<bf>;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
   constexpr int MT = M / 16, NT = N / 16;
-  for (int tile = wave; tile < MT * NT; tile += 4) {
+  for (int tile = wave; tile < MT * NT; tile += kChunkWaves) {
     const int mt = tile / NT, nt = tile % NT;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -55,12 +56,12 @@ __device__ inline void gemm_lds(const bf* A, int lda, const bf* Bt, int ldb, Epi
 }
 
 // ---------------------------------------------------------------------------------------------
-// Kernel 1: per-chunk WY solve and chunk-local products.  One workgroup (4 waves) per chunk.
+// Kernel 1: per-chunk WY solve and chunk-local products.  One workgroup (kChunkWaves waves) per chunk.
 // Outputs (workspace, per chunk): Qc [C][DK] bf16, P_z [DK][DK] bf16, H_z [DK][DV] bf16,
 // intra-chunk output [C][DV] fp32.
 // ---------------------------------------------------------------------------------------------
 template <int C, int DK, int DV, bool HAS_LAMBDA>
-__global__ __launch_bounds__(256) void k_gdn_chunk(const bf* __restrict__ q, const bf* __restrict__ k,
+__global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __restrict__ q, const bf* __restrict__ k,
                                                    const bf* __restrict__ v, const float* __restrict__ log_alpha,
                                                    const float* __restrict__ beta, const float* __restrict__ lam,
                                                    bf* __restrict__ qc_out, bf* __restrict__ pz_out,
@@ -114,13 +115,13 @@ __global__ __launch_bounds__(256) void k_gdn_chunk(const bf* __restrict__ q, con
     }
   }
   if constexpr (HAS_LAMBDA) {
-    for (int idx = tid; idx < C * (LOG2C + 1); idx += 256) {
+    for (int idx = tid; idx < C * (LOG2C + 1); idx += 64 * kChunkWaves) {
       const int t = idx / (LOG2C + 1), l = idx % (LOG2C + 1);
       lam_s[idx] = lam[((tok0 + t) * H + h) * L + l];
     }
   }
   __syncthreads();
-  for (int idx = tid; idx < C * DK / VEC; idx += 256) {
+  for (int idx = tid; idx < C * DK / VEC; idx += 64 * kChunkWaves) {
     const int t = idx / (DK / VEC), d0 = (idx % (DK / VEC)) * VEC;
     const bf16x8 kv = *reinterpret_cast<const bf16x8*>(k + ((tok0 + t) * H + h) * DK + d0);
     const bf16x8 qv = *reinterpret_cast<const bf16x8*>(q + ((tok0 + t) * H + h) * DK + d0);
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(256) void k_gdn_chunk(const bf* __restrict__ q, con
       kdt_s[(d0 + e) * LDC + t] = static_cast<bf>(x * dt);
     }
   }
-  for (int idx = tid; idx < C * DV / VEC; idx += 256) {
+  for (int idx = tid; idx < C * DV / VEC; idx += 64 * kChunkWaves) {
     const int t = idx / (DV / VEC), d0 = (idx % (DV / VEC)) * VEC;
     const bf16x8 vv = *reinterpret_cast<const bf16x8*>(v + ((tok0 + t) * H + h) * DV + d0);
 #pragma unroll
@@ -153,12 +154,12 @@ __global__ __launch_bounds__(256) void k_gdn_chunk(const bf* __restrict__ q, con
 
   // ---- phase B: X = (I + L)^{-1} by forward substitution, lane c = column c (wave 0), each
   //      row's dot product split over four independent partial sums;
-  //      T_G = X diag(beta): z_s[t][c] and zt_s[c][t].  Meanwhile waves 1-3 form P_G.
+  //      T_G = X diag(beta): z_s[t][c] and zt_s[c][t].  Meanwhile the other waves form P_G.
   if (wave != 0) {
-    // P_G[t][s] = (q_t . k_s) Gamma[t,s], s <= t, 16 x 16 tiles dealt to waves 1-3
+    // P_G[t][s] = (q_t . k_s) Gamma[t,s], s <= t, 16 x 16 tiles dealt to the other waves
     using MF = Mfma<bf>;
     constexpr int MT = C / 16;
-    for (int tile = wave - 1; tile < MT * MT; tile += 3) {
+    for (int tile = wave - 1; tile < MT * MT; tile += kChunkWaves - 1) {
       const int mt = tile / MT, nt = tile % MT;
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -458,10 +459,10 @@ hipError_t launch_gdn(const GdnArgs& a, hipStream_t st, hipEvent_t* ev) {
   __bf16* o = static_cast<__bf16*>(a.o);
   if (ev) (void)hipEventRecord(ev[0], st);
   if (a.lambda)
-    hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, true>), g1, dim3(256), 0, st, q, k, v, a.log_alpha, a.beta,
+    hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, true>), g1, dim3(64 * gdn::kChunkWaves), 0, st, q, k, v, a.log_alpha, a.beta,
                        a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L);
   else
-    hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, false>), g1, dim3(256), 0, st, q, k, v, a.log_alpha, a.beta,
+    hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, false>), g1, dim3(64 * gdn::kChunkWaves), 0, st, q, k, v, a.log_alpha, a.beta,
                        a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L);
   if (ev) (void)hipEventRecord(ev[1], st);
   if (a.lambda)
