@@ -344,7 +344,8 @@ __device__ inline void scan_gaps(float* dyn_s, const float* __restrict__ tot, fl
 
 // lambda given: grid (element blocks of 512 + 1, B * H).  Each thread owns two state entries and
 // walks the blocks of its (b, h) in order, keeping one accumulator per level >= 4.  JMAX bounds
-// J at compile time so that the unrolled per-block level loop stays short.
+// J at compile time so that the unrolled per-block level loop stays short (the launch picks the
+// smallest instance with JMAX >= J).
 template <typename T, int JMAX>
 __global__ __launch_bounds__(256) void k_level_scan(Nodes<T> nodes, const float* __restrict__ tot2,
                                                     float* __restrict__ gaps2, int64_t N, int J, int SZ) {
@@ -397,17 +398,21 @@ __global__ __launch_bounds__(256) void k_level_scan(Nodes<T> nodes, const float*
     for (int i = 0; i < kScanUnroll; ++i) {
       const int64_t bl = bl0 + i;
       if (bl < NB) {
-        const float e = fast_exp2(btot_s[bl]);
+        // the block's decay is the same for every lane: keep it in a scalar register
+        const float e = __builtin_bit_cast(
+            float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, fast_exp2(btot_s[bl]))));
         const float s0 = to_f32(sv[i][0]), s1 = to_f32(sv[i][1]);
 #pragma unroll
         for (int j = 4; j <= JMAX; ++j) {
-          // tile level j: source groups of 2^(j-3) blocks, the even-indexed ones
+          // tile level j: groups of 2^(j-3) blocks; every group is accumulated (the decay factor
+          // is 0 at a group's first block), the even-indexed ones (source groups) are stored.
+          // Levels above J never satisfy the store condition.
           const int sh = j - 3;
           const int64_t m = bl >> sh;
-          if (j <= J && !(m & 1)) {
-            const bool first = (bl & ((int64_t(1) << sh) - 1)) == 0;
-            a0[j] = first ? s0 : a0[j] * e + s0;
-            a1[j] = first ? s1 : a1[j] * e + s1;
+          const float ej = (bl & ((int64_t(1) << sh) - 1)) == 0 ? 0.f : e;
+          a0[j] = a0[j] * ej + s0;
+          a1[j] = a1[j] * ej + s1;
+          if (!(m & 1)) {
             const bool last = ((bl + 1) & ((int64_t(1) << sh) - 1)) == 0;
             const int64_t first_tile = (m << sh) * kBlockTiles;
             if (last && first_tile + (int64_t(1) << (j - 1)) < N) {
@@ -1125,9 +1130,19 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
     hipLaunchKernelGGL((k_block_state<T, C, DK, DV, false>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
                        a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H);
   if (ev) (void)hipEventRecord(ev[1], st);
-  if (a.lambda && w.J <= 12)
-    hipLaunchKernelGGL((k_level_scan<T, 12>), gscan, dim3(256), 2 * w.N * sizeof(float), st, nodes,
-                       (const float*)tot2, gaps2, w.N, w.J, SZ);
+  // the level scan is instantiated for the smallest level bound >= J
+  auto level_scan = [&](auto jmax_c) {
+    hipLaunchKernelGGL((k_level_scan<T, decltype(jmax_c)::value>), gscan, dim3(256), 2 * w.N * sizeof(float), st,
+                       nodes, (const float*)tot2, gaps2, w.N, w.J, SZ);
+  };
+  if (a.lambda && w.J <= 8)
+    level_scan(std::integral_constant<int, 8>{});
+  else if (a.lambda && w.J <= 10)
+    level_scan(std::integral_constant<int, 10>{});
+  else if (a.lambda && w.J <= 12)
+    level_scan(std::integral_constant<int, 12>{});
+  else if (a.lambda && w.J <= 16)
+    level_scan(std::integral_constant<int, 16>{});
   else if (a.lambda)
     hipLaunchKernelGGL((k_level_scan<T, kMaxLevels>), gscan, dim3(256), 2 * w.N * sizeof(float), st, nodes,
                        (const float*)tot2, gaps2, w.N, w.J, SZ);
