@@ -58,22 +58,28 @@ struct Nodes {
 
 // Tile-local inclusive cumulative sum of log2 gates for the R rows of a tile (rows >= nrow get
 // a zero gate), computed by the first 4 waves of the workgroup (R/4 <= 64 rows each) into cl_s[R].
-// Starts and ends with a barrier.
+//
+// tile_gate issues this thread's load of the raw log-gate (always from a valid address); the
+// scaling to log2 and the masking of rows outside the tile happen in tile_cumsum_of, where the
+// value is first needed, so that issuing the load never makes the wave wait for it.
 template <int R>
 __device__ inline float tile_gate(const float* __restrict__ log_alpha, int64_t row0, int nrow, int H, int h) {
   constexpr int RPW = R / 4;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = wave * RPW + lane;
-  return (wave < 4 && lane < RPW && r < nrow) ? log_alpha[(row0 + r) * H + h] * kLog2e : 0.f;
+  const int rs = (wave < 4 && lane < RPW && r < nrow) ? r : 0;
+  return log_alpha[(row0 + rs) * H + h];
 }
 
-// Scan of the gates returned by tile_gate (which may be loaded well before the scan).
+// Scan of the raw gates returned by tile_gate for a tile of nrow rows.  Starts and ends with a
+// barrier.
 template <int R>
-__device__ inline void tile_cumsum_of(float la, float* cl_s, float* wsum_s) {
+__device__ inline void tile_cumsum_of(float la_raw, int nrow, float* cl_s, float* wsum_s) {
   constexpr int RPW = R / 4;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = wave * RPW + lane;
   const bool mine = wave < 4 && lane < RPW;  // waves beyond the first four only take the barriers
+  const float la = (mine && r < nrow) ? la_raw * kLog2e : 0.f;
   float cl = wave_inclusive_scan(la);
   __syncthreads();
   if (wave < 4 && lane == 63) wsum_s[wave] = cl;
@@ -87,12 +93,13 @@ __device__ inline void tile_cumsum_of(float la, float* cl_s, float* wsum_s) {
 template <int R>
 __device__ inline void tile_cumsum(const float* __restrict__ log_alpha, int64_t row0, int nrow, int H, int h,
                                    float* cl_s, float* wsum_s) {
-  tile_cumsum_of<R>(tile_gate<R>(log_alpha, row0, nrow, H, h), cl_s, wsum_s);
+  tile_cumsum_of<R>(tile_gate<R>(log_alpha, row0, nrow, H, h), nrow, cl_s, wsum_s);
 }
 
 // Register staging of one 64-row block of a [rows, H, D] tensor, loaded with 16-byte vectors by
 // the NT threads of the workgroup (thread unit = one row's 16-byte column group, consecutive
-// threads along the row); rows at or beyond `nrow` read as zero.  D is the width loaded
+// threads along the row); rows at or beyond `nrow` repeat row nrow - 1 (callers give them zero
+// weight).  D is the width loaded
 // (elements per row) and LDROW the row length of the tensor in memory.  Stored row-major.
 template <typename T, int D, int NT, int LDROW = D>
 struct RowBlock {
@@ -106,9 +113,13 @@ struct RowBlock {
     for (int i = 0; i < LOADS; ++i) {
       const int idx = threadIdx.x + NT * i;
       const int t = idx / PER_ROW, d0 = (idx % PER_ROW) * VEC;
-      x[i] = typename Vec16<T>::type{};
-      if (idx < TOTAL && r0 + t < nrow)
-        x[i] = *reinterpret_cast<const typename Vec16<T>::type*>(src + ((row0 + r0 + t) * H + h) * LDROW + d0);
+      // rows at or beyond nrow repeat row nrow - 1 (no branch: the number of loads in flight
+      // stays the same on every path)
+      const int rr = r0 + t < nrow ? r0 + t : nrow - 1;
+      if (TOTAL % NT == 0 || idx < TOTAL)
+        x[i] = *reinterpret_cast<const typename Vec16<T>::type*>(src + ((row0 + rr) * H + h) * LDROW + d0);
+      else
+        x[i] = typename Vec16<T>::type{};
     }
   }
   __device__ inline void store_rows(T* dst, int ld) const {
@@ -136,10 +147,12 @@ struct RowBlock {
 };
 
 // ---------------------------------------------------------------------------------------------
-// Kernel 1: block states.  One workgroup (8 waves) per (block of 4 tiles, head, batch).  The K/V
-// rows of the 64-row steps are loaded into registers two steps ahead of their use (two register
-// buffers, across tile boundaries), the next tile's gates one tile ahead.  Finished summaries
-// are staged in LDS and written with 16-byte stores.
+// Kernel 1: block states.  One workgroup (8 waves) per (block of 4 tiles, head, batch).  The
+// gates of all the block's tiles are scanned once on entry (one row per thread); the K/V rows of
+// the 64-row steps are loaded into registers two steps ahead of their use (two register buffers,
+// across tile boundaries).  The steps are unrolled over the block, so that every step issues the
+// same loads and stores and the waits for the loads can count them.  Finished summaries are
+// staged in LDS and written with 16-byte stores.
 // ---------------------------------------------------------------------------------------------
 constexpr int kStateThreads = 512;  // block_state workgroup: 8 waves
 
@@ -161,12 +174,14 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
   constexpr int SZ = DK * DV;
   constexpr int VEC = Vec16<T>::N;
   constexpr int STEPS = R / kKB;                                 // 64-row steps per tile
+  constexpr int GATES = kBlockTiles * R;                         // gate rows of a block
+  static_assert(GATES <= kStateThreads && R % 64 == 0, "one gate row per thread, whole waves per tile");
   __shared__ T v_s[kKB * LDV];   // V rows of the current 64-row step
   __shared__ T k_s[kKB * LDK];   // decay * K rows
   __shared__ T out_s[2][SZ];     // summaries on their way out ([p][n], d_v x d_k)
-  __shared__ float cl_s[R];
-  __shared__ float dec_s[R];
-  __shared__ float wsum_s[4];
+  __shared__ float cl_s[GATES];  // per tile: inclusive cumulative log2-gates
+  __shared__ float dec_s[GATES]; // per tile: decay from each row to the tile end (0 past it)
+  __shared__ float wsum_s[NW];
 
   const int64_t N = (Tlen + R - 1) / R;  // tiles
   const int64_t NB = (N + kBlockTiles - 1) / kBlockTiles;
@@ -186,23 +201,40 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
 
   RowBlock<T, DK, kStateThreads> kr0, kr1;
   RowBlock<T, DV, kStateThreads> vr0, vr1;
+  // loads of step s; past the last step the last one is loaded again (an L2 hit)
   auto load_step = [&](int s, RowBlock<T, DK, kStateThreads>& kr, RowBlock<T, DV, kStateThreads>& vr) {
-    if (s >= nsteps) return;
+    s = s < nsteps ? s : nsteps - 1;
     const int64_t u = u0 + s / STEPS;
     const int kb = s % STEPS;
     kr.load(k, tile_row0(u), kb * kKB, nrow_of(u), H, h);
     vr.load(v, tile_row0(u), kb * kKB, nrow_of(u), H, h);
   };
-  float la_next = tile_gate<R>(log_alpha, tile_row0(u0), nrow_of(u0), H, h);
-  load_step(0, kr0, vr0);
-  load_step(1, kr1, vr1);
+
+  // ---- gates of the block: thread tid holds row tid % R of tile tid / R
+  {
+    const int a = tid / R, r = tid % R;
+    const int ac = a < ntile ? a : ntile - 1;
+    const int nr = nrow_of(u0 + ac);
+    const bool valid = tid < GATES && a < ntile && r < nr;
+    const float la_raw = log_alpha[(tile_row0(u0 + ac) + (r < nr ? r : nr - 1)) * H + h];
+    load_step(0, kr0, vr0);
+    load_step(1, kr1, vr1);
+    __builtin_amdgcn_sched_barrier(0);  // the gate's first use stays below the step loads
+    float cl = wave_inclusive_scan(valid ? la_raw * kLog2e : 0.f);
+    if (lane == 63) wsum_s[wave] = cl;
+    __syncthreads();
+    for (int w = (a * R) / 64; w < wave; ++w) cl += wsum_s[w];  // preceding waves of this tile
+    if (tid < GATES) cl_s[tid] = cl;
+    __syncthreads();
+    if (tid < GATES) dec_s[tid] = valid ? fast_exp2(cl_s[a * R + R - 1] - cl) : 0.f;
+    if (tid < ntile) tot2_out[bh * N + u0 + tid] = cl_s[tid * R + R - 1];
+  }
 
   f32x4 run[TM][TN], acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int jn = 0; jn < TN; ++jn) run[i][jn] = acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float tot = 0.f;
 
   // stage a summary (registers of the active waves) in out_s[slot]
   auto stage = [&](int slot, const f32x4 (&x)[TM][TN]) {
@@ -217,29 +249,29 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
         }
   };
   auto flush = [&](int slot, T* dst) {
-    for (int idx = tid; idx < SZ / VEC; idx += kStateThreads)
-      *reinterpret_cast<V16*>(dst + idx * VEC) = *reinterpret_cast<const V16*>(&out_s[slot][idx * VEC]);
+    constexpr int PASSES = (SZ / VEC + kStateThreads - 1) / kStateThreads;
+#pragma unroll
+    for (int it = 0; it < PASSES; ++it) {
+      const int idx = tid + it * kStateThreads;
+      if ((SZ / VEC) % kStateThreads == 0 || idx < SZ / VEC)
+        *reinterpret_cast<V16*>(dst + idx * VEC) = *reinterpret_cast<const V16*>(&out_s[slot][idx * VEC]);
+    }
   };
 
-  auto step = [&](int s, RowBlock<T, DK, kStateThreads>& kr, RowBlock<T, DV, kStateThreads>& vr) {
-    const int a = s / STEPS, kb = s % STEPS;
+  // step s = (tile a, 64-row step kb); a and kb are compile-time after unrolling
+  auto step = [&](int a, int kb, RowBlock<T, DK, kStateThreads>& kr, RowBlock<T, DV, kStateThreads>& vr) {
     const int64_t u = u0 + a;
-    const int nrow = nrow_of(u);
     if (kb == 0) {
-      tile_cumsum_of<R>(la_next, cl_s, wsum_s);  // starts and ends with a barrier
-      if (a + 1 < ntile) la_next = tile_gate<R>(log_alpha, tile_row0(u + 1), nrow_of(u + 1), H, h);
-      tot = cl_s[R - 1];
-      for (int r = tid; r < R; r += kStateThreads) dec_s[r] = r < nrow ? fast_exp2(tot - cl_s[r]) : 0.f;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int jn = 0; jn < TN; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    __syncthreads();  // previous step's readers done; dec_s visible
+    __syncthreads();  // previous step's readers done (and dec_s visible on entry)
     vr.store_rows(v_s, LDV);
-    kr.store_rows_scaled(k_s, LDK, dec_s + kb * kKB);
+    kr.store_rows_scaled(k_s, LDK, dec_s + a * R + kb * kKB);
     __syncthreads();
-    load_step(s + 2, kr, vr);
+    load_step(a * STEPS + kb + 2, kr, vr);
     if (active) {
       // S^T[p][n] += sum_t V[t][p] (dK)[t][n]: both operands read down the token rows
 #pragma unroll
@@ -264,11 +296,10 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
     }
     if (kb == STEPS - 1) {
       // tile done: fold it into the block's summaries and write the ones readers need
-      if (tid == 0) tot2_out[bh * N + u] = tot;
       T* dst0 = nullptr;
       T* dst1 = nullptr;
       if constexpr (HAS_LAMBDA) {
-        const float e = fast_exp2(tot);
+        const float e = fast_exp2(cl_s[a * R + R - 1]);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -289,9 +320,14 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
     }
   };
 
-  for (int s = 0; s < nsteps; s += 2) {
-    step(s, kr0, vr0);
-    if (s + 1 < nsteps) step(s + 1, kr1, vr1);
+#pragma unroll
+  for (int a = 0; a < kBlockTiles; ++a) {
+    if (a >= ntile) break;
+#pragma unroll
+    for (int kb = 0; kb < STEPS; ++kb) {
+      if (((a * STEPS + kb) & 1) == 0) step(a, kb, kr0, vr0);
+      else step(a, kb, kr1, vr1);
+    }
   }
 }
 
@@ -596,7 +632,7 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
       }
     }
   }
-  tile_cumsum_of<R>(la, cl_s, wsum_s);
+  tile_cumsum_of<R>(la, nrow, cl_s, wsum_s);
   // key-side decay to the end of each 16-key tile: kdec[j] = exp2(cl[j | 15] - cl[j])
   for (int r = tid; r < R; r += NT) kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
   const float* lrow = &lam_s[(16 * wave + r16) * L];  // this lane's lambda row
@@ -835,7 +871,10 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
   lds_copy_rows<DK, R, NT>(k_s, k + (row0 * H + h) * DK, (int64_t)H * DK, nrow);
   lds_copy_rows<DV, R, NT>(v_s, v + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
   if constexpr (HAS_LAMBDA) lds_copy_lambda<R, NT>(lam_s, lam, row0, H, h, L, nrow);
-  tile_cumsum_of<R>(la, cl_s, wsum_s);
+  // keep the first use of the gate below every load issue: a use scheduled earlier makes the
+  // wave wait for the gate before the remaining loads are issued
+  __builtin_amdgcn_sched_barrier(0);
+  tile_cumsum_of<R>(la, nrow, cl_s, wsum_s);
   for (int r = tid; r < R; r += NT) kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
   wait_vmem();
   __syncthreads();  // K, V, lambda, kdec visible
