@@ -117,15 +117,11 @@ __device__ inline int swz(int r, int c) {
   return r * D + ((c ^ (r & (D / 8 - 1))) << 3);
 }
 
-// Cache policy of a load: kCoherent (sc1) makes it device-coherent, i.e. it sees data written by
-// device-coherent stores of other workgroups on any XCD once those stores have completed.
-constexpr int kCoherent = 16;
-
 // Copies ROWS rows of D bf16 elements (row r at src + r * stride) into the swizzled LDS tile
 // `dst` by direct global->LDS loads, one 1 KiB span per wave instruction, spans dealt to the NT/64
 // waves in turn.  Rows at or beyond `nrow` are filled from row nrow - 1 (callers never read
 // them).  The copy is complete once the issuing wave has waited for its vector-memory operations.
-template <int D, int ROWS, int NT, int POLICY = 0>
+template <int D, int ROWS, int NT>
 __device__ inline void lds_copy_rows(__bf16* dst, const __bf16* __restrict__ src, int64_t stride, int nrow) {
   constexpr int CH = D / 8;      // chunks per row
   constexpr int RPI = NT / CH;   // rows per pass of all waves
@@ -140,7 +136,7 @@ __device__ inline void lds_copy_rows(__bf16* dst, const __bf16* __restrict__ src
     const int rs = r < nrow ? r : nrow - 1;
     __builtin_amdgcn_global_load_lds(src + rs * stride + c * 8,
                                      (__attribute__((address_space(3))) void*)(dst + (it * NT + wave * 64) * 8), 16, 0,
-                                     POLICY);
+                                     0);
   }
 }
 
@@ -209,13 +205,6 @@ __device__ inline float wave_inclusive_scan(float x) {
     float y = __shfl_up(x, off, 64);
     if (lane >= off) x += y;
   }
-  return x;
-}
-
-// Sum across the 64 lanes of a wave, returned to every lane.
-__device__ inline float wave_sum(float x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
   return x;
 }
 

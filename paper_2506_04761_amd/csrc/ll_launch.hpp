@@ -14,8 +14,6 @@ struct WsLayout {
   int J = 0;           // inter-tile levels
   int64_t n1 = 0, n2 = 0, nb = 0, nup = 0;  // per-(b,h) summary slots: levels 1, 2, 3 (blocks), >= 4
   int64_t tot2 = 0, gaps2 = 0, lvl1 = 0, lvl2 = 0, blocks = 0, upper = 0, tiles = 0, running = 0;
-  bool fused = false;  // single-pass kernel: one node per tile, node totals, tile flags, ticket
-  int64_t fnode = 0, ftot = 0, fflags = 0, fticket = 0;
   int64_t total = 0;
 };
 

@@ -1085,416 +1085,6 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
 }
 
 // ---------------------------------------------------------------------------------------------
-// Fused single pass (bf16 storage, 128-row tiles): one workgroup per tile computes the tile's
-// state, its Fenwick node, the intra-tile output and the inter-tile levels, so that K and V are
-// read from HBM once.
-//
-// Node(u), for tile u with t trailing one bits: the summary, as seen from the end of tile u, of
-// the 2^t tiles ending at u, Node(u) = sum over their rows s of exp2(cl_end - cl_s) k_s v_s^T
-// (stored [d_v][d_k] row-major).  Tile u forms it from its own state and the nodes of tiles
-// u - 2^(k-1), k = 1..t, each covering the 2^(k-1) tiles before the part already summed:
-// Node = exp2(total log2-gate of the later part) * Node(earlier part) + later part.  At tile
-// level j (bit j-1 of u set, Sec. 3.3) tile u reads Node(e_j), e_j = (u with the bits below j-1
-// cleared) - 1, which covers exactly the 2^(j-1) tiles of its level-j source group; the decay
-// from the end of that group to row i is exp2(cl_i + gap_j), gap_j the summed log2-gates of tiles
-// e_j + 1 .. u - 1.  With lambda absent (Mamba-2, lambda = 1) the same levels sum to the full
-// prefix state.
-//
-// Synchronisation.  Tiles take tickets in (tile, head) order and only wait for earlier tiles of
-// their own head, which hold smaller tickets and are therefore already running: every wait ends.
-// Each tile publishes its summed log2-gate right after its gate scan (the value itself, replacing
-// a NaN sentinel) and its node once built (data, then a flag).  Everything another workgroup reads
-// is written and read with device-coherent accesses (sc1), and the node data are complete
-// (vmcnt 0) before the flag is set.  A wait is bounded; one that runs out fills the tile's output
-// with NaN.
-// ---------------------------------------------------------------------------------------------
-constexpr int kSpinLimit = 1 << 18;            // polls of one wait (a coherent load and a sleep)
-constexpr uint32_t kTotPending = 0xFFFFFFFFu;  // bits of an unpublished tile total (a NaN)
-
-__device__ inline uint32_t load_flag(const uint32_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline void store_flag(uint32_t* p, uint32_t x) {
-  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Waits (wave 0 polling, lane b for bit b) until Node(e) is flagged for every set bit b of
-// `need`, e = ((u >> b) << b) - 1; the whole workgroup then passes a barrier.  Returns false if
-// the wait ran out.
-__device__ inline bool wait_nodes(const uint32_t* flags, uint32_t u, uint32_t need) {
-  __shared__ int ok_s;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (wave == 0) {
-    const bool mine = lane < 32 && ((need >> lane) & 1u);
-    const int64_t e = mine ? (int64_t)((u >> lane) << lane) - 1 : 0;
-    bool ok = !mine;
-    bool all = false;
-    for (int it = 0; it < kSpinLimit; ++it) {
-      if (!ok) ok = load_flag(flags + e) != 0;
-      all = __all(ok);
-      if (all) break;
-      __builtin_amdgcn_s_sleep(1);
-    }
-    if (lane == 0) ok_s = all;
-  }
-  __syncthreads();
-  return ok_s != 0;
-}
-
-// Published tile totals of one head, tiles [lo, lo + 256) clipped to [lo, hi): lane l, slot i
-// holds tile lo + 64 i + l (0 outside the range).  `issue` loads, `settle` polls until every
-// value is published (clearing `ok` if a wait runs out).
-struct TotChunk {
-  uint32_t bits[4];
-  int64_t lo, hi;
-  __device__ inline void issue(const uint32_t* tot, int64_t lo_, int64_t hi_) {
-    lo = lo_;
-    hi = hi_;
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t s = lo + 64 * i + lane;
-      bits[i] = s < hi ? load_flag(tot + s) : 0u;
-    }
-  }
-  __device__ inline void settle(const uint32_t* tot, bool& ok) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t s = lo + 64 * i + lane;
-      for (int it = 0; bits[i] == kTotPending && it < kSpinLimit; ++it) {
-        __builtin_amdgcn_s_sleep(4);
-        bits[i] = load_flag(tot + s);
-      }
-      if (bits[i] == kTotPending) {
-        ok = false;
-        bits[i] = 0u;
-      }
-    }
-  }
-  // wave-wide sum over the tiles in [a, b) of this chunk
-  __device__ inline float sum(int64_t a, int64_t b) const {
-    const int lane = threadIdx.x & 63;
-    float x = 0.f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t s = lo + 64 * i + lane;
-      if (s >= a && s < b) x += __uint_as_float(bits[i]);
-    }
-    return wave_sum(x);
-  }
-};
-
-// Wave-level sums of published tile totals: out_s[r] = sum over the tiles [a_r, b_r) (range(r),
-// all inside [lo, hi)) for r < nr, chunk by chunk; `first` already holds the loads of the first
-// chunk.  Lane 0 writes out_s.  Clears `ok` if a wait runs out.
-template <typename RangeFn>
-__device__ inline void sum_totals(const uint32_t* tot, int64_t lo, int64_t hi, TotChunk& first, int nr,
-                                  RangeFn range, float* out_s, bool& ok) {
-  const int lane = threadIdx.x & 63;
-  for (int r = 0; r < nr; ++r)
-    if (lane == 0) out_s[r] = 0.f;
-  for (int64_t c0 = lo; c0 < hi; c0 += 256) {
-    if (c0 != lo) first.issue(tot, c0, hi);
-    first.settle(tot, ok);
-    for (int r = 0; r < nr; ++r) {
-      int64_t a, b;
-      range(r, a, b);
-      const float s = first.sum(a, b);
-      if (lane == 0) out_s[r] += s;
-    }
-  }
-}
-
-template <int DK, int DV, bool HAS_LAMBDA>
-__global__ __launch_bounds__(kFastThreads, 2) void k_fused(
-    const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
-    const float* __restrict__ log_alpha, const float* __restrict__ lam, __bf16* node, uint32_t* ttot,
-    uint32_t* flags, int* ticket, __bf16* __restrict__ o, int64_t Tlen, int BH, int H, int L) {
-  using M = Mfma<__bf16>;
-  typedef __bf16 bf;
-  typedef typename M::frag frag;
-  constexpr int R = kFastRows, LOG2R = 7;
-  constexpr int NT = kFastThreads;
-  constexpr int MT = DV / 16, KS = DK / M::KSTEP, KC = M::KSTEP / 8;  // KC: 16-byte chunks per k step
-  constexpr int SZ = DK * DV;
-  constexpr int SN = DK / 32, SP = DV / 32;  // state tiles per wave along d_k and d_v (2 x 2 waves)
-  static_assert(DK <= R && DV <= R, "a node must fit in the K and in the V region");
-  __shared__ bf k_s[R * DK];
-  __shared__ bf v_s[R * DV];
-  __shared__ float lam_s[HAS_LAMBDA ? R * kMaxLevels : 1];
-  __shared__ float cl_s[R];
-  __shared__ float kdec_s[R];
-  __shared__ float dec_s[R];
-  __shared__ float wsum_s[4];
-  __shared__ float gap_s[32];    // gap of the level of each set bit of u
-  __shared__ float chain_s[32];  // summed log2-gate of the group of Node(u - 2^k), k < t
-  __shared__ int ticket_s, cok_s, gok_s;  // ticket; tile totals of the chain / the gaps complete
-  __shared__ uint32_t ready_s;             // bits of u whose level node is known to be published
-
-  const int64_t N = (Tlen + R - 1) / R;
-  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  if (tid == 0) ticket_s = atomicAdd(ticket, 1);
-  __syncthreads();
-  const int tk = __builtin_amdgcn_readfirstlane(ticket_s);  // logical order (u, b, h)
-  const int u = tk / BH;
-  const int64_t bh = tk % BH;
-  const int h = (int)(bh % H), b = (int)(bh / H);
-  const int64_t row0 = (int64_t)b * Tlen + (int64_t)u * R;
-  const int nrow = (int)((Tlen - (int64_t)u * R) < R ? (Tlen - (int64_t)u * R) : R);
-  const int gA = wave, gB = 7 - wave;          // this wave's 16-row groups
-  const int iA = 16 * gA + r16, iB = 16 * gB + r16;
-  const bool liveB = 16 * gB < nrow;           // nrow is a multiple of C = 64
-  uint32_t* const hflags = flags + bh * N;     // this head's node flags and tile totals
-  const uint32_t* const htot = ttot + bh * N;
-  bf* const hnode = node + bh * N * SZ;
-  const int t = __builtin_ctz(~(uint32_t)u);   // trailing one bits of u
-
-  // ---- loads: gates first (needed first), then Q into registers, then K, V, lambda into LDS
-  const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);
-  frag qA[KS], qB[KS];
-  {
-    const int rA = iA < nrow ? iA : nrow - 1, rB = iB < nrow ? iB : nrow - 1;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      qA[ks] = M::load(q + ((row0 + rA) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
-      qB[ks] = M::load(q + ((row0 + rB) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
-    }
-  }
-  lds_copy_rows<DK, R, NT>(k_s, k + (row0 * H + h) * DK, (int64_t)H * DK, nrow);
-  lds_copy_rows<DV, R, NT>(v_s, v + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
-  if constexpr (HAS_LAMBDA) lds_copy_lambda<R, NT>(lam_s, lam, row0, H, h, L, nrow);
-  __builtin_amdgcn_sched_barrier(0);  // the gate's first use stays below every load issue
-  tile_cumsum_of<R>(la, nrow, cl_s, wsum_s);
-  const float tot = cl_s[R - 1];
-  if (tid == 0) store_flag(ttot + bh * N + u, __float_as_uint(tot));  // this tile's total, early
-  for (int r = tid; r < R; r += NT) {
-    kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
-    dec_s[r] = r < nrow ? fast_exp2(tot - cl_s[r]) : 0.f;
-  }
-  // totals of the tiles before u in its chain (u - 2^t + 1 .. u - 1), first 256 loaded meanwhile
-  const int64_t clo = (int64_t)u - ((int64_t)1 << t) + 1;
-  TotChunk chain;
-  if (wave == 0) chain.issue(htot, clo, u);
-  wait_vmem();
-  __syncthreads();  // K, V, lambda, kdec, dec visible
-  if (!liveB) {
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qB[ks] = frag{};  // rows past the end contribute nothing
-  }
-
-  // ---- the tile's state S[n][p] = sum_r dec_r k_r[n] v_r[p]; waves on a 2 x 2 grid of (d_k, d_v)
-  //      quarters, lane holding n = 16 nt + 4g + {0..3} at p = 16 pt + r16 (8 contiguous bytes
-  //      of the [d_v][d_k] node)
-  bool ok = true;
-  {
-    const int wn = wave & 1, wp = wave >> 1;
-    f32x4 sacc[SN][SP];
-#pragma unroll
-    for (int i = 0; i < SN; ++i)
-#pragma unroll
-      for (int jp = 0; jp < SP; ++jp) sacc[i][jp] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < R / 32; ++ks) {
-      // k slots of a lane: rows 32 ks + 4g + {0..3} and 32 ks + 16 + 4g + {0..3}
-      const f32x4 d0 = *reinterpret_cast<const f32x4*>(&dec_s[ks * 32 + 4 * g]);
-      const f32x4 d1 = *reinterpret_cast<const f32x4*>(&dec_s[ks * 32 + 16 + 4 * g]);
-      frag a[SN];
-#pragma unroll
-      for (int i = 0; i < SN; ++i) {
-        const frag x = frag_down_rows_swz<DK>(k_s, ks * 32, (wn * SN + i) * 16);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          a[i][e] = from_f32<bf>(to_f32(x[e]) * d0[e]);
-          a[i][4 + e] = from_f32<bf>(to_f32(x[4 + e]) * d1[e]);
-        }
-      }
-#pragma unroll
-      for (int jp = 0; jp < SP; ++jp) {
-        const frag bv = frag_down_rows_swz<DV>(v_s, ks * 32, (wp * SP + jp) * 16);
-#pragma unroll
-        for (int i = 0; i < SN; ++i) sacc[i][jp] = M::mma(a[i], bv, sacc[i][jp]);
-      }
-    }
-    auto at = [&](int i, int jp) { return ((wp * SP + jp) * 16 + r16) * DK + (wn * SN + i) * 16 + 4 * g; };
-    // ---- Node(u): fold in the nodes of tiles u - 2^(k-1), k = 1..t (every wave sums the totals)
-    if (t > 0) {
-      if (wave == 0) {
-        bool cok = true;
-        sum_totals(htot, clo, u, chain, t,
-                   [&](int r, int64_t& a, int64_t& b) {
-                     a = (int64_t)u - ((int64_t)2 << r) + 1;
-                     b = (int64_t)u - ((int64_t)1 << r) + 1;
-                   },
-                   chain_s, cok);
-        if (lane == 0) cok_s = cok;
-      }
-      ok = wait_nodes(hflags, (uint32_t)u, (1u << t) - 1u) && cok_s;  // its barrier publishes chain_s
-    }
-    float later = tot;  // summed log2-gate of the part already folded in
-    for (int kk = 1; kk <= t; ++kk) {
-      const int64_t e = (int64_t)u - (1 << (kk - 1));
-      const bf* src = hnode + e * SZ;
-      const float sc = fast_exp2(later);
-#pragma unroll
-      for (int i = 0; i < SN; ++i)
-#pragma unroll
-        for (int jp = 0; jp < SP; ++jp) {
-          const uint64_t w = __hip_atomic_load(reinterpret_cast<const uint64_t*>(src + at(i, jp)), __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
-          const bf16x4 x = __builtin_bit_cast(bf16x4, w);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) sacc[i][jp][r] += sc * to_f32(x[r]);
-        }
-      later += chain_s[kk - 1];
-    }
-    if (u + 1 < N) {  // the last tile's node has no reader
-      bf* dst = hnode + (int64_t)u * SZ;
-#pragma unroll
-      for (int i = 0; i < SN; ++i)
-#pragma unroll
-        for (int jp = 0; jp < SP; ++jp) {
-          bf16x4 y;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) y[r] = from_f32<bf>(sacc[i][jp][r]);
-          __hip_atomic_store(reinterpret_cast<uint64_t*>(dst + at(i, jp)), __builtin_bit_cast(uint64_t, y),
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-      wait_vmem();      // this wave's node stores are complete
-      __syncthreads();  // ... and every other wave's
-      if (tid == 0) store_flag(hflags + u, 1u);  // Node(u) published
-    }
-  }
-
-  // totals of tiles hb .. u - 1 (hb = u without its bits below the top one), for the gaps; the
-  // first 256 are loaded during the intra-tile phase
-  const int64_t hb = u ? (int64_t)1 << (31 - __builtin_clz((uint32_t)u)) : 0;
-  TotChunk gaps;
-  // flags of the nodes of the levels not acquired with the chain (lane = bit), read meanwhile
-  uint32_t fl = 1u;
-  if (wave == 0) {
-    gaps.issue(htot, hb, u);
-    if (lane < 32 && lane >= t && ((u >> lane) & 1)) fl = load_flag(hflags + (((u >> lane) << lane) - 1));
-  }
-
-  // ---- intra-tile (every wave)
-  const float cliA = cl_s[iA], cliB = cl_s[iB];
-  const float* lrowA = &lam_s[HAS_LAMBDA ? iA * kMaxLevels : 0];
-  const float* lrowB = &lam_s[HAS_LAMBDA ? iB * kMaxLevels : 0];
-  f32x4 oA[MT], oB[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) oA[mt] = oB[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  fast_intra<DK, DV, HAS_LAMBDA>(wave, k_s, v_s, cl_s, kdec_s, qA, qB, cliA, cliB, lrowA, lrowB, oA, oB);
-
-  // ---- gaps: gap_j = summed log2-gates of tiles [u with bits below j-1 cleared, u), per set bit
-  //      (entries of clear bits are not used)
-  if (wave == 0) {
-    bool gok = true;
-    sum_totals(htot, hb, u, gaps, u ? 32 - __builtin_clz((uint32_t)u) : 0,
-               [&](int r, int64_t& a, int64_t& b) {
-                 a = (int64_t)(((uint32_t)u >> r) << r);
-                 b = u;
-               },
-               gap_s, gok);
-    const uint64_t rm = __ballot(fl != 0u);  // levels whose node was already flagged
-    if (lane == 0) {
-      gok_s = gok;
-      ready_s = (uint32_t)rm;
-    }
-  }
-
-  // ---- inter-tile levels, highest (oldest node) first; nodes alternate between the K and V
-  //      regions, the next one copied in while the current one is used
-  auto node_of = [&](int bit) { return hnode + ((((int64_t)u >> bit) << bit) - 1) * SZ; };
-  auto lower = [&](int bit) -> int {  // next lower set bit of u, -1 if none
-    const uint32_t m = (uint32_t)u & ((1u << bit) - 1u);
-    return m ? 31 - __builtin_clz(m) : -1;
-  };
-  // nodes seen flagged already need no wait; another one is waited for just before its copy
-  uint32_t known = 0;
-  auto ready = [&](int bit) { return ((known >> bit) & 1u) ? true : wait_nodes(hflags, (uint32_t)u, 1u << bit); };
-  auto copy_node = [&](bf* dst, int bit) { lds_copy_rows<DK, DV, NT, kCoherent>(dst, node_of(bit), DK, DV); };
-  // One level (bit) from `cur` (already being copied in); the next level's node goes to `nxt`.
-  auto level_step = [&](int& bit, const bf* cur, bf* nxt) {
-    const int bn = lower(bit);
-    bool nok = true;
-    if (bn >= 0) nok = ready(bn);   // ends with a barrier: every wave is done with `nxt`
-    wait_vmem();
-    __syncthreads();  // `cur` complete and visible
-    if (bn >= 0) copy_node(nxt, bn);
-    const float gap = gap_s[bit];
-    const int j = bit + 1;
-    float wA = fast_exp2(cliA + gap), wB = fast_exp2(cliB + gap);
-    if constexpr (HAS_LAMBDA) {
-      wA *= lrowA[LOG2R + j];
-      wB *= lrowB[LOG2R + j];
-    }
-    // node fragments read one 16-row block ahead of their use
-    frag uf[2][KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) uf[0][ks] = frag_along_row_swz<DK>(cur, 0, ks * KC);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      if (mt + 1 < MT) {
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) uf[(mt + 1) & 1][ks] = frag_along_row_swz<DK>(cur, 16 * (mt + 1), ks * KC);
-      }
-      f32x4 tA = {0.f, 0.f, 0.f, 0.f}, tB = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        tA = M::mma(uf[mt & 1][ks], qA[ks], tA);
-        tB = M::mma(uf[mt & 1][ks], qB[ks], tB);
-      }
-      oA[mt] += wA * tA;
-      oB[mt] += wB * tB;
-    }
-    ok = ok && nok;
-    bit = bn;
-  };
-
-  int bit = u ? 31 - __builtin_clz((uint32_t)u) : -1;
-  __syncthreads();  // every wave is done with K and V; gaps visible
-  ok = ok && gok_s;
-  known = __builtin_amdgcn_readfirstlane(ready_s);
-  if (bit >= 0) {
-    ok = ready(bit) && ok;
-    copy_node(k_s, bit);
-  }
-  while (bit >= 0) {
-    level_step(bit, k_s, v_s);
-    if (bit < 0) break;
-    level_step(bit, v_s, k_s);
-  }
-
-  // ---- store O: lane holds rows iA, iB, d_v entries 16 mt + 4g .. +3 (NaN if a wait ran out)
-  auto store_rows = [&](const f32x4* acc, int i) {
-    bf* orow = o + ((row0 + i) * H + h) * DV + 4 * g;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      bf16x4 val;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) val[r] = from_f32<bf>(ok ? acc[mt][r] : __builtin_nanf(""));
-      *reinterpret_cast<bf16x4*>(orow + mt * 16) = val;
-    }
-  };
-  if (iA < nrow) store_rows(oA, iA);
-  if (liveB) store_rows(oB, iB);
-}
-
-// Prepares the fused pass: node flags cleared, tile totals set to the unpublished sentinel,
-// ticket counter cleared (run before every fused pass).
-__global__ void k_fused_reset(uint32_t* flags, uint32_t* ttot, int64_t n, int* ticket) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) {
-    flags[i] = 0u;
-    ttot[i] = kTotPending;
-  }
-  if (i == 0) *ticket = 0;
-}
-
-// ---------------------------------------------------------------------------------------------
 // Debug level map: the level each (t, s) pair receives from the device functions the kernels use.
 // ---------------------------------------------------------------------------------------------
 __global__ void k_debug_level_map(int64_t Tlen, int R, int log2R, int J, int8_t* out) {
@@ -1543,16 +1133,6 @@ int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv
   w.nup = 0;
   for (int j = 4; j <= J; ++j) w.nup += (N + (int64_t(1) << j) - 1) >> j;
   int64_t cur = 0;
-  if (esize == 2 && tile_rows((int)C) == kFastRows) {
-    w.fused = true;
-    w.fticket = cur; cur += 256;
-    w.fflags = cur; cur += al(BH * N * 4);
-    w.ftot = cur; cur += al(BH * N * 4);
-    w.fnode = cur; cur += al(BH * N * SZ * esize);
-    w.total = cur;
-    if (lay) *lay = w;
-    return cur;
-  }
   w.tot2 = cur; cur += al(BH * N * 4);
   if (has_lambda) {
     w.gaps2 = cur; cur += al(BH * N * (J > 0 ? J : 1) * 4);
@@ -1577,32 +1157,6 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
   WsLayout w;
   mamba2_workspace(a.B, a.T, a.H, DK, DV, C, sizeof(T), a.lambda != nullptr, &w);
   char* base = static_cast<char*>(a.workspace);
-  constexpr bool kFast = std::is_same<T, __bf16>::value && tile_rows(C) == kFastRows;
-  if constexpr (kFast) {
-    // single pass: clear the flags, then one workgroup per tile (stages 2 and 3 of the staged
-    // entry point: the reset, then the fused kernel; stage 1 is empty)
-    const int64_t BH = a.B * a.H;
-    uint32_t* flags = reinterpret_cast<uint32_t*>(base + w.fflags);
-    int* ticket = reinterpret_cast<int*>(base + w.fticket);
-    uint32_t* ttot = reinterpret_cast<uint32_t*>(base + w.ftot);
-    __bf16* node = reinterpret_cast<__bf16*>(base + w.fnode);
-    if (ev) (void)hipEventRecord(ev[0], st);
-    if (ev) (void)hipEventRecord(ev[1], st);
-    hipLaunchKernelGGL(k_fused_reset, dim3((unsigned)((BH * w.N + 255) / 256)), dim3(256), 0, st, flags, ttot, BH * w.N,
-                       ticket);
-    if (ev) (void)hipEventRecord(ev[2], st);
-    const dim3 grid((unsigned)(w.N * BH));
-    if (a.lambda)
-      hipLaunchKernelGGL((k_fused<DK, DV, true>), grid, dim3(kFastThreads), 0, st, (const T*)a.q, (const T*)a.k,
-                         (const T*)a.v, a.log_alpha, a.lambda, node, ttot, flags, ticket, (T*)a.o, a.T, (int)BH,
-                         (int)a.H, a.L);
-    else
-      hipLaunchKernelGGL((k_fused<DK, DV, false>), grid, dim3(kFastThreads), 0, st, (const T*)a.q, (const T*)a.k,
-                         (const T*)a.v, a.log_alpha, a.lambda, node, ttot, flags, ticket, (T*)a.o, a.T, (int)BH,
-                         (int)a.H, a.L);
-    if (ev) (void)hipEventRecord(ev[3], st);
-    return hipGetLastError();
-  }
   float* tot2 = reinterpret_cast<float*>(base + w.tot2);
   Nodes<T> nodes{};
   T* tiles = nullptr;
@@ -1624,6 +1178,7 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
   }
   const dim3 gblk((unsigned)(w.nb * a.H * a.B));
   const dim3 gscan((unsigned)((SZ / 2 + 255) / 256 + 1), (unsigned)(a.B * a.H));
+  constexpr bool kFast = std::is_same<T, __bf16>::value && tile_rows(C) == kFastRows;
   const dim3 gtile((unsigned)(w.N * (kFast ? 1 : RowMap<tile_rows(C)>::RS) * a.H * a.B));
   if (ev) (void)hipEventRecord(ev[0], st);
   if (a.lambda)
