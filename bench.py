@@ -1,7 +1,8 @@
 """Benchmark: log-linear Mamba-2 chunkwise forward on one MI355X.
 
 One step = one ll_mamba2_fwd call over the whole workload (all three kernel stages: tile
-states, level scan, tile outputs), inputs already resident in HBM.  Default workload:
+states, the scan -- the block tree of summaries, or the running state when lambda == NULL -- and
+tile outputs), inputs already resident in HBM.  Default workload:
 B=1, H=16, T=65536, d_k=d_v=128, C=64, bf16 q/k/v with fp32 gates and lambda (17 levels).
 
 Prints ONE JSON line with throughput (tokens/s), TFLOP/s against the bf16 MFMA peak, the
@@ -45,19 +46,30 @@ def flops_mamba2(w):
     return w.B * w.H * w.T * (2 * w.C * (w.dk + w.dv) + 4 * w.dk * w.dv)
 
 
-STAGES = ["block_state", "block_scan", "tile_out"]
+STAGES = ["block_state", "scan", "tile_out"]
 KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_mamba2.hip", "paper_2506_04761_amd/csrc/ll_device.hpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tile_out_ll_mamba2_bf16_T65536_hbm_traffic.md")
+
+
+def tree_nodes_read(N):
+    """Block-tree nodes above the blocks that tiles of a sequence of N tiles read: node (l, k)
+    covers blocks [k 2^l, (k+1) 2^l) and is read when k is even and a tile follows its group."""
+    nb = -(-N // 4)
+    count, l = 0, 1
+    while (1 << (l + 2)) < N:
+        count += sum(1 for k in range(0, -(-nb // (1 << l)), 2) if ((k + 1) << (l + 2)) < N)
+        l += 1
+    return count
 
 
 def stage_figures(w, has_lambda=True):
     """Algorithmic work of one launch of each stage: {stage: (flops, bytes)}.
 
     FLOPs follow the convention above.  Bytes: block_state reads k, v and the log-gates and
-    writes the summaries it produces; block_scan reads block summaries and tile totals and writes
-    the upper-level summaries and gaps (lambda == NULL: tile states in, running states out);
-    tile_out reads q, k, v, the log-gates and lambda and writes o -- the path's algorithmic bytes.
-    Summary reads inside tile_out are implementation traffic (see the rocprofv3 counters)."""
+    writes the summaries it produces; scan reads the block summaries and writes the block-tree
+    nodes tiles read (lambda == NULL: tile states in, running states out); tile_out reads q, k,
+    v, the log-gates and lambda and writes o -- the path's algorithmic bytes.  Summary reads
+    inside tile_out are implementation traffic (see the rocprofv3 counters)."""
     es = 2 if w.dtype == "bf16" else 4
     BH, BHT = w.B * w.H, w.B * w.H * w.T
     SZ = w.dk * w.dv
@@ -65,20 +77,18 @@ def stage_figures(w, has_lambda=True):
     R = max(2 * w.C, 64)                     # tile rows
     N = -(-w.T // R)                         # tiles per sequence
     NB = -(-N // 4)                          # 4-tile blocks
-    J = (N - 1).bit_length() if N > 1 else 0  # inter-tile levels
     L = w.levels if has_lambda else 0
     f_state = 2.0 * BHT * w.dk * w.dv
     f_out = BHT * (2 * w.C * (w.dk + w.dv) + (w.dk * w.dv * J_chunk if has_lambda else 2 * w.dk * w.dv))
     if has_lambda:
-        n_state_out = (-(-N // 2) + -(-N // 4) + NB)  # even tile states, pair and block summaries
-        nup = sum(-(-(N - (1 << (j - 1))) // (1 << j)) for j in range(4, J + 1) if N > (1 << (j - 1)))
-        b_scan = BH * ((NB + nup) * SZ * es + N * 4 + N * J * 4)
+        n_state_out = -(-N // 2) + -(-N // 4) + NB  # even tile states, pair and block summaries
+        b_scan = BH * ((NB + tree_nodes_read(N)) * SZ * es + NB * 4)
     else:
         n_state_out = N
         b_scan = BH * (2 * N * SZ * es + N * 4)
     b_state = BHT * ((w.dk + w.dv) * es + 4) + BH * (n_state_out * SZ * es + N * 4)
     b_out = BHT * ((2 * w.dk + 2 * w.dv) * es + 4 + L * 4)
-    return {"block_state": (f_state, b_state), "block_scan": (0.0, b_scan), "tile_out": (f_out, b_out)}
+    return {"block_state": (f_state, b_state), "scan": (0.0, b_scan), "tile_out": (f_out, b_out)}
 
 
 def roofline(w, flops, nbytes, ms):

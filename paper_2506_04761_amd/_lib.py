@@ -162,7 +162,8 @@ def _event_handles(events, n, stream):
 def ll_mamba2_fwd_staged(q, k, v, log_alpha, lam, C, events, out=None, workspace=None, stream=None):
     """As ll_mamba2_fwd, and records the four torch.cuda.Event objects in `events` (created with
     enable_timing=True) on the stream around the three kernel stages: events[i] before stage i
-    (tile states, level scan, tile outputs) and events[3] after the last.  Asynchronous; read
+    (tile states, scan -- summary tree, or running states for lam=None -- and tile outputs) and
+    events[3] after the last.  Asynchronous; read
     the durations with events[i].elapsed_time(events[i + 1]) after synchronising."""
     handles, s = _event_handles(events, 4, stream)
     (B, T, H, dk, dv, code), out, ws = _prepare(LL_MAMBA2, q, k, v, log_alpha, None, lam, C, out, workspace)

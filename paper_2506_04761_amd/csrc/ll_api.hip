@@ -8,7 +8,7 @@
 namespace {
 
 constexpr int kMaxL = 24;          // lambda levels the kernels stage (T <= 2^23)
-constexpr int64_t kMaxTiles = 8192; // tiles per sequence (the gap tree lives in LDS)
+constexpr int64_t kMaxTiles = 8192; // tiles per sequence (the running scan stages their totals in LDS)
 
 inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 inline bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }

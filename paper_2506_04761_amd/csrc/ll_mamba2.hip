@@ -8,17 +8,18 @@
 // the bit length of (tile(t) XOR tile(s)), and are computed from summaries of whole source
 // groups of tiles (the masked Q S products of the chunkwise algorithm, App. C Alg. 1).
 //
-// Three kernels:
+// Kernels:
 //   block_state  per block of 4 tiles: the tile states S_u = sum_t exp(tot_u - cl_t) v_t k_t^T
 //                (MFMA, K = R tokens), folded on chip into the summaries the first three
 //                tile levels read: S_u of even tiles (level 1), the pair summary of tiles 0-1
-//                (level 2) and the whole-block summary (level 3, and the input of the scan).
-//   block_scan   per (b, h), elementwise over state entries, sequential over blocks: the
-//                summaries of the source groups of levels >= 4, and the decay gaps from each
-//                group's end to the tiles that read it.  With lambda == NULL: the single running
-//                state entering every tile.
+//                (level 2) and the whole-block summary (level 3), each with its summed log2-gate.
+//   level_scan   per (b, h), elementwise over state entries: above the blocks the summaries form
+//                a binary tree over the blocks of one sequence (tile level 3 + l for tree level
+//                l), built chunk by chunk.  With lambda == NULL instead (running_scan): the
+//                single running state entering every tile.
 //   tile_out     per tile: the causal R x R masked contraction and, for every set bit j-1 of
-//                the tile index, the lambda-weighted term  lambda_t^(log2 R + j) exp(cl_t + gap) q_t^T U_j.
+//                the tile index, the lambda-weighted term  lambda_t^(log2 R + j) exp(cl_t + gap) q_t^T U_j,
+//                gap_j being the summed totals of the tile's lower-level source groups.
 //
 // Decays are kept in the log2 domain (gates pre-multiplied by log2 e) and every exp2 argument
 // is <= 0: tile-local cumulative sums and exact range sums of tile totals, never differences of
@@ -37,24 +38,63 @@ constexpr int kBlockTiles = 4;    // tiles per block_state workgroup
 constexpr int kKB = 64;           // keys staged in LDS at a time
 constexpr int kMaxLevels = 24;    // Fenwick levels handled (T <= 2^23)
 
-// Device view of the summaries (all in the storage dtype, layout [p][n] = d_v x d_k).
+// Device view of the summaries (all in the storage dtype, layout [p][n] = d_v x d_k) and of their
+// summed log2-gates.  Above the blocks, node (l, k) of the block tree (l >= 1) covers blocks
+// [k 2^l, (k + 1) 2^l), i.e. the tiles of the level-(l + 3) source group with index k.
 template <typename T>
 struct Nodes {
-  T* lvl1;       // [BH][ceil(N/2)]  tile states of even tiles
-  T* lvl2;       // [BH][ceil(N/4)]  pair summaries of tiles 4b, 4b+1
-  T* blocks;     // [BH][NB]         block summaries (4 tiles)
-  T* upper;      // [BH][nup]        levels >= 4
+  T* lvl1;         // [BH][ceil(N/2)]  tile states of even tiles
+  T* lvl2;         // [BH][ceil(N/4)]  pair summaries of tiles 4b, 4b+1
+  T* blocks;       // [BH][NB]         block summaries (4 tiles)
+  T* upper;        // [BH][nup]        block-tree nodes of levels >= 1 (tile levels >= 4)
+  const float* t1; // [BH][N]          tile totals (the level-1 source groups are single tiles)
+  float* t2;       // [BH][ceil(N/4)]  totals of the pairs in lvl2
+  float* t3;       // [BH][NB]         block totals
+  float* tup;      // [BH][nup]        totals of the upper nodes
   int64_t n1, n2, nb, nup;  // per-(b,h) slot counts
-  // Summary of the level-j source group that starts at tile f (f a multiple of 2^j).
+  // Slot of block-tree node (l >= 1, k): tree levels 1 .. l-1 come first, ceil(nb / 2^l') slots each.
+  __device__ __host__ int64_t up_slot(int64_t bh, int l, int64_t k) const {
+    int64_t off = 0;
+    for (int ll = 1; ll < l; ++ll) off += (nb + (int64_t(1) << ll) - 1) >> ll;
+    return bh * nup + off + k;
+  }
+  // Summary of the level-j source group that starts at tile f (f a multiple of 2^(j-1)).
   __device__ __host__ T* at(int64_t bh, int64_t N, int j, int64_t f, int SZ) const {
     if (j == 1) return lvl1 + (bh * n1 + (f >> 1)) * SZ;
     if (j == 2) return lvl2 + (bh * n2 + (f >> 2)) * SZ;
     if (j == 3) return blocks + (bh * nb + (f >> 2)) * SZ;
-    int64_t off = 0;
-    for (int jj = 4; jj < j; ++jj) off += (N + (int64_t(1) << jj) - 1) >> jj;
-    return upper + (bh * nup + off + (f >> j)) * SZ;
+    return upper + up_slot(bh, j - 3, f >> (j - 1)) * SZ;
+  }
+  // Summed log2-gate of the same group.
+  __device__ __host__ float tot(int64_t bh, int64_t N, int j, int64_t f) const {
+    if (j == 1) return t1[bh * N + f];
+    if (j == 2) return t2[bh * n2 + (f >> 2)];
+    if (j == 3) return t3[bh * nb + (f >> 2)];
+    return tup[up_slot(bh, j - 3, f >> (j - 1))];
   }
 };
+
+// Whether block-tree node (l, k) is read: as the level-(l + 3) source group, by the tiles of the
+// next aligned group, when k is even and that group has a tile.  A read node covers whole blocks.
+__device__ __host__ inline bool tree_node_read(int l, int64_t k, int64_t N) {
+  return !(k & 1) && ((k + 1) << (l + 2)) < N;
+}
+
+// Log2-decay gaps of tile u's levels, lane j - 1 holding gap_j: the summed log2-gates of the
+// tiles between the end of level j's source group and u.  Those tiles are exactly the source
+// groups of u's lower set bits, so gap_j is the sum of their totals (an exclusive wave scan).
+template <typename T>
+__device__ inline float level_gaps(const Nodes<T>& nodes, int64_t bh, int64_t N, int64_t u, int J) {
+  const int j = (threadIdx.x & 63) + 1;
+  float t = 0.f;
+  if (j <= J && reads_level(u, j)) t = nodes.tot(bh, N, j, source_first(u, j));
+  return wave_inclusive_scan(t) - t;
+}
+
+// gap_j from the lane-per-level values of level_gaps (j uniform across the wave)
+__device__ inline float gap_of(float gapv, int j) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gapv), j - 1));
+}
 
 // Tile-local inclusive cumulative sum of log2 gates for the R rows of a tile (rows >= nrow get
 // a zero gate), computed by the first 4 waves of the workgroup (R/4 <= 64 rows each) into cl_s[R].
@@ -248,13 +288,16 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
           out_s[slot][p * DK + n] = from_f32<T>(x[i][jn][r]);
         }
   };
+  // (streaming stores: the summaries are read back by later kernels, not from the caches this
+  // kernel's K/V stream passes through)
   auto flush = [&](int slot, T* dst) {
     constexpr int PASSES = (SZ / VEC + kStateThreads - 1) / kStateThreads;
 #pragma unroll
     for (int it = 0; it < PASSES; ++it) {
       const int idx = tid + it * kStateThreads;
       if ((SZ / VEC) % kStateThreads == 0 || idx < SZ / VEC)
-        *reinterpret_cast<V16*>(dst + idx * VEC) = *reinterpret_cast<const V16*>(&out_s[slot][idx * VEC]);
+        __builtin_nontemporal_store(*reinterpret_cast<const V16*>(&out_s[slot][idx * VEC]),
+                                    reinterpret_cast<V16*>(dst + idx * VEC));
     }
   };
 
@@ -307,6 +350,12 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
         if ((a & 1) == 0) dst0 = nodes.at(bh, N, 1, u, SZ);                // even tile: its own state
         if (a == 1) dst1 = nodes.at(bh, N, 2, u - 1, SZ);                  // pair summary, tiles 0-1
         if (a == kBlockTiles - 1) dst1 = nodes.at(bh, N, 3, u - 3, SZ);    // block summary
+        if (tid == 0 && a == 1) nodes.t2[bh * nodes.n2 + blk] = cl_s[R - 1] + cl_s[2 * R - 1];
+        if (tid == 0 && a == kBlockTiles - 1) {
+          float t = 0.f;
+          for (int x = 0; x < kBlockTiles; ++x) t += cl_s[x * R + R - 1];
+          nodes.t3[bh * nodes.nb + blk] = t;
+        }
       } else {
         dst0 = tiles + (bh * N + u) * SZ;
       }
@@ -329,149 +378,125 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
       else step(a, kb, kr1, vr1);
     }
   }
+
 }
 
 // ---------------------------------------------------------------------------------------------
-// Kernel 2: block scan.  grid.x = element blocks + 1; the extra workgroup computes the gaps.
-//
-// Summaries (elementwise over the d_v*d_k state entries, 2 per thread, sequential over the
-// blocks of one (b, h)): tile level j >= 4 is block level jb = j - 2 (groups of 2^(jb-1) blocks).
-// The source groups are the even-indexed groups; inside one, acc <- exp2(block total) acc +
-// block summary, reset at the group start; the summary is stored at the group end.
-// lambda == NULL: the running state entering tile u, R_0 = 0, R_{u+1} = exp2(tot_u) R_u + S_u.
-//
-// Gaps: gap_j(u) = sum of tile totals over the tiles of u's own aligned 2^(j-1)-tile block that
-// precede u.  That range is the union, over the set bits k <= j-2 of u, of the aligned 2^k-tile
-// blocks ending where the next one starts, so gap_j(u) = gap_(j-1)(u) + [bit j-2 of u] *
-// (sum of tot over the 2^(j-2)-block with index (u >> (j-2)) - 1): a sum over exact ranges,
-// built from a tree of block sums in LDS.
+// Kernel 2 (lambda given): the block tree.  grid (d_v*d_k / 512, B * H); each thread owns two
+// state entries of one (b, h).  Node (l, k) of tree level l >= 1 summarises blocks
+// [k 2^l, (k + 1) 2^l):  node(l, k) = exp2(total of node(l-1, 2k+1)) node(l-1, 2k) + node(l-1, 2k+1).
+// The blocks are taken in chunks of kScanChunk: the chunk's block summaries are loaded together
+// (the next chunk's loads issued before the current chunk is used), the levels inside the chunk
+// are built in registers (fp32), and each level above accumulates the chunk nodes across chunks.
+// Nodes some tile reads are stored (bf16 or the storage type).  The node totals come from a tree
+// of block totals in LDS; workgroup x = 0 stores them.
 // ---------------------------------------------------------------------------------------------
-constexpr int kMaxGapTiles = 8192;  // tiles per sequence the scan stages in LDS (T <= 8192 R)
-constexpr int kScanUnroll = 8;      // summary loads in flight per thread
+constexpr int kScanChunk = 32;      // blocks per chunk
+constexpr int kScanChunkLevels = 5; // tree levels inside a chunk
+constexpr int kScanThreads = 256;
 
-// Gaps of every (tile, level) of one (b, h): one workgroup, block sums in LDS (see above).
-__device__ inline void scan_gaps(float* dyn_s, const float* __restrict__ tot, float* __restrict__ gaps, int64_t N,
-                                 int J) {
-  const int tid = threadIdx.x;
-  float* bs = dyn_s;  // level k block sums follow level k-1's (level 0 = the tile totals)
-  for (int64_t u = tid; u < N; u += 256) bs[u] = tot[u];
-  __syncthreads();
-  int64_t off_prev = 0, off = N;
-  for (int k = 1; k < J; ++k) {
-    const int64_t len = N >> k;
-    for (int64_t m = tid; m < len; m += 256) bs[off + m] = bs[off_prev + 2 * m] + bs[off_prev + 2 * m + 1];
-    __syncthreads();
-    off_prev = off;
-    off += len;
-  }
-  for (int64_t u = tid; u < N; u += 256) {
-    float gsum = 0.f;
-    int64_t ok = 0;  // offset of the level-(j-2) block sums
-    for (int j = 1; j <= J; ++j) {
-      if (j >= 2) {
-        const int k = j - 2;
-        if ((u >> k) & 1) gsum += bs[ok + (u >> k) - 1];
-        ok += N >> k;
-      }
-      gaps[u * J + (j - 1)] = gsum;
-    }
-  }
-}
-
-// lambda given: grid (element blocks of 512 + 1, B * H).  Each thread owns two state entries and
-// walks the blocks of its (b, h) in order, keeping one accumulator per level >= 4.  JMAX bounds
-// J at compile time so that the unrolled per-block level loop stays short (the launch picks the
-// smallest instance with JMAX >= J).
-template <typename T, int JMAX>
-__global__ __launch_bounds__(256) void k_level_scan(Nodes<T> nodes, const float* __restrict__ tot2,
-                                                    float* __restrict__ gaps2, int64_t N, int J, int SZ) {
+template <typename T, int LMAX>
+__global__ __launch_bounds__(kScanThreads) void k_level_scan(Nodes<T> nodes, int64_t N, int J, int SZ) {
   typedef T T2 __attribute__((ext_vector_type(2)));
-  extern __shared__ float dyn_s[];  // gaps: 2 N floats; summaries: the NB block totals
+  constexpr int CB = kScanChunk, CL = kScanChunkLevels;
+  extern __shared__ float tt_s[];  // totals tree: level 0 (blocks) first, then level 1, ...
   const int64_t bh = blockIdx.y;
   const int tid = threadIdx.x;
-  const float* tot = tot2 + bh * N;
-  if (blockIdx.x == gridDim.x - 1) {
-    if (J > 0) scan_gaps(dyn_s, tot, gaps2 + bh * N * J, N, J);
-    return;
-  }
-  const int64_t NB = (N + kBlockTiles - 1) / kBlockTiles;
-  float* btot_s = dyn_s;
-  for (int64_t bl = tid; bl < NB; bl += 256) {
-    float t = 0.f;
-    for (int a = 0; a < kBlockTiles; ++a)
-      if (bl * kBlockTiles + a < N) t += tot[bl * kBlockTiles + a];
-    btot_s[bl] = t;
-  }
+  const int64_t nb = nodes.nb;
+  const int64_t nbp = (nb + CB - 1) / CB * CB;  // blocks rounded up to whole chunks
+  const int LB = J - 3;                         // highest tree level with a read node
+  const int LT = LB > CL ? LB : CL;             // levels of the totals tree (the chunk's at least)
+  auto toff = [&](int l) {
+    int64_t o = 0;
+    for (int x = 0; x < l; ++x) o += (nbp + (int64_t(1) << x) - 1) >> x;
+    return o;
+  };
+  // ---- totals tree (blocks past the last whole one count 0; no read node covers them)
+  for (int64_t m = tid; m < nbp; m += kScanThreads) tt_s[m] = (m + 1) * kBlockTiles <= N ? nodes.t3[bh * nb + m] : 0.f;
   __syncthreads();
-  const int e0 = (blockIdx.x * 256 + tid) * 2;
-  if (J < 4 || e0 >= SZ) return;
-
-  // output slot base of each level: levels 4 .. j-1 come first, ceil(N / 2^jj) slots each
-  int64_t lvl_off[JMAX + 1];
-  {
-    int64_t off = 0;
-#pragma unroll
-    for (int j = 4; j <= JMAX; ++j) {
-      lvl_off[j] = off;
-      if (j <= J) off += (N + (int64_t(1) << j) - 1) >> j;
+  for (int l = 1; l <= LT; ++l) {
+    const int64_t o = toff(l), op = toff(l - 1), n = (nbp + (int64_t(1) << l) - 1) >> l;
+    const int64_t np = (nbp + (int64_t(1) << (l - 1)) - 1) >> (l - 1);
+    for (int64_t k = tid; k < n; k += kScanThreads)
+      tt_s[o + k] = tt_s[op + 2 * k] + (2 * k + 1 < np ? tt_s[op + 2 * k + 1] : 0.f);
+    __syncthreads();
+  }
+  auto tt = [&](int l, int64_t k) { return tt_s[toff(l) + k]; };
+  if (blockIdx.x == 0) {
+    for (int l = 1; l <= LB; ++l) {
+      const int64_t n = (nbp + (int64_t(1) << l) - 1) >> l;
+      for (int64_t k = tid; k < n; k += kScanThreads)
+        if (tree_node_read(l, k, N)) nodes.tup[nodes.up_slot(bh, l, k)] = tt(l, k);
     }
   }
-  T* const up = nodes.upper + bh * nodes.nup * SZ + e0;
-  const T* const src = nodes.blocks + bh * nodes.nb * SZ + e0;
-  float a0[JMAX + 1], a1[JMAX + 1];
+  const int e0 = (blockIdx.x * kScanThreads + tid) * 2;
+  if (e0 >= SZ) return;
+
+  const T* src = nodes.blocks + bh * nb * SZ + e0;
+  auto store = [&](int l, int64_t k, float a0, float a1) {
+    T2 out;
+    out[0] = from_f32<T>(a0);
+    out[1] = from_f32<T>(a1);
+    *reinterpret_cast<T2*>(nodes.upper + nodes.up_slot(bh, l, k) * SZ + e0) = out;
+  };
+  auto load_chunk = [&](int64_t c, T2 (&x)[CB]) {
 #pragma unroll
-  for (int j = 0; j <= JMAX; ++j) a0[j] = a1[j] = 0.f;
-  // batches of kScanUnroll blocks; the next batch's loads are issued before the current one is used
-  auto load_batch = [&](int64_t bl0, T2 (&sv)[kScanUnroll]) {
-#pragma unroll
-    for (int i = 0; i < kScanUnroll; ++i) {
-      const int64_t bl = bl0 + i < NB ? bl0 + i : NB - 1;
-      sv[i] = *reinterpret_cast<const T2*>(src + bl * SZ);
+    for (int i = 0; i < CB; ++i) {
+      const int64_t m = c * CB + i < nb ? c * CB + i : nb - 1;
+      x[i] = *reinterpret_cast<const T2*>(src + m * SZ);
     }
   };
-  auto use_batch = [&](int64_t bl0, const T2 (&sv)[kScanUnroll]) {
+  float acc0[LMAX + 1], acc1[LMAX + 1];  // levels above the chunk
 #pragma unroll
-    for (int i = 0; i < kScanUnroll; ++i) {
-      const int64_t bl = bl0 + i;
-      if (bl < NB) {
-        // the block's decay is the same for every lane: keep it in a scalar register
-        const float e = __builtin_bit_cast(
-            float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, fast_exp2(btot_s[bl]))));
-        const float s0 = to_f32(sv[i][0]), s1 = to_f32(sv[i][1]);
+  for (int l = 0; l <= LMAX; ++l) acc0[l] = acc1[l] = 0.f;
+  auto use_chunk = [&](int64_t c, const T2 (&x)[CB]) {
+    float v0[CB], v1[CB];
 #pragma unroll
-        for (int j = 4; j <= JMAX; ++j) {
-          // tile level j: groups of 2^(j-3) blocks; every group is accumulated (the decay factor
-          // is 0 at a group's first block), the even-indexed ones (source groups) are stored.
-          // Levels above J never satisfy the store condition.
-          const int sh = j - 3;
-          const int64_t m = bl >> sh;
-          const float ej = (bl & ((int64_t(1) << sh) - 1)) == 0 ? 0.f : e;
-          a0[j] = a0[j] * ej + s0;
-          a1[j] = a1[j] * ej + s1;
-          if (!(m & 1)) {
-            const bool last = ((bl + 1) & ((int64_t(1) << sh) - 1)) == 0;
-            const int64_t first_tile = (m << sh) * kBlockTiles;
-            if (last && first_tile + (int64_t(1) << (j - 1)) < N) {
-              T2 out;
-              out[0] = from_f32<T>(a0[j]);
-              out[1] = from_f32<T>(a1[j]);
-              *reinterpret_cast<T2*>(up + (lvl_off[j] + (first_tile >> j)) * SZ) = out;
-            }
-          }
-        }
+    for (int i = 0; i < CB; ++i) {
+      v0[i] = to_f32(x[i][0]);
+      v1[i] = to_f32(x[i][1]);
+    }
+#pragma unroll
+    for (int l = 1; l <= CL; ++l) {
+#pragma unroll
+      for (int i = 0; i < (CB >> l); ++i) {
+        const int64_t k = ((c * CB) >> l) + i;
+        const float e = fast_exp2(tt(l - 1, 2 * k + 1));
+        v0[i] = e * v0[2 * i] + v0[2 * i + 1];
+        v1[i] = e * v1[2 * i] + v1[2 * i + 1];
+        if (l <= LB && tree_node_read(l, k, N)) store(l, k, v0[i], v1[i]);
       }
     }
+    // v0[0], v1[0]: the whole chunk, node (CL, c)
+#pragma unroll
+    for (int l = CL + 1; l <= LMAX; ++l) {
+      if (l > LB) break;
+      const int sh = l - CL;
+      const bool first = (c & ((int64_t(1) << sh) - 1)) == 0;
+      const float e = first ? 0.f : fast_exp2(tt(CL, c));
+      acc0[l] = acc0[l] * e + v0[0];
+      acc1[l] = acc1[l] * e + v1[0];
+      const int64_t k = c >> sh;
+      if (((c + 1) & ((int64_t(1) << sh) - 1)) == 0 && tree_node_read(l, k, N)) store(l, k, acc0[l], acc1[l]);
+    }
   };
-  T2 sa[kScanUnroll], sb[kScanUnroll];
-  load_batch(0, sa);
-  for (int64_t bl0 = 0; bl0 < NB; bl0 += 2 * kScanUnroll) {
-    if (bl0 + kScanUnroll < NB) load_batch(bl0 + kScanUnroll, sb);
-    use_batch(bl0, sa);
-    if (bl0 + kScanUnroll >= NB) break;
-    if (bl0 + 2 * kScanUnroll < NB) load_batch(bl0 + 2 * kScanUnroll, sa);
-    use_batch(bl0 + kScanUnroll, sb);
+  const int64_t nch = nbp / CB;
+  T2 xa[CB], xb[CB];
+  load_chunk(0, xa);
+  for (int64_t c = 0; c < nch; c += 2) {
+    if (c + 1 < nch) load_chunk(c + 1, xb);
+    use_chunk(c, xa);
+    if (c + 1 >= nch) break;
+    if (c + 2 < nch) load_chunk(c + 2, xa);
+    use_chunk(c + 1, xb);
   }
 }
+
+// ---------------------------------------------------------------------------------------------
+// Kernel 2 (lambda == NULL only): running scan, elementwise over the d_v*d_k state entries
+// (2 per thread), sequential over the tiles of one (b, h).
+// ---------------------------------------------------------------------------------------------
+constexpr int kScanUnroll = 8;      // summary loads in flight per thread
 
 // lambda == NULL: the running state entering each tile, R_0 = 0, R_(u+1) = exp2(tot_u) R_u + S_u.
 template <typename T>
@@ -560,8 +585,8 @@ struct RowMap {
 template <typename T, int C, int DK, int DV, bool HAS_LAMBDA>
 __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ log_alpha,
-    const float* __restrict__ lam, Nodes<T> nodes, const T* __restrict__ running, const float* __restrict__ gaps2,
-    T* __restrict__ o, int64_t Tlen, int H, int L, int J) {
+    const float* __restrict__ lam, Nodes<T> nodes, const T* __restrict__ running, T* __restrict__ o, int64_t Tlen,
+    int H, int L, int J) {
   using M = Mfma<T>;
   typedef typename Vec16<T>::type V16;
   constexpr int R = tile_rows(C);
@@ -639,9 +664,11 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
 
   // ---- summaries of the inter-tile levels (set bits of u); the first one is prefetched while
   //      the last key block is being used, each next one while the current level is
+  float gapv = 0.f;
+  if constexpr (HAS_LAMBDA) gapv = level_gaps(nodes, bh, N, u, J);
   auto level_src = [&](int j, float* gap) -> const T* {
     if constexpr (HAS_LAMBDA) {
-      *gap = gaps2[(bh * N + u) * J + (j - 1)];
+      *gap = gap_of(gapv, j);
       return nodes.at(bh, N, j, source_first(u, j), SZ);
     } else {
       *gap = 0.f;
@@ -937,7 +964,7 @@ template <int DK, int DV, bool HAS_LAMBDA>
 __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const float* __restrict__ log_alpha, const float* __restrict__ lam, Nodes<__bf16> nodes,
-    const __bf16* __restrict__ running, const float* __restrict__ gaps2, __bf16* __restrict__ o, int64_t Tlen,
+    const __bf16* __restrict__ running, __bf16* __restrict__ o, int64_t Tlen,
     int H, int L, int J) {
   using M = Mfma<__bf16>;
   typedef __bf16 bf;
@@ -981,6 +1008,9 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
   lds_copy_rows<DK, R, NT>(k_s, k + (row0 * H + h) * DK, (int64_t)H * DK, nrow);
   lds_copy_rows<DV, R, NT>(v_s, v + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
   if constexpr (HAS_LAMBDA) lds_copy_lambda<R, NT>(lam_s, lam, row0, H, h, L, nrow);
+  // decay gaps of the tile's levels, lane j - 1 holding level j's
+  float gapv = 0.f;
+  if constexpr (HAS_LAMBDA) gapv = level_gaps(nodes, bh, N, u, J);
   // keep the first use of the gate below every load issue: a use scheduled earlier makes the
   // wave wait for the gate before the remaining loads are issued
   __builtin_amdgcn_sched_barrier(0);
@@ -1008,7 +1038,7 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
   // ---- inter-tile levels (set bits of u): summaries alternate between the K and V regions
   auto level_src = [&](int j, float* gap) -> const bf* {
     if constexpr (HAS_LAMBDA) {
-      *gap = gaps2[(bh * N + u) * J + (j - 1)];
+      *gap = gap_of(gapv, j);
       return nodes.at(bh, N, j, source_first(u, j), SZ);
     } else {
       *gap = 0.f;
@@ -1131,15 +1161,18 @@ int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv
   w.n2 = (N + 3) / 4;
   w.nb = (N + kBlockTiles - 1) / kBlockTiles;
   w.nup = 0;
-  for (int j = 4; j <= J; ++j) w.nup += (N + (int64_t(1) << j) - 1) >> j;
+  for (int l = 1; l <= J - 3; ++l) w.nup += (w.nb + (int64_t(1) << l) - 1) >> l;  // block-tree levels
+  const int64_t nup1 = w.nup > 0 ? w.nup : 1;
   int64_t cur = 0;
   w.tot2 = cur; cur += al(BH * N * 4);
   if (has_lambda) {
-    w.gaps2 = cur; cur += al(BH * N * (J > 0 ? J : 1) * 4);
+    w.t2 = cur; cur += al(BH * w.n2 * 4);
+    w.t3 = cur; cur += al(BH * w.nb * 4);
+    w.tup = cur; cur += al(BH * nup1 * 4);
     w.lvl1 = cur; cur += al(BH * w.n1 * SZ * esize);
     w.lvl2 = cur; cur += al(BH * w.n2 * SZ * esize);
     w.blocks = cur; cur += al(BH * w.nb * SZ * esize);
-    w.upper = cur; cur += al(BH * (w.nup > 0 ? w.nup : 1) * SZ * esize);
+    w.upper = cur; cur += al(BH * nup1 * SZ * esize);
   } else {
     w.tiles = cur; cur += al(BH * N * SZ * esize);
     w.running = cur; cur += al(BH * N * SZ * esize);
@@ -1149,8 +1182,9 @@ int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv
   return cur;
 }
 
-// Enqueues the three stages on `st`.  With `ev` non-null, ev[i] is recorded before stage i
-// and ev[3] after the last one (used by the staged entry point).
+// Enqueues the stages on `st`.  With `ev` non-null, ev[i] is recorded before stage i and ev[3]
+// after the last one (used by the staged entry point): stage 0 block_state, stage 1 the level
+// scan (lambda given) or the running scan (lambda == NULL), stage 2 tile_out.
 template <typename T, int C, int DK, int DV>
 hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
   constexpr int SZ = DK * DV;
@@ -1161,13 +1195,15 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
   Nodes<T> nodes{};
   T* tiles = nullptr;
   T* running = nullptr;
-  float* gaps2 = nullptr;
+  nodes.t1 = tot2;
   if (a.lambda) {
-    gaps2 = reinterpret_cast<float*>(base + w.gaps2);
     nodes.lvl1 = reinterpret_cast<T*>(base + w.lvl1);
     nodes.lvl2 = reinterpret_cast<T*>(base + w.lvl2);
     nodes.blocks = reinterpret_cast<T*>(base + w.blocks);
     nodes.upper = reinterpret_cast<T*>(base + w.upper);
+    nodes.t2 = reinterpret_cast<float*>(base + w.t2);
+    nodes.t3 = reinterpret_cast<float*>(base + w.t3);
+    nodes.tup = reinterpret_cast<float*>(base + w.tup);
     nodes.n1 = w.n1;
     nodes.n2 = w.n2;
     nodes.nb = w.nb;
@@ -1177,55 +1213,54 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
     running = reinterpret_cast<T*>(base + w.running);
   }
   const dim3 gblk((unsigned)(w.nb * a.H * a.B));
-  const dim3 gscan((unsigned)((SZ / 2 + 255) / 256 + 1), (unsigned)(a.B * a.H));
+  const dim3 gscan((unsigned)((SZ / 2 + 255) / 256), (unsigned)(a.B * a.H));
   constexpr bool kFast = std::is_same<T, __bf16>::value && tile_rows(C) == kFastRows;
   const dim3 gtile((unsigned)(w.N * (kFast ? 1 : RowMap<tile_rows(C)>::RS) * a.H * a.B));
   if (ev) (void)hipEventRecord(ev[0], st);
-  if (a.lambda)
+  if (a.lambda) {
     hipLaunchKernelGGL((k_block_state<T, C, DK, DV, true>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
                        a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H);
-  else
+  } else {
     hipLaunchKernelGGL((k_block_state<T, C, DK, DV, false>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
                        a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H);
+  }
   if (ev) (void)hipEventRecord(ev[1], st);
-  // the level scan is instantiated for the smallest level bound >= J
-  auto level_scan = [&](auto jmax_c) {
-    hipLaunchKernelGGL((k_level_scan<T, decltype(jmax_c)::value>), gscan, dim3(256), 2 * w.N * sizeof(float), st,
-                       nodes, (const float*)tot2, gaps2, w.N, w.J, SZ);
-  };
-  if (a.lambda && w.J <= 8)
-    level_scan(std::integral_constant<int, 8>{});
-  else if (a.lambda && w.J <= 10)
-    level_scan(std::integral_constant<int, 10>{});
-  else if (a.lambda && w.J <= 12)
-    level_scan(std::integral_constant<int, 12>{});
-  else if (a.lambda && w.J <= 16)
-    level_scan(std::integral_constant<int, 16>{});
-  else if (a.lambda)
-    hipLaunchKernelGGL((k_level_scan<T, kMaxLevels>), gscan, dim3(256), 2 * w.N * sizeof(float), st, nodes,
-                       (const float*)tot2, gaps2, w.N, w.J, SZ);
-  else
-    hipLaunchKernelGGL((k_running_scan<T>), dim3(gscan.x - 1, gscan.y), dim3(256), w.N * sizeof(float), st,
-                       (const T*)tiles, running, (const float*)tot2, w.N, SZ);
+  if (a.lambda && w.J >= 4) {
+    // LDS: the totals tree (the block count rounded up to whole chunks, and its levels)
+    const int64_t nbp = (w.nb + kScanChunk - 1) / kScanChunk * kScanChunk;
+    int64_t tt = 0;
+    const int lt = w.J - 3 > kScanChunkLevels ? w.J - 3 : kScanChunkLevels;
+    for (int l = 0; l <= lt; ++l) tt += (nbp + (int64_t(1) << l) - 1) >> l;
+    const dim3 glev((unsigned)((SZ + 2 * kScanThreads - 1) / (2 * kScanThreads)), (unsigned)(a.B * a.H));
+    if (w.J - 3 <= kScanChunkLevels)
+      hipLaunchKernelGGL((k_level_scan<T, kScanChunkLevels>), glev, dim3(kScanThreads), tt * sizeof(float), st, nodes,
+                         w.N, w.J, SZ);
+    else
+      hipLaunchKernelGGL((k_level_scan<T, kMaxLevels>), glev, dim3(kScanThreads), tt * sizeof(float), st, nodes, w.N,
+                         w.J, SZ);
+  }
+  if (!a.lambda)
+    hipLaunchKernelGGL((k_running_scan<T>), gscan, dim3(256), w.N * sizeof(float), st, (const T*)tiles, running,
+                       (const float*)tot2, w.N, SZ);
   if (ev) (void)hipEventRecord(ev[2], st);
   if constexpr (kFast) {
     if (a.lambda)
       hipLaunchKernelGGL((k_tile_out_fast<DK, DV, true>), gtile, dim3(kFastThreads), 0, st, (const T*)a.q,
-                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running,
-                         (const float*)gaps2, (T*)a.o, a.T, (int)a.H, a.L, w.J);
+                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (T*)a.o, a.T,
+                         (int)a.H, a.L, w.J);
     else
       hipLaunchKernelGGL((k_tile_out_fast<DK, DV, false>), gtile, dim3(kFastThreads), 0, st, (const T*)a.q,
-                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running,
-                         (const float*)gaps2, (T*)a.o, a.T, (int)a.H, a.L, w.J);
+                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (T*)a.o, a.T,
+                         (int)a.H, a.L, w.J);
   } else {
     if (a.lambda)
       hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, true>), gtile, dim3(RowMap<tile_rows(C)>::NT), 0, st, (const T*)a.q,
-                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running,
-                         (const float*)gaps2, (T*)a.o, a.T, (int)a.H, a.L, w.J);
+                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (T*)a.o, a.T,
+                         (int)a.H, a.L, w.J);
     else
       hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, false>), gtile, dim3(RowMap<tile_rows(C)>::NT), 0, st, (const T*)a.q,
-                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running,
-                         (const float*)gaps2, (T*)a.o, a.T, (int)a.H, a.L, w.J);
+                         (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (T*)a.o, a.T,
+                         (int)a.H, a.L, w.J);
   }
   if (ev) (void)hipEventRecord(ev[3], st);
   return hipGetLastError();
