@@ -385,15 +385,16 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
 // Kernel 2 (lambda given): the block tree.  grid (d_v*d_k / 512, B * H); each thread owns two
 // state entries of one (b, h).  Node (l, k) of tree level l >= 1 summarises blocks
 // [k 2^l, (k + 1) 2^l):  node(l, k) = exp2(total of node(l-1, 2k+1)) node(l-1, 2k) + node(l-1, 2k+1).
-// The blocks are taken in chunks of kScanChunk: the chunk's block summaries are loaded together
-// (the next chunk's loads issued before the current chunk is used), the levels inside the chunk
-// are built in registers (fp32), and each level above accumulates the chunk nodes across chunks.
+// The blocks are taken in chunks of kScanChunk, a batch of chunks loaded together (128 block
+// summaries for bf16: one load latency for a 512-tile sequence), the levels inside a chunk built
+// in registers (fp32), and each level above accumulating the chunk nodes across chunks.
 // Nodes some tile reads are stored (bf16 or the storage type).  The node totals come from a tree
 // of block totals in LDS; workgroup x = 0 stores them.
 // ---------------------------------------------------------------------------------------------
 constexpr int kScanChunk = 32;      // blocks per chunk
 constexpr int kScanChunkLevels = 5; // tree levels inside a chunk
 constexpr int kScanThreads = 256;
+constexpr int kScanBatch = 4;       // chunks whose loads are in flight together (bf16; half for fp32)
 
 template <typename T, int LMAX>
 __global__ __launch_bounds__(kScanThreads) void k_level_scan(Nodes<T> nodes, int64_t N, int J, int SZ) {
@@ -480,15 +481,17 @@ __global__ __launch_bounds__(kScanThreads) void k_level_scan(Nodes<T> nodes, int
       if (((c + 1) & ((int64_t(1) << sh) - 1)) == 0 && tree_node_read(l, k, N)) store(l, k, acc0[l], acc1[l]);
     }
   };
+  // batches of kScanBatch chunks: every load of a batch is issued before its first chunk is used
+  constexpr int NBAT = kScanBatch * sizeof(__bf16) / sizeof(T);
   const int64_t nch = nbp / CB;
-  T2 xa[CB], xb[CB];
-  load_chunk(0, xa);
-  for (int64_t c = 0; c < nch; c += 2) {
-    if (c + 1 < nch) load_chunk(c + 1, xb);
-    use_chunk(c, xa);
-    if (c + 1 >= nch) break;
-    if (c + 2 < nch) load_chunk(c + 2, xa);
-    use_chunk(c + 1, xb);
+  for (int64_t c0 = 0; c0 < nch; c0 += NBAT) {
+    T2 x[NBAT][CB];
+#pragma unroll
+    for (int bi = 0; bi < NBAT; ++bi)
+      if (c0 + bi < nch) load_chunk(c0 + bi, x[bi]);
+#pragma unroll
+    for (int bi = 0; bi < NBAT; ++bi)
+      if (c0 + bi < nch) use_chunk(c0 + bi, x[bi]);
   }
 }
 
