@@ -1102,19 +1102,29 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
     level_step(j, gap, v_s, k_s);
   }
 
-  // ---- store O: lane holds rows iA, iB, d_v entries 16 mt + 4g .. +3
-  auto store_rows = [&](const f32x4* acc, int i) {
-    bf* orow = o + ((row0 + i) * H + h) * DV + 4 * g;
+  // ---- store O through LDS: the lane's pieces (rows iA, iB, d_v entries 16 mt + 4g .. +3) go to
+  //      a swizzled row-major tile in the V region, then whole rows leave as 16-byte pieces, 16
+  //      consecutive lanes per 256-byte row
+  __syncthreads();  // every wave is done with the last summary
+  auto stage_rows = [&](const f32x4* acc, int i) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       bf16x4 val;
 #pragma unroll
       for (int r = 0; r < 4; ++r) val[r] = from_f32<bf>(acc[mt][r]);
-      *reinterpret_cast<bf16x4*>(orow + mt * 16) = val;
+      *reinterpret_cast<bf16x4*>(v_s + swz<DV>(i, 2 * mt + (g >> 1)) + 4 * (g & 1)) = val;
     }
   };
-  if (iA < nrow) store_rows(oA, iA);
-  if (liveB) store_rows(oB, iB);
+  stage_rows(oA, iA);
+  stage_rows(oB, iB);
+  __syncthreads();
+  constexpr int OCH = DV / 8;  // 16-byte pieces per row
+#pragma unroll
+  for (int it = 0; it < R * OCH / NT; ++it) {
+    const int idx = it * NT + tid, r = idx / OCH, c = idx % OCH;
+    if (r < nrow)
+      *reinterpret_cast<bf16x8*>(o + ((row0 + r) * H + h) * DV + 8 * c) = *reinterpret_cast<const bf16x8*>(v_s + swz<DV>(r, c));
+  }
 }
 
 // ---------------------------------------------------------------------------------------------
