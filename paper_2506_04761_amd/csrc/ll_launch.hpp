@@ -14,7 +14,7 @@ struct WsLayout {
   int J = 0;           // inter-tile levels
   int64_t n1 = 0, n2 = 0, nb = 0, nup = 0;  // per-(b,h) summary slots: levels 1, 2, 3 (blocks), >= 4
   int64_t tot2 = 0, t2 = 0, t3 = 0, lvl1 = 0, lvl2 = 0, blocks = 0, upper = 0, tup = 0, cnt = 0;
-  int64_t tiles = 0, running = 0;
+  int64_t tiles = 0, running = 0, cl = 0;
   int64_t total = 0;
 };
 

@@ -51,6 +51,7 @@ struct Nodes {
   float* t2;       // [BH][ceil(N/4)]  totals of the pairs in lvl2
   float* t3;       // [BH][NB]         block totals
   float* tup;      // [BH][nup]        totals of the upper nodes
+  float* cl;       // [BH][N][R]       tile-local inclusive cumulative log2-gates (rows past T repeat the last)
   int64_t n1, n2, nb, nup;  // per-(b,h) slot counts
   // Slot of block-tree node (l >= 1, k): tree levels 1 .. l-1 come first, ceil(nb / 2^l') slots each.
   __device__ __host__ int64_t up_slot(int64_t bh, int l, int64_t k) const {
@@ -265,6 +266,7 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
     __syncthreads();
     for (int w = (a * R) / 64; w < wave; ++w) cl += wsum_s[w];  // preceding waves of this tile
     if (tid < GATES) cl_s[tid] = cl;
+    if (tid < GATES && a < ntile) nodes.cl[(bh * N + u0) * R + tid] = cl;
     __syncthreads();
     if (tid < GATES) dec_s[tid] = valid ? fast_exp2(cl_s[a * R + R - 1] - cl) : 0.f;
     if (tid < ntile) tot2_out[bh * N + u0 + tid] = cl_s[tid * R + R - 1];
@@ -982,7 +984,6 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
   __shared__ float lam_s[HAS_LAMBDA ? R * kMaxLevels : 1];
   __shared__ float cl_s[R];
   __shared__ float kdec_s[R];
-  __shared__ float wsum_s[4];
 
   const int64_t N = (Tlen + R - 1) / R;
   const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // logical order (b, h, u)
@@ -997,8 +998,9 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
   const int iA = 16 * gA + r16, iB = 16 * gB + r16;
   const bool liveB = 16 * gB < nrow;           // nrow is a multiple of C = 64
 
-  // ---- loads: gates first (needed first), then Q into registers, then K, V, lambda into LDS
-  const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);
+  // ---- loads: the tile's cumulative log2-gates (written by block_state) first, then Q into
+  //      registers, then K, V, lambda into LDS
+  lds_gather4<NT>(cl_s, R, [&](int x) { return nodes.cl + (bh * N + u) * R + x; });
   frag qA[KS], qB[KS];
   {
     const int rA = iA < nrow ? iA : nrow - 1, rB = iB < nrow ? iB : nrow - 1;
@@ -1014,13 +1016,10 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
   // decay gaps of the tile's levels, lane j - 1 holding level j's
   float gapv = 0.f;
   if constexpr (HAS_LAMBDA) gapv = level_gaps(nodes, bh, N, u, J);
-  // keep the first use of the gate below every load issue: a use scheduled earlier makes the
-  // wave wait for the gate before the remaining loads are issued
-  __builtin_amdgcn_sched_barrier(0);
-  tile_cumsum_of<R>(la, nrow, cl_s, wsum_s);
-  for (int r = tid; r < R; r += NT) kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
   wait_vmem();
-  __syncthreads();  // K, V, lambda, kdec visible
+  __syncthreads();  // gates, K, V, lambda visible
+  for (int r = tid; r < R; r += NT) kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
+  __syncthreads();  // kdec visible
   if (!liveB) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qB[ks] = frag{};  // rows past the end contribute nothing
@@ -1178,6 +1177,7 @@ int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv
   const int64_t nup1 = w.nup > 0 ? w.nup : 1;
   int64_t cur = 0;
   w.tot2 = cur; cur += al(BH * N * 4);
+  w.cl = cur; cur += al(BH * N * tile_rows((int)C) * 4);
   if (has_lambda) {
     w.t2 = cur; cur += al(BH * w.n2 * 4);
     w.t3 = cur; cur += al(BH * w.nb * 4);
@@ -1209,6 +1209,7 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
   T* tiles = nullptr;
   T* running = nullptr;
   nodes.t1 = tot2;
+  nodes.cl = reinterpret_cast<float*>(base + w.cl);
   if (a.lambda) {
     nodes.lvl1 = reinterpret_cast<T*>(base + w.lvl1);
     nodes.lvl2 = reinterpret_cast<T*>(base + w.lvl2);
