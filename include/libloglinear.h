@@ -81,6 +81,17 @@ ll_status ll_mamba2_fwd(const void* q, const void* k, const void* v, const float
                         int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                         void* workspace, size_t workspace_bytes, void* stream);
 
+/* Log-linear Mamba-2 forward with query/key heads shared by groups of heads: q and k are
+ * [B, T, H_qk, d_k] and head h (of H) uses query/key head h / (H / H_qk); v, o, log_alpha and
+ * lambda keep H heads.  H_qk = 1 is the multi-value form of Mamba-2 (one B/C projection for
+ * every head), 1 < H_qk < H the grouped form; H_qk = H is ll_mamba2_fwd.  The result equals
+ * ll_mamba2_fwd on q and k repeated across each group.  H_qk < 1, H_qk > H or H % H_qk != 0
+ * returns LL_ERR_BAD_SHAPE; otherwise as ll_mamba2_fwd (same workspace size for the same H). */
+ll_status ll_mamba2_fwd_grouped(const void* q, const void* k, const void* v, const float* log_alpha,
+                                const float* lambda, void* o, int64_t B, int64_t T, int64_t H,
+                                int64_t H_qk, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
 /* Same computation as ll_mamba2_fwd, for measurement: also records the caller's HIP events
  * (hipEvent_t handles passed as void*) on `stream`, events[i] right before kernel stage i and
  * events[3] after the last stage, so that the caller can read each stage's duration with

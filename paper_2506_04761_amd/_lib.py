@@ -37,6 +37,9 @@ lib.ll_workspace_size.argtypes = [_i32, _i32, _i64, _i64, _i64, _i64, _i64, _i64
 lib.ll_workspace_size.restype = _sz
 lib.ll_mamba2_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _sz, _vp]
 lib.ll_mamba2_fwd.restype = _i32
+lib.ll_mamba2_fwd_grouped.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i32,
+                                       _vp, _sz, _vp]
+lib.ll_mamba2_fwd_grouped.restype = _i32
 lib.ll_mamba2_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp,
                                       _sz, _vp, ctypes.POINTER(_vp)]
 lib.ll_mamba2_fwd_staged.restype = _i32
@@ -111,12 +114,13 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _prepare(variant, q, k, v, log_alpha, beta, lam, C, out, workspace):
+def _prepare(variant, q, k, v, log_alpha, beta, lam, C, out, workspace, grouped=False):
     torch = _torch()
-    B, T, H, dk = q.shape
+    B, T, Hqk, dk = q.shape
+    H = v.shape[2] if grouped else Hqk
     dv = v.shape[-1]
     _check(q, "q")
-    _check(k, "k", q.dtype, (B, T, H, dk))
+    _check(k, "k", q.dtype, (B, T, Hqk, dk))
     _check(v, "v", q.dtype, (B, T, H, dv))
     _check(log_alpha, "log_alpha", torch.float32, (B, T, H))
     if beta is not None:
@@ -142,6 +146,19 @@ def ll_mamba2_fwd(q, k, v, log_alpha, lam, C, out=None, workspace=None, stream=N
     (B, T, H, dk, dv, code), out, ws = _prepare(LL_MAMBA2, q, k, v, log_alpha, None, lam, C, out, workspace)
     st = lib.ll_mamba2_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(lam), _ptr(out),
                            B, T, H, dk, dv, C, code, _ptr(ws), ws.numel(), _stream(stream))
+    if st != LL_OK:
+        raise LLError(st)
+    return out
+
+
+def ll_mamba2_fwd_grouped(q, k, v, log_alpha, lam, C, out=None, workspace=None, stream=None):
+    """As ll_mamba2_fwd with query/key heads shared by groups of heads: q, k are [B, T, H_qk, d_k]
+    and v, log_alpha, lam, out have H heads (H a multiple of H_qk; head h uses query/key head
+    h // (H // H_qk)).  Returns `out`."""
+    (B, T, H, dk, dv, code), out, ws = _prepare(LL_MAMBA2, q, k, v, log_alpha, None, lam, C, out, workspace,
+                                                grouped=True)
+    st = lib.ll_mamba2_fwd_grouped(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(lam), _ptr(out),
+                                   B, T, H, q.shape[2], dk, dv, C, code, _ptr(ws), ws.numel(), _stream(stream))
     if st != LL_OK:
         raise LLError(st)
     return out

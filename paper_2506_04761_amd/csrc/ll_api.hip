@@ -77,11 +77,12 @@ const char* ll_status_string(ll_status s) {
 
 namespace {
 ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
-                      void* o, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
-                      void* workspace, size_t workspace_bytes, void* stream, void* const* events) {
+                      void* o, int64_t B, int64_t T, int64_t H, int64_t Hqk, int64_t d_k, int64_t d_v, int64_t C,
+                      int32_t dtype, void* workspace, size_t workspace_bytes, void* stream, void* const* events) {
   if (!q || !k || !v || !log_alpha || !o) return LL_ERR_NULL_ARG;
   ll_status st = check_shape(B, T, H, d_k, d_v, C);
   if (st != LL_OK) return st;
+  if (Hqk < 1 || Hqk > H || H % Hqk != 0) return LL_ERR_BAD_SHAPE;
   if (dtype != LL_F32 && dtype != LL_BF16) return LL_ERR_UNSUPPORTED;
   const ll::KernelEntry* e = find_mamba2(dtype, C, d_k, d_v);
   if (!e) return LL_ERR_UNSUPPORTED;
@@ -96,6 +97,7 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   ll::Mamba2Args a;
   a.q = q; a.k = k; a.v = v; a.log_alpha = log_alpha; a.lambda = lambda; a.o = o;
   a.B = B; a.T = T; a.H = H; a.dk = d_k; a.dv = d_v; a.C = C;
+  a.Hqk = Hqk;
   a.L = L;
   a.workspace = workspace;
   hipStream_t hs = static_cast<hipStream_t>(stream);
@@ -139,8 +141,16 @@ extern "C" {
 ll_status ll_mamba2_fwd(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
                         void* o, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                         void* workspace, size_t workspace_bytes, void* stream) {
-  return mamba2_impl(q, k, v, log_alpha, lambda, o, B, T, H, d_k, d_v, C, dtype, workspace, workspace_bytes, stream,
+  return mamba2_impl(q, k, v, log_alpha, lambda, o, B, T, H, H, d_k, d_v, C, dtype, workspace, workspace_bytes, stream,
                      nullptr);
+}
+
+ll_status ll_mamba2_fwd_grouped(const void* q, const void* k, const void* v, const float* log_alpha,
+                                const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t H_qk,
+                                int64_t d_k, int64_t d_v, int64_t C, int32_t dtype, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  return mamba2_impl(q, k, v, log_alpha, lambda, o, B, T, H, H_qk, d_k, d_v, C, dtype, workspace, workspace_bytes,
+                     stream, nullptr);
 }
 
 ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
@@ -150,7 +160,7 @@ ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, cons
   if (!events) return LL_ERR_NULL_ARG;
   for (int i = 0; i <= ll::kMamba2Stages; ++i)
     if (!events[i]) return LL_ERR_NULL_ARG;
-  return mamba2_impl(q, k, v, log_alpha, lambda, o, B, T, H, d_k, d_v, C, dtype, workspace, workspace_bytes, stream,
+  return mamba2_impl(q, k, v, log_alpha, lambda, o, B, T, H, H, d_k, d_v, C, dtype, workspace, workspace_bytes, stream,
                      events);
 }
 

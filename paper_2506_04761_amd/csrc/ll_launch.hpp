@@ -33,6 +33,7 @@ struct Mamba2Args {
   const float* lambda;  // may be null
   void* o;
   int64_t B, T, H, dk, dv, C;
+  int64_t Hqk;          // query/key heads (H % Hqk == 0; head h uses query/key head h / (H / Hqk))
   int L;                // Fenwick levels of T
   void* workspace;      // at least mamba2_workspace(...) bytes, 256-byte aligned
 };

@@ -201,7 +201,7 @@ template <typename T, int C, int DK, int DV, bool HAS_LAMBDA>
 __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restrict__ k, const T* __restrict__ v,
                                                      const float* __restrict__ log_alpha, Nodes<T> nodes,
                                                      T* __restrict__ tiles, float* __restrict__ tot2_out,
-                                                     int64_t Tlen, int H) {
+                                                     int64_t Tlen, int H, int Hqk) {
   using M = Mfma<T>;
   typedef typename Vec16<T>::type V16;
   constexpr int R = tile_rows(C);
@@ -230,6 +230,7 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
   const int blk = (int)(work % NB);
   const int64_t bh = work / NB;
   const int h = (int)(bh % H), b = (int)(bh / H);
+  const int hq = h / (H / Hqk);  // this head's query/key head (heads share them in groups)
   const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool active = wave < WM * WN;
@@ -247,7 +248,7 @@ __global__ __launch_bounds__(kStateThreads) void k_block_state(const T* __restri
     s = s < nsteps ? s : nsteps - 1;
     const int64_t u = u0 + s / STEPS;
     const int kb = s % STEPS;
-    kr.load(k, tile_row0(u), kb * kKB, nrow_of(u), H, h);
+    kr.load(k, tile_row0(u), kb * kKB, nrow_of(u), Hqk, hq);
     vr.load(v, tile_row0(u), kb * kKB, nrow_of(u), H, h);
   };
 
@@ -591,7 +592,7 @@ template <typename T, int C, int DK, int DV, bool HAS_LAMBDA>
 __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ log_alpha,
     const float* __restrict__ lam, Nodes<T> nodes, const T* __restrict__ running, T* __restrict__ o, int64_t Tlen,
-    int H, int L, int J) {
+    int H, int Hqk, int L, int J) {
   using M = Mfma<T>;
   typedef typename Vec16<T>::type V16;
   constexpr int R = tile_rows(C);
@@ -622,6 +623,7 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
   const int u = (int)((work / RM::RS) % N);
   const int64_t bh = work / (RM::RS * N);
   const int h = (int)(bh % H), b = (int)(bh / H);
+  const int hq = h / (H / Hqk);  // this head's query/key head
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
   const int64_t row0 = (int64_t)b * Tlen + (int64_t)u * R;
   const int nrow = (int)((Tlen - (int64_t)u * R) < R ? (Tlen - (int64_t)u * R) : R);
@@ -632,7 +634,7 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
 
   RowBlock<T, DK, NT> kr;
   RowBlock<T, DV, NT> vr;
-  kr.load(k, row0, 0, nrow, H, h);
+  kr.load(k, row0, 0, nrow, Hqk, hq);
   vr.load(v, row0, 0, nrow, H, h);
   const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);  // issued with the other loads
 
@@ -640,7 +642,7 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
   typename M::frag qf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
-    if (i < nrow) qf[ks] = M::load(q + ((row0 + i) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
+    if (i < nrow) qf[ks] = M::load(q + ((row0 + i) * Hqk + hq) * DK + ks * M::KSTEP + g * M::KPL);
     else qf[ks] = typename M::frag{};
   }
   if constexpr (HAS_LAMBDA) {
@@ -711,7 +713,7 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
     vr.store_rows(v_s, LDV);
     __syncthreads();
     if (kb + 1 < nkb) {
-      kr.load(k, row0, (kb + 1) * kKB, nrow, H, h);
+      kr.load(k, row0, (kb + 1) * kKB, nrow, Hqk, hq);
       vr.load(v, row0, (kb + 1) * kKB, nrow, H, h);
     } else if (HAS_LAMBDA && j) {
       load_u(level_src(j, &gap));
@@ -970,7 +972,7 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const float* __restrict__ log_alpha, const float* __restrict__ lam, Nodes<__bf16> nodes,
     const __bf16* __restrict__ running, __bf16* __restrict__ o, int64_t Tlen,
-    int H, int L, int J) {
+    int H, int Hqk, int L, int J) {
   using M = Mfma<__bf16>;
   typedef __bf16 bf;
   typedef typename M::frag frag;
@@ -990,6 +992,7 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
   const int u = (int)(work % N);
   const int64_t bh = work / N;
   const int h = (int)(bh % H), b = (int)(bh / H);
+  const int hq = h / (H / Hqk);  // this head's query/key head
   const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int64_t row0 = (int64_t)b * Tlen + (int64_t)u * R;
@@ -1006,11 +1009,11 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
     const int rA = iA < nrow ? iA : nrow - 1, rB = iB < nrow ? iB : nrow - 1;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      qA[ks] = M::load(q + ((row0 + rA) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
-      qB[ks] = M::load(q + ((row0 + rB) * H + h) * DK + ks * M::KSTEP + g * M::KPL);
+      qA[ks] = M::load(q + ((row0 + rA) * Hqk + hq) * DK + ks * M::KSTEP + g * M::KPL);
+      qB[ks] = M::load(q + ((row0 + rB) * Hqk + hq) * DK + ks * M::KSTEP + g * M::KPL);
     }
   }
-  lds_copy_rows<DK, R, NT>(k_s, k + (row0 * H + h) * DK, (int64_t)H * DK, nrow);
+  lds_copy_rows<DK, R, NT>(k_s, k + (row0 * Hqk + hq) * DK, (int64_t)Hqk * DK, nrow);
   lds_copy_rows<DV, R, NT>(v_s, v + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
   if constexpr (HAS_LAMBDA) lds_copy_lambda<R, NT>(lam_s, lam, row0, H, h, L, nrow);
   // decay gaps of the tile's levels, lane j - 1 holding level j's
@@ -1233,10 +1236,10 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
   if (ev) (void)hipEventRecord(ev[0], st);
   if (a.lambda) {
     hipLaunchKernelGGL((k_block_state<T, C, DK, DV, true>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
-                       a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H);
+                       a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H, (int)a.Hqk);
   } else {
     hipLaunchKernelGGL((k_block_state<T, C, DK, DV, false>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
-                       a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H);
+                       a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H, (int)a.Hqk);
   }
   if (ev) (void)hipEventRecord(ev[1], st);
   if (a.lambda && w.J >= 4) {
@@ -1261,20 +1264,20 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
     if (a.lambda)
       hipLaunchKernelGGL((k_tile_out_fast<DK, DV, true>), gtile, dim3(kFastThreads), 0, st, (const T*)a.q,
                          (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (T*)a.o, a.T,
-                         (int)a.H, a.L, w.J);
+                         (int)a.H, (int)a.Hqk, a.L, w.J);
     else
       hipLaunchKernelGGL((k_tile_out_fast<DK, DV, false>), gtile, dim3(kFastThreads), 0, st, (const T*)a.q,
                          (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (T*)a.o, a.T,
-                         (int)a.H, a.L, w.J);
+                         (int)a.H, (int)a.Hqk, a.L, w.J);
   } else {
     if (a.lambda)
       hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, true>), gtile, dim3(RowMap<tile_rows(C)>::NT), 0, st, (const T*)a.q,
                          (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (T*)a.o, a.T,
-                         (int)a.H, a.L, w.J);
+                         (int)a.H, (int)a.Hqk, a.L, w.J);
     else
       hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, false>), gtile, dim3(RowMap<tile_rows(C)>::NT), 0, st, (const T*)a.q,
                          (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda, nodes, (const T*)running, (T*)a.o, a.T,
-                         (int)a.H, a.L, w.J);
+                         (int)a.H, (int)a.Hqk, a.L, w.J);
   }
   if (ev) (void)hipEventRecord(ev[3], st);
   return hipGetLastError();

@@ -33,6 +33,17 @@ def run_mamba2(inp, dtype, C, with_lambda=True, out=None, workspace=None):
     return o.float().cpu().numpy().astype(np.float64)
 
 
+def run_mamba2_grouped(inp, q, k, dtype, C, with_lambda=True):
+    """ll_mamba2_fwd_grouped with the given shared q, k ([B, T, H_qk, d_k]) and the rest of `inp`."""
+    import torch
+    import paper_2506_04761_amd as ll
+    d = device_inputs(inp, dtype)
+    o = ll.ll_mamba2_fwd_grouped(to_dev(q, dtype), to_dev(k, dtype), d["v"], d["log_alpha"],
+                                 d["lam"] if with_lambda else None, C)
+    torch.cuda.synchronize()
+    return o.float().cpu().numpy().astype(np.float64)
+
+
 def rel_err(got, ref):
     return float(np.max(np.abs(got - ref)) / max(float(np.max(np.abs(ref))), 1e-30))
 

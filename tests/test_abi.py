@@ -64,6 +64,19 @@ def _m2(q=FAKE, k=FAKE, v=FAKE, la=FAKE, lam=FAKE, o=FAKE, B=1, T=128, H=2, dk=6
     return lib.ll_mamba2_fwd(q, k, v, la, lam, o, B, T, H, dk, dv, C, dtype, ws, wsb, None)
 
 
+def _m2g(H=4, Hqk=2, q=FAKE, T=128, dk=64, dv=64, C=64):
+    return lib.ll_mamba2_fwd_grouped(q, FAKE, FAKE, FAKE, FAKE, FAKE, 1, T, H, Hqk, dk, dv, C, 1, FAKE, 1 << 40, None)
+
+
+def test_mamba2_grouped_argument_checks_return_before_launch():
+    assert _m2g(q=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _m2g(Hqk=0) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _m2g(Hqk=3) == ll._lib.LL_ERR_BAD_SHAPE   # 4 heads do not split into groups of 3
+    assert _m2g(Hqk=8) == ll._lib.LL_ERR_BAD_SHAPE   # more query/key heads than heads
+    assert _m2g(T=100) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _m2g(dk=96) == ll._lib.LL_ERR_UNSUPPORTED
+
+
 def test_mamba2_argument_checks_return_before_launch():
     assert _m2(q=None) == ll._lib.LL_ERR_NULL_ARG
     assert _m2(la=None) == ll._lib.LL_ERR_NULL_ARG

@@ -9,7 +9,7 @@ import pytest
 
 from oracle import fenwick, mamba2
 from synthetic import WORKLOADS, generate
-from tests.gpu_util import rel_err, run_mamba2
+from tests.gpu_util import rel_err, run_mamba2, run_mamba2_grouped
 
 pytestmark = pytest.mark.gpu
 
@@ -97,6 +97,30 @@ def test_parity_stress_gates(dist):
     x = generate(w)
     err = rel_err(run_mamba2(x, "bf16", 64), _oracle_full(x))
     assert err <= TOL["bf16"], err
+
+
+# ------------------------------------------------------------------ query/key heads shared in groups
+
+@pytest.mark.parametrize("dtype,C,dk,dv,H,Hqk,T", [
+    ("bf16", 64, 128, 128, 8, 1, 2048),   # multi-value form: one query/key head for all heads
+    ("bf16", 64, 128, 64, 8, 2, 64 * 19),  # grouped, ragged tile count
+    ("bf16", 64, 64, 64, 6, 3, 512),
+    ("f32", 16, 16, 16, 4, 2, 256),
+])
+def test_parity_grouped_qk_heads(dtype, C, dk, dv, H, Hqk, T):
+    """Sharing q, k across each group of H / H_qk heads equals the per-head computation with the
+    group's q, k repeated to every head of the group (head h uses query/key head h // group)."""
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(dtype=dtype, B=2, H=H, T=T, dk=dk, dv=dv, C=C, seed=80 + H + Hqk)
+    x = generate(w)
+    G = H // Hqk
+    q, k = np.ascontiguousarray(x["q"][:, :, ::G]), np.ascontiguousarray(x["k"][:, :, ::G])
+    qr, kr = np.repeat(q, G, axis=2), np.repeat(k, G, axis=2)
+    for with_lambda in (True, False):
+        lam = x["lam"] if with_lambda else np.ones_like(x["lam"])
+        ref = mamba2.quadratic(qr, kr, x["v"], x["log_alpha"], lam)
+        err = rel_err(run_mamba2_grouped(x, q, k, dtype, C, with_lambda=with_lambda), ref)
+        print(f"H={H} H_qk={Hqk} T={T} {dtype} lambda={with_lambda}: rel err {err:.3e}")
+        assert err <= TOL[dtype], err
 
 
 # ------------------------------------------------------------------ one level at a time
