@@ -29,7 +29,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from synthetic import WORKLOADS, generate  # noqa: E402
+from synthetic import WORKLOADS, generate, shared_qk  # noqa: E402
 
 METRIC = "fwd tokens/sec + TFLOP/s (% bf16 MFMA peak), log-linear Mamba-2, T=64K"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
@@ -86,8 +86,9 @@ def stage_figures(w, has_lambda=True):
     else:
         n_state_out = N
         b_scan = BH * (2 * N * SZ * es + N * 4)
-    b_state = BHT * ((w.dk + w.dv) * es + 4) + BH * (n_state_out * SZ * es + N * 4)
-    b_out = BHT * ((2 * w.dk + 2 * w.dv) * es + 4 + L * 4)
+    qk = qk_share(w)  # q, k bytes per head relative to one q/k head per head
+    b_state = BHT * ((w.dk * qk + w.dv) * es + 4) + BH * (n_state_out * SZ * es + N * 4)
+    b_out = BHT * ((2 * w.dk * qk + 2 * w.dv) * es + 4 + L * 4)
     return {"block_state": (f_state, b_state), "scan": (0.0, b_scan), "tile_out": (f_out, b_out)}
 
 
@@ -145,10 +146,15 @@ def recorded_traffic(workload):
         return None
 
 
+def qk_share(w):
+    """Query/key heads per head: 1, or H_qk / H when heads share them in groups."""
+    return (w.qk_heads or w.H) / w.H
+
+
 def algorithmic_bytes(w):
     es = 2 if w.dtype == "bf16" else 4
     BTH = w.B * w.T * w.H
-    return BTH * ((w.dk * 2 + w.dv) * es + 4 + w.levels * 4 + w.dv * es)
+    return BTH * ((w.dk * 2 * qk_share(w) + w.dv) * es + 4 + w.levels * 4 + w.dv * es)
 
 
 def cpu_baseline(w, budget_s):
@@ -156,6 +162,10 @@ def cpu_baseline(w, budget_s):
     growing the prefix until one run takes at least `budget_s` / 2; report tokens/s."""
     from oracle import gdn, mamba2
     x = generate(w.with_(T=min(w.T, 16384)))
+    if w.qk_heads:  # the shared q, k repeated to every head of its group: the same computation
+        G = w.H // w.qk_heads
+        q, k = shared_qk(x, w)
+        x["q"], x["k"] = np.repeat(q, G, axis=2), np.repeat(k, G, axis=2)
     L = w.levels
     lam_full = np.zeros(x["lam"].shape[:-1] + (L,), np.float32)
     lam_full[..., :x["lam"].shape[-1]] = x["lam"]
@@ -210,6 +220,8 @@ def main():
     torch.cuda.set_device(dev)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     x = generate(w)
+    if w.qk_heads:
+        x["q"], x["k"] = shared_qk(x, w)
     d = {n: torch.from_numpy(x[n]).to(dev).to(dt).contiguous() for n in ("q", "k", "v")}
     la = torch.from_numpy(x["log_alpha"]).to(dev)
     lam = torch.from_numpy(x["lam"]).to(dev)
@@ -221,8 +233,10 @@ def main():
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
+    fwd = ll.ll_mamba2_fwd_grouped if w.qk_heads else ll.ll_mamba2_fwd
+
     def run(lmb):
-        ll.ll_mamba2_fwd(d["q"], d["k"], d["v"], la, lmb, w.C, out=out, workspace=ws, stream=stream)
+        fwd(d["q"], d["k"], d["v"], la, lmb, w.C, out=out, workspace=ws, stream=stream)
 
     def timed_plain(lmb, K, W):
         for _ in range(W):
@@ -283,6 +297,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "variant": "log-linear Mamba-2", "B": w.B, "H": w.H, "T": w.T,
                    "d_k": w.dk, "d_v": w.dv, "C": w.C, "levels": w.levels,
+                   **({"qk_heads": w.qk_heads} if w.qk_heads else {}),
                    "inputs": "bf16 q/k/v, fp32 log-gates and lambda, seeded synthetic (numpy PCG64)"},
         "tflops": tflops,
         "mfma_peak_frac": tflops / (PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS),

@@ -92,7 +92,8 @@ ll_status ll_mamba2_fwd_grouped(const void* q, const void* k, const void* v, con
                                 int64_t H_qk, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
-/* Same computation as ll_mamba2_fwd, for measurement: also records the caller's HIP events
+/* Same computation as ll_mamba2_fwd_grouped (ll_mamba2_fwd for H_qk = H), for measurement:
+ * also records the caller's HIP events
  * (hipEvent_t handles passed as void*) on `stream`, events[i] right before kernel stage i and
  * events[3] after the last stage, so that the caller can read each stage's duration with
  * hipEventElapsedTime once the stream has passed them.  Stages: 0 tile states and the
@@ -102,7 +103,7 @@ ll_status ll_mamba2_fwd_grouped(const void* q, const void* k, const void* v, con
  * == NULL or any events[i] == NULL returns LL_ERR_NULL_ARG; the events stay owned by the caller. */
 ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
                                const float* lambda, void* o, int64_t B, int64_t T, int64_t H,
-                               int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                               int64_t H_qk, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                                void* workspace, size_t workspace_bytes, void* stream,
                                void* const* events);
 

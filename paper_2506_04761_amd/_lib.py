@@ -40,8 +40,8 @@ lib.ll_mamba2_fwd.restype = _i32
 lib.ll_mamba2_fwd_grouped.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i32,
                                        _vp, _sz, _vp]
 lib.ll_mamba2_fwd_grouped.restype = _i32
-lib.ll_mamba2_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp,
-                                      _sz, _vp, ctypes.POINTER(_vp)]
+lib.ll_mamba2_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i32,
+                                      _vp, _sz, _vp, ctypes.POINTER(_vp)]
 lib.ll_mamba2_fwd_staged.restype = _i32
 lib.ll_gdn_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _sz, _vp]
 lib.ll_gdn_fwd.restype = _i32
@@ -177,15 +177,17 @@ def _event_handles(events, n, stream):
 
 
 def ll_mamba2_fwd_staged(q, k, v, log_alpha, lam, C, events, out=None, workspace=None, stream=None):
-    """As ll_mamba2_fwd, and records the four torch.cuda.Event objects in `events` (created with
-    enable_timing=True) on the stream around the three kernel stages: events[i] before stage i
-    (tile states, scan -- summary tree, or running states for lam=None -- and tile outputs) and
-    events[3] after the last.  Asynchronous; read
-    the durations with events[i].elapsed_time(events[i + 1]) after synchronising."""
+    """As ll_mamba2_fwd (ll_mamba2_fwd_grouped when q, k have fewer heads than v), and records
+    the four torch.cuda.Event objects in `events` (created with enable_timing=True) on the stream
+    around the three kernel stages: events[i] before stage i (tile states, scan -- summary tree,
+    or running states for lam=None -- and tile outputs) and events[3] after the last.
+    Asynchronous; read the durations with events[i].elapsed_time(events[i + 1]) after
+    synchronising."""
     handles, s = _event_handles(events, 4, stream)
-    (B, T, H, dk, dv, code), out, ws = _prepare(LL_MAMBA2, q, k, v, log_alpha, None, lam, C, out, workspace)
+    (B, T, H, dk, dv, code), out, ws = _prepare(LL_MAMBA2, q, k, v, log_alpha, None, lam, C, out, workspace,
+                                                grouped=True)
     st = lib.ll_mamba2_fwd_staged(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(lam), _ptr(out),
-                                  B, T, H, dk, dv, C, code, _ptr(ws), ws.numel(), _stream(s), handles)
+                                  B, T, H, q.shape[2], dk, dv, C, code, _ptr(ws), ws.numel(), _stream(s), handles)
     if st != LL_OK:
         raise LLError(st)
     return out

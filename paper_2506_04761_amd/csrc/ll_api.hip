@@ -154,14 +154,14 @@ ll_status ll_mamba2_fwd_grouped(const void* q, const void* k, const void* v, con
 }
 
 ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
-                               const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t d_k,
-                               int64_t d_v, int64_t C, int32_t dtype, void* workspace, size_t workspace_bytes,
-                               void* stream, void* const* events) {
+                               const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t H_qk,
+                               int64_t d_k, int64_t d_v, int64_t C, int32_t dtype, void* workspace,
+                               size_t workspace_bytes, void* stream, void* const* events) {
   if (!events) return LL_ERR_NULL_ARG;
   for (int i = 0; i <= ll::kMamba2Stages; ++i)
     if (!events[i]) return LL_ERR_NULL_ARG;
-  return mamba2_impl(q, k, v, log_alpha, lambda, o, B, T, H, H, d_k, d_v, C, dtype, workspace, workspace_bytes, stream,
-                     events);
+  return mamba2_impl(q, k, v, log_alpha, lambda, o, B, T, H, H_qk, d_k, d_v, C, dtype, workspace, workspace_bytes,
+                     stream, events);
 }
 
 ll_status ll_gdn_fwd(const void* q, const void* k, const void* v, const float* log_alpha, const float* beta,

@@ -3,6 +3,8 @@
 Draw order (numpy PCG64 `default_rng(seed)`, float32 standard normals, each a full array
 in [B, T, H, ...] row-major order): q, k, v, the log-gate pre-activation x_a, the level
 weight pre-activation x_l, and (delta-rule workloads only) the beta pre-activation x_b.
+Workloads whose query/key heads are shared (qk_heads > 0) take q, k of the first head of each
+group of H / qk_heads heads (see shared_qk).
 
 Transforms by distribution name:
   "unit"     q, k ~ N/sqrt(d_k), v ~ N/sqrt(d_v), log alpha = -softplus(x_a),     lambda = softplus(x_l)
@@ -35,6 +37,7 @@ class Workload:
     C: int
     seed: int
     dist: str
+    qk_heads: int = 0  # query/key heads shared by groups of heads (0: one per head)
 
     @property
     def levels(self) -> int:
@@ -52,6 +55,9 @@ WORKLOADS = {
         Workload("ll_mamba2_bf16_T8192", "mamba2", "bf16", 4, 32, 8192, 128, 64, 64, 3, "unit"),
         Workload("ll_mamba2_bf16_T65536", "mamba2", "bf16", 1, 16, 65536, 128, 128, 64, 4, "unit"),
         Workload("ll_gdn_bf16_T8192", "gdn", "bf16", 2, 16, 8192, 128, 128, 64, 5, "gdn"),
+        # the shape of the paper's kernel benchmark (B = 2, 48 heads, head dim 64, state dim 128,
+        # chunk 64, one query/key head for all heads), at T = 16384
+        Workload("ll_mamba2_mva_bf16_T16384", "mamba2", "bf16", 2, 48, 16384, 128, 64, 64, 6, "unit", 1),
     ]
 }
 
@@ -70,6 +76,12 @@ def to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
         import torch
         return torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
     raise ValueError(dtype)
+
+
+def shared_qk(x: dict, w: Workload):
+    """q, k of a workload with shared query/key heads: those of the first head of each group."""
+    G = w.H // w.qk_heads
+    return np.ascontiguousarray(x["q"][:, :, ::G]), np.ascontiguousarray(x["k"][:, :, ::G])
 
 
 def generate(w: Workload, T: int = None, heads=None):
