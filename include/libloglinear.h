@@ -107,6 +107,40 @@ ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, cons
                                void* workspace, size_t workspace_bytes, void* stream,
                                void* const* events);
 
+/* ---- Decoding (one token at a time, Sec. 3.2) -------------------------------------------------
+ *
+ * Log-linear Mamba-2 keeps, per (b, h), one state per Fenwick level: O(log t) states of d_v x d_k.
+ * Token t (0-based) updates them as Sec. 3.2 describes, gated: for t >= 1, with p = lssb(t), level
+ * p+1 takes the sum of levels 0..p, levels 1..p are emptied, the others carry over, every carried
+ * or merged level is multiplied by alpha_t, and level 0 becomes v_t k_t^T; the output is
+ * o_t = sum_l lambda_t^(l) S_t^(l) q_t (Eq. 3).  Feeding tokens 0..T-1 in order gives the rows of
+ * ll_mamba2_fwd on the same sequence.
+ *
+ * The state lives in one caller-owned device buffer of ll_decode_state_bytes(B, H, d_k, d_v, L)
+ * bytes, 256-byte aligned, whose layout is private to the library; L levels hold tokens
+ * t < 2^(L-1) (L = ll_num_levels(T) for a sequence of T tokens, at most 32).  Per-token tensors
+ * are q, k [B, H, d_k], v, o [B, H, d_v] in the storage dtype, log_alpha [B, H] and lambda
+ * [B, H, L] float32 (lambda == NULL: all level weights 1, i.e. Mamba-2 decoding).  Supported
+ * (dtype, d_k, d_v): fp32 (16, 16), (64, 64); bf16 (64, 64), (128, 64), (128, 128).  Steps on one
+ * state must be enqueued in token order on one stream (each step reads what the previous one
+ * wrote); the state is read and written in place. */
+
+/* Bytes of decode state for these sizes; 0 if an argument is < 1.  Pure host function. */
+size_t ll_decode_state_bytes(int64_t B, int64_t H, int64_t d_k, int64_t d_v, int32_t L);
+
+/* Resets a decode state to the empty sequence (enqueued on `stream`). */
+ll_status ll_mamba2_decode_init(void* state, size_t state_bytes, int64_t B, int64_t H, int64_t d_k,
+                                int64_t d_v, int32_t L, int32_t dtype, void* stream);
+
+/* Feeds token t to every (b, h) and writes its output o.  t must be the number of tokens fed
+ * since the last ll_mamba2_decode_init and below 2^(L-1) (else LL_ERR_BAD_SHAPE); a state
+ * buffer too small or misaligned gives LL_ERR_WORKSPACE; an uncompiled (dtype, d_k, d_v),
+ * L > 32 or B*H > 65535 gives LL_ERR_UNSUPPORTED. */
+ll_status ll_mamba2_decode_step(const void* q, const void* k, const void* v, const float* log_alpha,
+                                const float* lambda, void* o, void* state, size_t state_bytes,
+                                int64_t t, int64_t B, int64_t H, int64_t d_k, int64_t d_v,
+                                int32_t L, int32_t dtype, void* stream);
+
 /* Log-linear Gated DeltaNet forward (Sec. 3.4), with the delta-rule transition
  * alpha_t (I - beta_t k_t k_t^T) applied chunkwise through a WY (UT) representation.
  * beta is required; lambda == NULL gives plain Gated DeltaNet.  Returns LL_ERR_UNSUPPORTED

@@ -77,6 +77,32 @@ def test_mamba2_grouped_argument_checks_return_before_launch():
     assert _m2g(dk=96) == ll._lib.LL_ERR_UNSUPPORTED
 
 
+def test_decode_state_bytes():
+    n = ll.ll_decode_state_bytes(2, 3, 64, 64, 10)
+    assert n > 0 and n % 256 == 0 and n >= 2 * 3 * 10 * 64 * 64 * 4
+    assert ll.ll_decode_state_bytes(0, 3, 64, 64, 10) == 0
+    assert ll.ll_decode_state_bytes(2, 3, 64, 64, 0) == 0
+
+
+def _dec(q=FAKE, state=FAKE, t=5, B=2, H=3, dk=64, dv=64, L=10, dtype=1, sb=1 << 40):
+    return lib.ll_mamba2_decode_step(q, FAKE, FAKE, FAKE, FAKE, FAKE, state, sb, t, B, H, dk, dv, L, dtype, None)
+
+
+def test_decode_argument_checks_return_before_launch():
+    assert _dec(q=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _dec(state=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _dec(B=0) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _dec(t=-1) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _dec(t=512, L=10) == ll._lib.LL_ERR_BAD_SHAPE     # 10 levels hold tokens t < 2^9
+    assert _dec(dk=96) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _dec(dtype=4) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _dec(L=33) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _dec(sb=1000) == ll._lib.LL_ERR_WORKSPACE
+    assert _dec(state=ctypes.c_void_p(4096 + 16)) == ll._lib.LL_ERR_WORKSPACE
+    assert lib.ll_mamba2_decode_init(None, 1 << 40, 2, 3, 64, 64, 10, 1, None) == ll._lib.LL_ERR_NULL_ARG
+    assert lib.ll_mamba2_decode_init(FAKE, 1000, 2, 3, 64, 64, 10, 1, None) == ll._lib.LL_ERR_WORKSPACE
+
+
 def test_mamba2_argument_checks_return_before_launch():
     assert _m2(q=None) == ll._lib.LL_ERR_NULL_ARG
     assert _m2(la=None) == ll._lib.LL_ERR_NULL_ARG
