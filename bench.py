@@ -216,6 +216,8 @@ def main():
     w = WORKLOADS[args.workload]
     if w.variant == "gdn":
         return main_gdn(args, w, torch, ll)
+    if w.variant == "decode":
+        return main_decode(args, w, torch, ll)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
@@ -351,6 +353,95 @@ def gdn_issued(w, has_lambda=True):
     L = w.levels if has_lambda else 0
     nbytes = w.B * w.T * w.H * ((2 * dk + 2 * dv) * es + 8 + 4 * L)
     return BH * N * f_chunk, BH * f_scan, nbytes
+
+
+def decode_level_reads(T):
+    """Per token t < T: the number of level states (d_v x d_k, fp32) a decode step reads -- the
+    nonempty levels >= 1 other than the one it overwrites -- following the Sec. 3.2 occupancy
+    (level p+1 filled and levels 1..p emptied at t, p = lssb(t))."""
+    occupied, reads = set(), []
+    for t in range(T):
+        if t == 0:
+            reads.append(0)
+            continue
+        p = (t & -t).bit_length() - 1
+        reads.append(len([lv for lv in occupied if lv != p + 1]))
+        occupied -= set(range(1, p + 1))
+        occupied.add(p + 1)
+    return reads
+
+
+def main_decode(args, w, torch, ll):
+    """Log-linear Mamba-2 decoding: B sequences, one token each per step, timed over the last
+    steps before position T (the state then holds up to log2 T levels)."""
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    T0 = 1024  # distinct token inputs, cycled
+    L = w.levels
+    x = generate(w.with_(T=T0))
+    dt = torch.bfloat16
+    per_t = {n: torch.from_numpy(x[n]).to(dev).to(dt).transpose(0, 1).contiguous() for n in ("q", "k", "v")}
+    la = torch.from_numpy(x["log_alpha"]).to(dev).transpose(0, 1).contiguous()
+    lam = torch.zeros((T0, w.B, w.H, L), dtype=torch.float32, device=dev)
+    lam[..., :x["lam"].shape[-1]] = torch.from_numpy(x["lam"]).to(dev).transpose(0, 1)
+    del x
+    state = torch.empty(ll.ll_decode_state_bytes(w.B, w.H, w.dk, w.dv, L), dtype=torch.uint8, device=dev)
+    out = torch.empty((w.B, w.H, w.dv), dtype=dt, device=dev)
+    stream = torch.cuda.current_stream()
+    M = min(args.steps * 50, w.T // 2)  # timed tokens: the last M positions before T
+
+    def step(t, lmb=True):
+        i = t % T0
+        ll.ll_mamba2_decode_step(per_t["q"][i], per_t["k"][i], per_t["v"][i], la[i], lam[i] if lmb else None,
+                                 state, t, L, out=out, stream=stream)
+
+    def run(lmb):
+        ll.ll_mamba2_decode_init(state, w.B, w.H, w.dk, w.dv, L, dt, stream=stream)
+        for t in range(w.T - M):
+            step(t, lmb)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for t in range(w.T - M, w.T):
+            step(t, lmb)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / M
+
+    print(f"[bench] {w.name}: {w.T - M} untimed tokens, {M} timed", file=sys.stderr, flush=True)
+    ms = run(True)
+    ms_null = run(False)
+    print(f"[bench] decode {ms * 1e3:.1f} us/token-step (lambda), {ms_null * 1e3:.1f} (lambda=NULL)",
+          file=sys.stderr, flush=True)
+    reads = decode_level_reads(w.T)[w.T - M:]
+    BH = w.B * w.H
+    SZ4 = w.dk * w.dv * 4
+    per_step = BH * (np.mean(reads) + 1) * SZ4 + BH * ((2 * w.dk + 2 * w.dv) * 2 + 4 + 4 * L + 2 * (w.dv + w.dk) * 4)
+    gbs = per_step / (ms * 1e-3) / 1e9
+    res = {
+        "metric": "decode tokens/sec (one token per sequence per step), log-linear Mamba-2",
+        "value": w.B / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": M, "warmup": w.T - M, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "variant": "log-linear Mamba-2 decoding", "B": w.B, "H": w.H,
+                   "positions": f"{w.T - M}..{w.T - 1}", "d_k": w.dk, "d_v": w.dv, "levels": L,
+                   "inputs": f"bf16 q/k/v, fp32 log-gates and lambda, the seeded T={T0} draw cycled"},
+        "mamba2_lambda_null": {"ms_per_step": ms_null, "tokens_per_s": w.B / (ms_null * 1e-3)},
+        "roofline": {"kernel": "decode_step", "bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": None,
+                     "algorithmic_bytes_per_step": per_step,
+                     "bytes_note": "per head: the nonempty level states read (mean over the timed positions) "
+                                   "and the merged one written, fp32, plus the token's inputs and output; the "
+                                   "states re-read every token are partly served by the 256 MB Infinity Cache, "
+                                   "so the rate can exceed the HBM peak"},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(w.with_(variant="mamba2", B=1), args.cpu_budget)
+        res["cpu_baseline"]["sample"] += " (the oracle's recurrent form is itself token-by-token decoding)"
+    print(json.dumps(res), flush=True)
 
 
 def main_gdn(args, w, torch, ll):

@@ -27,7 +27,7 @@ import numpy as np
 @dataclass(frozen=True)
 class Workload:
     name: str
-    variant: str      # "mamba2" or "gdn"
+    variant: str      # "mamba2", "gdn" or "decode" (log-linear Mamba-2 decoding)
     dtype: str        # "f32" or "bf16": storage dtype of q, k, v and o
     B: int
     H: int
@@ -58,6 +58,9 @@ WORKLOADS = {
         # the shape of the paper's kernel benchmark (B = 2, 48 heads, head dim 64, state dim 128,
         # chunk 64, one query/key head for all heads), at T = 16384
         Workload("ll_mamba2_mva_bf16_T16384", "mamba2", "bf16", 2, 48, 16384, 128, 64, 64, 6, "unit", 1),
+        # decoding: 64 sequences x 16 heads fed one token per step up to position 8191 (the token
+        # inputs are the T = 1024 draw, cycled)
+        Workload("ll_mamba2_decode_bf16_T8192", "decode", "bf16", 64, 16, 8192, 128, 128, 64, 7, "unit"),
     ]
 }
 
