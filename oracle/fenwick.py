@@ -64,6 +64,24 @@ def level_row(t: int) -> np.ndarray:
     return row
 
 
+def level_of(t: int, s: int) -> int:
+    """l(t, s) for one pair s <= t: the level of the greedy bucket of t that holds s."""
+    if not 0 <= s <= t:
+        raise ValueError("need 0 <= s <= t")
+    if s == t:
+        return 0
+    b = greedy_boundaries(t)
+    for i in range(len(b) - 1):
+        if b[i + 1] <= s < b[i]:
+            return lssb(b[i]) + 1
+    raise AssertionError("the buckets of t cover 0..t-1")
+
+
+def level_col(s: int, T: int) -> np.ndarray:
+    """Levels l(t, s) for t = s .. T-1 (one column of Eq. 4's level pattern)."""
+    return np.array([level_of(t, s) for t in range(s, T)], dtype=np.int64)
+
+
 def level_matrix(T: int) -> np.ndarray:
     """T x T int matrix with l(t, s) for s <= t and -1 above the diagonal."""
     out = np.full((T, T), -1, dtype=np.int64)
