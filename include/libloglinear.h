@@ -57,7 +57,7 @@ typedef enum {
 
 typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
 
-typedef enum { LL_MAMBA2 = 0, LL_GDN = 1 } ll_variant;
+typedef enum { LL_MAMBA2 = 0, LL_GDN = 1, LL_MAMBA2_BWD = 2 } ll_variant;  /* LL_MAMBA2_BWD: the backward call */
 
 /* Number of Fenwick levels L for a sequence of length T (Sec. 3.1): one more than the largest
  * level l(t,s) over all 0 <= s <= t < T, i.e. ceil(log2 T) + 1 for T >= 2 and 1 for T = 1.
@@ -68,7 +68,8 @@ int32_t ll_num_levels(int64_t T);
 int32_t ll_supported(int32_t variant, int32_t dtype, int64_t C, int64_t d_k, int64_t d_v);
 
 /* Bytes of workspace the forward call needs for these arguments; `has_lambda` = 0 sizes the
- * lambda == NULL path.  Returns 0 if the arguments are invalid.  Pure host function. */
+ * lambda == NULL path.  With variant LL_MAMBA2_BWD: bytes for ll_mamba2_bwd (has_lambda must be
+ * 1).  Returns 0 if the arguments are invalid.  Pure host function. */
 size_t ll_workspace_size(int32_t variant, int32_t dtype, int64_t B, int64_t T, int64_t H,
                          int64_t d_k, int64_t d_v, int64_t C, int32_t has_lambda);
 
@@ -104,6 +105,41 @@ ll_status ll_mamba2_fwd_grouped(const void* q, const void* k, const void* v, con
 ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
                                const float* lambda, void* o, int64_t B, int64_t T, int64_t H,
                                int64_t H_qk, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                               void* workspace, size_t workspace_bytes, void* stream,
+                               void* const* events);
+
+/* ---- Backward pass of log-linear Mamba-2 -----------------------------------------------------
+ *
+ * Gradients of the scalar sum(O (.) dO) for O = (Q K^T (.) M^S (.) M^H) V (Sec. 3.4), with respect
+ * to every input.  Per (b, h), with w(t, s) = lambda_t^(l(t,s)) exp(cum_t - cum_s) (s <= t),
+ * cum the running sum of log_alpha, P = Q K^T and G = dO V^T:
+ *   dq = (w (.) G) K,   dk = (w (.) G)^T Q,   dv = (w (.) P)^T dO,
+ *   dlambda_t^(l) = sum over s at level l of exp(cum_t - cum_s) P[t,s] G[t,s]  (0 for levels no
+ *                   pair of row t reaches),
+ *   dlog_alpha_tau = sum over t >= tau of (q_t . dq_t - k_t . dk_t).
+ * Computed chunkwise like the forward (Sec. 3.3): the forward's level summaries for the query
+ * side, and per-level summaries of later tokens (lambda-weighted, since lambda belongs to the
+ * query) for the key side.  The forward output is not needed.
+ *
+ * d_o, dq, dk, dv have the layout and storage dtype of v, q, k, v; dlog_alpha [B, T, H] and
+ * dlambda [B, T, H, L] are float32.  Every output is written in full (caller-owned device
+ * memory, not read).  lambda is required (pass ones for Mamba-2): NULL gives LL_ERR_NULL_ARG.
+ * Shapes, dtypes and compiled (C, d_k, d_v) as for ll_mamba2_fwd; the workspace is
+ * ll_workspace_size(LL_MAMBA2_BWD, ...) bytes.  Asynchronous on `stream`. */
+ll_status ll_mamba2_bwd(const void* q, const void* k, const void* v, const float* log_alpha,
+                        const float* lambda, const void* d_o, void* dq, void* dk, void* dv,
+                        float* dlog_alpha, float* dlambda, int64_t B, int64_t T, int64_t H,
+                        int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Same computation as ll_mamba2_bwd, for measurement, recording the caller's HIP events on
+ * `stream`: events[i] right before stage i and events[4] after the last.  Stages: 0 the forward's
+ * level summaries, 1 the key-side level summaries, 2 dq and dlambda, 3 dk, dv and dlog_alpha.
+ * events == NULL or any events[i] == NULL returns LL_ERR_NULL_ARG. */
+ll_status ll_mamba2_bwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
+                               const float* lambda, const void* d_o, void* dq, void* dk, void* dv,
+                               float* dlog_alpha, float* dlambda, int64_t B, int64_t T, int64_t H,
+                               int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                                void* workspace, size_t workspace_bytes, void* stream,
                                void* const* events);
 

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "libloglinear.so")
 
 LL_OK, LL_ERR_NULL_ARG, LL_ERR_BAD_SHAPE, LL_ERR_UNSUPPORTED, LL_ERR_WORKSPACE, LL_ERR_HIP = range(6)
 LL_F32, LL_BF16 = 0, 1
-LL_MAMBA2, LL_GDN = 0, 1
+LL_MAMBA2, LL_GDN, LL_MAMBA2_BWD = 0, 1, 2
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(
@@ -55,6 +55,10 @@ lib.ll_gdn_fwd.restype = _i32
 lib.ll_gdn_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _sz,
                                    _vp, ctypes.POINTER(_vp)]
 lib.ll_gdn_fwd_staged.restype = _i32
+lib.ll_mamba2_bwd.argtypes = [_vp] * 11 + [_i64] * 6 + [_i32, _vp, _sz, _vp]
+lib.ll_mamba2_bwd.restype = _i32
+lib.ll_mamba2_bwd_staged.argtypes = [_vp] * 11 + [_i64] * 6 + [_i32, _vp, _sz, _vp, _vp]
+lib.ll_mamba2_bwd_staged.restype = _i32
 lib.ll_debug_level_map.argtypes = [_i64, _i64, _vp, _vp]
 lib.ll_debug_level_map.restype = _i32
 lib.ll_status_string.argtypes = [_i32]
@@ -234,6 +238,56 @@ def ll_mamba2_fwd_staged(q, k, v, log_alpha, lam, C, events, out=None, workspace
     if st != LL_OK:
         raise LLError(st)
     return out
+
+
+def _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, handles):
+    torch = _torch()
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    _check(q, "q")
+    _check(k, "k", q.dtype, (B, T, H, dk))
+    _check(v, "v", q.dtype, (B, T, H, dv))
+    _check(d_o, "d_o", q.dtype, (B, T, H, dv))
+    _check(log_alpha, "log_alpha", torch.float32, (B, T, H))
+    L = ll_num_levels(T)
+    _check(lam, "lambda", torch.float32, (B, T, H, L))
+    code = _dtype_code(q)
+    if grads is None:
+        dev = q.device
+        grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v),
+                 torch.empty((B, T, H), dtype=torch.float32, device=dev),
+                 torch.empty((B, T, H, L), dtype=torch.float32, device=dev))
+    dq, dk_, dv_, dla, dlam = grads
+    _check(dq, "dq", q.dtype, q.shape)
+    _check(dk_, "dk", q.dtype, k.shape)
+    _check(dv_, "dv", q.dtype, v.shape)
+    _check(dla, "dlog_alpha", torch.float32, (B, T, H))
+    _check(dlam, "dlambda", torch.float32, (B, T, H, L))
+    need = ll_workspace_size(LL_MAMBA2_BWD, code, B, T, H, dk, dv, C, True)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _check(workspace, "workspace", torch.uint8)
+    args = [_ptr(x) for x in (q, k, v, log_alpha, lam, d_o, dq, dk_, dv_, dla, dlam)]
+    args += [B, T, H, dk, dv, C, code, _ptr(workspace), workspace.numel(), _stream(stream)]
+    st = lib.ll_mamba2_bwd(*args) if handles is None else lib.ll_mamba2_bwd_staged(*args, handles)
+    if st != LL_OK:
+        raise LLError(st)
+    return grads
+
+
+def ll_mamba2_bwd(q, k, v, log_alpha, lam, d_o, C, grads=None, workspace=None, stream=None):
+    """Gradients of sum(O * d_o) for the log-linear Mamba-2 forward O on the same inputs:
+    returns (dq, dk, dv, dlog_alpha, dlambda) (dq, dk, dv in the dtype of q; the others float32),
+    written into `grads` when given.  `lam` is required.  Enqueued on `stream` (default: torch's
+    current stream), not synchronised."""
+    return _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, None)
+
+
+def ll_mamba2_bwd_staged(q, k, v, log_alpha, lam, d_o, C, events, grads=None, workspace=None, stream=None):
+    """As ll_mamba2_bwd, and records the five torch.cuda.Event objects in `events` around the four
+    stages (forward summaries, key-side summaries, dq and dlambda, dk dv and dlog_alpha)."""
+    handles, s = _event_handles(events, 5, stream)
+    return _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, s, handles)
 
 
 def ll_gdn_fwd(q, k, v, log_alpha, beta, lam, C, out=None, workspace=None, stream=None):

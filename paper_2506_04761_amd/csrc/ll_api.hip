@@ -25,6 +25,14 @@ const ll::KernelEntry* find_mamba2(int32_t dtype, int64_t C, int64_t dk, int64_t
   return nullptr;
 }
 
+const ll::BwdEntry* find_mamba2_bwd(int32_t dtype, int64_t C, int64_t dk, int64_t dv) {
+  int n = 0;
+  const ll::BwdEntry* t = ll::mamba2_bwd_table(&n);
+  for (int i = 0; i < n; ++i)
+    if (t[i].dtype == dtype && t[i].C == C && t[i].dk == dk && t[i].dv == dv) return &t[i];
+  return nullptr;
+}
+
 const ll::GdnEntry* find_gdn(int32_t dtype, int64_t C, int64_t dk, int64_t dv) {
   if (dtype != LL_BF16) return nullptr;
   int n = 0;
@@ -48,6 +56,7 @@ int32_t ll_num_levels(int64_t T) { return levels_of(T); }
 int32_t ll_supported(int32_t variant, int32_t dtype, int64_t C, int64_t d_k, int64_t d_v) {
   if (variant == LL_MAMBA2) return find_mamba2(dtype, C, d_k, d_v) ? 1 : 0;
   if (variant == LL_GDN) return find_gdn(dtype, C, d_k, d_v) ? 1 : 0;
+  if (variant == LL_MAMBA2_BWD) return find_mamba2_bwd(dtype, C, d_k, d_v) ? 1 : 0;
   return 0;
 }
 
@@ -58,6 +67,8 @@ size_t ll_workspace_size(int32_t variant, int32_t dtype, int64_t B, int64_t T, i
   if (variant == LL_MAMBA2)
     return (size_t)ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), has_lambda != 0, nullptr);
   if (variant == LL_GDN) return (size_t)ll::gdn_workspace(B, T, H, d_k, d_v, C, nullptr);
+  if (variant == LL_MAMBA2_BWD && has_lambda)
+    return (size_t)ll::mamba2_bwd_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), nullptr);
   return 0;
 }
 
@@ -105,6 +116,36 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   if (events)
     for (int i = 0; i <= ll::kMamba2Stages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);
   const hipError_t err = e->launch(a, hs, events ? ev : nullptr);
+  return err == hipSuccess ? LL_OK : LL_ERR_HIP;
+}
+ll_status mamba2_bwd_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
+                          const void* d_o, void* dq, void* dk, void* dv, float* dlog_alpha, float* dlambda, int64_t B,
+                          int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype, void* workspace,
+                          size_t workspace_bytes, void* stream, void* const* events) {
+  if (!q || !k || !v || !log_alpha || !lambda || !d_o || !dq || !dk || !dv || !dlog_alpha || !dlambda)
+    return LL_ERR_NULL_ARG;
+  ll_status st = check_shape(B, T, H, d_k, d_v, C);
+  if (st != LL_OK) return st;
+  if (dtype != LL_F32 && dtype != LL_BF16) return LL_ERR_UNSUPPORTED;
+  const ll::BwdEntry* e = find_mamba2_bwd(dtype, C, d_k, d_v);
+  if (!e) return LL_ERR_UNSUPPORTED;
+  const int L = levels_of(T);
+  const int64_t tiles = ll::tiles_of(T, C);
+  if (L > kMaxL || tiles > kMaxTiles || H > 65535 || B > 65535 || tiles * H * B >= (int64_t(1) << 31))
+    return LL_ERR_UNSUPPORTED;
+  const int64_t need = ll::mamba2_bwd_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), nullptr);
+  if (!workspace) return LL_ERR_NULL_ARG;
+  if ((int64_t)workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
+  ll::Mamba2BwdArgs a;
+  a.q = q; a.k = k; a.v = v; a.dout = d_o; a.log_alpha = log_alpha; a.lambda = lambda;
+  a.dq = dq; a.dk = dk; a.dv = dv; a.dlog_alpha = dlog_alpha; a.dlambda = dlambda;
+  a.B = B; a.T = T; a.H = H; a.C = C;
+  a.L = L;
+  a.workspace = workspace;
+  hipEvent_t ev[ll::kMamba2BwdStages + 1];
+  if (events)
+    for (int i = 0; i <= ll::kMamba2BwdStages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);
+  const hipError_t err = e->launch(a, static_cast<hipStream_t>(stream), events ? ev : nullptr);
   return err == hipSuccess ? LL_OK : LL_ERR_HIP;
 }
 ll_status gdn_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* beta,
@@ -162,6 +203,26 @@ ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, cons
     if (!events[i]) return LL_ERR_NULL_ARG;
   return mamba2_impl(q, k, v, log_alpha, lambda, o, B, T, H, H_qk, d_k, d_v, C, dtype, workspace, workspace_bytes,
                      stream, events);
+}
+
+ll_status ll_mamba2_bwd(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
+                        const void* d_o, void* dq, void* dk, void* dv, float* dlog_alpha, float* dlambda, int64_t B,
+                        int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, d_k, d_v, C, dtype,
+                         workspace, workspace_bytes, stream, nullptr);
+}
+
+ll_status ll_mamba2_bwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
+                               const float* lambda, const void* d_o, void* dq, void* dk, void* dv, float* dlog_alpha,
+                               float* dlambda, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C,
+                               int32_t dtype, void* workspace, size_t workspace_bytes, void* stream,
+                               void* const* events) {
+  if (!events) return LL_ERR_NULL_ARG;
+  for (int i = 0; i <= ll::kMamba2BwdStages; ++i)
+    if (!events[i]) return LL_ERR_NULL_ARG;
+  return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, d_k, d_v, C, dtype,
+                         workspace, workspace_bytes, stream, events);
 }
 
 ll_status ll_gdn_fwd(const void* q, const void* k, const void* v, const float* log_alpha, const float* beta,

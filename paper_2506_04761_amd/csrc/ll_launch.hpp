@@ -49,6 +49,41 @@ struct KernelEntry {
 
 const KernelEntry* mamba2_table(int* n);
 
+// Log-linear Mamba-2 backward: the forward's summary workspace followed by the key-side level
+// summaries (byte offsets).
+struct BwdLayout {
+  WsLayout fwd;
+  int64_t NR = 0, nd = 0, npart = 0;  // 8-tile regions; key-side summaries and partials per (b, h)
+  int64_t d = 0, dtot = 0, part = 0, qdq = 0, tsum = 0, total = 0;
+};
+int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, int64_t esize,
+                             BwdLayout* lay);
+
+struct Mamba2BwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* dout;
+  const float* log_alpha;
+  const float* lambda;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* dlog_alpha;
+  float* dlambda;
+  int64_t B, T, H, C;
+  int L;
+  void* workspace;
+};
+typedef hipError_t (*Mamba2BwdLaunch)(const Mamba2BwdArgs&, hipStream_t, hipEvent_t* /* null or 5 events */);
+constexpr int kMamba2BwdStages = 4;
+struct BwdEntry {
+  int dtype;
+  int C, dk, dv;
+  Mamba2BwdLaunch launch;
+};
+const BwdEntry* mamba2_bwd_table(int* n);
+
 // Gated DeltaNet: per-chunk buffers carved from the workspace (byte offsets).
 struct GdnLayout {
   int64_t qc = 0, pz = 0, hz = 0, oin = 0, total = 0;

@@ -26,166 +26,9 @@
 // sequence-long prefix sums.
 #include <type_traits>
 
-#include "ll_device.hpp"
-#include "ll_launch.hpp"
+#include "ll_mamba2_common.hpp"
 
 namespace ll {
-
-// Tile rows R: two chunks (C >= 32), at least 64 tokens.  Levels up to log2 R are computed densely
-// inside a tile, the ones above from summaries of whole tiles.
-__host__ __device__ constexpr int tile_rows(int C) { return 2 * C >= 64 ? 2 * C : 64; }
-constexpr int kBlockTiles = 4;    // tiles per block_state workgroup
-constexpr int kKB = 64;           // keys staged in LDS at a time
-constexpr int kMaxLevels = 24;    // Fenwick levels handled (T <= 2^23)
-
-// Device view of the summaries (all in the storage dtype, layout [p][n] = d_v x d_k) and of their
-// summed log2-gates.  Above the blocks, node (l, k) of the block tree (l >= 1) covers blocks
-// [k 2^l, (k + 1) 2^l), i.e. the tiles of the level-(l + 3) source group with index k.
-template <typename T>
-struct Nodes {
-  T* lvl1;         // [BH][ceil(N/2)]  tile states of even tiles
-  T* lvl2;         // [BH][ceil(N/4)]  pair summaries of tiles 4b, 4b+1
-  T* blocks;       // [BH][NB]         block summaries (4 tiles)
-  T* upper;        // [BH][nup]        block-tree nodes of levels >= 1 (tile levels >= 4)
-  const float* t1; // [BH][N]          tile totals (the level-1 source groups are single tiles)
-  float* t2;       // [BH][ceil(N/4)]  totals of the pairs in lvl2
-  float* t3;       // [BH][NB]         block totals
-  float* tup;      // [BH][nup]        totals of the upper nodes
-  float* cl;       // [BH][N][R]       tile-local inclusive cumulative log2-gates (rows past T repeat the last)
-  int64_t n1, n2, nb, nup;  // per-(b,h) slot counts
-  // Slot of block-tree node (l >= 1, k): tree levels 1 .. l-1 come first, ceil(nb / 2^l') slots each.
-  __device__ __host__ int64_t up_slot(int64_t bh, int l, int64_t k) const {
-    int64_t off = 0;
-    for (int ll = 1; ll < l; ++ll) off += (nb + (int64_t(1) << ll) - 1) >> ll;
-    return bh * nup + off + k;
-  }
-  // Summary of the level-j source group that starts at tile f (f a multiple of 2^(j-1)).
-  __device__ __host__ T* at(int64_t bh, int64_t N, int j, int64_t f, int SZ) const {
-    if (j == 1) return lvl1 + (bh * n1 + (f >> 1)) * SZ;
-    if (j == 2) return lvl2 + (bh * n2 + (f >> 2)) * SZ;
-    if (j == 3) return blocks + (bh * nb + (f >> 2)) * SZ;
-    return upper + up_slot(bh, j - 3, f >> (j - 1)) * SZ;
-  }
-  // Summed log2-gate of the same group.
-  __device__ __host__ float tot(int64_t bh, int64_t N, int j, int64_t f) const {
-    if (j == 1) return t1[bh * N + f];
-    if (j == 2) return t2[bh * n2 + (f >> 2)];
-    if (j == 3) return t3[bh * nb + (f >> 2)];
-    return tup[up_slot(bh, j - 3, f >> (j - 1))];
-  }
-};
-
-// Whether block-tree node (l, k) is read: as the level-(l + 3) source group, by the tiles of the
-// next aligned group, when k is even and that group has a tile.  A read node covers whole blocks.
-__device__ __host__ inline bool tree_node_read(int l, int64_t k, int64_t N) {
-  return !(k & 1) && ((k + 1) << (l + 2)) < N;
-}
-
-// Log2-decay gaps of tile u's levels, lane j - 1 holding gap_j: the summed log2-gates of the
-// tiles between the end of level j's source group and u.  Those tiles are exactly the source
-// groups of u's lower set bits, so gap_j is the sum of their totals (an exclusive wave scan).
-template <typename T>
-__device__ inline float level_gaps(const Nodes<T>& nodes, int64_t bh, int64_t N, int64_t u, int J) {
-  const int j = (threadIdx.x & 63) + 1;
-  float t = 0.f;
-  if (j <= J && reads_level(u, j)) t = nodes.tot(bh, N, j, source_first(u, j));
-  return wave_inclusive_scan(t) - t;
-}
-
-// gap_j from the lane-per-level values of level_gaps (j uniform across the wave)
-__device__ inline float gap_of(float gapv, int j) {
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gapv), j - 1));
-}
-
-// Tile-local inclusive cumulative sum of log2 gates for the R rows of a tile (rows >= nrow get
-// a zero gate), computed by the first 4 waves of the workgroup (R/4 <= 64 rows each) into cl_s[R].
-//
-// tile_gate issues this thread's load of the raw log-gate (always from a valid address); the
-// scaling to log2 and the masking of rows outside the tile happen in tile_cumsum_of, where the
-// value is first needed, so that issuing the load never makes the wave wait for it.
-template <int R>
-__device__ inline float tile_gate(const float* __restrict__ log_alpha, int64_t row0, int nrow, int H, int h) {
-  constexpr int RPW = R / 4;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r = wave * RPW + lane;
-  const int rs = (wave < 4 && lane < RPW && r < nrow) ? r : 0;
-  return log_alpha[(row0 + rs) * H + h];
-}
-
-// Scan of the raw gates returned by tile_gate for a tile of nrow rows.  Starts and ends with a
-// barrier.
-template <int R>
-__device__ inline void tile_cumsum_of(float la_raw, int nrow, float* cl_s, float* wsum_s) {
-  constexpr int RPW = R / 4;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r = wave * RPW + lane;
-  const bool mine = wave < 4 && lane < RPW;  // waves beyond the first four only take the barriers
-  const float la = (mine && r < nrow) ? la_raw * kLog2e : 0.f;
-  float cl = wave_inclusive_scan(la);
-  __syncthreads();
-  if (wave < 4 && lane == 63) wsum_s[wave] = cl;
-  __syncthreads();
-  float base = 0.f;
-  for (int w = 0; w < wave && w < 4; ++w) base += wsum_s[w];
-  if (mine) cl_s[r] = base + cl;
-  __syncthreads();
-}
-
-template <int R>
-__device__ inline void tile_cumsum(const float* __restrict__ log_alpha, int64_t row0, int nrow, int H, int h,
-                                   float* cl_s, float* wsum_s) {
-  tile_cumsum_of<R>(tile_gate<R>(log_alpha, row0, nrow, H, h), nrow, cl_s, wsum_s);
-}
-
-// Register staging of one 64-row block of a [rows, H, D] tensor, loaded with 16-byte vectors by
-// the NT threads of the workgroup (thread unit = one row's 16-byte column group, consecutive
-// threads along the row); rows at or beyond `nrow` repeat row nrow - 1 (callers give them zero
-// weight).  D is the width loaded
-// (elements per row) and LDROW the row length of the tensor in memory.  Stored row-major.
-template <typename T, int D, int NT, int LDROW = D>
-struct RowBlock {
-  static constexpr int VEC = Vec16<T>::N;
-  static constexpr int PER_ROW = D / VEC;
-  static constexpr int TOTAL = kKB * PER_ROW;
-  static constexpr int LOADS = (TOTAL + NT - 1) / NT;
-  typename Vec16<T>::type x[LOADS];
-  __device__ inline void load(const T* __restrict__ src, int64_t row0, int r0, int nrow, int H, int h) {
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int idx = threadIdx.x + NT * i;
-      const int t = idx / PER_ROW, d0 = (idx % PER_ROW) * VEC;
-      // rows at or beyond nrow repeat row nrow - 1 (no branch: the number of loads in flight
-      // stays the same on every path)
-      const int rr = r0 + t < nrow ? r0 + t : nrow - 1;
-      if (TOTAL % NT == 0 || idx < TOTAL)
-        x[i] = *reinterpret_cast<const typename Vec16<T>::type*>(src + ((row0 + rr) * H + h) * LDROW + d0);
-      else
-        x[i] = typename Vec16<T>::type{};
-    }
-  }
-  __device__ inline void store_rows(T* dst, int ld) const {
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int idx = threadIdx.x + NT * i;
-      const int t = idx / PER_ROW, d0 = (idx % PER_ROW) * VEC;
-      if (idx < TOTAL) *reinterpret_cast<typename Vec16<T>::type*>(&dst[t * ld + d0]) = x[i];
-    }
-  }
-  // row-major copy with a per-row scale: dst[t * ld + d] = x[t][d] * scale[t]
-  __device__ inline void store_rows_scaled(T* dst, int ld, const float* scale) const {
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int idx = threadIdx.x + NT * i;
-      const int t = idx / PER_ROW, d0 = (idx % PER_ROW) * VEC;
-      if (idx >= TOTAL) continue;
-      const float sc = scale[t];
-      typename Vec16<T>::type y;
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) y[e] = from_f32<T>(to_f32(x[i][e]) * sc);
-      *reinterpret_cast<typename Vec16<T>::type*>(&dst[t * ld + d0]) = y;
-    }
-  }
-};
 
 // ---------------------------------------------------------------------------------------------
 // Kernel 1: block states.  One workgroup (8 waves) per (block of 4 tiles, head, batch).  The
@@ -1198,51 +1041,15 @@ int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv
   return cur;
 }
 
-// Enqueues the stages on `st`.  With `ev` non-null, ev[i] is recorded before stage i and ev[3]
-// after the last one (used by the staged entry point): stage 0 block_state, stage 1 the level
-// scan (lambda given) or the running scan (lambda == NULL), stage 2 tile_out.
 template <typename T, int C, int DK, int DV>
-hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
+hipError_t launch_mamba2_summaries(const Mamba2Args& a, const WsLayout& w, const Nodes<T>& nodes, hipStream_t st,
+                                   hipEvent_t ev_mid) {
   constexpr int SZ = DK * DV;
-  WsLayout w;
-  mamba2_workspace(a.B, a.T, a.H, DK, DV, C, sizeof(T), a.lambda != nullptr, &w);
-  char* base = static_cast<char*>(a.workspace);
-  float* tot2 = reinterpret_cast<float*>(base + w.tot2);
-  Nodes<T> nodes{};
-  T* tiles = nullptr;
-  T* running = nullptr;
-  nodes.t1 = tot2;
-  nodes.cl = reinterpret_cast<float*>(base + w.cl);
-  if (a.lambda) {
-    nodes.lvl1 = reinterpret_cast<T*>(base + w.lvl1);
-    nodes.lvl2 = reinterpret_cast<T*>(base + w.lvl2);
-    nodes.blocks = reinterpret_cast<T*>(base + w.blocks);
-    nodes.upper = reinterpret_cast<T*>(base + w.upper);
-    nodes.t2 = reinterpret_cast<float*>(base + w.t2);
-    nodes.t3 = reinterpret_cast<float*>(base + w.t3);
-    nodes.tup = reinterpret_cast<float*>(base + w.tup);
-    nodes.n1 = w.n1;
-    nodes.n2 = w.n2;
-    nodes.nb = w.nb;
-    nodes.nup = w.nup;
-  } else {
-    tiles = reinterpret_cast<T*>(base + w.tiles);
-    running = reinterpret_cast<T*>(base + w.running);
-  }
   const dim3 gblk((unsigned)(w.nb * a.H * a.B));
-  const dim3 gscan((unsigned)((SZ / 2 + 255) / 256), (unsigned)(a.B * a.H));
-  constexpr bool kFast = std::is_same<T, __bf16>::value && tile_rows(C) == kFastRows;
-  const dim3 gtile((unsigned)(w.N * (kFast ? 1 : RowMap<tile_rows(C)>::RS) * a.H * a.B));
-  if (ev) (void)hipEventRecord(ev[0], st);
-  if (a.lambda) {
-    hipLaunchKernelGGL((k_block_state<T, C, DK, DV, true>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
-                       a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H, (int)a.Hqk);
-  } else {
-    hipLaunchKernelGGL((k_block_state<T, C, DK, DV, false>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
-                       a.log_alpha, nodes, tiles, tot2, a.T, (int)a.H, (int)a.Hqk);
-  }
-  if (ev) (void)hipEventRecord(ev[1], st);
-  if (a.lambda && w.J >= 4) {
+  hipLaunchKernelGGL((k_block_state<T, C, DK, DV, true>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
+                     a.log_alpha, nodes, (T*)nullptr, const_cast<float*>(nodes.t1), a.T, (int)a.H, (int)a.Hqk);
+  if (ev_mid) (void)hipEventRecord(ev_mid, st);
+  if (w.J >= 4) {
     // LDS: the totals tree (the block count rounded up to whole chunks, and its levels)
     const int64_t nbp = (w.nb + kScanChunk - 1) / kScanChunk * kScanChunk;
     int64_t tt = 0;
@@ -1256,9 +1063,40 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
       hipLaunchKernelGGL((k_level_scan<T, kMaxLevels>), glev, dim3(kScanThreads), tt * sizeof(float), st, nodes, w.N,
                          w.J, SZ);
   }
-  if (!a.lambda)
+  return hipGetLastError();
+}
+
+// Enqueues the stages on `st`.  With `ev` non-null, ev[i] is recorded before stage i and ev[3]
+// after the last one (used by the staged entry point): stage 0 block_state, stage 1 the level
+// scan (lambda given) or the running scan (lambda == NULL), stage 2 tile_out.
+template <typename T, int C, int DK, int DV>
+hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
+  constexpr int SZ = DK * DV;
+  WsLayout w;
+  mamba2_workspace(a.B, a.T, a.H, DK, DV, C, sizeof(T), a.lambda != nullptr, &w);
+  const Nodes<T> nodes = mamba2_nodes<T>(w, a.workspace, a.lambda != nullptr);
+  char* base = static_cast<char*>(a.workspace);
+  T* tiles = nullptr;
+  T* running = nullptr;
+  if (!a.lambda) {
+    tiles = reinterpret_cast<T*>(base + w.tiles);
+    running = reinterpret_cast<T*>(base + w.running);
+  }
+  constexpr bool kFast = std::is_same<T, __bf16>::value && tile_rows(C) == kFastRows;
+  const dim3 gtile((unsigned)(w.N * (kFast ? 1 : RowMap<tile_rows(C)>::RS) * a.H * a.B));
+  if (ev) (void)hipEventRecord(ev[0], st);
+  if (a.lambda) {
+    const hipError_t e = launch_mamba2_summaries<T, C, DK, DV>(a, w, nodes, st, ev ? ev[1] : nullptr);
+    if (e != hipSuccess) return e;
+  } else {
+    const dim3 gblk((unsigned)(w.nb * a.H * a.B));
+    const dim3 gscan((unsigned)((SZ / 2 + 255) / 256), (unsigned)(a.B * a.H));
+    hipLaunchKernelGGL((k_block_state<T, C, DK, DV, false>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,
+                       a.log_alpha, nodes, tiles, const_cast<float*>(nodes.t1), a.T, (int)a.H, (int)a.Hqk);
+    if (ev) (void)hipEventRecord(ev[1], st);
     hipLaunchKernelGGL((k_running_scan<T>), gscan, dim3(256), w.N * sizeof(float), st, (const T*)tiles, running,
-                       (const float*)tot2, w.N, SZ);
+                       (const float*)nodes.t1, w.N, SZ);
+  }
   if (ev) (void)hipEventRecord(ev[2], st);
   if constexpr (kFast) {
     if (a.lambda)
@@ -1290,12 +1128,11 @@ hipError_t launch_debug_level_map(int64_t T, int64_t C, int8_t* out, hipStream_t
   return hipGetLastError();
 }
 
-#define LL_MAMBA2_SHAPES(X)        \
-  X(float, 16, 16, 16)             \
-  X(float, 64, 64, 64)             \
-  X(__bf16, 64, 64, 64)            \
-  X(__bf16, 64, 128, 64)           \
-  X(__bf16, 64, 128, 128)
+#define LL_SUMMARIES_INST(T, C, DK, DV)                                                                     \
+  template hipError_t launch_mamba2_summaries<T, C, DK, DV>(const Mamba2Args&, const WsLayout&, const Nodes<T>&, \
+                                                            hipStream_t, hipEvent_t);
+LL_MAMBA2_SHAPES(LL_SUMMARIES_INST)
+#undef LL_SUMMARIES_INST
 
 const KernelEntry* mamba2_table(int* n) {
 #define LL_ENTRY(T, C, DK, DV) {std::is_same<T, float>::value ? 0 : 1, C, DK, DV, &launch_mamba2<T, C, DK, DV>},

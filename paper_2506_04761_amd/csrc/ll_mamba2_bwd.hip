@@ -1,0 +1,849 @@
+// Log-linear Mamba-2 backward: the gradients of O = (Q K^T (.) M^S (.) M^H) V (Sec. 3.4) with
+// respect to q, k, v, the log-gates and lambda, computed chunkwise in the forward's tiles of R
+// rows (Sec. 3.3 organisation; the gradient formulas follow from the forward by the chain rule).
+//
+// Per (b, h), with w(t, s) = lambda_t^(l(t, s)) exp(cum_t - cum_s) for s <= t, P = Q K^T and
+// G = dO V^T:
+//   dQ = (w (.) G) K,   dK = (w (.) G)^T Q,   dV = (w (.) P)^T dO,
+//   dlambda_t^(l) = sum over s at level l of exp(cum_t - cum_s) P[t, s] G[t, s],
+//   dlog_alpha_tau = sum_{t >= tau} (q_t . dq_t - k_t . dk_t).
+//
+// Query side (dq, dlambda): pairs inside a tile densely; pairs in different tiles through the
+// forward's level summaries U_j (d_v x d_k), which tile u reads at every set bit j-1 of u:
+//   dq_t += lambda_t^(log2 R + j) exp2(cl_t + gap_j) U_j^T dO_t,
+//   dlambda_t^(log2 R + j) = exp2(cl_t + gap_j) dO_t . (U_j q_t).
+// Key side (dk, dv): the same pairs seen from the key.  lambda belongs to the later (query)
+// token, so every level needs summaries of its own: key tile s with bit j-1 clear sends its keys
+// to the group G'_j(s) of the 2^(j-1) tiles that follow s's aligned 2^(j-1)-tile block, and
+//   D_j = sum_{t in G'_j} lambda_t^(log2 R + j) exp2(c_t) dO_t q_t^T   (d_v x d_k; c_t = summed
+//         log2-gates from the start of G'_j through t),
+//   dk_s += exp2(tot_s - cl_s + gap'_j) D_j^T v_s,   dv_s += exp2(...) D_j k_s,
+// gap'_j being the summed gates of the tiles strictly between s and G'_j: the groups of s's
+// lower key-side levels.  One D_j serves both dk and dv.
+//
+// Kernels, in stream order:
+//   (forward block_state and level scan)  the summaries U_j and the tile gates
+//   k_rev_state   one workgroup per (level, up to 8 tiles of one group): D_j of the groups of at
+//                 most 8 tiles, fp32 partial sums over 8-tile regions of the larger groups
+//   k_rev_reduce  the groups of >= 16 tiles: sums of their regions' partials
+//   k_bwd_dq      per tile: dq, dlambda and q . dq
+//   k_bwd_dkv     per tile: dk, dv, and the tile-local suffix sums of q . dq - k . dk into dlog_alpha
+//   k_bwd_dgate   adds the sums of all later tiles to dlog_alpha
+#include <type_traits>
+
+#include "ll_mamba2_common.hpp"
+
+namespace ll {
+
+namespace {
+
+constexpr int kRegionTiles = 8;   // tiles per region (the unit of k_rev_state's partial sums)
+constexpr int kRevThreads = 512;  // k_rev_state workgroup: 8 waves
+
+template <int R>
+struct Log2 {
+  static constexpr int v = R == 64 ? 6 : R == 128 ? 7 : -1;
+};
+
+// Device view of the key-side level summaries.  Level j's groups are the upper halves of the
+// aligned 2^j-tile blocks whose first tile exists; group m starts at tile (2m + 1) 2^(j-1).
+template <typename T>
+struct RevNodes {
+  T* d;          // [BH][nd] D_j per group, [p][n] = d_v x d_k, storage type
+  float* dtot;   // [BH][nd] summed log2-gates of each group
+  float* part;   // [BH][npart] fp32 sums over one 8-tile region of a level >= 5 group, [p][n]
+  int64_t N, NR, nd, npart;
+  __device__ __host__ static int64_t groups(int64_t N, int j) {
+    const int64_t a = (N - 1) >> (j - 1);
+    return a >= 1 ? (a + 1) / 2 : 0;
+  }
+  __device__ __host__ int64_t slot(int64_t bh, int j, int64_t m) const {
+    int64_t off = 0;
+    for (int l = 1; l < j; ++l) off += groups(N, l);
+    return bh * nd + off + m;
+  }
+  // regions rg < NR with bit j - 4 set: the regions of level-j groups (j >= 5)
+  __device__ __host__ static int64_t parts(int64_t NR, int j) {
+    const int64_t lo = int64_t(1) << (j - 4), rem = NR & (2 * lo - 1);
+    return ((NR >> (j - 3)) << (j - 4)) + (rem > lo ? rem - lo : 0);
+  }
+  __device__ __host__ int64_t pslot(int64_t bh, int j, int64_t rg) const {
+    int64_t off = 0;
+    for (int l = 5; l < j; ++l) off += parts(NR, l);
+    const int64_t lo = int64_t(1) << (j - 4);
+    return bh * npart + off + ((rg >> (j - 3)) << (j - 4)) + (rg & (lo - 1));
+  }
+};
+
+// Whether key tile s sends its keys to a level-j group (bit j-1 clear, and the group exists).
+__device__ inline bool key_level(int64_t s, int j, int64_t N) {
+  return !((s >> (j - 1)) & 1) && ((((s >> (j - 1)) | 1) << (j - 1)) < N);
+}
+
+// Sum of a value over the 4 lane groups (g = lane / 16) holding the rows of one MFMA column.
+__device__ inline float sum_over_groups(float x) {
+  x += __shfl_xor(x, 16, 64);
+  x += __shfl_xor(x, 32, 64);
+  return x;
+}
+
+// Adds x to acc[lv] for a level lv < NL known only at run time.
+template <int NL>
+__device__ inline void add_level(float (&acc)[NL], int lv, float x) {
+#pragma unroll
+  for (int l = 0; l < NL; ++l)
+    if (l == lv) acc[l] += x;
+}
+
+// Operand fragment with its k slots running down rows r0 .. r0 + KSTEP - 1 of a row-major
+// matrix in LDS (column col0 + lane % 16).  The k slots are assigned the way a B operand built
+// from MFMA result tiles assigns them (bf16: two 16-row result tiles per k step, fp32: one k step
+// per result row r of a 16-row tile), so such pairs contract correctly.
+template <typename T>
+__device__ inline typename Mfma<T>::frag frag_rows(const T* m, int ld, int r0, int col0, int r);
+template <>
+__device__ inline bf16x8 frag_rows<__bf16>(const __bf16* m, int ld, int r0, int col0, int) {
+  return frag_down_rows(m, ld, r0, col0);
+}
+template <>
+__device__ inline float frag_rows<float>(const float* m, int ld, int r0, int col0, int r) {
+  const int lane = threadIdx.x & 63;
+  return m[(r0 + 4 * (lane >> 4) + r) * ld + col0 + (lane & 15)];
+}
+
+// B operand from result-layout values: bf16 packs two 16-row tiles (slots 0-3 from a, 4-7 from
+// b); fp32 takes value r of one tile.
+__device__ inline bf16x8 pack_rl(const f32x4& a, const f32x4& b) {
+  bf16x8 f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    f[r] = static_cast<__bf16>(a[r]);
+    f[4 + r] = static_cast<__bf16>(b[r]);
+  }
+  return f;
+}
+
+// Copies rows 0 .. R-1 of a [rows, H, D] tensor (tile rows from row0; rows at or beyond nrow
+// repeat row nrow - 1) into a row-major LDS tile of row stride LD.
+template <typename T, int D, int LD, int R, int NT>
+__device__ inline void load_tile(T* dst, const T* __restrict__ src, int64_t row0, int nrow, int H, int h) {
+  typedef typename Vec16<T>::type V16;
+  constexpr int VEC = Vec16<T>::N, PER = D / VEC;
+  for (int idx = threadIdx.x; idx < R * PER; idx += NT) {
+    const int r = idx / PER, c = idx % PER;
+    const int rs = r < nrow ? r : nrow - 1;
+    *reinterpret_cast<V16*>(&dst[r * LD + c * VEC]) =
+        *reinterpret_cast<const V16*>(src + ((row0 + rs) * H + h) * D + c * VEC);
+  }
+}
+
+// lambda of the tile's rows into dst[r * L + l] (rows < nrow).
+template <int NT>
+__device__ inline void load_lambda(float* dst, const float* __restrict__ lam, int64_t row0, int nrow, int H, int h,
+                                   int L) {
+  for (int idx = threadIdx.x; idx < nrow * L; idx += NT) {
+    const int r = idx / L, l = idx % L;
+    dst[idx] = lam[((row0 + r) * H + h) * L + l];
+  }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------------------------
+// k_rev_state: one workgroup per (b, h, 8-tile region rg, item).  Items 0-3: level 1, tile
+// 8 rg + 2 i + 1; items 4-5: level 2, tiles 8 rg + 4 (i - 4) + {2, 3}; item 6: level 3, tiles
+// 8 rg + 4 .. 8 rg + 7; item 3 + j (j >= 4): level j, the whole region, present when bit j - 4 of
+// rg is set.  Each item forms sum_t w_t dO_t q_t^T over its tiles with
+// w_t = lambda_t^(log2 R + j) exp2(c_t), c_t the summed log2-gates from the item's first row through
+// t, 64 rows per step: (w q) and dO staged in LDS, both MFMA operands read down the token rows.
+// Items of levels <= 4 cover their whole group and write D_j; the others write fp32 partials.
+// ---------------------------------------------------------------------------------------------
+template <typename T, int C, int DK, int DV>
+__global__ __launch_bounds__(kRevThreads) void k_rev_state(const T* __restrict__ q, const T* __restrict__ dout,
+                                                           const float* __restrict__ lam, Nodes<T> nodes,
+                                                           RevNodes<T> rev, int64_t Tlen, int H, int L, int J,
+                                                           int items) {
+  using M = Mfma<T>;
+  typedef typename Vec16<T>::type V16;
+  constexpr int R = tile_rows(C), LOG2R = Log2<R>::v;
+  constexpr int VEC = Vec16<T>::N;
+  constexpr int LDQ = DK + 16, LDO = DV + 16;
+  constexpr int MT = DV / 16, NTN = DK / 16;
+  constexpr int NW = kRevThreads / 64;
+  constexpr int WM = MT >= 2 ? 2 : 1;
+  constexpr int WN = (NW / WM) < NTN ? (NW / WM) : NTN;
+  constexpr int TM = MT / WM, TN = NTN / WN;
+  constexpr int SZ = DK * DV;
+  constexpr int STEPS = R / kKB;
+  __shared__ T q_s[kKB * LDQ];
+  __shared__ T o_s[kKB * LDO];
+  __shared__ T out_s[SZ];
+  __shared__ float w_s[kKB];
+
+  const int64_t N = rev.N, NR = rev.NR;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // logical order (b, h, rg, item)
+  const int it = (int)(work % items);
+  const int64_t rg = (work / items) % NR;
+  const int64_t bh = work / (items * NR);
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  int j, nt;
+  int64_t u0;
+  if (it < 4) { j = 1; u0 = kRegionTiles * rg + 2 * it + 1; nt = 1; }
+  else if (it < 6) { j = 2; u0 = kRegionTiles * rg + 4 * (it - 4) + 2; nt = 2; }
+  else if (it == 6) { j = 3; u0 = kRegionTiles * rg + 4; nt = 4; }
+  else { j = it - 3; u0 = kRegionTiles * rg; nt = kRegionTiles; }
+  if (j > J || u0 >= N) return;
+  if (j >= 4 && !((rg >> (j - 4)) & 1)) return;
+  if (u0 + nt > N) nt = (int)(N - u0);
+
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool active = wave < WM * WN;
+  const int wm = wave / WN, wn = wave % WN;
+  const int nsteps = nt * STEPS;
+  auto nrow_of = [&](int64_t u) { return (int)((Tlen - u * R) < R ? (Tlen - u * R) : R); };
+  auto tile_row0 = [&](int64_t u) { return (int64_t)b * Tlen + u * R; };
+
+  RowBlock<T, DK, kRevThreads> qr;
+  RowBlock<T, DV, kRevThreads> dr;
+  float wv = 0.f;
+  float base = 0.f;  // summed log2-gates of the item's tiles before the current one
+  auto load_step = [&](int s) {
+    const int64_t u = u0 + s / STEPS;
+    const int r0 = (s % STEPS) * kKB;
+    qr.load(q, tile_row0(u), r0, nrow_of(u), H, h);
+    dr.load(dout, tile_row0(u), r0, nrow_of(u), H, h);
+    if (tid < kKB) {
+      const int r = r0 + tid;
+      const float c = base + nodes.cl[(bh * N + u) * R + r];
+      wv = r < nrow_of(u) ? lam[((tile_row0(u) + r) * H + h) * L + LOG2R + j] * fast_exp2(c) : 0.f;
+    }
+  };
+
+  f32x4 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int jn = 0; jn < TN; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  load_step(0);
+  for (int s = 0; s < nsteps; ++s) {
+    __syncthreads();  // previous step's readers are done
+    if (tid < kKB) w_s[tid] = wv;
+    dr.store_rows(o_s, LDO);
+    __syncthreads();
+    qr.store_rows_scaled(q_s, LDQ, w_s);
+    if ((s + 1) % STEPS == 0) base += nodes.t1[bh * N + u0 + s / STEPS];
+    if (s + 1 < nsteps) load_step(s + 1);
+    __syncthreads();
+    if (active) {
+#pragma unroll
+      for (int ks = 0; ks < kKB / M::KSTEP; ++ks) {
+        typename M::frag bf[TN];
+#pragma unroll
+        for (int jn = 0; jn < TN; ++jn) {
+          const int n0 = (wn * TN + jn) * 16;
+          if constexpr (M::KPL == 8) bf[jn] = frag_down_rows(q_s, LDQ, ks * 32, n0);
+          else bf[jn] = q_s[(ks * 4 + g) * LDQ + n0 + r16];
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int p0 = (wm * TM + i) * 16;
+          typename M::frag af;
+          if constexpr (M::KPL == 8) af = frag_down_rows(o_s, LDO, ks * 32, p0);
+          else af = o_s[(ks * 4 + g) * LDO + p0 + r16];
+#pragma unroll
+          for (int jn = 0; jn < TN; ++jn) acc[i][jn] = M::mma(af, bf[jn], acc[i][jn]);
+        }
+      }
+    }
+  }
+
+  if (j <= 4) {
+    const int64_t sl = rev.slot(bh, j, u0 >> j);
+    if (active) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int jn = 0; jn < TN; ++jn)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int p = (wm * TM + i) * 16 + 4 * g + r, n = (wn * TN + jn) * 16 + r16;
+            out_s[p * DK + n] = from_f32<T>(acc[i][jn][r]);
+          }
+    }
+    __syncthreads();
+    T* dst = rev.d + sl * SZ;
+    for (int idx = tid; idx < SZ / VEC; idx += kRevThreads)
+      *reinterpret_cast<V16*>(dst + idx * VEC) = *reinterpret_cast<const V16*>(&out_s[idx * VEC]);
+    if (tid == 0) rev.dtot[sl] = base;
+  } else if (active) {
+    float* dst = rev.part + rev.pslot(bh, j, rg) * SZ;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < TN; ++jn)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int p = (wm * TM + i) * 16 + 4 * g + r, n = (wn * TN + jn) * 16 + r16;
+          dst[p * DK + n] = acc[i][jn][r];
+        }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// k_rev_reduce: grid (SZ / 1024 entry blocks, level >= 5 groups, B * H); each thread sums four
+// entries of one group's region partials, region by region, each weighted by the gates of the
+// group's regions before it.
+// ---------------------------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_rev_reduce(Nodes<T> nodes, RevNodes<T> rev, int J, int SZ) {
+  const int64_t N = rev.N, NR = rev.NR;
+  const int64_t bh = blockIdx.z;
+  int64_t y = blockIdx.y;
+  int j = 5;
+  for (; j <= J; ++j) {
+    const int64_t ng = RevNodes<T>::groups(N, j);
+    if (y < ng) break;
+    y -= ng;
+  }
+  if (j > J) return;
+  const int64_t first = (2 * y + 1) << (j - 1);
+  const int64_t rg0 = first / kRegionTiles;
+  int64_t nreg = int64_t(1) << (j - 4);
+  if (rg0 + nreg > NR) nreg = NR - rg0;
+  const int e0 = (blockIdx.x * 256 + threadIdx.x) * 4;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float base = 0.f;
+  for (int64_t r = 0; r < nreg; ++r) {
+    const int64_t rgn = rg0 + r;
+    if (e0 < SZ) {
+      const f32x4 x = *reinterpret_cast<const f32x4*>(rev.part + rev.pslot(bh, j, rgn) * SZ + e0);
+      acc += fast_exp2(base) * x;
+    }
+    const int64_t x1 = (rgn + 1) * kRegionTiles < N ? (rgn + 1) * kRegionTiles : N;
+    for (int64_t x = rgn * kRegionTiles; x < x1; ++x) base += nodes.t1[bh * N + x];
+  }
+  const int64_t sl = rev.slot(bh, j, y);
+  if (e0 < SZ)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) rev.d[sl * SZ + e0 + e] = from_f32<T>(acc[e]);
+  if (blockIdx.x == 0 && threadIdx.x == 0) rev.dtot[sl] = base;
+}
+
+// ---------------------------------------------------------------------------------------------
+// k_bwd_dq: one workgroup of R/16 waves per (b, h, tile); wave w owns query rows 16 w .. 16 w + 15,
+// one per MFMA column (lane % 16).  K and V of the tile resident in LDS.
+//   intra: S^T = K Q^T and G^T = V dO^T per 16-key tile; weights lambda_i^(l) exp2(cl_i - cl_j);
+//          dq^T += K^T (w (.) G)^T; dlambda_i^(l) += exp2(cl_i - cl_j) S G, summed per level;
+//   inter: per level read, U_j copied into LDS: y^T = U_j Q^T (dlambda = dO . y), and
+//          dq^T += (lambda exp2(cl + gap)) U_j^T dO^T.
+// ---------------------------------------------------------------------------------------------
+template <typename T, int C, int DK, int DV>
+__global__ __launch_bounds__(4 * tile_rows(C)) void k_bwd_dq(const T* __restrict__ q, const T* __restrict__ k,
+                                                            const T* __restrict__ v, const T* __restrict__ dout,
+                                                            const float* __restrict__ log_alpha,
+                                                            const float* __restrict__ lam, Nodes<T> nodes,
+                                                            T* __restrict__ dq, float* __restrict__ dlam,
+                                                            float* __restrict__ qdq, int64_t Tlen, int H, int L, int J) {
+  using M = Mfma<T>;
+  typedef typename Vec16<T>::type V16;
+  constexpr int R = tile_rows(C), LOG2R = Log2<R>::v, NW = R / 16, NT = 64 * NW;
+  constexpr int VEC = Vec16<T>::N;
+  constexpr int LDK = DK + 16, LDV = DV + 16;
+  constexpr int KSK = DK / M::KSTEP, KSV = DV / M::KSTEP, MTK = DK / 16, MTV = DV / 16;
+  constexpr int SZ = DK * DV;
+  constexpr int NL = LOG2R + 1;  // levels inside a tile
+  static_assert(DV <= R, "a summary fits in the K region");
+  __shared__ T k_s[R * LDK];
+  __shared__ T v_s[R * LDV];
+  __shared__ float cl_s[R];
+  __shared__ float wsum_s[4];
+  __shared__ float lam_s[R * kMaxLevels];
+  __shared__ float dl_s[R * kMaxLevels];
+  T* u_s = k_s;
+
+  const int64_t N = (Tlen + R - 1) / R;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // logical order (b, h, u)
+  const int u = (int)(work % N);
+  const int64_t bh = work / N;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t row0 = (int64_t)b * Tlen + (int64_t)u * R;
+  const int nrow = (int)((Tlen - (int64_t)u * R) < R ? (Tlen - (int64_t)u * R) : R);
+  const int i = 16 * wave + r16;  // this lane's query row
+  const bool rowok = i < nrow;
+  const int64_t qrow = (row0 + (rowok ? i : 0)) * H + h;
+
+  const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);
+  load_tile<T, DK, LDK, R, NT>(k_s, k, row0, nrow, H, h);
+  load_tile<T, DV, LDV, R, NT>(v_s, v, row0, nrow, H, h);
+  load_lambda<NT>(lam_s, lam, row0, nrow, H, h, L);
+  for (int x = tid; x < R * kMaxLevels; x += NT) dl_s[x] = 0.f;
+
+  typename M::frag qf[KSK], df[KSV];
+#pragma unroll
+  for (int ks = 0; ks < KSK; ++ks)
+    qf[ks] = rowok ? M::load(q + qrow * DK + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
+#pragma unroll
+  for (int ks = 0; ks < KSV; ++ks)
+    df[ks] = rowok ? M::load(dout + qrow * DV + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
+  f32x4 dorl[MTV];  // dO of row i at d_v entries 16 mt + 4 g + r
+#pragma unroll
+  for (int mt = 0; mt < MTV; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dorl[mt][r] = rowok ? to_f32(dout[qrow * DV + 16 * mt + 4 * g + r]) : 0.f;
+
+  tile_cumsum_of<R>(la, nrow, cl_s, wsum_s);  // barriers: the LDS tiles are visible after it
+  const float cli = cl_s[i];
+  const float* lrow = &lam_s[(rowok ? i : 0) * L];
+
+  f32x4 acc[MTK];
+#pragma unroll
+  for (int mt = 0; mt < MTK; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float dl[NL];
+#pragma unroll
+  for (int l = 0; l < NL; ++l) dl[l] = 0.f;
+
+  // weights of one 16-key tile KT <= wave, in the result layout (key 16 KT + 4 g + r, query i)
+  auto key_tile = [&](int KT, f32x4& wg) {
+    f32x4 s = {0.f, 0.f, 0.f, 0.f}, gg = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KSK; ++ks)
+      s = M::mma(M::load(&k_s[(KT * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]), qf[ks], s);
+#pragma unroll
+    for (int ks = 0; ks < KSV; ++ks)
+      gg = M::mma(M::load(&v_s[(KT * 16 + r16) * LDV + ks * M::KSTEP + g * M::KPL]), df[ks], gg);
+    if (KT < wave) {
+      const int lv = level_local(16 * wave, 16 * KT);  // one level for the whole 16 x 16 tile
+      const float lw = rowok ? lrow[lv] : 0.f;
+      float pg = 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float e = fast_exp2(cli - cl_s[16 * KT + 4 * g + r]);
+        pg += e * s[r] * gg[r];
+        wg[r] = lw * e * gg[r];
+      }
+      add_level(dl, lv, pg);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int jj = 16 * KT + 4 * g + r;
+        const bool ok = jj <= i && rowok;
+        const int lv = level_local(i, jj);
+        const float e = ok ? fast_exp2(cli - cl_s[jj]) : 0.f;
+        add_level(dl, ok ? lv : 0, e * s[r] * gg[r]);
+        wg[r] = ok ? lrow[lv] * e * gg[r] : 0.f;
+      }
+    }
+  };
+
+  if constexpr (M::KPL == 8) {
+    for (int st = 0; 2 * st <= wave; ++st) {
+      f32x4 w0, w1 = {0.f, 0.f, 0.f, 0.f};
+      key_tile(2 * st, w0);
+      if (2 * st + 1 <= wave) key_tile(2 * st + 1, w1);
+      const bf16x8 bp = pack_rl(w0, w1);
+#pragma unroll
+      for (int mt = 0; mt < MTK; ++mt) acc[mt] = M::mma(frag_rows<T>(k_s, LDK, 32 * st, 16 * mt, 0), bp, acc[mt]);
+    }
+  } else {
+    for (int KT = 0; KT <= wave; ++KT) {
+      f32x4 w0;
+      key_tile(KT, w0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int mt = 0; mt < MTK; ++mt)
+          acc[mt] = M::mma(frag_rows<T>(k_s, LDK, 16 * KT, 16 * mt, r), w0[r], acc[mt]);
+    }
+  }
+#pragma unroll
+  for (int l = 0; l < NL; ++l) {
+    const float x = sum_over_groups(dl[l]);
+    if (g == 0 && rowok && l < L) dl_s[i * L + l] = x;
+  }
+
+  // ---- inter-tile levels (set bits of u) through the forward's summaries
+  const float gapv = level_gaps(nodes, bh, N, u, J);
+  for (int j = 1; j <= J; ++j) {
+    if (!reads_level(u, j)) continue;
+    __syncthreads();  // K region free
+    {
+      const T* U = nodes.at(bh, N, j, source_first(u, j), SZ);
+      for (int idx = tid; idx < SZ / VEC; idx += NT) {
+        const int p = idx / (DK / VEC), c = idx % (DK / VEC);
+        *reinterpret_cast<V16*>(&u_s[p * LDK + c * VEC]) = *reinterpret_cast<const V16*>(U + idx * VEC);
+      }
+    }
+    __syncthreads();
+    const float wdec = rowok ? fast_exp2(cli + gap_of(gapv, j)) : 0.f;
+    float yd = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MTV; ++mt) {
+      f32x4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KSK; ++ks)
+        t = M::mma(M::load(&u_s[(mt * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]), qf[ks], t);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) yd += t[r] * dorl[mt][r];
+    }
+    yd = sum_over_groups(yd);
+    if (g == 0 && rowok) dl_s[i * L + LOG2R + j] = wdec * yd;
+    const float sc = rowok ? wdec * lrow[LOG2R + j] : 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MTK; ++mt) {
+      f32x4 t = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (M::KPL == 8) {
+#pragma unroll
+        for (int st = 0; st < DV / 32; ++st)
+          t = M::mma(frag_rows<T>(u_s, LDK, 32 * st, 16 * mt, 0), pack_rl(dorl[2 * st], dorl[2 * st + 1]), t);
+      } else {
+#pragma unroll
+        for (int tt = 0; tt < MTV; ++tt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) t = M::mma(frag_rows<T>(u_s, LDK, 16 * tt, 16 * mt, r), dorl[tt][r], t);
+      }
+      acc[mt] += sc * t;
+    }
+  }
+
+  // ---- outputs: dq (row i, d_k entries 16 mt + 4 g + r), q . dq, dlambda rows
+  float qd = 0.f;
+#pragma unroll
+  for (int mt = 0; mt < MTK; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t e = qrow * DK + 16 * mt + 4 * g + r;
+      if (rowok) {
+        dq[e] = from_f32<T>(acc[mt][r]);
+        qd += acc[mt][r] * to_f32(q[e]);
+      }
+    }
+  qd = sum_over_groups(qd);
+  if (g == 0 && rowok) qdq[qrow] = qd;
+  __syncthreads();
+  for (int idx = tid; idx < nrow * L; idx += NT) {
+    const int r = idx / L, l = idx % L;
+    dlam[((row0 + r) * H + h) * L + l] = dl_s[idx];
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// k_bwd_dkv: one workgroup of R/16 waves per (b, h, tile); wave w owns key rows 16 w .. 16 w + 15,
+// one per MFMA column.  Q and dO of the tile resident in LDS.
+//   intra: S = Q K^T and G = dO V^T per 16-query tile (queries >= keys), weights from the query's
+//          lambda row; dk^T += Q^T (w (.) G), dv^T += dO^T (w (.) S);
+//   inter: per key-side level, D_j copied into LDS: dk^T += w' D_j^T V^T, dv^T += w' D_j K^T;
+//   then dcum = q . dq - k . dk per row, summed from each row to the tile end into dlog_alpha,
+//   and the tile's total into tsum.
+// ---------------------------------------------------------------------------------------------
+template <typename T, int C, int DK, int DV>
+__global__ __launch_bounds__(4 * tile_rows(C)) void k_bwd_dkv(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ dout,
+    const float* __restrict__ log_alpha, const float* __restrict__ lam, RevNodes<T> rev, const float* __restrict__ qdq,
+    T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ dla, float* __restrict__ tsum, int64_t Tlen, int H,
+    int L, int J) {
+  using M = Mfma<T>;
+  typedef typename Vec16<T>::type V16;
+  constexpr int R = tile_rows(C), NW = R / 16, NT = 64 * NW;
+  constexpr int VEC = Vec16<T>::N;
+  constexpr int LDQ = DK + 16, LDO = DV + 16;
+  constexpr int KSK = DK / M::KSTEP, KSV = DV / M::KSTEP, MTK = DK / 16, MTV = DV / 16;
+  constexpr int SZ = DK * DV;
+  static_assert(DV <= R, "a summary fits in the Q region");
+  __shared__ T q_s[R * LDQ];
+  __shared__ T o_s[R * LDO];
+  __shared__ float cl_s[R];
+  __shared__ float wsum_s[4];
+  __shared__ float lam_s[R * kMaxLevels];
+  __shared__ float dc_s[R];
+  T* d_s = q_s;
+
+  const int64_t N = (Tlen + R - 1) / R;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // logical order (b, h, u)
+  const int u = (int)(work % N);
+  const int64_t bh = work / N;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t row0 = (int64_t)b * Tlen + (int64_t)u * R;
+  const int nrow = (int)((Tlen - (int64_t)u * R) < R ? (Tlen - (int64_t)u * R) : R);
+  const int jk = 16 * wave + r16;  // this lane's key row
+  const bool keyok = jk < nrow;
+  const int64_t krow = (row0 + (keyok ? jk : 0)) * H + h;
+
+  const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);
+  load_tile<T, DK, LDQ, R, NT>(q_s, q, row0, nrow, H, h);
+  load_tile<T, DV, LDO, R, NT>(o_s, dout, row0, nrow, H, h);
+  load_lambda<NT>(lam_s, lam, row0, nrow, H, h, L);
+
+  typename M::frag kf[KSK], vf[KSV];
+#pragma unroll
+  for (int ks = 0; ks < KSK; ++ks)
+    kf[ks] = keyok ? M::load(k + krow * DK + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
+#pragma unroll
+  for (int ks = 0; ks < KSV; ++ks)
+    vf[ks] = keyok ? M::load(v + krow * DV + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
+  f32x4 vrl[MTV];  // v of key row jk at d_v entries 16 mt + 4 g + r
+#pragma unroll
+  for (int mt = 0; mt < MTV; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) vrl[mt][r] = keyok ? to_f32(v[krow * DV + 16 * mt + 4 * g + r]) : 0.f;
+
+  tile_cumsum_of<R>(la, nrow, cl_s, wsum_s);
+  const float clj = cl_s[jk];
+
+  f32x4 ak[MTK], av[MTV];
+#pragma unroll
+  for (int mt = 0; mt < MTK; ++mt) ak[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int mt = 0; mt < MTV; ++mt) av[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // weights of one 16-query tile QT >= wave, result layout (query 16 QT + 4 g + r, key jk)
+  auto query_tile = [&](int QT, f32x4& wg, f32x4& wp) {
+    f32x4 s = {0.f, 0.f, 0.f, 0.f}, gg = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KSK; ++ks)
+      s = M::mma(M::load(&q_s[(QT * 16 + r16) * LDQ + ks * M::KSTEP + g * M::KPL]), kf[ks], s);
+#pragma unroll
+    for (int ks = 0; ks < KSV; ++ks)
+      gg = M::mma(M::load(&o_s[(QT * 16 + r16) * LDO + ks * M::KSTEP + g * M::KPL]), vf[ks], gg);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int ii = 16 * QT + 4 * g + r;
+      const bool ok = ii >= jk && ii < nrow && keyok;
+      const int lv = QT > wave ? level_local(16 * QT, 16 * wave) : level_local(ii, jk);
+      const float lw = ok ? lam_s[ii * L + lv] * fast_exp2(cl_s[ii] - clj) : 0.f;
+      wg[r] = lw * gg[r];
+      wp[r] = lw * s[r];
+    }
+  };
+
+  if constexpr (M::KPL == 8) {
+    for (int st = wave / 2; st < NW / 2; ++st) {
+      f32x4 g0 = {0.f, 0.f, 0.f, 0.f}, p0 = g0, g1, p1;
+      if (2 * st >= wave) query_tile(2 * st, g0, p0);
+      query_tile(2 * st + 1, g1, p1);
+      const bf16x8 bg = pack_rl(g0, g1), bq = pack_rl(p0, p1);
+#pragma unroll
+      for (int mt = 0; mt < MTK; ++mt) ak[mt] = M::mma(frag_rows<T>(q_s, LDQ, 32 * st, 16 * mt, 0), bg, ak[mt]);
+#pragma unroll
+      for (int mt = 0; mt < MTV; ++mt) av[mt] = M::mma(frag_rows<T>(o_s, LDO, 32 * st, 16 * mt, 0), bq, av[mt]);
+    }
+  } else {
+    for (int QT = wave; QT < NW; ++QT) {
+      f32x4 g0, p0;
+      query_tile(QT, g0, p0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+#pragma unroll
+        for (int mt = 0; mt < MTK; ++mt) ak[mt] = M::mma(frag_rows<T>(q_s, LDQ, 16 * QT, 16 * mt, r), g0[r], ak[mt]);
+#pragma unroll
+        for (int mt = 0; mt < MTV; ++mt) av[mt] = M::mma(frag_rows<T>(o_s, LDO, 16 * QT, 16 * mt, r), p0[r], av[mt]);
+      }
+    }
+  }
+
+  // ---- key-side levels: gap'_j (lane j - 1) is the exclusive sum over the lower key-side levels
+  float gapr;
+  {
+    const int jl = lane + 1;
+    float t = 0.f;
+    if (jl <= J && key_level(u, jl, N)) t = rev.dtot[rev.slot(bh, jl, (int64_t)u >> jl)];
+    gapr = wave_inclusive_scan(t) - t;
+  }
+  const float tot_u = cl_s[R - 1];
+  for (int j = 1; j <= J; ++j) {
+    if (!key_level(u, j, N)) continue;
+    __syncthreads();  // Q region free
+    {
+      const T* D = rev.d + rev.slot(bh, j, (int64_t)u >> j) * SZ;
+      for (int idx = tid; idx < SZ / VEC; idx += NT) {
+        const int p = idx / (DK / VEC), c = idx % (DK / VEC);
+        *reinterpret_cast<V16*>(&d_s[p * LDQ + c * VEC]) = *reinterpret_cast<const V16*>(D + idx * VEC);
+      }
+    }
+    __syncthreads();
+    const float wk = keyok ? fast_exp2(tot_u - clj + gap_of(gapr, j)) : 0.f;
+    // dk^T[n][jk] += wk sum_p D[p][n] v[p]
+#pragma unroll
+    for (int mt = 0; mt < MTK; ++mt) {
+      f32x4 t = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (M::KPL == 8) {
+#pragma unroll
+        for (int st = 0; st < DV / 32; ++st)
+          t = M::mma(frag_rows<T>(d_s, LDQ, 32 * st, 16 * mt, 0), pack_rl(vrl[2 * st], vrl[2 * st + 1]), t);
+      } else {
+#pragma unroll
+        for (int tt = 0; tt < MTV; ++tt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) t = M::mma(frag_rows<T>(d_s, LDQ, 16 * tt, 16 * mt, r), vrl[tt][r], t);
+      }
+      ak[mt] += wk * t;
+    }
+    // dv^T[p][jk] += wk sum_n D[p][n] k[n]
+#pragma unroll
+    for (int mt = 0; mt < MTV; ++mt) {
+      f32x4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KSK; ++ks)
+        t = M::mma(M::load(&d_s[(mt * 16 + r16) * LDQ + ks * M::KSTEP + g * M::KPL]), kf[ks], t);
+      av[mt] += wk * t;
+    }
+  }
+
+  // ---- outputs
+  float kd = 0.f;
+#pragma unroll
+  for (int mt = 0; mt < MTK; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t e = krow * DK + 16 * mt + 4 * g + r;
+      if (keyok) {
+        dk[e] = from_f32<T>(ak[mt][r]);
+        kd += ak[mt][r] * to_f32(k[e]);
+      }
+    }
+#pragma unroll
+  for (int mt = 0; mt < MTV; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (keyok) dv[krow * DV + 16 * mt + 4 * g + r] = from_f32<T>(av[mt][r]);
+  kd = sum_over_groups(kd);
+  if (g == 0) dc_s[jk] = keyok ? qdq[krow] - kd : 0.f;
+  __syncthreads();
+  // suffix sums of dcum within the tile: thread x < R (whole waves) scans row R - 1 - x
+  const int row = R - 1 - tid;
+  float x = 0.f;
+  if (tid < R) x = wave_inclusive_scan(dc_s[row]);
+  if (tid < R && lane == 63) wsum_s[wave] = x;
+  __syncthreads();
+  if (tid < R) {
+    for (int w = 0; w < wave; ++w) x += wsum_s[w];
+    if (row < nrow) dla[(row0 + row) * H + h] = x;
+    if (tid == R - 1) tsum[bh * N + u] = x;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// k_bwd_dgate: grid (ceil(T / 256), B * H); adds to each row's tile-local suffix sum the totals
+// of all later tiles of its sequence.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_bwd_dgate(const float* __restrict__ tsum, float* __restrict__ dla,
+                                                   int64_t Tlen, int H, int R) {
+  __shared__ float red_s[4];
+  const int64_t N = (Tlen + R - 1) / R;
+  const int64_t bh = blockIdx.y;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int64_t t0 = (int64_t)blockIdx.x * 256;
+  const int64_t t1 = t0 + 255 < Tlen - 1 ? t0 + 255 : Tlen - 1;
+  const int64_t ulast = t1 / R;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  float s = 0.f;
+  for (int64_t x = ulast + 1 + tid; x < N; x += 256) s += tsum[bh * N + x];
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (lane == 0) red_s[wave] = s;
+  __syncthreads();
+  const float after = red_s[0] + red_s[1] + red_s[2] + red_s[3];  // tiles after the last one here
+  const int64_t t = t0 + tid;
+  if (t < Tlen) {
+    float add = after;
+    for (int64_t x = t / R + 1; x <= ulast; ++x) add += tsum[bh * N + x];
+    dla[((int64_t)b * Tlen + t) * H + h] += add;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------------------------
+int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, int64_t esize,
+                             BwdLayout* lay) {
+  BwdLayout w{};
+  int64_t cur = mamba2_workspace(B, T, H, dk, dv, C, esize, true, &w.fwd);
+  auto al = [](int64_t x) { return (x + 255) & ~int64_t(255); };
+  const int64_t N = w.fwd.N, BH = B * H, SZ = dk * dv;
+  const int J = w.fwd.J;
+  w.NR = (N + kRegionTiles - 1) / kRegionTiles;
+  w.nd = 0;
+  for (int j = 1; j <= J; ++j) w.nd += RevNodes<float>::groups(N, j);
+  w.npart = 0;
+  for (int j = 5; j <= J; ++j) w.npart += RevNodes<float>::parts(w.NR, j);
+  const int64_t nd1 = w.nd > 0 ? w.nd : 1, np1 = w.npart > 0 ? w.npart : 1;
+  w.d = cur; cur += al(BH * nd1 * SZ * esize);
+  w.dtot = cur; cur += al(BH * nd1 * 4);
+  w.part = cur; cur += al(BH * np1 * SZ * 4);
+  w.qdq = cur; cur += al(B * T * H * 4);
+  w.tsum = cur; cur += al(BH * N * 4);
+  w.total = cur;
+  if (lay) *lay = w;
+  return cur;
+}
+
+// Stages (ev[i] recorded before stage i, ev[4] after the last): 0 the forward summaries, 1 the
+// key-side summaries, 2 dq and dlambda, 3 dk, dv and dlog_alpha.
+template <typename T, int C, int DK, int DV>
+hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t* ev) {
+  constexpr int R = tile_rows(C), SZ = DK * DV;
+  BwdLayout w;
+  mamba2_bwd_workspace(a.B, a.T, a.H, DK, DV, C, sizeof(T), &w);
+  const Nodes<T> nodes = mamba2_nodes<T>(w.fwd, a.workspace, true);
+  char* base = static_cast<char*>(a.workspace);
+  RevNodes<T> rev;
+  rev.d = reinterpret_cast<T*>(base + w.d);
+  rev.dtot = reinterpret_cast<float*>(base + w.dtot);
+  rev.part = reinterpret_cast<float*>(base + w.part);
+  rev.N = w.fwd.N;
+  rev.NR = w.NR;
+  rev.nd = w.nd;
+  rev.npart = w.npart;
+  float* qdq = reinterpret_cast<float*>(base + w.qdq);
+  float* tsum = reinterpret_cast<float*>(base + w.tsum);
+  const int J = w.fwd.J;
+  const int64_t BH = a.B * a.H;
+
+  Mamba2Args fa{};
+  fa.q = a.q; fa.k = a.k; fa.v = a.v; fa.log_alpha = a.log_alpha; fa.lambda = a.lambda; fa.o = nullptr;
+  fa.B = a.B; fa.T = a.T; fa.H = a.H; fa.dk = DK; fa.dv = DV; fa.C = C; fa.Hqk = a.H; fa.L = a.L;
+  fa.workspace = a.workspace;
+  if (ev) (void)hipEventRecord(ev[0], st);
+  hipError_t e = launch_mamba2_summaries<T, C, DK, DV>(fa, w.fwd, nodes, st, nullptr);
+  if (e != hipSuccess) return e;
+  if (ev) (void)hipEventRecord(ev[1], st);
+  if (J >= 1) {
+    const int items = 7 + (J > 3 ? J - 3 : 0);
+    hipLaunchKernelGGL((k_rev_state<T, C, DK, DV>), dim3((unsigned)(BH * w.NR * items)), dim3(kRevThreads), 0, st,
+                       (const T*)a.q, (const T*)a.dout, a.lambda, nodes, rev, a.T, (int)a.H, a.L, J, items);
+  }
+  if (J >= 5) {
+    int64_t ng = 0;
+    for (int j = 5; j <= J; ++j) ng += RevNodes<T>::groups(w.fwd.N, j);
+    hipLaunchKernelGGL((k_rev_reduce<T>), dim3((unsigned)((SZ + 1023) / 1024), (unsigned)ng, (unsigned)BH), dim3(256),
+                       0, st, nodes, rev, J, SZ);
+  }
+  if (ev) (void)hipEventRecord(ev[2], st);
+  const dim3 gtile((unsigned)(w.fwd.N * BH));
+  hipLaunchKernelGGL((k_bwd_dq<T, C, DK, DV>), gtile, dim3(4 * R), 0, st, (const T*)a.q, (const T*)a.k,
+                     (const T*)a.v, (const T*)a.dout, a.log_alpha, a.lambda, nodes, (T*)a.dq, a.dlambda, qdq, a.T,
+                     (int)a.H, a.L, J);
+  if (ev) (void)hipEventRecord(ev[3], st);
+  hipLaunchKernelGGL((k_bwd_dkv<T, C, DK, DV>), gtile, dim3(4 * R), 0, st, (const T*)a.q, (const T*)a.k,
+                     (const T*)a.v, (const T*)a.dout, a.log_alpha, a.lambda, rev, (const float*)qdq, (T*)a.dk,
+                     (T*)a.dv, a.dlog_alpha, tsum, a.T, (int)a.H, a.L, J);
+  hipLaunchKernelGGL(k_bwd_dgate, dim3((unsigned)((a.T + 255) / 256), (unsigned)BH), dim3(256), 0, st,
+                     (const float*)tsum, a.dlog_alpha, a.T, (int)a.H, R);
+  if (ev) (void)hipEventRecord(ev[4], st);
+  return hipGetLastError();
+}
+
+const BwdEntry* mamba2_bwd_table(int* n) {
+#define LL_BWD_ENTRY(T, C, DK, DV) {std::is_same<T, float>::value ? 0 : 1, C, DK, DV, &launch_mamba2_bwd<T, C, DK, DV>},
+  static const BwdEntry table[] = {LL_MAMBA2_SHAPES(LL_BWD_ENTRY)};
+#undef LL_BWD_ENTRY
+  *n = sizeof(table) / sizeof(table[0]);
+  return table;
+}
+
+}  // namespace ll

@@ -27,7 +27,7 @@ import numpy as np
 @dataclass(frozen=True)
 class Workload:
     name: str
-    variant: str      # "mamba2", "gdn" or "decode" (log-linear Mamba-2 decoding)
+    variant: str      # "mamba2", "gdn", "mamba2_bwd" (backward pass) or "decode" (decoding)
     dtype: str        # "f32" or "bf16": storage dtype of q, k, v and o
     B: int
     H: int
@@ -60,6 +60,8 @@ WORKLOADS = {
         Workload("ll_mamba2_mva_bf16_T16384", "mamba2", "bf16", 2, 48, 16384, 128, 64, 64, 6, "unit", 1),
         # decoding: 64 sequences x 16 heads fed one token per step up to position 8191 (the token
         # inputs are the T = 1024 draw, cycled)
+        # backward pass over the same inputs as the T = 65536 forward workload
+        Workload("ll_mamba2_bwd_bf16_T65536", "mamba2_bwd", "bf16", 1, 16, 65536, 128, 128, 64, 4, "unit"),
         Workload("ll_mamba2_decode_bf16_T8192", "decode", "bf16", 64, 16, 8192, 128, 128, 64, 7, "unit"),
     ]
 }
@@ -131,3 +133,14 @@ def generate(w: Workload, T: int = None, heads=None):
                 a = a[..., :Lt]
             out[key] = np.ascontiguousarray(a)
     return out
+
+
+def upstream_grad(w: Workload, T: int = None, heads=None):
+    """The upstream gradient dO [B, T, H, d_v] for a backward pass over workload w: standard
+    normals from their own stream (PCG64 seeded with seed + 1000), rounded to the storage dtype.
+    `T` and `heads` select a prefix and a subset of heads of the full draw, as in generate."""
+    rng = np.random.default_rng(w.seed + 1000)
+    do = to_storage(rng.standard_normal((w.B, w.T, w.H, w.dv), dtype=np.float32), w.dtype)
+    if T is not None or heads is not None:
+        do = np.ascontiguousarray(do[:, :w.T if T is None else T][:, :, slice(None) if heads is None else heads])
+    return do

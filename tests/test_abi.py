@@ -119,6 +119,38 @@ def test_mamba2_argument_checks_return_before_launch():
     assert _m2(ws=ctypes.c_void_p(4096 + 8)) == ll._lib.LL_ERR_WORKSPACE
 
 
+def _bwd(lam=FAKE, do=FAKE, dla=FAKE, T=128, dk=64, dv=64, C=64, dtype=1, ws=FAKE, wsb=1 << 40, staged=False, ev=None):
+    args = [FAKE, FAKE, FAKE, FAKE, lam, do, FAKE, FAKE, FAKE, dla, FAKE, 1, T, 2, dk, dv, C, dtype, ws, wsb, None]
+    if staged:
+        return lib.ll_mamba2_bwd_staged(*args, ev)
+    return lib.ll_mamba2_bwd(*args)
+
+
+def test_mamba2_bwd_argument_checks_return_before_launch():
+    assert _bwd(lam=None) == ll._lib.LL_ERR_NULL_ARG     # lambda is required by the backward
+    assert _bwd(do=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _bwd(dla=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _bwd(ws=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _bwd(T=100) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _bwd(dk=96) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _bwd(dtype=3) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _bwd(wsb=1000) == ll._lib.LL_ERR_WORKSPACE
+    assert _bwd(ws=ctypes.c_void_p(4096 + 64)) == ll._lib.LL_ERR_WORKSPACE
+    assert _bwd(staged=True, ev=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _bwd(staged=True, ev=(ctypes.c_void_p * 5)(4096, 4096, None, 4096, 4096)) == ll._lib.LL_ERR_NULL_ARG
+
+
+def test_mamba2_bwd_workspace_and_support():
+    for shape in ((ll.LL_F32, 16, 16, 16), (ll.LL_BF16, 64, 128, 128), (ll.LL_BF16, 64, 128, 64)):
+        assert ll.ll_supported(ll.LL_MAMBA2_BWD, *shape)
+    assert not ll.ll_supported(ll.LL_MAMBA2_BWD, ll.LL_BF16, 64, 96, 64)
+    fwd = ll.ll_workspace_size(ll.LL_MAMBA2, ll.LL_BF16, 1, 65536, 16, 128, 128, 64, 1)
+    bwd = ll.ll_workspace_size(ll.LL_MAMBA2_BWD, ll.LL_BF16, 1, 65536, 16, 128, 128, 64, 1)
+    assert bwd > fwd and bwd % 256 == 0
+    assert ll.ll_workspace_size(ll.LL_MAMBA2_BWD, ll.LL_BF16, 1, 65536, 16, 128, 128, 64, 0) == 0
+    assert ll.ll_workspace_size(ll.LL_MAMBA2_BWD, ll.LL_BF16, 1, 64, 1, 128, 128, 64, 1) > 0
+
+
 def test_gdn_argument_checks_return_before_launch():
     def g(beta=FAKE, T=128, ws=FAKE, wsb=1 << 40, dk=128, dv=128):
         return lib.ll_gdn_fwd(FAKE, FAKE, FAKE, FAKE, beta, FAKE, FAKE, 1, T, 2, dk, dv, 64, 1, ws, wsb, None)

@@ -1,0 +1,109 @@
+"""GPU parity of ll_mamba2_bwd against the float64 oracle's gradients, through the C ABI.
+
+Every gradient (dq, dk, dv, dlog_alpha, dlambda) is compared on its own, by the normalised
+max-abs error max|g_gpu - g_ref| / max|g_ref| that the forward uses: at most 1e-4 for fp32
+storage and 2e-2 for bf16 storage (inputs and dO rounded to bf16; the oracle receives the same
+rounded values in float64).  Cases span several tiles, ragged tails, every tile level up to the
+reduced ones (groups of >= 16 tiles), and the full T = 65536 workload on sampled rows and
+columns (dlog_alpha there through its differences, which the oracle computes per position)."""
+
+import numpy as np
+import pytest
+
+from oracle import mamba2_grad
+from synthetic import WORKLOADS, generate, upstream_grad
+from tests.gpu_util import rel_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+NAMES = ("dq", "dk", "dv", "dlog_alpha", "dlambda")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2506_04761_amd  # noqa: F401  (fails loudly if the library is missing)
+
+
+def run_bwd(x, do, dtype, C):
+    import torch
+    import paper_2506_04761_amd as ll
+    args = [to_dev(x[n], dtype) for n in ("q", "k", "v")]
+    args += [to_dev(x["log_alpha"]), to_dev(x["lam"]), to_dev(do, dtype)]
+    grads = ll.ll_mamba2_bwd(*args, C)
+    torch.cuda.synchronize()
+    return [g.float().cpu().numpy().astype(np.float64) for g in grads]
+
+
+def _check_all(w, x, do, label):
+    got = run_bwd(x, do, w.dtype, w.C)
+    ref = mamba2_grad.quadratic_grad(x["q"], x["k"], x["v"], x["log_alpha"], x["lam"], do)
+    errs = {n: rel_err(g, r) for n, g, r in zip(NAMES, got, ref)}
+    print(label, " ".join(f"{n} {e:.2e}" for n, e in errs.items()), flush=True)
+    for n, e in errs.items():
+        assert e <= TOL[w.dtype], (label, n, e)
+
+
+@pytest.mark.parametrize("name", ["ll_mamba2_f32_T64", "ll_mamba2_bf16_T2048"])
+def test_bwd_parity_small_workloads(name):
+    w = WORKLOADS[name]
+    _check_all(w, generate(w), upstream_grad(w), name)
+
+
+@pytest.mark.parametrize("T", [16, 64 * 19, 64 * 37])
+def test_bwd_parity_f32_chunk16(T):
+    # fp32, C = 16 (tiles of 64 rows): 1216 tokens = 19 tiles (tile levels 1..5, a partial
+    # last region); 2368 tokens = 37 tiles
+    w = WORKLOADS["ll_mamba2_f32_T64"].with_(B=1, H=2, T=T, seed=60 + T % 97)
+    _check_all(w, generate(w), upstream_grad(w), f"f32 C=16 T={T}")
+
+
+def test_bwd_parity_f32_chunk64():
+    w = WORKLOADS["ll_mamba2_f32_T64"].with_(B=1, H=2, T=64 * 23, dk=64, dv=64, C=64, seed=71)
+    _check_all(w, generate(w), upstream_grad(w), "f32 C=64 T=1472")
+
+
+@pytest.mark.parametrize("chunks", [1, 2, 3, 7, 33, 66])
+@pytest.mark.parametrize("dk,dv", [(128, 64), (128, 128), (64, 64)])
+def test_bwd_parity_bf16_ragged(chunks, dk, dv):
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=1, H=2, T=64 * chunks, dk=dk, dv=dv, seed=80 + chunks)
+    _check_all(w, generate(w), upstream_grad(w), f"bf16 {dk}x{dv} chunks={chunks}")
+
+
+@pytest.mark.parametrize("dist", ["slow", "nodecay", "shifted"])
+def test_bwd_parity_gate_regimes(dist):
+    # slow decay and alpha = 1 keep every level's terms large; "shifted" is the second reading
+    # of the input distribution (v ~ N(0, 1), log alpha = -softplus(x + 2))
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=2, H=1, T=64 * 40, dist=dist, seed=90)
+    _check_all(w, generate(w), upstream_grad(w), f"bf16 {dist}")
+
+
+def test_bwd_full_size_sampled():
+    """The T = 65536, 16-head workload in the launch configuration the benchmark times: sampled
+    query rows (dq, dlambda), key columns (dk, dv) and positions of dlog_alpha's differences
+    (dlog_alpha_t - dlog_alpha_{t+1} = q_t . dq_t - k_t . dk_t), for two heads."""
+    w = WORKLOADS["ll_mamba2_bwd_bf16_T65536"]
+    x = generate(w)
+    do = upstream_grad(w)
+    dq, dk, dv, dla, dlam = run_bwd(x, do, w.dtype, w.C)
+    pos = np.array([0, 1, 127, 128, 4095, 4096, 32767, 40000, 65535])
+    heads = [0, 11]
+    xs = {n: x[n][:, :, heads] for n in x}
+    do_s = do[:, :, heads]
+    rq, rl = mamba2_grad.grad_rows(xs["q"], xs["k"], xs["v"], xs["log_alpha"], xs["lam"], do_s, pos)
+    ck, cv = mamba2_grad.grad_cols(xs["q"], xs["k"], xs["v"], xs["log_alpha"], xs["lam"], do_s, pos)
+    dc = mamba2_grad.dcum_at(xs["q"], xs["k"], xs["v"], xs["log_alpha"], xs["lam"], do_s, pos)
+    nxt = np.concatenate([dla[:, 1:], np.zeros_like(dla[:, :1])], axis=1)
+    diffs = (dla - nxt)[:, pos][:, :, heads]
+    errs = {"dq": rel_err(dq[:, pos][:, :, heads], rq), "dlambda": rel_err(dlam[:, pos][:, :, heads], rl),
+            "dk": rel_err(dk[:, pos][:, :, heads], ck), "dv": rel_err(dv[:, pos][:, :, heads], cv),
+            "dlog_alpha differences": rel_err(diffs, dc)}
+    print("T=65536 sampled", " ".join(f"{n} {e:.2e}" for n, e in errs.items()), flush=True)
+    for n, e in errs.items():
+        assert e <= TOL["bf16"], (n, e)
+    # the first gate only shifts every cumulative sum: its gradient vanishes
+    assert np.max(np.abs(dla[:, 0])) <= TOL["bf16"] * np.max(np.abs(dla))
+    assert np.all(np.isfinite(dq)) and np.all(np.isfinite(dk)) and np.all(np.isfinite(dv))
