@@ -218,6 +218,8 @@ def main():
         return main_gdn(args, w, torch, ll)
     if w.variant == "decode":
         return main_decode(args, w, torch, ll)
+    if w.variant == "mamba2_bwd":
+        return main_bwd(args, w, torch, ll)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
@@ -325,6 +327,173 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+# ------------------------------------------------------------------------- backward pass
+
+BWD_STAGES = ["fwd_summaries", "rev_summaries", "dq", "dkv"]
+
+
+def flops_bwd(w):
+    """Algorithmic FLOPs of the log-linear Mamba-2 gradient, chunk convention as the forward:
+    per chunk the dense C x C products S = Q K^T, G = dO V^T, dq = (W G) K, dk = (W G)^T Q,
+    dv = (W S)^T dO; the chunk states of the forward summaries; per (chunk, set bit) the query
+    side's two products (dq, and U q for dlambda) and the key-side summary of that level; per
+    (chunk, clear bit) the key side's two products (dk, dv)."""
+    J = math.log2(w.T // w.C) if w.T > w.C else 0.0
+    return w.B * w.H * w.T * (2 * w.C * (3 * w.dk + 2 * w.dv) + 2 * w.dk * w.dv + 5 * w.dk * w.dv * J)
+
+
+def bwd_stage_figures(w):
+    """Work of one launch of each backward stage: {stage: (flops, bytes)}.  dq and dkv each
+    recompute S and G for their tile (counted in both).  Bytes: what each stage must read and
+    write once (inputs, dO, the summaries it produces, the gradients it writes)."""
+    es = 2 if w.dtype == "bf16" else 4
+    BH, BHT = w.B * w.H, w.B * w.H * w.T
+    SZ = w.dk * w.dv
+    J = math.log2(w.T // w.C) if w.T > w.C else 0.0
+    L = w.levels
+    R = max(2 * w.C, 64)
+    N = -(-w.T // R)
+    Jt = (N - 1).bit_length() if N > 1 else 0
+    n_rev = sum(((N - 1) >> (j - 1)) // 2 + 1 if ((N - 1) >> (j - 1)) >= 1 else 0 for j in range(1, Jt + 1))
+    fwd = stage_figures(w)
+    f_sum = fwd["block_state"][0]
+    b_sum = fwd["block_state"][1] + fwd["scan"][1]
+    f_rev = BHT * w.dk * w.dv * J
+    b_rev = BHT * ((w.dk + w.dv) * es + 4 * Jt) + BH * n_rev * SZ * es
+    f_dq = BHT * (2 * w.C * (2 * w.dk + w.dv) + 2 * w.dk * w.dv * J)
+    f_dkv = BHT * (2 * w.C * (2 * w.dk + 2 * w.dv) + 2 * w.dk * w.dv * J)
+    b_in = BHT * ((2 * w.dk + 2 * w.dv) * es + 4 + 4 * L)
+    b_dq = b_in + BHT * (w.dk * es + 4 * L + 4)
+    b_dkv = b_in + BHT * ((w.dk + w.dv) * es + 4 + 4)
+    return {"fwd_summaries": (f_sum, b_sum), "rev_summaries": (f_rev, b_rev), "dq": (f_dq, b_dq),
+            "dkv": (f_dkv, b_dkv)}
+
+
+def cpu_baseline_bwd(w, budget_s):
+    """The float64 oracle's gradients (quadratic form) on a prefix of the workload, all heads,
+    growing the prefix until one run takes at least `budget_s` / 2; tokens/s of that prefix."""
+    from oracle import mamba2_grad
+    from synthetic import upstream_grad
+    x = generate(w)
+    do = upstream_grad(w)
+    T = 64
+    while True:
+        L = 1 if T == 1 else (T - 1).bit_length() + 1
+        args = [np.ascontiguousarray(x[n][:, :T]) for n in ("q", "k", "v", "log_alpha")]
+        args += [np.ascontiguousarray(x["lam"][:, :T, :, :L]), np.ascontiguousarray(do[:, :T])]
+        t0, c0 = time.perf_counter(), time.process_time()
+        mamba2_grad.quadratic_grad(*args)
+        wall, cpu = time.perf_counter() - t0, time.process_time() - c0
+        # stop at half the budget, or before a doubling (about 4x the work) would overshoot it
+        if wall >= budget_s / 2 or 4 * wall > 1.5 * budget_s or 2 * T > w.T:
+            break
+        T *= 2
+    return {
+        "value": w.B * T / wall, "unit": "tokens/s", "cores": max(1, round(cpu / wall)),
+        "host_cores_available": len(os.sched_getaffinity(0)), "kind": "oracle",
+        "sample": f"float64 gradients of the quadratic form (chain rule, every input), first {T} tokens "
+                  f"of all {w.H} heads, B={w.B}; {wall:.2f} s wall, {cpu:.2f} s CPU (the quadratic form's "
+                  f"cost grows with T, so longer prefixes run slower per token)",
+    }
+
+
+def main_bwd(args, w, torch, ll):
+    """Log-linear Mamba-2 backward: one step = one ll_mamba2_bwd call (forward summaries,
+    key-side summaries, dq and dlambda, dk dv and dlog_alpha), inputs and dO resident."""
+    from synthetic import upstream_grad
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    x = generate(w)
+    d = {n: torch.from_numpy(x[n]).to(dev).to(dt).contiguous() for n in ("q", "k", "v")}
+    la = torch.from_numpy(x["log_alpha"]).to(dev)
+    lam = torch.from_numpy(x["lam"]).to(dev)
+    del x
+    do = torch.from_numpy(upstream_grad(w)).to(dev).to(dt).contiguous()
+    code = ll.LL_BF16 if w.dtype == "bf16" else ll.LL_F32
+    ws = torch.empty(ll.ll_workspace_size(ll.LL_MAMBA2_BWD, code, w.B, w.T, w.H, w.dk, w.dv, w.C, 1),
+                     dtype=torch.uint8, device=dev)
+    fws = torch.empty(ll.ll_workspace_size(ll.LL_MAMBA2, code, w.B, w.T, w.H, w.dk, w.dv, w.C, 1),
+                      dtype=torch.uint8, device=dev)
+    out = torch.empty((w.B, w.T, w.H, w.dv), dtype=dt, device=dev)
+    grads = (torch.empty_like(d["q"]), torch.empty_like(d["k"]), torch.empty_like(d["v"]),
+             torch.empty_like(la), torch.empty_like(lam))
+    stream = torch.cuda.current_stream()
+    K, W = args.steps, args.warmup
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
+
+    def bwd(e=None):
+        if e is None:
+            ll.ll_mamba2_bwd(d["q"], d["k"], d["v"], la, lam, do, w.C, grads=grads, workspace=ws, stream=stream)
+        else:
+            ll.ll_mamba2_bwd_staged(d["q"], d["k"], d["v"], la, lam, do, w.C, e, grads=grads, workspace=ws,
+                                    stream=stream)
+
+    def fwd():
+        ll.ll_mamba2_fwd(d["q"], d["k"], d["v"], la, lam, w.C, out=out, workspace=fws, stream=stream)
+
+    print(f"[bench] {w.name}: warmup {W}, steps {K}", file=sys.stderr, flush=True)
+    for i in range(W):
+        bwd(evs[i % K])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(K):
+        bwd(evs[i])
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    stage_ms = np.array([[e[s].elapsed_time(e[s + 1]) for s in range(4)] for e in evs]).mean(axis=0)
+    # forward + backward, as one training step of the operator would run them
+    for _ in range(W):
+        fwd()
+        bwd()
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(K):
+        fwd()
+        bwd()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_fb = e0.elapsed_time(e1) / K
+    print(f"[bench] backward {ms:.3f} ms/step (stages {', '.join(f'{x:.3f}' for x in stage_ms)}), "
+          f"forward + backward {ms_fb:.3f} ms", file=sys.stderr, flush=True)
+
+    figs = bwd_stage_figures(w)
+    dom = int(np.argmax(stage_ms))
+    roof = roofline(w, *figs[BWD_STAGES[dom]], stage_ms[dom])
+    F = flops_bwd(w)
+    Ff = flops_loglinear(w)
+    tflops = F / (ms * 1e-3) / 1e12
+    es = 2 if w.dtype == "bf16" else 4
+    # read q, k, v, dO, log alpha, lambda; write dq, dk, dv, dlog_alpha, dlambda
+    nbytes = w.B * w.T * w.H * ((4 * w.dk + 3 * w.dv) * es + 8 + 8 * w.levels)
+    res = {
+        "metric": "bwd tokens/sec + TFLOP/s (% bf16 MFMA peak), log-linear Mamba-2, T=64K",
+        "value": w.B * w.T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "variant": "log-linear Mamba-2 backward", "B": w.B, "H": w.H, "T": w.T,
+                   "d_k": w.dk, "d_v": w.dv, "C": w.C, "levels": w.levels,
+                   "inputs": "bf16 q/k/v/dO, fp32 log-gates and lambda, seeded synthetic (numpy PCG64)"},
+        "tflops": tflops,
+        "mfma_peak_frac": tflops / (PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS),
+        "flop_convention": "B*H*T*[2C(3dk+2dv) + 2dk*dv + 5dk*dv*log2(T/C)]",
+        "hbm_GBps_algorithmic": nbytes / (ms * 1e-3) / 1e9,
+        "forward_plus_backward": {"ms": ms_fb, "tokens_per_s": w.B * w.T / (ms_fb * 1e-3),
+                                  "tflops": (F + Ff) / (ms_fb * 1e-3) / 1e12},
+        "stages_ms": dict(zip(BWD_STAGES, [float(x) for x in stage_ms])),
+        "roofline": {"kernel": BWD_STAGES[dom], **roof, "traffic": None,
+                     "traffic_note": "counter traffic of the backward kernels in the rocprofv3 summaries"},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline_bwd(w, args.cpu_budget)
     print(json.dumps(res), flush=True)
 
 
