@@ -681,25 +681,6 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
 constexpr int kFastRows = 128;
 constexpr int kFastThreads = 256;
 
-// Copies lambda of the tile's rows into dst[r * kMaxLevels + l] (l < L; the other slots receive
-// copies of valid entries and are never read) by direct global->LDS loads of one float per lane.
-template <int ROWS, int NT>
-__device__ inline void lds_copy_lambda(float* dst, const float* __restrict__ lam, int64_t row0, int H, int h, int L,
-                                       int nrow) {
-  constexpr int TOTAL = ROWS * kMaxLevels;
-  static_assert(TOTAL % NT == 0, "whole passes");
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-#pragma unroll
-  for (int it = 0; it < TOTAL / NT; ++it) {
-    const int pos = it * NT + wave * 64 + lane;
-    const int r = pos / kMaxLevels, l = pos % kMaxLevels;
-    const int rs = r < nrow ? r : nrow - 1, ls = l < L ? l : L - 1;
-    __builtin_amdgcn_global_load_lds(lam + ((row0 + rs) * H + h) * L + ls,
-                                     (__attribute__((address_space(3))) void*)(dst + it * NT + wave * 64), 4, 0, 0);
-  }
-}
-
 // Intra-tile part of the 128-row fast kernels: causal 128 x 128 masked contraction of the
 // tile's Q (registers: rows iA = 16 wave + r16 and iB = 16 (7 - wave) + r16 of this lane) with
 // its K and V (swizzled LDS tiles), 32 keys per step, no barrier.  The body is instantiated per

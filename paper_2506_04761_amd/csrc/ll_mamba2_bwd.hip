@@ -728,6 +728,561 @@ __global__ __launch_bounds__(4 * tile_rows(C)) void k_bwd_dkv(
 }
 
 // ---------------------------------------------------------------------------------------------
+// bf16 tiles of 128 rows (C = 64).  The tile's two operand tiles and the level summaries live in
+// swizzled LDS tiles filled by direct global->LDS loads; 4 waves, wave w owning the 16-row groups
+// w and 7 - w (equal causal work, and every LDS fragment feeds two MFMAs).  The inter-tile levels
+// run first, their summaries alternating between the two tile regions, the next one copied in
+// while the current one is used; the operand tiles are copied in behind the last level, and the
+// intra-tile part runs last.
+// ---------------------------------------------------------------------------------------------
+constexpr int kBwdFastThreads = 256;
+constexpr int kBwdFastRows = 128;
+
+namespace {
+
+// dO-style operand of one row in the result-row k order: slots 0-3 = x[32 st + 4 g + 0..3],
+// slots 4-7 = x[32 st + 16 + 4 g + 0..3] (pairs with frag_down_rows_swz reads of k rows 32 st ..).
+__device__ inline bf16x8 load_rl_pair(const __bf16* row, int st) {
+  const int g = (threadIdx.x & 63) >> 4;
+  const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row + 32 * st + 4 * g);
+  const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + 32 * st + 16 + 4 * g);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+}  // namespace
+
+template <int DK, int DV>
+__global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dq_fast(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
+    const __bf16* __restrict__ dout, const float* __restrict__ lam, Nodes<__bf16> nodes, __bf16* __restrict__ dq,
+    float* __restrict__ dlam, float* __restrict__ qdq, int64_t Tlen, int H, int L, int J) {
+  using M = Mfma<__bf16>;
+  typedef __bf16 bf;
+  typedef typename M::frag frag;
+  constexpr int R = kBwdFastRows, LOG2R = 7, NT = kBwdFastThreads;
+  constexpr int KSK = DK / 32, KSV = DV / 32, MTK = DK / 16, MTV = DV / 16;
+  constexpr int SZ = DK * DV;
+  static_assert(DK <= R && DV <= R, "a summary fits in either tile region");
+  __shared__ bf k_s[R * DK];
+  __shared__ bf v_s[R * DV];
+  __shared__ float lam_s[R * kMaxLevels];
+  __shared__ float cl_s[R];
+
+  const int64_t N = (Tlen + R - 1) / R;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // logical order (b, h, u)
+  const int u = (int)(work % N);
+  const int64_t bh = work / N;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t row0 = (int64_t)b * Tlen + (int64_t)u * R;
+  const int nrow = (int)((Tlen - (int64_t)u * R) < R ? (Tlen - (int64_t)u * R) : R);
+  const int gA = wave, gB = 7 - wave;            // this wave's 16-row groups
+  const int iA = 16 * gA + r16, iB = 16 * gB + r16;
+  const bool liveB = 16 * gB < nrow;             // nrow is a multiple of C = 64; group A is always live
+
+  // ---- loads: gates and lambda into LDS, this lane's rows of q and dO into registers, the first
+  //      level's summary (or, without levels, the K and V tiles) into the K region
+  lds_gather4<NT>(cl_s, R, [&](int x) { return nodes.cl + (bh * N + u) * R + x; });
+  lds_copy_lambda<R, NT>(lam_s, lam, row0, H, h, L, nrow);
+  frag qA[KSK], qB[KSK], dA[KSV], dB[KSV], pA[KSV], pB[KSV];
+  {
+    const int rB = iB < nrow ? iB : nrow - 1;
+    const bf* qa = q + ((row0 + iA) * H + h) * DK;
+    const bf* qb = q + ((row0 + rB) * H + h) * DK;
+    const bf* da = dout + ((row0 + iA) * H + h) * DV;
+    const bf* db = dout + ((row0 + rB) * H + h) * DV;
+#pragma unroll
+    for (int ks = 0; ks < KSK; ++ks) {
+      qA[ks] = M::load(qa + ks * 32 + g * 8);
+      qB[ks] = M::load(qb + ks * 32 + g * 8);
+    }
+#pragma unroll
+    for (int ks = 0; ks < KSV; ++ks) {
+      dA[ks] = M::load(da + ks * 32 + g * 8);
+      dB[ks] = M::load(db + ks * 32 + g * 8);
+      pA[ks] = load_rl_pair(da, ks);
+      pB[ks] = load_rl_pair(db, ks);
+    }
+  }
+  auto copy_tile = [&](bf* region) {
+    if (region == k_s) lds_copy_rows<DK, R, NT>(k_s, k + (row0 * H + h) * DK, (int64_t)H * DK, nrow);
+    else lds_copy_rows<DV, R, NT>(v_s, v + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
+  };
+  auto next_level = [&](int j) {
+    for (++j; j <= J; ++j)
+      if (reads_level(u, j)) return j;
+    return 0;
+  };
+  const float gapv = level_gaps(nodes, bh, N, u, J);
+  int j = next_level(0);
+  if (j) lds_copy_rows<DK, DV, NT>(k_s, nodes.at(bh, N, j, source_first(u, j), SZ), DK, DV);
+  else {
+    copy_tile(k_s);
+    copy_tile(v_s);
+  }
+  if (!liveB) {
+#pragma unroll
+    for (int ks = 0; ks < KSK; ++ks) qB[ks] = frag{};
+#pragma unroll
+    for (int ks = 0; ks < KSV; ++ks) dB[ks] = pB[ks] = frag{};
+  }
+  const float* lrowA = &lam_s[iA * kMaxLevels];
+  const float* lrowB = &lam_s[(liveB ? iB : 0) * kMaxLevels];
+  const int64_t growA = (row0 + iA) * H + h, growB = (row0 + (liveB ? iB : 0)) * H + h;
+
+  f32x4 accA[MTK], accB[MTK];
+#pragma unroll
+  for (int mt = 0; mt < MTK; ++mt) accA[mt] = accB[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // One inter-tile level from `cur`; the next level's summary (or, after the last level, the
+  // operand tile of that region) goes to `nxt`.
+  auto level_step = [&](const bf* cur, bf* nxt) {
+    wait_vmem();
+    __syncthreads();  // `cur` complete and visible; every wave is done with `nxt`
+    const int jn = next_level(j);
+    if (jn) lds_copy_rows<DK, DV, NT>(nxt, nodes.at(bh, N, jn, source_first(u, jn), SZ), DK, DV);
+    else copy_tile(nxt);
+    const float gap = gap_of(gapv, j);
+    const float wA = fast_exp2(cl_s[iA] + gap), wB = liveB ? fast_exp2(cl_s[iB] + gap) : 0.f;
+    // y^T = U Q^T, dlambda = dO . y
+    float yA = 0.f, yB = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MTV; ++mt) {
+      f32x4 tA = {0.f, 0.f, 0.f, 0.f}, tB = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KSK; ++ks) {
+        const frag uf = frag_along_row_swz<DK>(cur, 16 * mt, 4 * ks);
+        tA = M::mma(uf, qA[ks], tA);
+        tB = M::mma(uf, qB[ks], tB);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        yA += tA[r] * static_cast<float>(pA[mt >> 1][(mt & 1) * 4 + r]);
+        yB += tB[r] * static_cast<float>(pB[mt >> 1][(mt & 1) * 4 + r]);
+      }
+    }
+    yA = sum_over_groups(yA);
+    yB = sum_over_groups(yB);
+    if (g == 0) {
+      dlam[growA * L + LOG2R + j] = wA * yA;
+      if (liveB) dlam[growB * L + LOG2R + j] = wB * yB;
+    }
+    // dq^T += lambda w U^T dO^T
+    const float sA = wA * lrowA[LOG2R + j], sB = liveB ? wB * lrowB[LOG2R + j] : 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MTK; ++mt) {
+      f32x4 tA = {0.f, 0.f, 0.f, 0.f}, tB = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < KSV; ++st) {
+        const frag uf = frag_down_rows_swz<DK>(cur, 32 * st, 16 * mt);
+        tA = M::mma(uf, pA[st], tA);
+        tB = M::mma(uf, pB[st], tB);
+      }
+      accA[mt] += sA * tA;
+      accB[mt] += sB * tB;
+    }
+    j = jn;
+  };
+  if (j) {
+    bf* cur = k_s;
+    bf* nxt = v_s;
+    while (true) {
+      level_step(cur, nxt);
+      if (!j) break;
+      bf* t = cur;
+      cur = nxt;
+      nxt = t;
+    }
+    __syncthreads();  // every wave is done with the last summary
+    copy_tile(cur);
+  }
+  wait_vmem();
+  __syncthreads();  // K and V tiles (and gates, lambda) visible
+
+  // ---- intra-tile: key tiles 2 st, 2 st + 1 per step
+  const float cliA = cl_s[iA], cliB = cl_s[iB];
+  float dlA[LOG2R + 1], dlB[LOG2R + 1];
+#pragma unroll
+  for (int l = 0; l <= LOG2R; ++l) dlA[l] = dlB[l] = 0.f;
+  auto key_tile = [&](int KT, int gX, int iX, float cliX, const float* lrowX, const frag* kf, const frag* vf,
+                      const frag* qX, const frag* dX, f32x4& wg, float (&dl)[LOG2R + 1]) {
+    f32x4 s = {0.f, 0.f, 0.f, 0.f}, gg = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KSK; ++ks) s = M::mma(kf[ks], qX[ks], s);
+#pragma unroll
+    for (int ks = 0; ks < KSV; ++ks) gg = M::mma(vf[ks], dX[ks], gg);
+    if (KT < gX) {
+      const int lv = level_local(16 * gX, 16 * KT);
+      const float lw = lrowX[lv];
+      float pg = 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float e = fast_exp2(cliX - cl_s[16 * KT + 4 * g + r]);
+        pg += e * s[r] * gg[r];
+        wg[r] = lw * e * gg[r];
+      }
+      add_level(dl, lv, pg);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int jj = 16 * KT + 4 * g + r;
+        const bool ok = jj <= iX;
+        const int lv = level_local(iX, jj);
+        const float e = ok ? fast_exp2(cliX - cl_s[jj]) : 0.f;
+        add_level(dl, ok ? lv : 0, e * s[r] * gg[r]);
+        wg[r] = ok ? lrowX[lv] * e * gg[r] : 0.f;
+      }
+    }
+  };
+#pragma unroll
+  for (int st = 0; st < 4; ++st) {
+    const bool needA = 2 * st <= gA, needB = 2 * st <= gB && liveB;
+    if (!needA && !needB) break;
+    f32x4 wgA[2], wgB[2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int KT = 2 * st + hh;
+      wgA[hh] = wgB[hh] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const bool useA = KT <= gA, useB = KT <= gB && liveB;
+      if (!useA && !useB) continue;
+      frag kf[KSK], vf[KSV];
+#pragma unroll
+      for (int ks = 0; ks < KSK; ++ks) kf[ks] = frag_along_row_swz<DK>(k_s, 16 * KT, 4 * ks);
+#pragma unroll
+      for (int ks = 0; ks < KSV; ++ks) vf[ks] = frag_along_row_swz<DV>(v_s, 16 * KT, 4 * ks);
+      if (useA) key_tile(KT, gA, iA, cliA, lrowA, kf, vf, qA, dA, wgA[hh], dlA);
+      if (useB) key_tile(KT, gB, iB, cliB, lrowB, kf, vf, qB, dB, wgB[hh], dlB);
+    }
+    const bf16x8 bA = pack_rl(wgA[0], wgA[1]), bB = pack_rl(wgB[0], wgB[1]);
+#pragma unroll
+    for (int mt = 0; mt < MTK; ++mt) {
+      const frag kd = frag_down_rows_swz<DK>(k_s, 32 * st, 16 * mt);
+      if (needA) accA[mt] = M::mma(kd, bA, accA[mt]);
+      if (needB) accB[mt] = M::mma(kd, bB, accB[mt]);
+    }
+  }
+
+  // ---- dlambda of the intra-tile levels, zeros for the inter-tile levels this tile does not read
+#pragma unroll
+  for (int l = 0; l <= LOG2R; ++l) {
+    const float xA = sum_over_groups(dlA[l]), xB = sum_over_groups(dlB[l]);
+    if (g == 0 && l < L) {
+      dlam[growA * L + l] = xA;
+      if (liveB) dlam[growB * L + l] = xB;
+    }
+  }
+  for (int jj = 1; LOG2R + jj < L; ++jj)
+    if (jj > J || !reads_level(u, jj)) {
+      if (g == 0) {
+        dlam[growA * L + LOG2R + jj] = 0.f;
+        if (liveB) dlam[growB * L + LOG2R + jj] = 0.f;
+      }
+    }
+
+  // ---- q . dq (fp32 accumulators), then dq through LDS as whole rows
+  float qdA = 0.f, qdB = 0.f;
+  {
+    const bf* qa = q + growA * DK + 4 * g;
+    const bf* qb = q + growB * DK + 4 * g;
+#pragma unroll
+    for (int mt = 0; mt < MTK; ++mt) {
+      const bf16x4 xa = *reinterpret_cast<const bf16x4*>(qa + 16 * mt);
+      const bf16x4 xb = *reinterpret_cast<const bf16x4*>(qb + 16 * mt);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        qdA += accA[mt][r] * static_cast<float>(xa[r]);
+        qdB += accB[mt][r] * static_cast<float>(xb[r]);
+      }
+    }
+  }
+  qdA = sum_over_groups(qdA);
+  qdB = sum_over_groups(qdB);
+  if (g == 0) {
+    qdq[growA] = qdA;
+    if (liveB) qdq[growB] = qdB;
+  }
+  __syncthreads();  // every wave is done with K
+  auto stage_rows = [&](const f32x4* acc, int i) {
+#pragma unroll
+    for (int mt = 0; mt < MTK; ++mt) {
+      bf16x4 val;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) val[r] = static_cast<bf>(acc[mt][r]);
+      *reinterpret_cast<bf16x4*>(k_s + swz<DK>(i, 2 * mt + (g >> 1)) + 4 * (g & 1)) = val;
+    }
+  };
+  stage_rows(accA, iA);
+  stage_rows(accB, iB);
+  __syncthreads();
+  constexpr int OCH = DK / 8;
+#pragma unroll
+  for (int it = 0; it < R * OCH / NT; ++it) {
+    const int idx = it * NT + tid, r = idx / OCH, c = idx % OCH;
+    if (r < nrow)
+      *reinterpret_cast<bf16x8*>(dq + ((row0 + r) * H + h) * DK + 8 * c) =
+          *reinterpret_cast<const bf16x8*>(k_s + swz<DK>(r, c));
+  }
+}
+
+template <int DK, int DV>
+__global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dkv_fast(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
+    const __bf16* __restrict__ dout, const float* __restrict__ lam, Nodes<__bf16> nodes, RevNodes<__bf16> rev,
+    const float* __restrict__ qdq, __bf16* __restrict__ dk, __bf16* __restrict__ dv, float* __restrict__ dla,
+    float* __restrict__ tsum, int64_t Tlen, int H, int L, int J) {
+  using M = Mfma<__bf16>;
+  typedef __bf16 bf;
+  typedef typename M::frag frag;
+  constexpr int R = kBwdFastRows, NT = kBwdFastThreads;
+  constexpr int KSK = DK / 32, KSV = DV / 32, MTK = DK / 16, MTV = DV / 16;
+  constexpr int SZ = DK * DV;
+  static_assert(DK <= R && DV <= R, "a summary fits in either tile region");
+  __shared__ bf q_s[R * DK];
+  __shared__ bf o_s[R * DV];
+  __shared__ float lam_s[R * kMaxLevels];
+  __shared__ float cl_s[R];
+  __shared__ float dc_s[R];
+  __shared__ float wsum_s[2];
+
+  const int64_t N = (Tlen + R - 1) / R;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // logical order (b, h, u)
+  const int u = (int)(work % N);
+  const int64_t bh = work / N;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t row0 = (int64_t)b * Tlen + (int64_t)u * R;
+  const int nrow = (int)((Tlen - (int64_t)u * R) < R ? (Tlen - (int64_t)u * R) : R);
+  const int gA = wave, gB = 7 - wave;            // this wave's 16-key groups
+  const int jA = 16 * gA + r16, jB = 16 * gB + r16;
+  const bool liveB = 16 * gB < nrow;
+  const int64_t growA = (row0 + jA) * H + h, growB = (row0 + (liveB ? jB : 0)) * H + h;
+
+  lds_gather4<NT>(cl_s, R, [&](int x) { return nodes.cl + (bh * N + u) * R + x; });
+  lds_copy_lambda<R, NT>(lam_s, lam, row0, H, h, L, nrow);
+  frag kA[KSK], kB[KSK], wA_[KSV], wB_[KSV];  // k rows (along d_k), v rows in the result-row k order
+#pragma unroll
+  for (int ks = 0; ks < KSK; ++ks) {
+    kA[ks] = M::load(k + growA * DK + ks * 32 + g * 8);
+    kB[ks] = M::load(k + growB * DK + ks * 32 + g * 8);
+  }
+#pragma unroll
+  for (int st = 0; st < KSV; ++st) {
+    wA_[st] = load_rl_pair(v + growA * DV, st);
+    wB_[st] = load_rl_pair(v + growB * DV, st);
+  }
+  auto copy_tile = [&](bf* region) {
+    if (region == q_s) lds_copy_rows<DK, R, NT>(q_s, q + (row0 * H + h) * DK, (int64_t)H * DK, nrow);
+    else lds_copy_rows<DV, R, NT>(o_s, dout + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
+  };
+  auto next_level = [&](int j) {
+    for (++j; j <= J; ++j)
+      if (key_level(u, j, N)) return j;
+    return 0;
+  };
+  float gapr;
+  {
+    const int jl = lane + 1;
+    float t = 0.f;
+    if (jl <= J && key_level(u, jl, N)) t = rev.dtot[rev.slot(bh, jl, (int64_t)u >> jl)];
+    gapr = wave_inclusive_scan(t) - t;
+  }
+  int j = next_level(0);
+  if (j) lds_copy_rows<DK, DV, NT>(q_s, rev.d + rev.slot(bh, j, (int64_t)u >> j) * SZ, DK, DV);
+  else {
+    copy_tile(q_s);
+    copy_tile(o_s);
+  }
+  if (!liveB) {
+#pragma unroll
+    for (int ks = 0; ks < KSK; ++ks) kB[ks] = frag{};
+#pragma unroll
+    for (int st = 0; st < KSV; ++st) wB_[st] = frag{};
+  }
+
+  f32x4 akA[MTK], akB[MTK], avA[MTV], avB[MTV];
+#pragma unroll
+  for (int mt = 0; mt < MTK; ++mt) akA[mt] = akB[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int mt = 0; mt < MTV; ++mt) avA[mt] = avB[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto level_step = [&](const bf* cur, bf* nxt) {
+    wait_vmem();
+    __syncthreads();
+    const int jn = next_level(j);
+    if (jn) lds_copy_rows<DK, DV, NT>(nxt, rev.d + rev.slot(bh, jn, (int64_t)u >> jn) * SZ, DK, DV);
+    else copy_tile(nxt);
+    // keys here are in a full tile (a later group exists): decay to the tile end, then the gap
+    const float tot = cl_s[R - 1], gp = gap_of(gapr, j);
+    const float wkA = fast_exp2(tot - cl_s[jA] + gp), wkB = liveB ? fast_exp2(tot - cl_s[jB] + gp) : 0.f;
+    // dk^T[n][key] += w sum_p D[p][n] v[key][p]
+#pragma unroll
+    for (int mt = 0; mt < MTK; ++mt) {
+      f32x4 tA = {0.f, 0.f, 0.f, 0.f}, tB = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < KSV; ++st) {
+        const frag df = frag_down_rows_swz<DK>(cur, 32 * st, 16 * mt);
+        tA = M::mma(df, wA_[st], tA);
+        tB = M::mma(df, wB_[st], tB);
+      }
+      akA[mt] += wkA * tA;
+      akB[mt] += wkB * tB;
+    }
+    // dv^T[p][key] += w sum_n D[p][n] k[key][n]
+#pragma unroll
+    for (int mt = 0; mt < MTV; ++mt) {
+      f32x4 tA = {0.f, 0.f, 0.f, 0.f}, tB = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KSK; ++ks) {
+        const frag df = frag_along_row_swz<DK>(cur, 16 * mt, 4 * ks);
+        tA = M::mma(df, kA[ks], tA);
+        tB = M::mma(df, kB[ks], tB);
+      }
+      avA[mt] += wkA * tA;
+      avB[mt] += wkB * tB;
+    }
+    j = jn;
+  };
+  if (j) {
+    bf* cur = q_s;
+    bf* nxt = o_s;
+    while (true) {
+      level_step(cur, nxt);
+      if (!j) break;
+      bf* t = cur;
+      cur = nxt;
+      nxt = t;
+    }
+    __syncthreads();
+    copy_tile(cur);
+  }
+  // v rows along d_v for the intra-tile G (the result-row order copies are no longer needed)
+  frag vA[KSV], vB[KSV];
+#pragma unroll
+  for (int ks = 0; ks < KSV; ++ks) {
+    vA[ks] = M::load(v + growA * DV + ks * 32 + g * 8);
+    vB[ks] = liveB ? M::load(v + growB * DV + ks * 32 + g * 8) : frag{};
+  }
+  wait_vmem();
+  __syncthreads();  // Q and dO tiles visible
+
+  // ---- intra-tile: query tiles 2 st, 2 st + 1 per step (queries at or after the keys)
+  const float clA = cl_s[jA], clB = cl_s[jB];
+  auto query_tile = [&](int QT, int gX, int jX, float clX, const frag* kX, const frag* vX, const frag* qf,
+                        const frag* of, bf16x8& bg, bf16x8& bp, int hh) {
+    f32x4 s = {0.f, 0.f, 0.f, 0.f}, gg = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KSK; ++ks) s = M::mma(qf[ks], kX[ks], s);
+#pragma unroll
+    for (int ks = 0; ks < KSV; ++ks) gg = M::mma(of[ks], vX[ks], gg);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * QT + 4 * g + r;
+      const bool ok = (QT > gX || i >= jX) && i < nrow;
+      const int lv = QT > gX ? level_local(16 * QT, 16 * gX) : level_local(i, jX);
+      const float lw = ok ? lam_s[i * kMaxLevels + lv] * fast_exp2(cl_s[i] - clX) : 0.f;
+      bg[4 * hh + r] = static_cast<bf>(lw * gg[r]);
+      bp[4 * hh + r] = static_cast<bf>(lw * s[r]);
+    }
+  };
+#pragma unroll
+  for (int st = 0; st < 4; ++st) {
+    const bool needA = 2 * st + 1 >= gA, needB = 2 * st + 1 >= gB && liveB;
+    if (!needA && !needB) continue;
+    bf16x8 bgA = {}, bpA = {}, bgB = {}, bpB = {};
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int QT = 2 * st + hh;
+      const bool useA = QT >= gA, useB = QT >= gB && liveB;
+      if (!useA && !useB) continue;
+      frag qf[KSK], of[KSV];
+#pragma unroll
+      for (int ks = 0; ks < KSK; ++ks) qf[ks] = frag_along_row_swz<DK>(q_s, 16 * QT, 4 * ks);
+#pragma unroll
+      for (int ks = 0; ks < KSV; ++ks) of[ks] = frag_along_row_swz<DV>(o_s, 16 * QT, 4 * ks);
+      if (useA) query_tile(QT, gA, jA, clA, kA, vA, qf, of, bgA, bpA, hh);
+      if (useB) query_tile(QT, gB, jB, clB, kB, vB, qf, of, bgB, bpB, hh);
+    }
+#pragma unroll
+    for (int mt = 0; mt < MTK; ++mt) {
+      const frag qd = frag_down_rows_swz<DK>(q_s, 32 * st, 16 * mt);
+      if (needA) akA[mt] = M::mma(qd, bgA, akA[mt]);
+      if (needB) akB[mt] = M::mma(qd, bgB, akB[mt]);
+    }
+#pragma unroll
+    for (int mt = 0; mt < MTV; ++mt) {
+      const frag od = frag_down_rows_swz<DV>(o_s, 32 * st, 16 * mt);
+      if (needA) avA[mt] = M::mma(od, bpA, avA[mt]);
+      if (needB) avB[mt] = M::mma(od, bpB, avB[mt]);
+    }
+  }
+
+  // ---- k . dk, dcum = q . dq - k . dk
+  float kdA = 0.f, kdB = 0.f;
+  {
+    const bf* ka = k + growA * DK + 4 * g;
+    const bf* kb = k + growB * DK + 4 * g;
+#pragma unroll
+    for (int mt = 0; mt < MTK; ++mt) {
+      const bf16x4 xa = *reinterpret_cast<const bf16x4*>(ka + 16 * mt);
+      const bf16x4 xb = *reinterpret_cast<const bf16x4*>(kb + 16 * mt);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        kdA += akA[mt][r] * static_cast<float>(xa[r]);
+        kdB += akB[mt][r] * static_cast<float>(xb[r]);
+      }
+    }
+  }
+  kdA = sum_over_groups(kdA);
+  kdB = sum_over_groups(kdB);
+  if (g == 0) {
+    dc_s[jA] = qdq[growA] - kdA;
+    dc_s[jB] = liveB ? qdq[growB] - kdB : 0.f;
+  }
+  __syncthreads();  // every wave is done with Q and dO; dc visible
+  // ---- dk and dv through LDS as whole rows
+  auto stage_rows = [&](bf* dst, const f32x4* acc, int MT, int D, int i) {
+    for (int mt = 0; mt < MT; ++mt) {
+      bf16x4 val;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) val[r] = static_cast<bf>(acc[mt][r]);
+      const int c = 2 * mt + (g >> 1);
+      *reinterpret_cast<bf16x4*>(dst + i * D + ((c ^ (i & (D / 8 - 1))) << 3) + 4 * (g & 1)) = val;
+    }
+  };
+  stage_rows(q_s, akA, MTK, DK, jA);
+  stage_rows(q_s, akB, MTK, DK, jB);
+  stage_rows(o_s, avA, MTV, DV, jA);
+  stage_rows(o_s, avB, MTV, DV, jB);
+  // suffix sums of dcum within the tile: thread x < R (two waves) scans row R - 1 - x
+  const int row = R - 1 - tid;
+  float x = 0.f;
+  if (tid < R) x = wave_inclusive_scan(dc_s[row]);
+  if (tid < R && lane == 63) wsum_s[wave] = x;
+  __syncthreads();
+  if (tid < R) {
+    if (wave == 1) x += wsum_s[0];
+    if (row < nrow) dla[(row0 + row) * H + h] = x;
+    if (tid == R - 1) tsum[bh * N + u] = x;
+  }
+#pragma unroll
+  for (int it = 0; it < R * (DK / 8) / NT; ++it) {
+    const int idx = it * NT + tid, r = idx / (DK / 8), c = idx % (DK / 8);
+    if (r < nrow)
+      *reinterpret_cast<bf16x8*>(dk + ((row0 + r) * H + h) * DK + 8 * c) =
+          *reinterpret_cast<const bf16x8*>(q_s + swz<DK>(r, c));
+  }
+#pragma unroll
+  for (int it = 0; it < R * (DV / 8) / NT; ++it) {
+    const int idx = it * NT + tid, r = idx / (DV / 8), c = idx % (DV / 8);
+    if (r < nrow)
+      *reinterpret_cast<bf16x8*>(dv + ((row0 + r) * H + h) * DV + 8 * c) =
+          *reinterpret_cast<const bf16x8*>(o_s + swz<DV>(r, c));
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
 // k_bwd_dgate: grid (ceil(T / 256), B * H); adds to each row's tile-local suffix sum the totals
 // of all later tiles of its sequence.
 // ---------------------------------------------------------------------------------------------
@@ -825,13 +1380,24 @@ hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t*
   }
   if (ev) (void)hipEventRecord(ev[2], st);
   const dim3 gtile((unsigned)(w.fwd.N * BH));
-  hipLaunchKernelGGL((k_bwd_dq<T, C, DK, DV>), gtile, dim3(4 * R), 0, st, (const T*)a.q, (const T*)a.k,
-                     (const T*)a.v, (const T*)a.dout, a.log_alpha, a.lambda, nodes, (T*)a.dq, a.dlambda, qdq, a.T,
-                     (int)a.H, a.L, J);
+  constexpr bool kFast = std::is_same<T, __bf16>::value && R == kBwdFastRows;
+  if constexpr (kFast)
+    hipLaunchKernelGGL((k_bwd_dq_fast<DK, DV>), gtile, dim3(kBwdFastThreads), 0, st, (const T*)a.q, (const T*)a.k,
+                       (const T*)a.v, (const T*)a.dout, a.lambda, nodes, (T*)a.dq, a.dlambda, qdq, a.T, (int)a.H,
+                       a.L, J);
+  else
+    hipLaunchKernelGGL((k_bwd_dq<T, C, DK, DV>), gtile, dim3(4 * R), 0, st, (const T*)a.q, (const T*)a.k,
+                       (const T*)a.v, (const T*)a.dout, a.log_alpha, a.lambda, nodes, (T*)a.dq, a.dlambda, qdq, a.T,
+                       (int)a.H, a.L, J);
   if (ev) (void)hipEventRecord(ev[3], st);
-  hipLaunchKernelGGL((k_bwd_dkv<T, C, DK, DV>), gtile, dim3(4 * R), 0, st, (const T*)a.q, (const T*)a.k,
-                     (const T*)a.v, (const T*)a.dout, a.log_alpha, a.lambda, rev, (const float*)qdq, (T*)a.dk,
-                     (T*)a.dv, a.dlog_alpha, tsum, a.T, (int)a.H, a.L, J);
+  if constexpr (kFast)
+    hipLaunchKernelGGL((k_bwd_dkv_fast<DK, DV>), gtile, dim3(kBwdFastThreads), 0, st, (const T*)a.q, (const T*)a.k,
+                       (const T*)a.v, (const T*)a.dout, a.lambda, nodes, rev, (const float*)qdq, (T*)a.dk, (T*)a.dv,
+                       a.dlog_alpha, tsum, a.T, (int)a.H, a.L, J);
+  else
+    hipLaunchKernelGGL((k_bwd_dkv<T, C, DK, DV>), gtile, dim3(4 * R), 0, st, (const T*)a.q, (const T*)a.k,
+                       (const T*)a.v, (const T*)a.dout, a.log_alpha, a.lambda, rev, (const float*)qdq, (T*)a.dk,
+                       (T*)a.dv, a.dlog_alpha, tsum, a.T, (int)a.H, a.L, J);
   hipLaunchKernelGGL(k_bwd_dgate, dim3((unsigned)((a.T + 255) / 256), (unsigned)BH), dim3(256), 0, st,
                      (const float*)tsum, a.dlog_alpha, a.T, (int)a.H, R);
   if (ev) (void)hipEventRecord(ev[4], st);

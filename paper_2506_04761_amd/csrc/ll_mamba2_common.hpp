@@ -164,6 +164,25 @@ struct RowBlock {
   }
 };
 
+// Copies lambda of the tile's rows into dst[r * kMaxLevels + l] (l < L; the other slots receive
+// copies of valid entries and are never read) by direct global->LDS loads of one float per lane.
+template <int ROWS, int NT>
+__device__ inline void lds_copy_lambda(float* dst, const float* __restrict__ lam, int64_t row0, int H, int h, int L,
+                                       int nrow) {
+  constexpr int TOTAL = ROWS * kMaxLevels;
+  static_assert(TOTAL % NT == 0, "whole passes");
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+#pragma unroll
+  for (int it = 0; it < TOTAL / NT; ++it) {
+    const int pos = it * NT + wave * 64 + lane;
+    const int r = pos / kMaxLevels, l = pos % kMaxLevels;
+    const int rs = r < nrow ? r : nrow - 1, ls = l < L ? l : L - 1;
+    __builtin_amdgcn_global_load_lds(lam + ((row0 + rs) * H + h) * L + ls,
+                                     (__attribute__((address_space(3))) void*)(dst + it * NT + wave * 64), 4, 0, 0);
+  }
+}
+
 int tile_levels(int64_t T, int64_t C);
 
 // Device view of the summaries in a forward workspace laid out by mamba2_workspace.
