@@ -864,12 +864,13 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dq_fast(
     }
     yA = sum_over_groups(yA);
     yB = sum_over_groups(yB);
-    if (g == 0) {
-      dlam[growA * L + LOG2R + j] = wA * yA;
-      if (liveB) dlam[growB * L + LOG2R + j] = wB * yB;
-    }
-    // dq^T += lambda w U^T dO^T
+    // dq^T += lambda w U^T dO^T.  lambda^(7 + j) of these rows is read here for the last time: its
+    // LDS slot takes dlambda^(7 + j) (each row is read and written by its own wave only).
     const float sA = wA * lrowA[LOG2R + j], sB = liveB ? wB * lrowB[LOG2R + j] : 0.f;
+    if (g == 0) {
+      lam_s[iA * kMaxLevels + LOG2R + j] = wA * yA;
+      if (liveB) lam_s[iB * kMaxLevels + LOG2R + j] = wB * yB;
+    }
 #pragma unroll
     for (int mt = 0; mt < MTK; ++mt) {
       f32x4 tA = {0.f, 0.f, 0.f, 0.f}, tB = {0.f, 0.f, 0.f, 0.f};
@@ -963,20 +964,22 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dq_fast(
     }
   }
 
-  // ---- dlambda of the intra-tile levels, zeros for the inter-tile levels this tile does not read
+  // ---- dlambda of the intra-tile levels and zeros for the inter-tile levels this tile does not
+  //      read go to the rows' lambda slots (the wave's own rows, no longer read), then every row
+  //      leaves whole
 #pragma unroll
   for (int l = 0; l <= LOG2R; ++l) {
     const float xA = sum_over_groups(dlA[l]), xB = sum_over_groups(dlB[l]);
-    if (g == 0 && l < L) {
-      dlam[growA * L + l] = xA;
-      if (liveB) dlam[growB * L + l] = xB;
+    if (g == 0) {
+      lam_s[iA * kMaxLevels + l] = xA;
+      lam_s[iB * kMaxLevels + l] = xB;
     }
   }
   for (int jj = 1; LOG2R + jj < L; ++jj)
     if (jj > J || !reads_level(u, jj)) {
       if (g == 0) {
-        dlam[growA * L + LOG2R + jj] = 0.f;
-        if (liveB) dlam[growB * L + LOG2R + jj] = 0.f;
+        lam_s[iA * kMaxLevels + LOG2R + jj] = 0.f;
+        lam_s[iB * kMaxLevels + LOG2R + jj] = 0.f;
       }
     }
 
@@ -1015,6 +1018,10 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dq_fast(
   stage_rows(accA, iA);
   stage_rows(accB, iB);
   __syncthreads();
+  for (int idx = tid; idx < nrow * L; idx += NT) {
+    const int r = idx / L, l = idx % L;
+    dlam[((row0 + r) * H + h) * L + l] = lam_s[r * kMaxLevels + l];
+  }
   constexpr int OCH = DK / 8;
 #pragma unroll
   for (int it = 0; it < R * OCH / NT; ++it) {
@@ -1169,13 +1176,10 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dkv_fast(
 
   // ---- intra-tile: query tiles 2 st, 2 st + 1 per step (queries at or after the keys)
   const float clA = cl_s[jA], clB = cl_s[jB];
-  auto query_tile = [&](int QT, int gX, int jX, float clX, const frag* kX, const frag* vX, const frag* qf,
-                        const frag* of, bf16x8& bg, bf16x8& bp, int hh) {
-    f32x4 s = {0.f, 0.f, 0.f, 0.f}, gg = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < KSK; ++ks) s = M::mma(qf[ks], kX[ks], s);
-#pragma unroll
-    for (int ks = 0; ks < KSV; ++ks) gg = M::mma(of[ks], vX[ks], gg);
+  // weights of query tile QT for one key group from its S and G tiles (result layout: query
+  // 16 QT + 4 g + r, key jX), into slots 4 hh + r of the packed B operands
+  auto weights = [&](int QT, int gX, int jX, float clX, const f32x4& s, const f32x4& gg, bf16x8& bg, bf16x8& bp,
+                     int hh) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int i = 16 * QT + 4 * g + r;
@@ -1196,13 +1200,22 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dkv_fast(
       const int QT = 2 * st + hh;
       const bool useA = QT >= gA, useB = QT >= gB && liveB;
       if (!useA && !useB) continue;
-      frag qf[KSK], of[KSV];
+      // S = Q K^T and G = dO V^T of this query tile for both key groups, one fragment at a time
+      f32x4 sA = {0.f, 0.f, 0.f, 0.f}, sB = sA, gA_ = sA, gB_ = sA;
 #pragma unroll
-      for (int ks = 0; ks < KSK; ++ks) qf[ks] = frag_along_row_swz<DK>(q_s, 16 * QT, 4 * ks);
+      for (int ks = 0; ks < KSK; ++ks) {
+        const frag f = frag_along_row_swz<DK>(q_s, 16 * QT, 4 * ks);
+        if (useA) sA = M::mma(f, kA[ks], sA);
+        if (useB) sB = M::mma(f, kB[ks], sB);
+      }
 #pragma unroll
-      for (int ks = 0; ks < KSV; ++ks) of[ks] = frag_along_row_swz<DV>(o_s, 16 * QT, 4 * ks);
-      if (useA) query_tile(QT, gA, jA, clA, kA, vA, qf, of, bgA, bpA, hh);
-      if (useB) query_tile(QT, gB, jB, clB, kB, vB, qf, of, bgB, bpB, hh);
+      for (int ks = 0; ks < KSV; ++ks) {
+        const frag f = frag_along_row_swz<DV>(o_s, 16 * QT, 4 * ks);
+        if (useA) gA_ = M::mma(f, vA[ks], gA_);
+        if (useB) gB_ = M::mma(f, vB[ks], gB_);
+      }
+      if (useA) weights(QT, gA, jA, clA, sA, gA_, bgA, bpA, hh);
+      if (useB) weights(QT, gB, jB, clB, sB, gB_, bgB, bpB, hh);
     }
 #pragma unroll
     for (int mt = 0; mt < MTK; ++mt) {
@@ -1242,19 +1255,28 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dkv_fast(
   }
   __syncthreads();  // every wave is done with Q and dO; dc visible
   // ---- dk and dv through LDS as whole rows
-  auto stage_rows = [&](bf* dst, const f32x4* acc, int MT, int D, int i) {
-    for (int mt = 0; mt < MT; ++mt) {
+  auto stage_k = [&](const f32x4 (&acc)[MTK], int i) {
+#pragma unroll
+    for (int mt = 0; mt < MTK; ++mt) {
       bf16x4 val;
 #pragma unroll
       for (int r = 0; r < 4; ++r) val[r] = static_cast<bf>(acc[mt][r]);
-      const int c = 2 * mt + (g >> 1);
-      *reinterpret_cast<bf16x4*>(dst + i * D + ((c ^ (i & (D / 8 - 1))) << 3) + 4 * (g & 1)) = val;
+      *reinterpret_cast<bf16x4*>(q_s + swz<DK>(i, 2 * mt + (g >> 1)) + 4 * (g & 1)) = val;
     }
   };
-  stage_rows(q_s, akA, MTK, DK, jA);
-  stage_rows(q_s, akB, MTK, DK, jB);
-  stage_rows(o_s, avA, MTV, DV, jA);
-  stage_rows(o_s, avB, MTV, DV, jB);
+  auto stage_v = [&](const f32x4 (&acc)[MTV], int i) {
+#pragma unroll
+    for (int mt = 0; mt < MTV; ++mt) {
+      bf16x4 val;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) val[r] = static_cast<bf>(acc[mt][r]);
+      *reinterpret_cast<bf16x4*>(o_s + swz<DV>(i, 2 * mt + (g >> 1)) + 4 * (g & 1)) = val;
+    }
+  };
+  stage_k(akA, jA);
+  stage_k(akB, jB);
+  stage_v(avA, jA);
+  stage_v(avB, jB);
   // suffix sums of dcum within the tile: thread x < R (two waves) scans row R - 1 - x
   const int row = R - 1 - tid;
   float x = 0.f;
