@@ -132,6 +132,18 @@ ll_status ll_mamba2_bwd(const void* q, const void* k, const void* v, const float
                         int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                         void* workspace, size_t workspace_bytes, void* stream);
 
+/* ll_mamba2_bwd without recomputing the forward's level summaries: for a backward that follows
+ * ll_mamba2_fwd on the same q, k, v, log_alpha and lambda (non-NULL) run with this same workspace
+ * (ll_workspace_size(LL_MAMBA2_BWD, ...) bytes: the forward uses its leading part and leaves its
+ * summaries there), with nothing else writing the workspace in between, on the same stream or
+ * ordered after it.  Any other use gives wrong gradients without an error.  Saves the forward's
+ * first two stages (block_state and the level scan).  Arguments and checks as ll_mamba2_bwd. */
+ll_status ll_mamba2_bwd_after_fwd(const void* q, const void* k, const void* v, const float* log_alpha,
+                                  const float* lambda, const void* d_o, void* dq, void* dk, void* dv,
+                                  float* dlog_alpha, float* dlambda, int64_t B, int64_t T, int64_t H,
+                                  int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
 /* Same computation as ll_mamba2_bwd, for measurement, recording the caller's HIP events on
  * `stream`: events[i] right before stage i and events[4] after the last.  Stages: 0 the forward's
  * level summaries, 1 the key-side level summaries, 2 dq and dlambda, 3 dk, dv and dlog_alpha.

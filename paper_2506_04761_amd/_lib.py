@@ -57,6 +57,8 @@ lib.ll_gdn_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64,
 lib.ll_gdn_fwd_staged.restype = _i32
 lib.ll_mamba2_bwd.argtypes = [_vp] * 11 + [_i64] * 6 + [_i32, _vp, _sz, _vp]
 lib.ll_mamba2_bwd.restype = _i32
+lib.ll_mamba2_bwd_after_fwd.argtypes = [_vp] * 11 + [_i64] * 6 + [_i32, _vp, _sz, _vp]
+lib.ll_mamba2_bwd_after_fwd.restype = _i32
 lib.ll_mamba2_bwd_staged.argtypes = [_vp] * 11 + [_i64] * 6 + [_i32, _vp, _sz, _vp, _vp]
 lib.ll_mamba2_bwd_staged.restype = _i32
 lib.ll_debug_level_map.argtypes = [_i64, _i64, _vp, _vp]
@@ -240,7 +242,7 @@ def ll_mamba2_fwd_staged(q, k, v, log_alpha, lam, C, events, out=None, workspace
     return out
 
 
-def _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, handles):
+def _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, handles, after_fwd=False):
     torch = _torch()
     B, T, H, dk = q.shape
     dv = v.shape[-1]
@@ -269,7 +271,10 @@ def _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, handles
     _check(workspace, "workspace", torch.uint8)
     args = [_ptr(x) for x in (q, k, v, log_alpha, lam, d_o, dq, dk_, dv_, dla, dlam)]
     args += [B, T, H, dk, dv, C, code, _ptr(workspace), workspace.numel(), _stream(stream)]
-    st = lib.ll_mamba2_bwd(*args) if handles is None else lib.ll_mamba2_bwd_staged(*args, handles)
+    if after_fwd:
+        st = lib.ll_mamba2_bwd_after_fwd(*args)
+    else:
+        st = lib.ll_mamba2_bwd(*args) if handles is None else lib.ll_mamba2_bwd_staged(*args, handles)
     if st != LL_OK:
         raise LLError(st)
     return grads
@@ -281,6 +286,21 @@ def ll_mamba2_bwd(q, k, v, log_alpha, lam, d_o, C, grads=None, workspace=None, s
     written into `grads` when given.  `lam` is required.  Enqueued on `stream` (default: torch's
     current stream), not synchronised."""
     return _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, None)
+
+
+def ll_mamba2_bwd_workspace(q, v, C):
+    """A workspace for ll_mamba2_bwd shaped for q [B, T, H, d_k] and v [..., d_v] (also usable by
+    ll_mamba2_fwd, whose summaries ll_mamba2_bwd_after_fwd then reuses)."""
+    torch = _torch()
+    B, T, H, dk = q.shape
+    need = ll_workspace_size(LL_MAMBA2_BWD, _dtype_code(q), B, T, H, dk, v.shape[-1], C, True)
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+
+
+def ll_mamba2_bwd_after_fwd(q, k, v, log_alpha, lam, d_o, C, workspace, grads=None, stream=None):
+    """As ll_mamba2_bwd, reusing the level summaries that ll_mamba2_fwd left in `workspace` (a
+    ll_mamba2_bwd_workspace) for the same inputs; see include/libloglinear.h for the contract."""
+    return _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, None, after_fwd=True)
 
 
 def ll_mamba2_bwd_staged(q, k, v, log_alpha, lam, d_o, C, events, grads=None, workspace=None, stream=None):

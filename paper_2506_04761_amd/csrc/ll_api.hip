@@ -121,7 +121,7 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
 ll_status mamba2_bwd_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
                           const void* d_o, void* dq, void* dk, void* dv, float* dlog_alpha, float* dlambda, int64_t B,
                           int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype, void* workspace,
-                          size_t workspace_bytes, void* stream, void* const* events) {
+                          size_t workspace_bytes, void* stream, void* const* events, bool reuse) {
   if (!q || !k || !v || !log_alpha || !lambda || !d_o || !dq || !dk || !dv || !dlog_alpha || !dlambda)
     return LL_ERR_NULL_ARG;
   ll_status st = check_shape(B, T, H, d_k, d_v, C);
@@ -142,6 +142,7 @@ ll_status mamba2_bwd_impl(const void* q, const void* k, const void* v, const flo
   a.B = B; a.T = T; a.H = H; a.C = C;
   a.L = L;
   a.workspace = workspace;
+  a.reuse_summaries = reuse;
   hipEvent_t ev[ll::kMamba2BwdStages + 1];
   if (events)
     for (int i = 0; i <= ll::kMamba2BwdStages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);
@@ -210,7 +211,15 @@ ll_status ll_mamba2_bwd(const void* q, const void* k, const void* v, const float
                         int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype, void* workspace,
                         size_t workspace_bytes, void* stream) {
   return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, d_k, d_v, C, dtype,
-                         workspace, workspace_bytes, stream, nullptr);
+                         workspace, workspace_bytes, stream, nullptr, false);
+}
+
+ll_status ll_mamba2_bwd_after_fwd(const void* q, const void* k, const void* v, const float* log_alpha,
+                                  const float* lambda, const void* d_o, void* dq, void* dk, void* dv, float* dlog_alpha,
+                                  float* dlambda, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C,
+                                  int32_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, d_k, d_v, C, dtype,
+                         workspace, workspace_bytes, stream, nullptr, true);
 }
 
 ll_status ll_mamba2_bwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
@@ -222,7 +231,7 @@ ll_status ll_mamba2_bwd_staged(const void* q, const void* k, const void* v, cons
   for (int i = 0; i <= ll::kMamba2BwdStages; ++i)
     if (!events[i]) return LL_ERR_NULL_ARG;
   return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, d_k, d_v, C, dtype,
-                         workspace, workspace_bytes, stream, events);
+                         workspace, workspace_bytes, stream, events, false);
 }
 
 ll_status ll_gdn_fwd(const void* q, const void* k, const void* v, const float* log_alpha, const float* beta,

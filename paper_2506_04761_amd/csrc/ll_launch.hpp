@@ -74,6 +74,7 @@ struct Mamba2BwdArgs {
   int64_t B, T, H, C;
   int L;
   void* workspace;
+  bool reuse_summaries;  // the workspace already holds the forward's summaries of these inputs
 };
 typedef hipError_t (*Mamba2BwdLaunch)(const Mamba2BwdArgs&, hipStream_t, hipEvent_t* /* null or 5 events */);
 constexpr int kMamba2BwdStages = 4;

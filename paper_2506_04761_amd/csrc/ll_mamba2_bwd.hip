@@ -1359,8 +1359,9 @@ int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_
   return cur;
 }
 
-// Stages (ev[i] recorded before stage i, ev[4] after the last): 0 the forward summaries, 1 the
-// key-side summaries, 2 dq and dlambda, 3 dk, dv and dlog_alpha.
+// Stages (ev[i] recorded before stage i, ev[4] after the last): 0 the forward summaries (skipped
+// when the workspace already holds them), 1 the key-side summaries, 2 dq and dlambda, 3 dk, dv and
+// dlog_alpha.
 template <typename T, int C, int DK, int DV>
 hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t* ev) {
   constexpr int R = tile_rows(C), SZ = DK * DV;
@@ -1386,8 +1387,10 @@ hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t*
   fa.B = a.B; fa.T = a.T; fa.H = a.H; fa.dk = DK; fa.dv = DV; fa.C = C; fa.Hqk = a.H; fa.L = a.L;
   fa.workspace = a.workspace;
   if (ev) (void)hipEventRecord(ev[0], st);
-  hipError_t e = launch_mamba2_summaries<T, C, DK, DV>(fa, w.fwd, nodes, st, nullptr);
-  if (e != hipSuccess) return e;
+  if (!a.reuse_summaries) {
+    const hipError_t e = launch_mamba2_summaries<T, C, DK, DV>(fa, w.fwd, nodes, st, nullptr);
+    if (e != hipSuccess) return e;
+  }
   if (ev) (void)hipEventRecord(ev[1], st);
   if (J >= 1) {
     const int items = 7 + (J > 3 ? J - 3 : 0);

@@ -140,6 +140,16 @@ def test_mamba2_bwd_argument_checks_return_before_launch():
     assert _bwd(staged=True, ev=(ctypes.c_void_p * 5)(4096, 4096, None, 4096, 4096)) == ll._lib.LL_ERR_NULL_ARG
 
 
+def test_mamba2_bwd_after_fwd_argument_checks():
+    def c(lam=FAKE, ws=FAKE, wsb=1 << 40, T=128):
+        return lib.ll_mamba2_bwd_after_fwd(FAKE, FAKE, FAKE, FAKE, lam, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, T, 2,
+                                           64, 64, 64, 1, ws, wsb, None)
+    assert c(lam=None) == ll._lib.LL_ERR_NULL_ARG
+    assert c(ws=None) == ll._lib.LL_ERR_NULL_ARG
+    assert c(T=100) == ll._lib.LL_ERR_BAD_SHAPE
+    assert c(wsb=1000) == ll._lib.LL_ERR_WORKSPACE
+
+
 def test_mamba2_bwd_workspace_and_support():
     for shape in ((ll.LL_F32, 16, 16, 16), (ll.LL_BF16, 64, 128, 128), (ll.LL_BF16, 64, 128, 64)):
         assert ll.ll_supported(ll.LL_MAMBA2_BWD, *shape)

@@ -107,3 +107,24 @@ def test_bwd_full_size_sampled():
     # the first gate only shifts every cumulative sum: its gradient vanishes
     assert np.max(np.abs(dla[:, 0])) <= TOL["bf16"] * np.max(np.abs(dla))
     assert np.all(np.isfinite(dq)) and np.all(np.isfinite(dk)) and np.all(np.isfinite(dv))
+
+
+@pytest.mark.parametrize("T,dk,dv", [(64 * 66, 128, 128), (64 * 19, 128, 64)])
+def test_bwd_after_fwd_reuses_the_forward_summaries(T, dk, dv):
+    """ll_mamba2_bwd_after_fwd on the workspace a forward just filled equals ll_mamba2_bwd bit for
+    bit (the same kernels on the same summaries), and so matches the oracle too."""
+    import torch
+    import paper_2506_04761_amd as ll
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=1, H=2, T=T, dk=dk, dv=dv, seed=97)
+    x = generate(w)
+    do = upstream_grad(w)
+    args = [to_dev(x[n], "bf16") for n in ("q", "k", "v")]
+    args += [to_dev(x["log_alpha"]), to_dev(x["lam"]), to_dev(do, "bf16")]
+    ref = [g.clone() for g in ll.ll_mamba2_bwd(*args, w.C)]
+    ws = ll.ll_mamba2_bwd_workspace(args[0], args[2], w.C)
+    ws.fill_(255)  # stale bytes: everything the backward reads must come from the forward
+    ll.ll_mamba2_fwd(*args[:5], w.C, workspace=ws)
+    got = ll.ll_mamba2_bwd_after_fwd(*args, w.C, ws)
+    torch.cuda.synchronize()
+    for n, a, b in zip(NAMES, got, ref):
+        assert torch.equal(a, b), n
