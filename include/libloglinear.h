@@ -189,6 +189,20 @@ ll_status ll_mamba2_decode_step(const void* q, const void* k, const void* v, con
                                 int64_t t, int64_t B, int64_t H, int64_t d_k, int64_t d_v,
                                 int32_t L, int32_t dtype, void* stream);
 
+/* Log-linear Gated DeltaNet decoding with the same state buffer (ll_decode_state_bytes) and
+ * conventions.  Token t applies the gated delta-rule transition alpha_t (I - beta_t k_t k_t^T) to
+ * every carried and merged level (Sec. 3.2 merges; every nonempty level is rewritten each step),
+ * then beta_t v_t k_t^T enters level 0; o_t = sum_l lambda_t^(l) S_t^(l) q_t.  beta [B, H] is
+ * float32 and required; lambda == NULL gives Gated DeltaNet decoding.  Feeding tokens 0..T-1 gives
+ * the rows of the log-linear Gated DeltaNet forward.  Same shapes, checks and statuses as the
+ * Mamba-2 calls (a state is used by one variant between initialisations). */
+ll_status ll_gdn_decode_init(void* state, size_t state_bytes, int64_t B, int64_t H, int64_t d_k,
+                             int64_t d_v, int32_t L, int32_t dtype, void* stream);
+ll_status ll_gdn_decode_step(const void* q, const void* k, const void* v, const float* log_alpha,
+                             const float* beta, const float* lambda, void* o, void* state,
+                             size_t state_bytes, int64_t t, int64_t B, int64_t H, int64_t d_k,
+                             int64_t d_v, int32_t L, int32_t dtype, void* stream);
+
 /* Log-linear Gated DeltaNet forward (Sec. 3.4), with the delta-rule transition
  * alpha_t (I - beta_t k_t k_t^T) applied chunkwise through a WY (UT) representation.
  * beta is required; lambda == NULL gives plain Gated DeltaNet.  Returns LL_ERR_UNSUPPORTED

@@ -47,6 +47,11 @@ lib.ll_mamba2_decode_init.restype = _i32
 lib.ll_mamba2_decode_step.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _i64, _i64, _i64, _i64, _i64, _i32,
                                       _i32, _vp]
 lib.ll_mamba2_decode_step.restype = _i32
+lib.ll_gdn_decode_init.argtypes = [_vp, _sz, _i64, _i64, _i64, _i64, _i32, _i32, _vp]
+lib.ll_gdn_decode_init.restype = _i32
+lib.ll_gdn_decode_step.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _i64, _i64, _i64, _i64, _i64, _i32,
+                                   _i32, _vp]
+lib.ll_gdn_decode_step.restype = _i32
 lib.ll_mamba2_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i32,
                                       _vp, _sz, _vp, ctypes.POINTER(_vp)]
 lib.ll_mamba2_fwd_staged.restype = _i32
@@ -208,6 +213,38 @@ def ll_mamba2_decode_step(q, k, v, log_alpha, lam, state, t, L, out=None, stream
     _check(out, "out", q.dtype, (B, H, dv))
     st = lib.ll_mamba2_decode_step(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(lam), _ptr(out), _ptr(state),
                                    state.numel(), t, B, H, dk, dv, L, _dtype_code(q), _stream(stream))
+    if st != LL_OK:
+        raise LLError(st)
+    return out
+
+
+def ll_gdn_decode_init(state, B, H, dk, dv, L, dtype, stream=None):
+    """Resets `state` for log-linear Gated DeltaNet decoding (same buffer as the Mamba-2 calls)."""
+    code = LL_BF16 if dtype == _torch().bfloat16 else LL_F32
+    st = lib.ll_gdn_decode_init(_ptr(state), state.numel(), B, H, dk, dv, L, code, _stream(stream))
+    if st != LL_OK:
+        raise LLError(st)
+
+
+def ll_gdn_decode_step(q, k, v, log_alpha, beta, lam, state, t, L, out=None, stream=None):
+    """Feeds token t to log-linear Gated DeltaNet decoding: as ll_mamba2_decode_step plus
+    beta [B, H] (float32, required)."""
+    torch = _torch()
+    B, H, dk = q.shape
+    dv = v.shape[-1]
+    _check(q, "q")
+    _check(k, "k", q.dtype, (B, H, dk))
+    _check(v, "v", q.dtype, (B, H, dv))
+    _check(log_alpha, "log_alpha", torch.float32, (B, H))
+    _check(beta, "beta", torch.float32, (B, H))
+    if lam is not None:
+        _check(lam, "lambda", torch.float32, (B, H, L))
+    _check(state, "state", torch.uint8)
+    if out is None:
+        out = torch.empty((B, H, dv), dtype=q.dtype, device=q.device)
+    _check(out, "out", q.dtype, (B, H, dv))
+    st = lib.ll_gdn_decode_step(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(beta), _ptr(lam), _ptr(out),
+                                _ptr(state), state.numel(), t, B, H, dk, dv, L, _dtype_code(q), _stream(stream))
     if st != LL_OK:
         raise LLError(st)
     return out

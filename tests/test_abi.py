@@ -103,6 +103,16 @@ def test_decode_argument_checks_return_before_launch():
     assert lib.ll_mamba2_decode_init(FAKE, 1000, 2, 3, 64, 64, 10, 1, None) == ll._lib.LL_ERR_WORKSPACE
 
 
+def test_gdn_decode_argument_checks_return_before_launch():
+    def d(beta=FAKE, t=5, L=10, dk=64, sb=1 << 40):
+        return lib.ll_gdn_decode_step(FAKE, FAKE, FAKE, FAKE, beta, FAKE, FAKE, FAKE, sb, t, 2, 3, dk, 64, L, 1, None)
+    assert d(beta=None) == ll._lib.LL_ERR_NULL_ARG
+    assert d(t=512) == ll._lib.LL_ERR_BAD_SHAPE
+    assert d(dk=96) == ll._lib.LL_ERR_UNSUPPORTED
+    assert d(sb=1000) == ll._lib.LL_ERR_WORKSPACE
+    assert lib.ll_gdn_decode_init(None, 1 << 40, 2, 3, 64, 64, 10, 1, None) == ll._lib.LL_ERR_NULL_ARG
+
+
 def test_mamba2_argument_checks_return_before_launch():
     assert _m2(q=None) == ll._lib.LL_ERR_NULL_ARG
     assert _m2(la=None) == ll._lib.LL_ERR_NULL_ARG
