@@ -216,7 +216,7 @@ def main():
     w = WORKLOADS[args.workload]
     if w.variant == "gdn":
         return main_gdn(args, w, torch, ll)
-    if w.variant == "decode":
+    if w.variant in ("decode", "gdn_decode"):
         return main_decode(args, w, torch, ll)
     if w.variant == "mamba2_bwd":
         return main_bwd(args, w, torch, ll)
@@ -544,9 +544,25 @@ def decode_level_reads(T):
     return reads
 
 
+def gdn_decode_level_traffic(T):
+    """Per token t < T of Gated DeltaNet decoding: (level states read, level states written).
+    Every nonempty level >= 1 after the step (bit l-1 of t set) is rewritten; the merged level
+    p+1 (p = lssb(t)) reads the previous levels 1..p, the others read themselves."""
+    out = []
+    for t in range(T):
+        if t == 0:
+            out.append((0, 0))
+            continue
+        p = (t & -t).bit_length() - 1
+        n = bin(t).count("1")
+        out.append((n - 1 + p, n))
+    return out
+
+
 def main_decode(args, w, torch, ll):
-    """Log-linear Mamba-2 decoding: B sequences, one token each per step, timed over the last
-    steps before position T (the state then holds up to log2 T levels)."""
+    """Log-linear Mamba-2 or Gated DeltaNet decoding: B sequences, one token each per step, timed
+    over the last steps before position T (the state then holds up to log2 T levels)."""
+    gdn = w.variant == "gdn_decode"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     T0 = 1024  # distinct token inputs, cycled
@@ -555,6 +571,7 @@ def main_decode(args, w, torch, ll):
     dt = torch.bfloat16
     per_t = {n: torch.from_numpy(x[n]).to(dev).to(dt).transpose(0, 1).contiguous() for n in ("q", "k", "v")}
     la = torch.from_numpy(x["log_alpha"]).to(dev).transpose(0, 1).contiguous()
+    beta = torch.from_numpy(x["beta"]).to(dev).transpose(0, 1).contiguous() if gdn else None
     lam = torch.zeros((T0, w.B, w.H, L), dtype=torch.float32, device=dev)
     lam[..., :x["lam"].shape[-1]] = torch.from_numpy(x["lam"]).to(dev).transpose(0, 1)
     del x
@@ -565,11 +582,16 @@ def main_decode(args, w, torch, ll):
 
     def step(t, lmb=True):
         i = t % T0
-        ll.ll_mamba2_decode_step(per_t["q"][i], per_t["k"][i], per_t["v"][i], la[i], lam[i] if lmb else None,
-                                 state, t, L, out=out, stream=stream)
+        if gdn:
+            ll.ll_gdn_decode_step(per_t["q"][i], per_t["k"][i], per_t["v"][i], la[i], beta[i],
+                                  lam[i] if lmb else None, state, t, L, out=out, stream=stream)
+        else:
+            ll.ll_mamba2_decode_step(per_t["q"][i], per_t["k"][i], per_t["v"][i], la[i], lam[i] if lmb else None,
+                                     state, t, L, out=out, stream=stream)
 
     def run(lmb):
-        ll.ll_mamba2_decode_init(state, w.B, w.H, w.dk, w.dv, L, dt, stream=stream)
+        (ll.ll_gdn_decode_init if gdn else ll.ll_mamba2_decode_init)(state, w.B, w.H, w.dk, w.dv, L, dt,
+                                                                     stream=stream)
         for t in range(w.T - M):
             step(t, lmb)
         torch.cuda.synchronize()
@@ -586,33 +608,43 @@ def main_decode(args, w, torch, ll):
     ms_null = run(False)
     print(f"[bench] decode {ms * 1e3:.1f} us/token-step (lambda), {ms_null * 1e3:.1f} (lambda=NULL)",
           file=sys.stderr, flush=True)
-    reads = decode_level_reads(w.T)[w.T - M:]
     BH = w.B * w.H
     SZ4 = w.dk * w.dv * 4
-    per_step = BH * (np.mean(reads) + 1) * SZ4 + BH * ((2 * w.dk + 2 * w.dv) * 2 + 4 + 4 * L + 2 * (w.dv + w.dk) * 4)
+    token_bytes = BH * ((2 * w.dk + 2 * w.dv) * 2 + 4 + 4 * L + 2 * (w.dv + w.dk) * 4 + (4 if gdn else 0))
+    if gdn:
+        rw = np.array(gdn_decode_level_traffic(w.T)[w.T - M:], dtype=np.float64)
+        per_step = BH * (rw[:, 0].mean() + rw[:, 1].mean()) * SZ4 + token_bytes
+        note = ("per head: the level states read (the carried levels and the merged level's inputs) and every "
+                "nonempty level rewritten by the delta-rule transition, fp32, means over the timed positions, plus "
+                "the token's inputs and output; states partly served by the 256 MB Infinity Cache")
+    else:
+        reads = decode_level_reads(w.T)[w.T - M:]
+        per_step = BH * (np.mean(reads) + 1) * SZ4 + token_bytes
+        note = ("per head: the nonempty level states read (mean over the timed positions) and the merged one "
+                "written, fp32, plus the token's inputs and output; the states re-read every token are partly "
+                "served by the 256 MB Infinity Cache, so the rate can exceed the HBM peak")
     gbs = per_step / (ms * 1e-3) / 1e9
+    name = "Gated DeltaNet" if gdn else "Mamba-2"
     res = {
-        "metric": "decode tokens/sec (one token per sequence per step), log-linear Mamba-2",
+        "metric": f"decode tokens/sec (one token per sequence per step), log-linear {name}",
         "value": w.B / (ms * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1, "steps": M, "warmup": w.T - M, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": w.dtype, "data": "synthetic",
-        "config": {"workload": w.name, "variant": "log-linear Mamba-2 decoding", "B": w.B, "H": w.H,
+        "config": {"workload": w.name, "variant": f"log-linear {name} decoding", "B": w.B, "H": w.H,
                    "positions": f"{w.T - M}..{w.T - 1}", "d_k": w.dk, "d_v": w.dv, "levels": L,
-                   "inputs": f"bf16 q/k/v, fp32 log-gates and lambda, the seeded T={T0} draw cycled"},
-        "mamba2_lambda_null": {"ms_per_step": ms_null, "tokens_per_s": w.B / (ms_null * 1e-3)},
-        "roofline": {"kernel": "decode_step", "bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": None,
-                     "algorithmic_bytes_per_step": per_step,
-                     "bytes_note": "per head: the nonempty level states read (mean over the timed positions) "
-                                   "and the merged one written, fp32, plus the token's inputs and output; the "
-                                   "states re-read every token are partly served by the 256 MB Infinity Cache, "
-                                   "so the rate can exceed the HBM peak"},
+                   "inputs": f"bf16 q/k/v, fp32 log-gates{', beta' if gdn else ''} and lambda, the seeded "
+                             f"T={T0} draw cycled"},
+        ("gated_deltanet_lambda_null" if gdn else "mamba2_lambda_null"):
+            {"ms_per_step": ms_null, "tokens_per_s": w.B / (ms_null * 1e-3)},
+        "roofline": {"kernel": "gdn_decode_step" if gdn else "decode_step", "bound": "hbm", "achieved": gbs,
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": None,
+                     "algorithmic_bytes_per_step": per_step, "bytes_note": note},
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(w.with_(variant="mamba2", B=1), args.cpu_budget)
+        res["cpu_baseline"] = cpu_baseline(w.with_(variant="gdn" if gdn else "mamba2", B=1), args.cpu_budget)
         res["cpu_baseline"]["sample"] += " (the oracle's recurrent form is itself token-by-token decoding)"
     print(json.dumps(res), flush=True)
 

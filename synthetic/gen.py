@@ -27,7 +27,7 @@ import numpy as np
 @dataclass(frozen=True)
 class Workload:
     name: str
-    variant: str      # "mamba2", "gdn", "mamba2_bwd" (backward pass) or "decode" (decoding)
+    variant: str      # "mamba2", "gdn", "mamba2_bwd" (backward pass), "decode" or "gdn_decode" (decoding)
     dtype: str        # "f32" or "bf16": storage dtype of q, k, v and o
     B: int
     H: int
@@ -62,6 +62,7 @@ WORKLOADS = {
         # inputs are the T = 1024 draw, cycled)
         # backward pass over the same inputs as the T = 65536 forward workload
         Workload("ll_mamba2_bwd_bf16_T65536", "mamba2_bwd", "bf16", 1, 16, 65536, 128, 128, 64, 4, "unit"),
+        Workload("ll_gdn_decode_bf16_T8192", "gdn_decode", "bf16", 64, 16, 8192, 128, 128, 64, 8, "gdn"),
         Workload("ll_mamba2_decode_bf16_T8192", "decode", "bf16", 64, 16, 8192, 128, 128, 64, 7, "unit"),
     ]
 }
@@ -103,7 +104,7 @@ def generate(w: Workload, T: int = None, heads=None):
     v = rng.standard_normal((B, TT, H, dv), dtype=np.float32)
     xa = rng.standard_normal((B, TT, H), dtype=np.float32)
     xl = rng.standard_normal((B, TT, H, L), dtype=np.float32)
-    xb = rng.standard_normal((B, TT, H), dtype=np.float32) if w.variant == "gdn" else None
+    xb = rng.standard_normal((B, TT, H), dtype=np.float32) if w.variant in ("gdn", "gdn_decode") else None
 
     q = q / np.float32(math.sqrt(dk))
     if w.dist.startswith("gdn"):
