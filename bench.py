@@ -47,7 +47,8 @@ def flops_mamba2(w):
 
 
 STAGES = ["block_state", "scan", "tile_out"]
-KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_mamba2.hip", "paper_2506_04761_amd/csrc/ll_device.hpp"]
+KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_mamba2.hip", "paper_2506_04761_amd/csrc/ll_mamba2_common.hpp",
+                  "paper_2506_04761_amd/csrc/ll_device.hpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tile_out_ll_mamba2_bf16_T65536_hbm_traffic.md")
 
 
