@@ -133,25 +133,42 @@ ll_status ll_mamba2_bwd(const void* q, const void* k, const void* v, const float
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ll_mamba2_bwd without recomputing the forward's level summaries: for a backward that follows
- * ll_mamba2_fwd on the same q, k, v, log_alpha and lambda (non-NULL) run with this same workspace
- * (ll_workspace_size(LL_MAMBA2_BWD, ...) bytes: the forward uses its leading part and leaves its
- * summaries there), with nothing else writing the workspace in between, on the same stream or
- * ordered after it.  Any other use gives wrong gradients without an error.  Saves the forward's
- * first two stages (block_state and the level scan).  Arguments and checks as ll_mamba2_bwd. */
+ * ll_mamba2_fwd_grouped (ll_mamba2_fwd for H_qk = H) on the same q, k, v, log_alpha and lambda
+ * (non-NULL) run with this same workspace (ll_mamba2_bwd_workspace_size(...) bytes: the forward
+ * uses its leading part and leaves its summaries there), with nothing else writing the workspace
+ * in between, on the same stream or ordered after it.  Any other use gives wrong gradients without
+ * an error.  Saves the forward's first two stages (block_state and the level scan).  Arguments
+ * and checks as ll_mamba2_bwd_grouped. */
 ll_status ll_mamba2_bwd_after_fwd(const void* q, const void* k, const void* v, const float* log_alpha,
                                   const float* lambda, const void* d_o, void* dq, void* dk, void* dv,
                                   float* dlog_alpha, float* dlambda, int64_t B, int64_t T, int64_t H,
-                                  int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                                  int64_t H_qk, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                                   void* workspace, size_t workspace_bytes, void* stream);
 
-/* Same computation as ll_mamba2_bwd, for measurement, recording the caller's HIP events on
+/* Backward of ll_mamba2_fwd_grouped: q, k, dq and dk are [B, T, H_qk, d_k]; head h (of H) reads
+ * query/key head h / (H / H_qk), so dq and dk of a shared head sum the gradients of its group of
+ * heads.  H_qk < 1, H_qk > H or H % H_qk != 0 gives LL_ERR_BAD_SHAPE; the workspace is
+ * ll_mamba2_bwd_workspace_size(dtype, B, T, H, H_qk, d_k, d_v, C) bytes (H_qk < H adds per-head
+ * dq and dk scratch); otherwise as ll_mamba2_bwd, which is the case H_qk = H. */
+ll_status ll_mamba2_bwd_grouped(const void* q, const void* k, const void* v, const float* log_alpha,
+                                const float* lambda, const void* d_o, void* dq, void* dk, void* dv,
+                                float* dlog_alpha, float* dlambda, int64_t B, int64_t T, int64_t H,
+                                int64_t H_qk, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes of the backward calls for H_qk query/key heads (0 if an argument is invalid);
+ * equals ll_workspace_size(LL_MAMBA2_BWD, ..., 1) for H_qk = H.  Pure host function. */
+size_t ll_mamba2_bwd_workspace_size(int32_t dtype, int64_t B, int64_t T, int64_t H, int64_t H_qk,
+                                    int64_t d_k, int64_t d_v, int64_t C);
+
+/* Same computation as ll_mamba2_bwd_grouped, for measurement, recording the caller's HIP events on
  * `stream`: events[i] right before stage i and events[4] after the last.  Stages: 0 the forward's
  * level summaries, 1 the key-side level summaries, 2 dq and dlambda, 3 dk, dv and dlog_alpha.
  * events == NULL or any events[i] == NULL returns LL_ERR_NULL_ARG. */
 ll_status ll_mamba2_bwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
                                const float* lambda, const void* d_o, void* dq, void* dk, void* dv,
                                float* dlog_alpha, float* dlambda, int64_t B, int64_t T, int64_t H,
-                               int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                               int64_t H_qk, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                                void* workspace, size_t workspace_bytes, void* stream,
                                void* const* events);
 

@@ -62,9 +62,13 @@ lib.ll_gdn_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64,
 lib.ll_gdn_fwd_staged.restype = _i32
 lib.ll_mamba2_bwd.argtypes = [_vp] * 11 + [_i64] * 6 + [_i32, _vp, _sz, _vp]
 lib.ll_mamba2_bwd.restype = _i32
-lib.ll_mamba2_bwd_after_fwd.argtypes = [_vp] * 11 + [_i64] * 6 + [_i32, _vp, _sz, _vp]
+lib.ll_mamba2_bwd_after_fwd.argtypes = [_vp] * 11 + [_i64] * 7 + [_i32, _vp, _sz, _vp]
+lib.ll_mamba2_bwd_grouped.argtypes = [_vp] * 11 + [_i64] * 7 + [_i32, _vp, _sz, _vp]
+lib.ll_mamba2_bwd_grouped.restype = _i32
+lib.ll_mamba2_bwd_workspace_size.argtypes = [_i32] + [_i64] * 7
+lib.ll_mamba2_bwd_workspace_size.restype = _sz
 lib.ll_mamba2_bwd_after_fwd.restype = _i32
-lib.ll_mamba2_bwd_staged.argtypes = [_vp] * 11 + [_i64] * 6 + [_i32, _vp, _sz, _vp, _vp]
+lib.ll_mamba2_bwd_staged.argtypes = [_vp] * 11 + [_i64] * 7 + [_i32, _vp, _sz, _vp, _vp]
 lib.ll_mamba2_bwd_staged.restype = _i32
 lib.ll_debug_level_map.argtypes = [_i64, _i64, _vp, _vp]
 lib.ll_debug_level_map.restype = _i32
@@ -281,10 +285,10 @@ def ll_mamba2_fwd_staged(q, k, v, log_alpha, lam, C, events, out=None, workspace
 
 def _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, handles, after_fwd=False):
     torch = _torch()
-    B, T, H, dk = q.shape
-    dv = v.shape[-1]
+    B, T, Hqk, dk = q.shape
+    H, dv = v.shape[2], v.shape[-1]
     _check(q, "q")
-    _check(k, "k", q.dtype, (B, T, H, dk))
+    _check(k, "k", q.dtype, (B, T, Hqk, dk))
     _check(v, "v", q.dtype, (B, T, H, dv))
     _check(d_o, "d_o", q.dtype, (B, T, H, dv))
     _check(log_alpha, "log_alpha", torch.float32, (B, T, H))
@@ -302,16 +306,20 @@ def _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, handles
     _check(dv_, "dv", q.dtype, v.shape)
     _check(dla, "dlog_alpha", torch.float32, (B, T, H))
     _check(dlam, "dlambda", torch.float32, (B, T, H, L))
-    need = ll_workspace_size(LL_MAMBA2_BWD, code, B, T, H, dk, dv, C, True)
     if workspace is None:
+        need = lib.ll_mamba2_bwd_workspace_size(code, B, T, H, Hqk, dk, dv, C)
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
     _check(workspace, "workspace", torch.uint8)
     args = [_ptr(x) for x in (q, k, v, log_alpha, lam, d_o, dq, dk_, dv_, dla, dlam)]
-    args += [B, T, H, dk, dv, C, code, _ptr(workspace), workspace.numel(), _stream(stream)]
+    tail = [dk, dv, C, code, _ptr(workspace), workspace.numel(), _stream(stream)]
     if after_fwd:
-        st = lib.ll_mamba2_bwd_after_fwd(*args)
+        st = lib.ll_mamba2_bwd_after_fwd(*args, B, T, H, Hqk, *tail)
+    elif handles is not None:
+        st = lib.ll_mamba2_bwd_staged(*args, B, T, H, Hqk, *tail, handles)
+    elif Hqk == H:
+        st = lib.ll_mamba2_bwd(*args, B, T, H, *tail)
     else:
-        st = lib.ll_mamba2_bwd(*args) if handles is None else lib.ll_mamba2_bwd_staged(*args, handles)
+        st = lib.ll_mamba2_bwd_grouped(*args, B, T, H, Hqk, *tail)
     if st != LL_OK:
         raise LLError(st)
     return grads
@@ -320,17 +328,18 @@ def _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, handles
 def ll_mamba2_bwd(q, k, v, log_alpha, lam, d_o, C, grads=None, workspace=None, stream=None):
     """Gradients of sum(O * d_o) for the log-linear Mamba-2 forward O on the same inputs:
     returns (dq, dk, dv, dlog_alpha, dlambda) (dq, dk, dv in the dtype of q; the others float32),
-    written into `grads` when given.  `lam` is required.  Enqueued on `stream` (default: torch's
-    current stream), not synchronised."""
+    written into `grads` when given.  `lam` is required.  When q and k have fewer heads than v
+    (shared query/key heads, as in ll_mamba2_fwd_grouped) this calls ll_mamba2_bwd_grouped and dq,
+    dk have q's shape.  Enqueued on `stream` (default: torch's current stream), not synchronised."""
     return _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, None)
 
 
 def ll_mamba2_bwd_workspace(q, v, C):
-    """A workspace for ll_mamba2_bwd shaped for q [B, T, H, d_k] and v [..., d_v] (also usable by
-    ll_mamba2_fwd, whose summaries ll_mamba2_bwd_after_fwd then reuses)."""
+    """A workspace for the backward shaped for q [B, T, H_qk, d_k] and v [B, T, H, d_v] (also usable
+    by the forward, whose summaries ll_mamba2_bwd_after_fwd then reuses)."""
     torch = _torch()
-    B, T, H, dk = q.shape
-    need = ll_workspace_size(LL_MAMBA2_BWD, _dtype_code(q), B, T, H, dk, v.shape[-1], C, True)
+    B, T, Hqk, dk = q.shape
+    need = lib.ll_mamba2_bwd_workspace_size(_dtype_code(q), B, T, v.shape[2], Hqk, dk, v.shape[-1], C)
     return torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
 
 

@@ -68,8 +68,16 @@ size_t ll_workspace_size(int32_t variant, int32_t dtype, int64_t B, int64_t T, i
     return (size_t)ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), has_lambda != 0, nullptr);
   if (variant == LL_GDN) return (size_t)ll::gdn_workspace(B, T, H, d_k, d_v, C, nullptr);
   if (variant == LL_MAMBA2_BWD && has_lambda)
-    return (size_t)ll::mamba2_bwd_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), nullptr);
+    return (size_t)ll::mamba2_bwd_workspace(B, T, H, H, d_k, d_v, C, elem_size(dtype), nullptr);
   return 0;
+}
+
+size_t ll_mamba2_bwd_workspace_size(int32_t dtype, int64_t B, int64_t T, int64_t H, int64_t H_qk, int64_t d_k,
+                                    int64_t d_v, int64_t C) {
+  if (check_shape(B, T, H, d_k, d_v, C) != LL_OK) return 0;
+  if (dtype != LL_F32 && dtype != LL_BF16) return 0;
+  if (H_qk < 1 || H_qk > H || H % H_qk != 0) return 0;
+  return (size_t)ll::mamba2_bwd_workspace(B, T, H, H_qk, d_k, d_v, C, elem_size(dtype), nullptr);
 }
 
 const char* ll_status_string(ll_status s) {
@@ -120,12 +128,13 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
 }
 ll_status mamba2_bwd_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
                           const void* d_o, void* dq, void* dk, void* dv, float* dlog_alpha, float* dlambda, int64_t B,
-                          int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype, void* workspace,
-                          size_t workspace_bytes, void* stream, void* const* events, bool reuse) {
+                          int64_t T, int64_t H, int64_t Hqk, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                          void* workspace, size_t workspace_bytes, void* stream, void* const* events, bool reuse) {
   if (!q || !k || !v || !log_alpha || !lambda || !d_o || !dq || !dk || !dv || !dlog_alpha || !dlambda)
     return LL_ERR_NULL_ARG;
   ll_status st = check_shape(B, T, H, d_k, d_v, C);
   if (st != LL_OK) return st;
+  if (Hqk < 1 || Hqk > H || H % Hqk != 0) return LL_ERR_BAD_SHAPE;
   if (dtype != LL_F32 && dtype != LL_BF16) return LL_ERR_UNSUPPORTED;
   const ll::BwdEntry* e = find_mamba2_bwd(dtype, C, d_k, d_v);
   if (!e) return LL_ERR_UNSUPPORTED;
@@ -133,13 +142,14 @@ ll_status mamba2_bwd_impl(const void* q, const void* k, const void* v, const flo
   const int64_t tiles = ll::tiles_of(T, C);
   if (L > kMaxL || tiles > kMaxTiles || H > 65535 || B > 65535 || tiles * H * B >= (int64_t(1) << 31))
     return LL_ERR_UNSUPPORTED;
-  const int64_t need = ll::mamba2_bwd_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), nullptr);
+  const int64_t need = ll::mamba2_bwd_workspace(B, T, H, Hqk, d_k, d_v, C, elem_size(dtype), nullptr);
   if (!workspace) return LL_ERR_NULL_ARG;
   if ((int64_t)workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
   ll::Mamba2BwdArgs a;
   a.q = q; a.k = k; a.v = v; a.dout = d_o; a.log_alpha = log_alpha; a.lambda = lambda;
   a.dq = dq; a.dk = dk; a.dv = dv; a.dlog_alpha = dlog_alpha; a.dlambda = dlambda;
   a.B = B; a.T = T; a.H = H; a.C = C;
+  a.Hqk = Hqk;
   a.L = L;
   a.workspace = workspace;
   a.reuse_summaries = reuse;
@@ -210,28 +220,37 @@ ll_status ll_mamba2_bwd(const void* q, const void* k, const void* v, const float
                         const void* d_o, void* dq, void* dk, void* dv, float* dlog_alpha, float* dlambda, int64_t B,
                         int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype, void* workspace,
                         size_t workspace_bytes, void* stream) {
-  return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, d_k, d_v, C, dtype,
-                         workspace, workspace_bytes, stream, nullptr, false);
+  return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, H, d_k, d_v, C,
+                         dtype, workspace, workspace_bytes, stream, nullptr, false);
+}
+
+ll_status ll_mamba2_bwd_grouped(const void* q, const void* k, const void* v, const float* log_alpha,
+                                const float* lambda, const void* d_o, void* dq, void* dk, void* dv, float* dlog_alpha,
+                                float* dlambda, int64_t B, int64_t T, int64_t H, int64_t H_qk, int64_t d_k, int64_t d_v,
+                                int64_t C, int32_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, H_qk, d_k, d_v, C,
+                         dtype, workspace, workspace_bytes, stream, nullptr, false);
 }
 
 ll_status ll_mamba2_bwd_after_fwd(const void* q, const void* k, const void* v, const float* log_alpha,
                                   const float* lambda, const void* d_o, void* dq, void* dk, void* dv, float* dlog_alpha,
-                                  float* dlambda, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C,
-                                  int32_t dtype, void* workspace, size_t workspace_bytes, void* stream) {
-  return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, d_k, d_v, C, dtype,
-                         workspace, workspace_bytes, stream, nullptr, true);
+                                  float* dlambda, int64_t B, int64_t T, int64_t H, int64_t H_qk, int64_t d_k,
+                                  int64_t d_v, int64_t C, int32_t dtype, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, H_qk, d_k, d_v, C,
+                         dtype, workspace, workspace_bytes, stream, nullptr, true);
 }
 
 ll_status ll_mamba2_bwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
                                const float* lambda, const void* d_o, void* dq, void* dk, void* dv, float* dlog_alpha,
-                               float* dlambda, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C,
-                               int32_t dtype, void* workspace, size_t workspace_bytes, void* stream,
+                               float* dlambda, int64_t B, int64_t T, int64_t H, int64_t H_qk, int64_t d_k, int64_t d_v,
+                               int64_t C, int32_t dtype, void* workspace, size_t workspace_bytes, void* stream,
                                void* const* events) {
   if (!events) return LL_ERR_NULL_ARG;
   for (int i = 0; i <= ll::kMamba2BwdStages; ++i)
     if (!events[i]) return LL_ERR_NULL_ARG;
-  return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, d_k, d_v, C, dtype,
-                         workspace, workspace_bytes, stream, events, false);
+  return mamba2_bwd_impl(q, k, v, log_alpha, lambda, d_o, dq, dk, dv, dlog_alpha, dlambda, B, T, H, H_qk, d_k, d_v, C,
+                         dtype, workspace, workspace_bytes, stream, events, false);
 }
 
 ll_status ll_gdn_fwd(const void* q, const void* k, const void* v, const float* log_alpha, const float* beta,

@@ -54,10 +54,11 @@ const KernelEntry* mamba2_table(int* n);
 struct BwdLayout {
   WsLayout fwd;
   int64_t NR = 0, nd = 0, npart = 0;  // 8-tile regions; key-side summaries and partials per (b, h)
-  int64_t d = 0, dtot = 0, part = 0, qdq = 0, tsum = 0, total = 0;
+  int64_t d = 0, dtot = 0, part = 0, qdq = 0, tsum = 0, dqh = 0, dkh = 0, total = 0;
 };
-int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, int64_t esize,
-                             BwdLayout* lay);
+// Hqk < H adds per-head dq and dk scratch (summed over each group of heads at the end).
+int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t Hqk, int64_t dk, int64_t dv, int64_t C,
+                             int64_t esize, BwdLayout* lay);
 
 struct Mamba2BwdArgs {
   const void* q;
@@ -72,6 +73,7 @@ struct Mamba2BwdArgs {
   float* dlog_alpha;
   float* dlambda;
   int64_t B, T, H, C;
+  int64_t Hqk;           // query/key heads (H % Hqk == 0); dq and dk have Hqk heads
   int L;
   void* workspace;
   bool reuse_summaries;  // the workspace already holds the forward's summaries of these inputs

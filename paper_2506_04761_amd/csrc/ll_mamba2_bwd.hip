@@ -161,8 +161,8 @@ __device__ inline void load_lambda(float* dst, const float* __restrict__ lam, in
 template <typename T, int C, int DK, int DV>
 __global__ __launch_bounds__(kRevThreads) void k_rev_state(const T* __restrict__ q, const T* __restrict__ dout,
                                                            const float* __restrict__ lam, Nodes<T> nodes,
-                                                           RevNodes<T> rev, int64_t Tlen, int H, int L, int J,
-                                                           int items) {
+                                                           RevNodes<T> rev, int64_t Tlen, int H, int Hqk, int L,
+                                                           int J, int items) {
   using M = Mfma<T>;
   typedef typename Vec16<T>::type V16;
   constexpr int R = tile_rows(C), LOG2R = Log2<R>::v;
@@ -195,6 +195,7 @@ __global__ __launch_bounds__(kRevThreads) void k_rev_state(const T* __restrict__
   if (j > J || u0 >= N) return;
   if (j >= 4 && !((rg >> (j - 4)) & 1)) return;
   if (u0 + nt > N) nt = (int)(N - u0);
+  const int hq = h / (H / Hqk);  // this head's query/key head
 
   const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -211,7 +212,7 @@ __global__ __launch_bounds__(kRevThreads) void k_rev_state(const T* __restrict__
   auto load_step = [&](int s) {
     const int64_t u = u0 + s / STEPS;
     const int r0 = (s % STEPS) * kKB;
-    qr.load(q, tile_row0(u), r0, nrow_of(u), H, h);
+    qr.load(q, tile_row0(u), r0, nrow_of(u), Hqk, hq);
     dr.load(dout, tile_row0(u), r0, nrow_of(u), H, h);
     if (tid < kKB) {
       const int r = r0 + tid;
@@ -345,7 +346,8 @@ __global__ __launch_bounds__(4 * tile_rows(C)) void k_bwd_dq(const T* __restrict
                                                             const float* __restrict__ log_alpha,
                                                             const float* __restrict__ lam, Nodes<T> nodes,
                                                             T* __restrict__ dq, float* __restrict__ dlam,
-                                                            float* __restrict__ qdq, int64_t Tlen, int H, int L, int J) {
+                                                            float* __restrict__ qdq, int64_t Tlen, int H, int Hqk, int L,
+                                                            int J) {
   using M = Mfma<T>;
   typedef typename Vec16<T>::type V16;
   constexpr int R = tile_rows(C), LOG2R = Log2<R>::v, NW = R / 16, NT = 64 * NW;
@@ -375,9 +377,11 @@ __global__ __launch_bounds__(4 * tile_rows(C)) void k_bwd_dq(const T* __restrict
   const int i = 16 * wave + r16;  // this lane's query row
   const bool rowok = i < nrow;
   const int64_t qrow = (row0 + (rowok ? i : 0)) * H + h;
+  const int hq = h / (H / Hqk);  // this head's query/key head
+  const int64_t qkrow = (row0 + (rowok ? i : 0)) * Hqk + hq;
 
   const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);
-  load_tile<T, DK, LDK, R, NT>(k_s, k, row0, nrow, H, h);
+  load_tile<T, DK, LDK, R, NT>(k_s, k, row0, nrow, Hqk, hq);
   load_tile<T, DV, LDV, R, NT>(v_s, v, row0, nrow, H, h);
   load_lambda<NT>(lam_s, lam, row0, nrow, H, h, L);
   for (int x = tid; x < R * kMaxLevels; x += NT) dl_s[x] = 0.f;
@@ -385,7 +389,7 @@ __global__ __launch_bounds__(4 * tile_rows(C)) void k_bwd_dq(const T* __restrict
   typename M::frag qf[KSK], df[KSV];
 #pragma unroll
   for (int ks = 0; ks < KSK; ++ks)
-    qf[ks] = rowok ? M::load(q + qrow * DK + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
+    qf[ks] = rowok ? M::load(q + qkrow * DK + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
 #pragma unroll
   for (int ks = 0; ks < KSV; ++ks)
     df[ks] = rowok ? M::load(dout + qrow * DV + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
@@ -518,7 +522,7 @@ __global__ __launch_bounds__(4 * tile_rows(C)) void k_bwd_dq(const T* __restrict
       const int64_t e = qrow * DK + 16 * mt + 4 * g + r;
       if (rowok) {
         dq[e] = from_f32<T>(acc[mt][r]);
-        qd += acc[mt][r] * to_f32(q[e]);
+        qd += acc[mt][r] * to_f32(q[qkrow * DK + 16 * mt + 4 * g + r]);
       }
     }
   qd = sum_over_groups(qd);
@@ -544,7 +548,7 @@ __global__ __launch_bounds__(4 * tile_rows(C)) void k_bwd_dkv(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ dout,
     const float* __restrict__ log_alpha, const float* __restrict__ lam, RevNodes<T> rev, const float* __restrict__ qdq,
     T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ dla, float* __restrict__ tsum, int64_t Tlen, int H,
-    int L, int J) {
+    int Hqk, int L, int J) {
   using M = Mfma<T>;
   typedef typename Vec16<T>::type V16;
   constexpr int R = tile_rows(C), NW = R / 16, NT = 64 * NW;
@@ -573,16 +577,18 @@ __global__ __launch_bounds__(4 * tile_rows(C)) void k_bwd_dkv(
   const int jk = 16 * wave + r16;  // this lane's key row
   const bool keyok = jk < nrow;
   const int64_t krow = (row0 + (keyok ? jk : 0)) * H + h;
+  const int hq = h / (H / Hqk);  // this head's query/key head
+  const int64_t kqrow = (row0 + (keyok ? jk : 0)) * Hqk + hq;
 
   const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);
-  load_tile<T, DK, LDQ, R, NT>(q_s, q, row0, nrow, H, h);
+  load_tile<T, DK, LDQ, R, NT>(q_s, q, row0, nrow, Hqk, hq);
   load_tile<T, DV, LDO, R, NT>(o_s, dout, row0, nrow, H, h);
   load_lambda<NT>(lam_s, lam, row0, nrow, H, h, L);
 
   typename M::frag kf[KSK], vf[KSV];
 #pragma unroll
   for (int ks = 0; ks < KSK; ++ks)
-    kf[ks] = keyok ? M::load(k + krow * DK + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
+    kf[ks] = keyok ? M::load(k + kqrow * DK + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
 #pragma unroll
   for (int ks = 0; ks < KSV; ++ks)
     vf[ks] = keyok ? M::load(v + krow * DV + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
@@ -703,7 +709,7 @@ __global__ __launch_bounds__(4 * tile_rows(C)) void k_bwd_dkv(
       const int64_t e = krow * DK + 16 * mt + 4 * g + r;
       if (keyok) {
         dk[e] = from_f32<T>(ak[mt][r]);
-        kd += ak[mt][r] * to_f32(k[e]);
+        kd += ak[mt][r] * to_f32(k[kqrow * DK + 16 * mt + 4 * g + r]);
       }
     }
 #pragma unroll
@@ -755,7 +761,7 @@ template <int DK, int DV>
 __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dq_fast(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lam, Nodes<__bf16> nodes, __bf16* __restrict__ dq,
-    float* __restrict__ dlam, float* __restrict__ qdq, int64_t Tlen, int H, int L, int J) {
+    float* __restrict__ dlam, float* __restrict__ qdq, int64_t Tlen, int H, int Hqk, int L, int J) {
   using M = Mfma<__bf16>;
   typedef __bf16 bf;
   typedef typename M::frag frag;
@@ -780,6 +786,7 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dq_fast(
   const int gA = wave, gB = 7 - wave;            // this wave's 16-row groups
   const int iA = 16 * gA + r16, iB = 16 * gB + r16;
   const bool liveB = 16 * gB < nrow;             // nrow is a multiple of C = 64; group A is always live
+  const int hq = h / (H / Hqk);                  // this head's query/key head
 
   // ---- loads: gates and lambda into LDS, this lane's rows of q and dO into registers, the first
   //      level's summary (or, without levels, the K and V tiles) into the K region
@@ -788,8 +795,8 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dq_fast(
   frag qA[KSK], qB[KSK], dA[KSV], dB[KSV], pA[KSV], pB[KSV];
   {
     const int rB = iB < nrow ? iB : nrow - 1;
-    const bf* qa = q + ((row0 + iA) * H + h) * DK;
-    const bf* qb = q + ((row0 + rB) * H + h) * DK;
+    const bf* qa = q + ((row0 + iA) * Hqk + hq) * DK;
+    const bf* qb = q + ((row0 + rB) * Hqk + hq) * DK;
     const bf* da = dout + ((row0 + iA) * H + h) * DV;
     const bf* db = dout + ((row0 + rB) * H + h) * DV;
 #pragma unroll
@@ -806,7 +813,7 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dq_fast(
     }
   }
   auto copy_tile = [&](bf* region) {
-    if (region == k_s) lds_copy_rows<DK, R, NT>(k_s, k + (row0 * H + h) * DK, (int64_t)H * DK, nrow);
+    if (region == k_s) lds_copy_rows<DK, R, NT>(k_s, k + (row0 * Hqk + hq) * DK, (int64_t)Hqk * DK, nrow);
     else lds_copy_rows<DV, R, NT>(v_s, v + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
   };
   auto next_level = [&](int j) {
@@ -986,8 +993,8 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dq_fast(
   // ---- q . dq (fp32 accumulators), then dq through LDS as whole rows
   float qdA = 0.f, qdB = 0.f;
   {
-    const bf* qa = q + growA * DK + 4 * g;
-    const bf* qb = q + growB * DK + 4 * g;
+    const bf* qa = q + ((row0 + iA) * Hqk + hq) * DK + 4 * g;
+    const bf* qb = q + ((row0 + (liveB ? iB : 0)) * Hqk + hq) * DK + 4 * g;
 #pragma unroll
     for (int mt = 0; mt < MTK; ++mt) {
       const bf16x4 xa = *reinterpret_cast<const bf16x4*>(qa + 16 * mt);
@@ -1037,7 +1044,7 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dkv_fast(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lam, Nodes<__bf16> nodes, RevNodes<__bf16> rev,
     const float* __restrict__ qdq, __bf16* __restrict__ dk, __bf16* __restrict__ dv, float* __restrict__ dla,
-    float* __restrict__ tsum, int64_t Tlen, int H, int L, int J) {
+    float* __restrict__ tsum, int64_t Tlen, int H, int Hqk, int L, int J) {
   using M = Mfma<__bf16>;
   typedef __bf16 bf;
   typedef typename M::frag frag;
@@ -1065,14 +1072,16 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dkv_fast(
   const int jA = 16 * gA + r16, jB = 16 * gB + r16;
   const bool liveB = 16 * gB < nrow;
   const int64_t growA = (row0 + jA) * H + h, growB = (row0 + (liveB ? jB : 0)) * H + h;
+  const int hq = h / (H / Hqk);  // this head's query/key head
+  const int64_t kqA = (row0 + jA) * Hqk + hq, kqB = (row0 + (liveB ? jB : 0)) * Hqk + hq;
 
   lds_gather4<NT>(cl_s, R, [&](int x) { return nodes.cl + (bh * N + u) * R + x; });
   lds_copy_lambda<R, NT>(lam_s, lam, row0, H, h, L, nrow);
   frag kA[KSK], kB[KSK], wA_[KSV], wB_[KSV];  // k rows (along d_k), v rows in the result-row k order
 #pragma unroll
   for (int ks = 0; ks < KSK; ++ks) {
-    kA[ks] = M::load(k + growA * DK + ks * 32 + g * 8);
-    kB[ks] = M::load(k + growB * DK + ks * 32 + g * 8);
+    kA[ks] = M::load(k + kqA * DK + ks * 32 + g * 8);
+    kB[ks] = M::load(k + kqB * DK + ks * 32 + g * 8);
   }
 #pragma unroll
   for (int st = 0; st < KSV; ++st) {
@@ -1080,7 +1089,7 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dkv_fast(
     wB_[st] = load_rl_pair(v + growB * DV, st);
   }
   auto copy_tile = [&](bf* region) {
-    if (region == q_s) lds_copy_rows<DK, R, NT>(q_s, q + (row0 * H + h) * DK, (int64_t)H * DK, nrow);
+    if (region == q_s) lds_copy_rows<DK, R, NT>(q_s, q + (row0 * Hqk + hq) * DK, (int64_t)Hqk * DK, nrow);
     else lds_copy_rows<DV, R, NT>(o_s, dout + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
   };
   auto next_level = [&](int j) {
@@ -1234,8 +1243,8 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dkv_fast(
   // ---- k . dk, dcum = q . dq - k . dk
   float kdA = 0.f, kdB = 0.f;
   {
-    const bf* ka = k + growA * DK + 4 * g;
-    const bf* kb = k + growB * DK + 4 * g;
+    const bf* ka = k + kqA * DK + 4 * g;
+    const bf* kb = k + kqB * DK + 4 * g;
 #pragma unroll
     for (int mt = 0; mt < MTK; ++mt) {
       const bf16x4 xa = *reinterpret_cast<const bf16x4*>(ka + 16 * mt);
@@ -1336,8 +1345,28 @@ __global__ __launch_bounds__(256) void k_bwd_dgate(const float* __restrict__ tsu
 // ---------------------------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------------------------
-int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, int64_t esize,
-                             BwdLayout* lay) {
+// ---------------------------------------------------------------------------------------------
+// k_group_sum: heads sharing one query/key head -- out[b, t, hq, :] = sum over the group's heads h
+// of in[b, t, h, :] (fp32 sums of the per-head gradients).  grid (ceil(rows * Hqk * D / 256)).
+// ---------------------------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_group_sum(const T* __restrict__ in, T* __restrict__ out, int64_t rows, int H,
+                                                   int Hqk, int D) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= rows * Hqk * D) return;
+  const int d = (int)(idx % D);
+  const int64_t rq = idx / D;  // (row, hq)
+  const int hq = (int)(rq % Hqk);
+  const int64_t row = rq / Hqk;
+  const int G = H / Hqk;
+  const T* src = in + (row * H + (int64_t)hq * G) * D + d;
+  float acc = 0.f;
+  for (int x = 0; x < G; ++x) acc += to_f32(src[(int64_t)x * D]);
+  out[idx] = from_f32<T>(acc);
+}
+
+int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t Hqk, int64_t dk, int64_t dv, int64_t C,
+                             int64_t esize, BwdLayout* lay) {
   BwdLayout w{};
   int64_t cur = mamba2_workspace(B, T, H, dk, dv, C, esize, true, &w.fwd);
   auto al = [](int64_t x) { return (x + 255) & ~int64_t(255); };
@@ -1354,6 +1383,10 @@ int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_
   w.part = cur; cur += al(BH * np1 * SZ * 4);
   w.qdq = cur; cur += al(B * T * H * 4);
   w.tsum = cur; cur += al(BH * N * 4);
+  if (Hqk < H) {  // per-head dq and dk before the sum over each group of heads
+    w.dqh = cur; cur += al(B * T * H * dk * esize);
+    w.dkh = cur; cur += al(B * T * H * dk * esize);
+  }
   w.total = cur;
   if (lay) *lay = w;
   return cur;
@@ -1366,7 +1399,7 @@ template <typename T, int C, int DK, int DV>
 hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t* ev) {
   constexpr int R = tile_rows(C), SZ = DK * DV;
   BwdLayout w;
-  mamba2_bwd_workspace(a.B, a.T, a.H, DK, DV, C, sizeof(T), &w);
+  mamba2_bwd_workspace(a.B, a.T, a.H, a.Hqk, DK, DV, C, sizeof(T), &w);
   const Nodes<T> nodes = mamba2_nodes<T>(w.fwd, a.workspace, true);
   char* base = static_cast<char*>(a.workspace);
   RevNodes<T> rev;
@@ -1381,10 +1414,14 @@ hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t*
   float* tsum = reinterpret_cast<float*>(base + w.tsum);
   const int J = w.fwd.J;
   const int64_t BH = a.B * a.H;
+  const bool grouped = a.Hqk < a.H;
+  // per-head dq, dk: the outputs themselves, or scratch summed over each group of heads at the end
+  T* dqh = grouped ? reinterpret_cast<T*>(base + w.dqh) : (T*)a.dq;
+  T* dkh = grouped ? reinterpret_cast<T*>(base + w.dkh) : (T*)a.dk;
 
   Mamba2Args fa{};
   fa.q = a.q; fa.k = a.k; fa.v = a.v; fa.log_alpha = a.log_alpha; fa.lambda = a.lambda; fa.o = nullptr;
-  fa.B = a.B; fa.T = a.T; fa.H = a.H; fa.dk = DK; fa.dv = DV; fa.C = C; fa.Hqk = a.H; fa.L = a.L;
+  fa.B = a.B; fa.T = a.T; fa.H = a.H; fa.dk = DK; fa.dv = DV; fa.C = C; fa.Hqk = a.Hqk; fa.L = a.L;
   fa.workspace = a.workspace;
   if (ev) (void)hipEventRecord(ev[0], st);
   if (!a.reuse_summaries) {
@@ -1395,7 +1432,8 @@ hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t*
   if (J >= 1) {
     const int items = 7 + (J > 3 ? J - 3 : 0);
     hipLaunchKernelGGL((k_rev_state<T, C, DK, DV>), dim3((unsigned)(BH * w.NR * items)), dim3(kRevThreads), 0, st,
-                       (const T*)a.q, (const T*)a.dout, a.lambda, nodes, rev, a.T, (int)a.H, a.L, J, items);
+                       (const T*)a.q, (const T*)a.dout, a.lambda, nodes, rev, a.T, (int)a.H, (int)a.Hqk, a.L, J,
+                       items);
   }
   if (J >= 5) {
     int64_t ng = 0;
@@ -1408,23 +1446,30 @@ hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t*
   constexpr bool kFast = std::is_same<T, __bf16>::value && R == kBwdFastRows;
   if constexpr (kFast)
     hipLaunchKernelGGL((k_bwd_dq_fast<DK, DV>), gtile, dim3(kBwdFastThreads), 0, st, (const T*)a.q, (const T*)a.k,
-                       (const T*)a.v, (const T*)a.dout, a.lambda, nodes, (T*)a.dq, a.dlambda, qdq, a.T, (int)a.H,
-                       a.L, J);
+                       (const T*)a.v, (const T*)a.dout, a.lambda, nodes, dqh, a.dlambda, qdq, a.T, (int)a.H,
+                       (int)a.Hqk, a.L, J);
   else
     hipLaunchKernelGGL((k_bwd_dq<T, C, DK, DV>), gtile, dim3(4 * R), 0, st, (const T*)a.q, (const T*)a.k,
-                       (const T*)a.v, (const T*)a.dout, a.log_alpha, a.lambda, nodes, (T*)a.dq, a.dlambda, qdq, a.T,
-                       (int)a.H, a.L, J);
+                       (const T*)a.v, (const T*)a.dout, a.log_alpha, a.lambda, nodes, dqh, a.dlambda, qdq, a.T,
+                       (int)a.H, (int)a.Hqk, a.L, J);
   if (ev) (void)hipEventRecord(ev[3], st);
   if constexpr (kFast)
     hipLaunchKernelGGL((k_bwd_dkv_fast<DK, DV>), gtile, dim3(kBwdFastThreads), 0, st, (const T*)a.q, (const T*)a.k,
-                       (const T*)a.v, (const T*)a.dout, a.lambda, nodes, rev, (const float*)qdq, (T*)a.dk, (T*)a.dv,
-                       a.dlog_alpha, tsum, a.T, (int)a.H, a.L, J);
+                       (const T*)a.v, (const T*)a.dout, a.lambda, nodes, rev, (const float*)qdq, dkh, (T*)a.dv,
+                       a.dlog_alpha, tsum, a.T, (int)a.H, (int)a.Hqk, a.L, J);
   else
     hipLaunchKernelGGL((k_bwd_dkv<T, C, DK, DV>), gtile, dim3(4 * R), 0, st, (const T*)a.q, (const T*)a.k,
-                       (const T*)a.v, (const T*)a.dout, a.log_alpha, a.lambda, rev, (const float*)qdq, (T*)a.dk,
-                       (T*)a.dv, a.dlog_alpha, tsum, a.T, (int)a.H, a.L, J);
+                       (const T*)a.v, (const T*)a.dout, a.log_alpha, a.lambda, rev, (const float*)qdq, dkh,
+                       (T*)a.dv, a.dlog_alpha, tsum, a.T, (int)a.H, (int)a.Hqk, a.L, J);
   hipLaunchKernelGGL(k_bwd_dgate, dim3((unsigned)((a.T + 255) / 256), (unsigned)BH), dim3(256), 0, st,
                      (const float*)tsum, a.dlog_alpha, a.T, (int)a.H, R);
+  if (grouped) {
+    const int64_t n = a.B * a.T * a.Hqk * DK;
+    hipLaunchKernelGGL((k_group_sum<T>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, (const T*)dqh, (T*)a.dq,
+                       a.B * a.T, (int)a.H, (int)a.Hqk, DK);
+    hipLaunchKernelGGL((k_group_sum<T>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, (const T*)dkh, (T*)a.dk,
+                       a.B * a.T, (int)a.H, (int)a.Hqk, DK);
+  }
   if (ev) (void)hipEventRecord(ev[4], st);
   return hipGetLastError();
 }

@@ -129,11 +129,15 @@ def test_mamba2_argument_checks_return_before_launch():
     assert _m2(ws=ctypes.c_void_p(4096 + 8)) == ll._lib.LL_ERR_WORKSPACE
 
 
-def _bwd(lam=FAKE, do=FAKE, dla=FAKE, T=128, dk=64, dv=64, C=64, dtype=1, ws=FAKE, wsb=1 << 40, staged=False, ev=None):
-    args = [FAKE, FAKE, FAKE, FAKE, lam, do, FAKE, FAKE, FAKE, dla, FAKE, 1, T, 2, dk, dv, C, dtype, ws, wsb, None]
+def _bwd(lam=FAKE, do=FAKE, dla=FAKE, T=128, dk=64, dv=64, C=64, dtype=1, ws=FAKE, wsb=1 << 40, staged=False, ev=None,
+         Hqk=None):
+    ptrs = [FAKE, FAKE, FAKE, FAKE, lam, do, FAKE, FAKE, FAKE, dla, FAKE]
+    tail = [dk, dv, C, dtype, ws, wsb, None]
     if staged:
-        return lib.ll_mamba2_bwd_staged(*args, ev)
-    return lib.ll_mamba2_bwd(*args)
+        return lib.ll_mamba2_bwd_staged(*ptrs, 1, T, 2, 2 if Hqk is None else Hqk, *tail, ev)
+    if Hqk is not None:
+        return lib.ll_mamba2_bwd_grouped(*ptrs, 1, T, 2, Hqk, *tail)
+    return lib.ll_mamba2_bwd(*ptrs, 1, T, 2, *tail)
 
 
 def test_mamba2_bwd_argument_checks_return_before_launch():
@@ -148,12 +152,16 @@ def test_mamba2_bwd_argument_checks_return_before_launch():
     assert _bwd(ws=ctypes.c_void_p(4096 + 64)) == ll._lib.LL_ERR_WORKSPACE
     assert _bwd(staged=True, ev=None) == ll._lib.LL_ERR_NULL_ARG
     assert _bwd(staged=True, ev=(ctypes.c_void_p * 5)(4096, 4096, None, 4096, 4096)) == ll._lib.LL_ERR_NULL_ARG
+    assert _bwd(Hqk=0) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _bwd(Hqk=3) == ll._lib.LL_ERR_BAD_SHAPE   # more query/key heads than heads
+    assert _bwd(Hqk=1, lam=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _bwd(Hqk=1, wsb=1000) == ll._lib.LL_ERR_WORKSPACE
 
 
 def test_mamba2_bwd_after_fwd_argument_checks():
     def c(lam=FAKE, ws=FAKE, wsb=1 << 40, T=128):
         return lib.ll_mamba2_bwd_after_fwd(FAKE, FAKE, FAKE, FAKE, lam, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, T, 2,
-                                           64, 64, 64, 1, ws, wsb, None)
+                                           2, 64, 64, 64, 1, ws, wsb, None)
     assert c(lam=None) == ll._lib.LL_ERR_NULL_ARG
     assert c(ws=None) == ll._lib.LL_ERR_NULL_ARG
     assert c(T=100) == ll._lib.LL_ERR_BAD_SHAPE
@@ -169,6 +177,13 @@ def test_mamba2_bwd_workspace_and_support():
     assert bwd > fwd and bwd % 256 == 0
     assert ll.ll_workspace_size(ll.LL_MAMBA2_BWD, ll.LL_BF16, 1, 65536, 16, 128, 128, 64, 0) == 0
     assert ll.ll_workspace_size(ll.LL_MAMBA2_BWD, ll.LL_BF16, 1, 64, 1, 128, 128, 64, 1) > 0
+    ws = lib.ll_mamba2_bwd_workspace_size
+    assert ws(ll.LL_BF16, 2, 16384, 48, 48, 128, 64, 64) == \
+        ll.ll_workspace_size(ll.LL_MAMBA2_BWD, ll.LL_BF16, 2, 16384, 48, 128, 64, 64, 1)
+    # shared heads add per-head dq and dk scratch (2 x B T H d_k bf16)
+    assert ws(ll.LL_BF16, 2, 16384, 48, 1, 128, 64, 64) >= ws(ll.LL_BF16, 2, 16384, 48, 48, 128, 64, 64) + \
+        2 * 2 * 16384 * 48 * 128 * 2
+    assert ws(ll.LL_BF16, 2, 16384, 48, 5, 128, 64, 64) == 0
 
 
 def test_gdn_argument_checks_return_before_launch():

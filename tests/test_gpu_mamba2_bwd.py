@@ -128,3 +128,35 @@ def test_bwd_after_fwd_reuses_the_forward_summaries(T, dk, dv):
     torch.cuda.synchronize()
     for n, a, b in zip(NAMES, got, ref):
         assert torch.equal(a, b), n
+
+
+@pytest.mark.parametrize("dtype,C,dk,dv,H,Hqk,T", [
+    ("bf16", 64, 128, 128, 8, 1, 2048),
+    ("bf16", 64, 128, 64, 8, 2, 64 * 19),
+    ("bf16", 64, 64, 64, 6, 3, 512),
+    ("f32", 16, 16, 16, 4, 2, 256),
+])
+def test_bwd_grouped_qk_heads(dtype, C, dk, dv, H, Hqk, T):
+    """Shared query/key heads: the gradient of a shared q (k) is the sum over its group of heads of
+    the per-head gradients of the same model with q and k repeated to every head (chain rule
+    through the repetition); the oracle computes the latter and sums it."""
+    import torch
+    import paper_2506_04761_amd as ll
+    from synthetic import shared_qk
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(dtype=dtype, B=1, H=H, T=T, dk=dk, dv=dv, C=C, seed=41 + H,
+                                                   qk_heads=Hqk)
+    x = generate(w)
+    q, k = shared_qk(x, w)
+    do = upstream_grad(w)
+    G = H // Hqk
+    qr, kr = np.repeat(q, G, axis=2), np.repeat(k, G, axis=2)
+    ref = mamba2_grad.quadratic_grad(qr, kr, x["v"], x["log_alpha"], x["lam"], do)
+    ref = [ref[0].reshape(1, T, Hqk, G, dk).sum(axis=3), ref[1].reshape(1, T, Hqk, G, dk).sum(axis=3)] + list(ref[2:])
+    grads = ll.ll_mamba2_bwd(to_dev(q, dtype), to_dev(k, dtype), to_dev(x["v"], dtype), to_dev(x["log_alpha"]),
+                             to_dev(x["lam"]), to_dev(do, dtype), C)
+    torch.cuda.synchronize()
+    got = [g.float().cpu().numpy().astype(np.float64) for g in grads]
+    errs = {n: rel_err(g, r) for n, g, r in zip(NAMES, got, ref)}
+    print(f"grouped H={H} H_qk={Hqk} T={T} {dtype}", " ".join(f"{n} {e:.2e}" for n, e in errs.items()), flush=True)
+    for n, e in errs.items():
+        assert e <= TOL[dtype], (n, e)
