@@ -379,6 +379,10 @@ def cpu_baseline_bwd(w, budget_s):
     from oracle import mamba2_grad
     from synthetic import upstream_grad
     x = generate(w)
+    if w.qk_heads:  # the shared q, k repeated to every head of its group: the same computation
+        G = w.H // w.qk_heads
+        q, k = shared_qk(x, w)
+        x["q"], x["k"] = np.repeat(q, G, axis=2), np.repeat(k, G, axis=2)
     do = upstream_grad(w)
     T = 64
     while True:
@@ -409,14 +413,14 @@ def main_bwd(args, w, torch, ll):
     torch.cuda.set_device(dev)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     x = generate(w)
+    if w.qk_heads:
+        x["q"], x["k"] = shared_qk(x, w)
     d = {n: torch.from_numpy(x[n]).to(dev).to(dt).contiguous() for n in ("q", "k", "v")}
     la = torch.from_numpy(x["log_alpha"]).to(dev)
     lam = torch.from_numpy(x["lam"]).to(dev)
     del x
     do = torch.from_numpy(upstream_grad(w)).to(dev).to(dt).contiguous()
-    code = ll.LL_BF16 if w.dtype == "bf16" else ll.LL_F32
-    ws = torch.empty(ll.ll_workspace_size(ll.LL_MAMBA2_BWD, code, w.B, w.T, w.H, w.dk, w.dv, w.C, 1),
-                     dtype=torch.uint8, device=dev)
+    ws = ll.ll_mamba2_bwd_workspace(d["q"], d["v"], w.C)
     out = torch.empty((w.B, w.T, w.H, w.dv), dtype=dt, device=dev)
     grads = (torch.empty_like(d["q"]), torch.empty_like(d["k"]), torch.empty_like(d["v"]),
              torch.empty_like(la), torch.empty_like(lam))
@@ -431,9 +435,11 @@ def main_bwd(args, w, torch, ll):
             ll.ll_mamba2_bwd_staged(d["q"], d["k"], d["v"], la, lam, do, w.C, e, grads=grads, workspace=ws,
                                     stream=stream)
 
+    fwd_call = ll.ll_mamba2_fwd_grouped if w.qk_heads else ll.ll_mamba2_fwd
+
     def fwd():
         # in the backward's workspace: the backward after it reuses the level summaries
-        ll.ll_mamba2_fwd(d["q"], d["k"], d["v"], la, lam, w.C, out=out, workspace=ws, stream=stream)
+        fwd_call(d["q"], d["k"], d["v"], la, lam, w.C, out=out, workspace=ws, stream=stream)
 
     def bwd_after_fwd():
         ll.ll_mamba2_bwd_after_fwd(d["q"], d["k"], d["v"], la, lam, do, w.C, ws, grads=grads, stream=stream)
@@ -473,8 +479,9 @@ def main_bwd(args, w, torch, ll):
     Ff = flops_loglinear(w)
     tflops = F / (ms * 1e-3) / 1e12
     es = 2 if w.dtype == "bf16" else 4
-    # read q, k, v, dO, log alpha, lambda; write dq, dk, dv, dlog_alpha, dlambda
-    nbytes = w.B * w.T * w.H * ((4 * w.dk + 3 * w.dv) * es + 8 + 8 * w.levels)
+    # read q, k, v, dO, log alpha, lambda; write dq, dk, dv, dlog_alpha, dlambda (q, k, dq, dk at the
+    # query/key heads)
+    nbytes = w.B * w.T * w.H * ((4 * w.dk * qk_share(w) + 3 * w.dv) * es + 8 + 8 * w.levels)
     res = {
         "metric": "bwd tokens/sec + TFLOP/s (% bf16 MFMA peak), log-linear Mamba-2, T=64K",
         "value": w.B * w.T / (ms * 1e-3),
@@ -484,6 +491,7 @@ def main_bwd(args, w, torch, ll):
         "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "variant": "log-linear Mamba-2 backward", "B": w.B, "H": w.H, "T": w.T,
                    "d_k": w.dk, "d_v": w.dv, "C": w.C, "levels": w.levels,
+                   **({"qk_heads": w.qk_heads} if w.qk_heads else {}),
                    "inputs": "bf16 q/k/v/dO, fp32 log-gates and lambda, seeded synthetic (numpy PCG64)"},
         "tflops": tflops,
         "mfma_peak_frac": tflops / (PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS),

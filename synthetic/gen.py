@@ -60,6 +60,8 @@ WORKLOADS = {
         Workload("ll_mamba2_mva_bf16_T16384", "mamba2", "bf16", 2, 48, 16384, 128, 64, 64, 6, "unit", 1),
         # decoding: 64 sequences x 16 heads fed one token per step up to position 8191 (the token
         # inputs are the T = 1024 draw, cycled)
+        # backward pass at the shared-head benchmark shape (one q/k head for all 48 heads)
+        Workload("ll_mamba2_mva_bwd_bf16_T16384", "mamba2_bwd", "bf16", 2, 48, 16384, 128, 64, 64, 6, "unit", 1),
         # backward pass over the same inputs as the T = 65536 forward workload
         Workload("ll_mamba2_bwd_bf16_T65536", "mamba2_bwd", "bf16", 1, 16, 65536, 128, 128, 64, 4, "unit"),
         Workload("ll_gdn_decode_bf16_T8192", "gdn_decode", "bf16", 64, 16, 8192, 128, 128, 64, 8, "gdn"),
