@@ -243,3 +243,20 @@ def test_workspace_reuse_alternating_inputs():
             xh = {n: x[n][b:b + 1, :, h:h + 1] for n in ("q", "k", "v", "log_alpha", "lam")}
             ref = mamba2.quadratic(xh["q"], xh["k"], xh["v"], xh["log_alpha"], xh["lam"], rows=rows)
             assert rel_err(got[b:b + 1, rows, h:h + 1], ref) <= TOL["bf16"]
+
+
+def test_parity_maximum_length_sampled():
+    """The longest sequence the library takes (8192 tiles of 128 rows; here 2^20 - 64 tokens, a
+    ragged last tile, 21 levels, the deepest block tree), with alpha = 1 so that every level's
+    terms stay large: sampled rows of two heads against the quadratic form."""
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=1, H=2, T=(1 << 20) - 64, dist="nodecay", seed=123)
+    x = generate(w)
+    got = run_mamba2(x, w.dtype, w.C)
+    rows = np.array([0, 127, 128, 65535, 65536, 524287, 524288, 777777, w.T - 65, w.T - 1])
+    worst = 0.0
+    for h in (0, 1):
+        xs = {n: x[n][:, :, h:h + 1] for n in ("q", "k", "v", "log_alpha", "lam")}
+        ref = mamba2.quadratic(xs["q"], xs["k"], xs["v"], xs["log_alpha"], xs["lam"], rows=rows)
+        worst = max(worst, rel_err(got[:, rows, h:h + 1], ref))
+    print(f"T={w.T}: sampled rel err {worst:.3e}")
+    assert worst <= TOL["bf16"]

@@ -160,3 +160,25 @@ def test_bwd_grouped_qk_heads(dtype, C, dk, dv, H, Hqk, T):
     print(f"grouped H={H} H_qk={Hqk} T={T} {dtype}", " ".join(f"{n} {e:.2e}" for n, e in errs.items()), flush=True)
     for n, e in errs.items():
         assert e <= TOL[dtype], (n, e)
+
+
+def test_bwd_maximum_length_sampled():
+    """The longest sequence the library takes (2^20 - 64 tokens: 8192 tiles, a ragged last tile,
+    21 levels, key-side groups of up to 4096 tiles), alpha = 1: sampled rows, columns and dcum
+    positions of one head against the oracle."""
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=1, H=2, T=(1 << 20) - 64, dist="nodecay", seed=124)
+    x = generate(w)
+    do = upstream_grad(w)
+    dq, dk, dv, dla, dlam = run_bwd(x, do, w.dtype, w.C)
+    rows = np.array([0, 128, 524288, 777777, w.T - 1])
+    cols = np.array([5, 600001, w.T - 1])
+    xs = {n: x[n][:, :, 1:2] for n in x}
+    do_s = do[:, :, 1:2]
+    rq, rl = mamba2_grad.grad_rows(xs["q"], xs["k"], xs["v"], xs["log_alpha"], xs["lam"], do_s, rows)
+    ck, cv = mamba2_grad.grad_cols(xs["q"], xs["k"], xs["v"], xs["log_alpha"], xs["lam"], do_s, cols)
+    errs = {"dq": rel_err(dq[:, rows, 1:2], rq), "dlambda": rel_err(dlam[:, rows, 1:2], rl),
+            "dk": rel_err(dk[:, cols, 1:2], ck), "dv": rel_err(dv[:, cols, 1:2], cv)}
+    print(f"T={w.T} sampled", " ".join(f"{n} {e:.2e}" for n, e in errs.items()), flush=True)
+    for n, e in errs.items():
+        assert e <= TOL["bf16"], (n, e)
+    assert np.all(np.isfinite(dla)) and np.max(np.abs(dla[:, 0])) <= TOL["bf16"] * np.max(np.abs(dla))
