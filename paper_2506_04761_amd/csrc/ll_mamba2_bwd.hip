@@ -150,12 +150,12 @@ __device__ inline void load_lambda(float* dst, const float* __restrict__ lam, in
 }  // namespace
 
 // ---------------------------------------------------------------------------------------------
-// k_rev_state: one workgroup per (b, h, 8-tile region rg, item).  Items 0-3: level 1, tile
+// k_rev_state: one workgroup per (b, h, 8-tile region rg, item), one tile per step.  Items 0-3: level 1, tile
 // 8 rg + 2 i + 1; items 4-5: level 2, tiles 8 rg + 4 (i - 4) + {2, 3}; item 6: level 3, tiles
 // 8 rg + 4 .. 8 rg + 7; item 3 + j (j >= 4): level j, the whole region, present when bit j - 4 of
 // rg is set.  Each item forms sum_t w_t dO_t q_t^T over its tiles with
 // w_t = lambda_t^(log2 R + j) exp2(c_t), c_t the summed log2-gates from the item's first row through
-// t, 64 rows per step: (w q) and dO staged in LDS, both MFMA operands read down the token rows.
+// t, one tile per step: (w q) and dO staged in LDS, both MFMA operands read down the token rows.
 // Items of levels <= 4 cover their whole group and write D_j; the others write fp32 partials.
 // ---------------------------------------------------------------------------------------------
 template <typename T, int C, int DK, int DV>
@@ -174,11 +174,12 @@ __global__ __launch_bounds__(kRevThreads) void k_rev_state(const T* __restrict__
   constexpr int WN = (NW / WM) < NTN ? (NW / WM) : NTN;
   constexpr int TM = MT / WM, TN = NTN / WN;
   constexpr int SZ = DK * DV;
-  constexpr int STEPS = R / kKB;
-  __shared__ T q_s[kKB * LDQ];
-  __shared__ T o_s[kKB * LDO];
-  __shared__ T out_s[SZ];
-  __shared__ float w_s[kKB];
+  constexpr int HALVES = R / kKB;  // 64-row register blocks per tile (one tile per step)
+  static_assert(SZ <= R * LDQ, "the finished summary is staged in the Q buffer");
+  __shared__ T q_s[R * LDQ];
+  __shared__ T o_s[R * LDO];
+  __shared__ float w_s[R];
+  T* out_s = q_s;
 
   const int64_t N = rev.N, NR = rev.NR;
   const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // logical order (b, h, rg, item)
@@ -201,23 +202,25 @@ __global__ __launch_bounds__(kRevThreads) void k_rev_state(const T* __restrict__
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool active = wave < WM * WN;
   const int wm = wave / WN, wn = wave % WN;
-  const int nsteps = nt * STEPS;
+  const int nsteps = nt;
   auto nrow_of = [&](int64_t u) { return (int)((Tlen - u * R) < R ? (Tlen - u * R) : R); };
   auto tile_row0 = [&](int64_t u) { return (int64_t)b * Tlen + u * R; };
 
-  RowBlock<T, DK, kRevThreads> qr;
-  RowBlock<T, DV, kRevThreads> dr;
+  RowBlock<T, DK, kRevThreads> qr[HALVES];
+  RowBlock<T, DV, kRevThreads> dr[HALVES];
   float wv = 0.f;
   float base = 0.f;  // summed log2-gates of the item's tiles before the current one
+  // loads of step s = tile u0 + s (rows past the sequence get weight 0)
   auto load_step = [&](int s) {
-    const int64_t u = u0 + s / STEPS;
-    const int r0 = (s % STEPS) * kKB;
-    qr.load(q, tile_row0(u), r0, nrow_of(u), Hqk, hq);
-    dr.load(dout, tile_row0(u), r0, nrow_of(u), H, h);
-    if (tid < kKB) {
-      const int r = r0 + tid;
-      const float c = base + nodes.cl[(bh * N + u) * R + r];
-      wv = r < nrow_of(u) ? lam[((tile_row0(u) + r) * H + h) * L + LOG2R + j] * fast_exp2(c) : 0.f;
+    const int64_t u = u0 + s;
+#pragma unroll
+    for (int x = 0; x < HALVES; ++x) {
+      qr[x].load(q, tile_row0(u), x * kKB, nrow_of(u), Hqk, hq);
+      dr[x].load(dout, tile_row0(u), x * kKB, nrow_of(u), H, h);
+    }
+    if (tid < R) {
+      const float c = base + nodes.cl[(bh * N + u) * R + tid];
+      wv = tid < nrow_of(u) ? lam[((tile_row0(u) + tid) * H + h) * L + LOG2R + j] * fast_exp2(c) : 0.f;
     }
   };
 
@@ -230,16 +233,18 @@ __global__ __launch_bounds__(kRevThreads) void k_rev_state(const T* __restrict__
   load_step(0);
   for (int s = 0; s < nsteps; ++s) {
     __syncthreads();  // previous step's readers are done
-    if (tid < kKB) w_s[tid] = wv;
-    dr.store_rows(o_s, LDO);
+    if (tid < R) w_s[tid] = wv;
+#pragma unroll
+    for (int x = 0; x < HALVES; ++x) dr[x].store_rows(o_s + x * kKB * LDO, LDO);
     __syncthreads();
-    qr.store_rows_scaled(q_s, LDQ, w_s);
-    if ((s + 1) % STEPS == 0) base += nodes.t1[bh * N + u0 + s / STEPS];
+#pragma unroll
+    for (int x = 0; x < HALVES; ++x) qr[x].store_rows_scaled(q_s + x * kKB * LDQ, LDQ, w_s + x * kKB);
+    base += nodes.t1[bh * N + u0 + s];
     if (s + 1 < nsteps) load_step(s + 1);
     __syncthreads();
     if (active) {
 #pragma unroll
-      for (int ks = 0; ks < kKB / M::KSTEP; ++ks) {
+      for (int ks = 0; ks < R / M::KSTEP; ++ks) {
         typename M::frag bf[TN];
 #pragma unroll
         for (int jn = 0; jn < TN; ++jn) {
@@ -262,6 +267,7 @@ __global__ __launch_bounds__(kRevThreads) void k_rev_state(const T* __restrict__
 
   if (j <= 4) {
     const int64_t sl = rev.slot(bh, j, u0 >> j);
+    __syncthreads();  // every wave is done with the Q buffer
     if (active) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
