@@ -73,8 +73,9 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   constexpr int LDD = DK + PD;          // rows of length d_k
   constexpr int LDC = C + PD;           // rows of length C
   constexpr int VEC = 8;
+  constexpr int LDL = C + 4;            // fp32 L rows: 16-byte aligned, read four entries at a time
   // region 1: phase A/B (K, Q row-major, fp32 L) reused in phase C/D (W^T, U^T, masked P)
-  constexpr int R1A = 2 * C * LDD * 2 + C * (C + 1) * 4;
+  constexpr int R1A = 2 * C * LDD * 2 + C * LDL * 4;
   constexpr int R1B = (DK * LDC + DV * LDC + C * LDC) * 2;
   constexpr int R1 = R1A > R1B ? R1A : R1B;
   __shared__ __attribute__((aligned(16))) char r1[R1];
@@ -147,7 +148,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int t = mt * 16 + 4 * g + r, s = nt * 16 + r16;
-      l_s[t * (C + 1) + s] = s < t ? bt_s[t] * acc[r] * fast_exp2(cl_s[t] - cl_s[s]) : 0.f;
+      l_s[t * LDL + s] = s < t ? bt_s[t] * acc[r] * fast_exp2(cl_s[t] - cl_s[s]) : 0.f;
     }
   });
   __syncthreads();
@@ -181,13 +182,14 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
       float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
 #pragma unroll
       for (int j = 0; j + 3 < i; j += 4) {
-        a0 += l_s[i * (C + 1) + j] * x[j];
-        a1 += l_s[i * (C + 1) + j + 1] * x[j + 1];
-        a2 += l_s[i * (C + 1) + j + 2] * x[j + 2];
-        a3 += l_s[i * (C + 1) + j + 3] * x[j + 3];
+        const f32x4 lv = *reinterpret_cast<const f32x4*>(&l_s[i * LDL + j]);  // broadcast read
+        a0 += lv[0] * x[j];
+        a1 += lv[1] * x[j + 1];
+        a2 += lv[2] * x[j + 2];
+        a3 += lv[3] * x[j + 3];
       }
 #pragma unroll
-      for (int j = i & ~3; j < i; ++j) a0 += l_s[i * (C + 1) + j] * x[j];
+      for (int j = i & ~3; j < i; ++j) a0 += l_s[i * LDL + j] * x[j];
       const float acc = ((i == c) ? 1.f : 0.f) - ((a0 + a1) + (a2 + a3));
       x[i] = (i < c) ? 0.f : acc;
     }
