@@ -17,7 +17,7 @@
 // (bit j-1 of z clear) and propagates through P_z everywhere; a chunk with bit j-1 set adds
 // lambda_t^(log2 C + j) q~_t^T R_j to its rows, with R_j taken at the chunk's start.
 //
-// Kernels: gdn_chunk (per chunk: the WY solve in fp32 and all chunk-local products on MFMA,
+// Kernels: gdn_chunk (per chunk: the WY solve in fp32, a blocked inversion, and all chunk-local products on MFMA,
 // bf16 operands with fp32 accumulation) and gdn_scan (per (b, h, 16 d_v columns): every level's
 // state slice in registers, P_z / Q~ streamed through LDS once per chunk).
 #include <type_traits>
@@ -67,7 +67,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
                                                    bf* __restrict__ qc_out, bf* __restrict__ pz_out,
                                                    bf* __restrict__ hz_out, float* __restrict__ oin_out,
                                                    int64_t Tlen, int H, int L) {
-  static_assert(C == 64, "the forward substitution maps one lane of wave 0 to each of the C columns");
+  static_assert(C == 64, "the inversion works on 4 x 4 blocks of 16 x 16 (one lane per column of wave 0)");
   constexpr int LOG2C = 6;
   constexpr int PD = 8;                 // row padding (elements)
   constexpr int LDD = DK + PD;          // rows of length d_k
@@ -87,6 +87,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   __shared__ bf zt_s[C * LDC];     // T_G^T
   __shared__ float cl_s[C], gm_s[C], dc_s[C], bt_s[C];
   __shared__ float lam_s[HAS_LAMBDA ? C * (LOG2C + 1) : 1];
+  __shared__ float xs_s[10 * 256];  // fp32 blocks (i, j), j <= i, of X = (I + L)^{-1}: block i(i+1)/2 + j
   bf* k_s = reinterpret_cast<bf*>(r1);
   bf* q_s = k_s + C * LDD;
   float* l_s = reinterpret_cast<float*>(r1 + 2 * C * LDD * 2);
@@ -153,9 +154,17 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   });
   __syncthreads();
 
-  // ---- phase B: X = (I + L)^{-1} by forward substitution, lane c = column c (wave 0), each
-  //      row's dot product split over four independent partial sums;
-  //      T_G = X diag(beta): z_s[t][c] and zt_s[c][t].  Meanwhile the other waves form P_G.
+  // ---- phase B: X = (I + L)^{-1} in 16 x 16 blocks (fp32), T_G = X diag(beta) into z_s[t][c] and
+  //      zt_s[c][t].  B1: wave 0 inverts the four diagonal blocks by forward substitution (lane
+  //      16 b + c = column c of block b) while the other waves form P_G and zero the blocks above
+  //      the diagonal.  B2: block row i = 1, 2, 3 in turn, X_ij = -X_ii sum_{k=j}^{i-1} L_ik X_kj,
+  //      tile (i, j) on wave j (fp32 MFMA).
+  auto blk = [](int i, int j) { return (i * (i + 1) / 2 + j) * 256; };
+  auto put_t = [&](int t, int c, float x) {  // T_G entry (t, c)
+    const bf zv = static_cast<bf>(x * bt_s[c]);
+    z_s[t * LDC + c] = zv;
+    zt_s[c * LDC + t] = zv;
+  };
   if (wave != 0) {
     // P_G[t][s] = (q_t . k_s) Gamma[t,s], s <= t, 16 x 16 tiles dealt to the other waves
     using MF = Mfma<bf>;
@@ -174,31 +183,65 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
         pg_s[t * LDC + s] = static_cast<bf>(s <= t ? acc[r] * fast_exp2(cl_s[t] - cl_s[s]) : 0.f);
       }
     }
+    // zeros above the diagonal blocks (rows of block i, columns of block j > i)
+    for (int idx = tid - 64; idx < 6 * 256; idx += 64 * (kChunkWaves - 1)) {
+      const int bj = idx >> 8, e = idx & 255;
+      const int bi = bj < 3 ? 0 : (bj < 5 ? 1 : 2);                // (0,1) (0,2) (0,3) (1,2) (1,3) (2,3)
+      const int bc = bj < 3 ? bj + 1 : (bj < 5 ? bj - 1 : 3);
+      const int t = 16 * bi + (e >> 4), c = 16 * bc + (e & 15);
+      z_s[t * LDC + c] = static_cast<bf>(0.f);
+      zt_s[c * LDC + t] = static_cast<bf>(0.f);
+    }
   } else {
-    const int c = lane;
-    float x[C];
+    const int bb = lane >> 4, c = lane & 15;
+    const float* lb = l_s + 16 * bb * LDL + 16 * bb;  // diagonal block bb of L
+    float x[16];
 #pragma unroll
-    for (int i = 0; i < C; ++i) {
+    for (int i = 0; i < 16; ++i) {
       float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
 #pragma unroll
       for (int j = 0; j + 3 < i; j += 4) {
-        const f32x4 lv = *reinterpret_cast<const f32x4*>(&l_s[i * LDL + j]);  // broadcast read
+        const f32x4 lv = *reinterpret_cast<const f32x4*>(&lb[i * LDL + j]);  // broadcast per block
         a0 += lv[0] * x[j];
         a1 += lv[1] * x[j + 1];
         a2 += lv[2] * x[j + 2];
         a3 += lv[3] * x[j + 3];
       }
 #pragma unroll
-      for (int j = i & ~3; j < i; ++j) a0 += l_s[i * LDL + j] * x[j];
+      for (int j = i & ~3; j < i; ++j) a0 += lb[i * LDL + j] * x[j];
       const float acc = ((i == c) ? 1.f : 0.f) - ((a0 + a1) + (a2 + a3));
       x[i] = (i < c) ? 0.f : acc;
     }
-    const float bc = bt_s[c];
 #pragma unroll
-    for (int i = 0; i < C; ++i) {
-      const bf zv = static_cast<bf>(x[i] * bc);
-      z_s[i * LDC + c] = zv;
-      zt_s[c * LDC + i] = zv;
+    for (int i = 0; i < 16; ++i) {
+      xs_s[blk(bb, bb) + i * 16 + c] = x[i];
+      put_t(16 * bb + i, 16 * bb + c, x[i]);
+    }
+  }
+  for (int i = 1; i < C / 16; ++i) {
+    __syncthreads();  // blocks of rows < i (and the diagonal ones) are in xs_s
+    if (wave < i) {
+      using MF = Mfma<float>;
+      const int jb = wave;
+      // Y = sum_{k=j}^{i-1} L_ik X_kj  (k slot 4 kk + g)
+      f32x4 y = {0.f, 0.f, 0.f, 0.f};
+      for (int kb = jb; kb < i; ++kb) {
+        const float* xb = xs_s + blk(kb, jb);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          y = MF::mma(l_s[(16 * i + r16) * LDL + 16 * kb + 4 * kk + g], xb[(4 * kk + g) * 16 + r16], y);
+      }
+      // X_ij = -X_ii Y  (k slot 4 g + r: Y in the result layout is the B operand directly)
+      const float* di = xs_s + blk(i, i);
+      f32x4 xv = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) xv = MF::mma(di[r16 * 16 + 4 * g + r], y[r], xv);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float xr = -xv[r];
+        xs_s[blk(i, jb) + (4 * g + r) * 16 + r16] = xr;
+        put_t(16 * i + 4 * g + r, 16 * jb + r16, xr);
+      }
     }
   }
   __syncthreads();
