@@ -25,7 +25,9 @@
  *           q, k, v and o share one storage dtype (ll_dtype); gates, beta and lambda are float32.
  *           NaN or Inf in any input propagates to o; values are not checked.
  * Shapes.   B, H >= 1; T >= 1 and T % C == 0; C a power of two; (dtype, C, d_k, d_v) must be one of
- *           the compiled kernel shapes (ll_supported).
+ *           the compiled kernel shapes (ll_supported).  Size limits (LL_ERR_UNSUPPORTED beyond them):
+ *           L <= 24 levels; for log-linear Mamba-2 at most 8192 tiles of max(2C, 64) tokens per
+ *           sequence and B * H <= 65535.
  * Ownership. Every pointer is caller-owned device memory.  The library allocates nothing, keeps no
  *           pointer after the call returns, and enqueues all work on `stream` (a hipStream_t passed
  *           as void*, NULL = the default stream).  Calls return before the work finishes: the caller
@@ -50,7 +52,8 @@ typedef enum {
   LL_OK = 0,
   LL_ERR_NULL_ARG = 1,     /* a required pointer is NULL                                        */
   LL_ERR_BAD_SHAPE = 2,    /* B, T or H < 1, T % C != 0, C not a power of two, or d_k/d_v < 1   */
-  LL_ERR_UNSUPPORTED = 3,  /* no compiled kernel for (dtype, C, d_k, d_v), or an unknown dtype  */
+  LL_ERR_UNSUPPORTED = 3,  /* no compiled kernel for (dtype, C, d_k, d_v), an unknown dtype, or
+                              sizes beyond the limits stated under Shapes                        */
   LL_ERR_WORKSPACE = 4,    /* workspace smaller than ll_workspace_size(...) or misaligned       */
   LL_ERR_HIP = 5           /* the HIP runtime reported an error when launching                   */
 } ll_status;

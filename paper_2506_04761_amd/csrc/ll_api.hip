@@ -107,7 +107,8 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   if (!e) return LL_ERR_UNSUPPORTED;
   const int L = levels_of(T);
   const int64_t tiles = ll::tiles_of(T, C);
-  if (L > kMaxL || tiles > kMaxTiles || H > 65535 || B > 65535 || tiles * 2 * H * B >= (int64_t(1) << 31))
+  // B * H indexes the second grid dimension of the scan kernels (at most 65535)
+  if (L > kMaxL || tiles > kMaxTiles || B * H > 65535 || tiles * 2 * H * B >= (int64_t(1) << 31))
     return LL_ERR_UNSUPPORTED;
   const int64_t need = ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), lambda != nullptr, nullptr);
   if (!workspace) return LL_ERR_NULL_ARG;
@@ -140,7 +141,10 @@ ll_status mamba2_bwd_impl(const void* q, const void* k, const void* v, const flo
   if (!e) return LL_ERR_UNSUPPORTED;
   const int L = levels_of(T);
   const int64_t tiles = ll::tiles_of(T, C);
-  if (L > kMaxL || tiles > kMaxTiles || H > 65535 || B > 65535 || tiles * H * B >= (int64_t(1) << 31))
+  // B * H indexes the second / third grid dimension of the scan, reduce and gate kernels; the
+  // group sums launch one thread per output element
+  if (L > kMaxL || tiles > kMaxTiles || B * H > 65535 || tiles * H * B >= (int64_t(1) << 31) ||
+      B * T * Hqk * d_k / 256 >= (int64_t(1) << 31))
     return LL_ERR_UNSUPPORTED;
   const int64_t need = ll::mamba2_bwd_workspace(B, T, H, Hqk, d_k, d_v, C, elem_size(dtype), nullptr);
   if (!workspace) return LL_ERR_NULL_ARG;

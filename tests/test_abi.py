@@ -186,6 +186,14 @@ def test_mamba2_bwd_workspace_and_support():
     assert ws(ll.LL_BF16, 2, 16384, 48, 5, 128, 64, 64) == 0
 
 
+def test_size_limits_return_before_launch():
+    # B * H beyond the second grid dimension; more tiles than a sequence may have
+    assert _m2(B=300, H=300) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _m2(T=128 * 8193) == ll._lib.LL_ERR_UNSUPPORTED
+    assert lib.ll_mamba2_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 300, 128, 300, 64, 64, 64, 1,
+                             FAKE, 1 << 40, None) == ll._lib.LL_ERR_UNSUPPORTED
+
+
 def test_gdn_argument_checks_return_before_launch():
     def g(beta=FAKE, T=128, ws=FAKE, wsb=1 << 40, dk=128, dv=128):
         return lib.ll_gdn_fwd(FAKE, FAKE, FAKE, FAKE, beta, FAKE, FAKE, 1, T, 2, dk, dv, 64, 1, ws, wsb, None)
