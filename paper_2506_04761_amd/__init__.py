@@ -10,4 +10,5 @@ from ._lib import (  # noqa: F401
     ll_gdn_decode_init, ll_gdn_decode_step, ll_gdn_fwd, ll_gdn_fwd_staged, ll_mamba2_bwd, ll_mamba2_bwd_after_fwd,
     ll_mamba2_bwd_staged, ll_mamba2_bwd_workspace, ll_mamba2_decode_init, ll_mamba2_decode_step, ll_mamba2_fwd,
     ll_mamba2_fwd_grouped, ll_mamba2_fwd_staged, ll_num_levels, ll_status_string, ll_supported, ll_workspace_size,
+    log_linear_mamba2,
 )

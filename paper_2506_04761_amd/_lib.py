@@ -386,3 +386,47 @@ def ll_debug_level_map(T, C, stream=None):
     if st != LL_OK:
         raise LLError(st)
     return out
+
+
+# ----------------------------------------------------------------------- autograd
+
+def _autograd_function():
+    torch = _torch()
+
+    class LogLinearMamba2(torch.autograd.Function):
+        """O = log-linear Mamba-2 attention of (q, k, v, log_alpha, lam) as a differentiable op: the
+        forward runs ll_mamba2_fwd (ll_mamba2_fwd_grouped when q, k have fewer heads than v) in a
+        backward-sized workspace kept until the backward, which runs ll_mamba2_bwd_after_fwd on it
+        (the forward's level summaries are reused, not recomputed).  Memory held between the two:
+        ll_mamba2_bwd_workspace_size(...) bytes plus the saved inputs."""
+
+        @staticmethod
+        def forward(ctx, q, k, v, log_alpha, lam, C):
+            q, k, v, log_alpha, lam = (x.contiguous() for x in (q, k, v, log_alpha, lam))
+            ws = ll_mamba2_bwd_workspace(q, v, C)
+            fwd = ll_mamba2_fwd_grouped if q.shape[2] != v.shape[2] else ll_mamba2_fwd
+            o = fwd(q, k, v, log_alpha, lam, C, workspace=ws)
+            ctx.save_for_backward(q, k, v, log_alpha, lam)
+            ctx.ws, ctx.C = ws, C
+            return o
+
+        @staticmethod
+        def backward(ctx, d_o):
+            q, k, v, log_alpha, lam = ctx.saved_tensors
+            grads = ll_mamba2_bwd_after_fwd(q, k, v, log_alpha, lam, d_o.contiguous(), ctx.C, ctx.ws)
+            ctx.ws = None
+            return (*grads, None)
+
+    return LogLinearMamba2
+
+
+_LLM2 = None
+
+
+def log_linear_mamba2(q, k, v, log_alpha, lam, C):
+    """Differentiable log-linear Mamba-2 attention (see LogLinearMamba2): returns O [B, T, H, d_v];
+    gradients flow to q, k, v, log_alpha and lam.  lam is required (pass ones for Mamba-2)."""
+    global _LLM2
+    if _LLM2 is None:
+        _LLM2 = _autograd_function()
+    return _LLM2.apply(q, k, v, log_alpha, lam, C)

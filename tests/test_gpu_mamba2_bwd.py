@@ -182,3 +182,29 @@ def test_bwd_maximum_length_sampled():
     for n, e in errs.items():
         assert e <= TOL["bf16"], (n, e)
     assert np.all(np.isfinite(dla)) and np.max(np.abs(dla[:, 0])) <= TOL["bf16"] * np.max(np.abs(dla))
+
+
+@pytest.mark.parametrize("Hqk", [2, 1])
+def test_autograd_function_matches_the_entry_points(Hqk):
+    """log_linear_mamba2 under torch.autograd: the output equals ll_mamba2_fwd(_grouped) and the
+    gradients of sum(O * dO) equal the backward entry point's, bit for bit."""
+    import torch
+    import paper_2506_04761_amd as ll
+    from synthetic import shared_qk
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=1, H=2, T=64 * 21, dk=128, dv=64, seed=61,
+                                                   qk_heads=Hqk if Hqk < 2 else 0)
+    x = generate(w)
+    if w.qk_heads:
+        x["q"], x["k"] = shared_qk(x, w)
+    do = to_dev(upstream_grad(w), "bf16")
+    leaves = [to_dev(x[n], "bf16").requires_grad_() for n in ("q", "k", "v")]
+    leaves += [to_dev(x["log_alpha"]).requires_grad_(), to_dev(x["lam"]).requires_grad_()]
+    o = ll.log_linear_mamba2(*leaves, w.C)
+    (o.float() * do.float()).sum().backward()
+    plain = [t.detach() for t in leaves]
+    fwd = ll.ll_mamba2_fwd_grouped if w.qk_heads else ll.ll_mamba2_fwd
+    assert torch.equal(o.detach(), fwd(*plain, w.C))
+    ref = ll.ll_mamba2_bwd(*plain, do, w.C)
+    torch.cuda.synchronize()
+    for n, t, r in zip(NAMES, leaves, ref):
+        assert torch.equal(t.grad, r), n
