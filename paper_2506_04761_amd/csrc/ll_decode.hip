@@ -207,14 +207,31 @@ __global__ __launch_bounds__(kDecodeThreads) void k_gdn_decode_step(
       for (int i = 0; i < NPT; ++i) m[i] += src[i];
     }
     step_level(m, level_row(p + 1), p + 1);
-    // the other nonempty levels (bits above p of t) carry over, transitioned in place
-    for (int l = p + 2; l < L; ++l) {
-      if (!((t >> (l - 1)) & 1)) continue;
-      float* src = level_row(l);
-      float x[NPT];
+    // the other nonempty levels (bits above p of t) carry over, transitioned in place; their
+    // rows are loaded kBatch levels at a time before any is processed (independent loads)
+    constexpr int kBatch = 4;
+    int64_t rest = t >> (p + 1);  // bit i: level p + 2 + i is nonempty
+    int l0 = p + 2;
+    while (rest) {
+      int lv[kBatch];
+      int n = 0;
+      while (rest && n < kBatch) {
+        const int sh = __builtin_ctzll((unsigned long long)rest);
+        lv[n++] = l0 + sh;
+        rest >>= sh + 1;
+        l0 += sh + 1;
+      }
+      float x[kBatch][NPT];
 #pragma unroll
-      for (int i = 0; i < NPT; ++i) x[i] = src[i];
-      step_level(x, src, l);
+      for (int b = 0; b < kBatch; ++b)
+        if (b < n) {
+          const float* src = level_row(lv[b]);
+#pragma unroll
+          for (int i = 0; i < NPT; ++i) x[b][i] = src[i];
+        }
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b)
+        if (b < n) step_level(x[b], level_row(lv[b]), lv[b]);
     }
   }
   // level 0 = beta_t v_t k_t^T: its term is beta_t v_t[row] (k_t . q_t)
