@@ -14,7 +14,9 @@ import os
 import torch  # noqa: F401
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libloglinear.so")
+# LIBLOGLINEAR_PATH selects another build of the same sources (the host-sanitized one of
+# build.py --asan); by default the in-tree library is loaded.
+LIB_PATH = os.environ.get("LIBLOGLINEAR_PATH") or os.path.join(HERE, "libloglinear.so")
 
 LL_OK, LL_ERR_NULL_ARG, LL_ERR_BAD_SHAPE, LL_ERR_UNSUPPORTED, LL_ERR_WORKSPACE, LL_ERR_HIP = range(6)
 LL_F32, LL_BF16 = 0, 1

@@ -208,3 +208,37 @@ def test_autograd_function_matches_the_entry_points(Hqk):
     torch.cuda.synchronize()
     for n, t, r in zip(NAMES, leaves, ref):
         assert torch.equal(t.grad, r), n
+
+
+@pytest.mark.parametrize("dtype,C,dk,dv,H,Hqk,T", [
+    ("bf16", 64, 128, 128, 2, 2, 64 * 67),
+    ("bf16", 64, 128, 64, 4, 1, 64 * 19),
+    ("f32", 16, 16, 16, 2, 2, 64 * 19 - 16),
+])
+def test_bwd_deterministic_and_writes_every_output(dtype, C, dk, dv, H, Hqk, T):
+    """Two backward calls on the same inputs are equal bit for bit (no order-dependent
+    accumulation), and every gradient element is written: the gradients and the workspace start
+    as NaN bit patterns, so an element left unwritten, or computed from workspace bytes no kernel
+    wrote, shows up as NaN."""
+    import torch
+    import paper_2506_04761_amd as ll
+    from synthetic import shared_qk
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(dtype=dtype, B=1, H=H, T=T, dk=dk, dv=dv, C=C, seed=131,
+                                                   qk_heads=Hqk if Hqk < H else 0)
+    x = generate(w)
+    if w.qk_heads:
+        x["q"], x["k"] = shared_qk(x, w)
+    args = [to_dev(x[n], dtype) for n in ("q", "k", "v")]
+    args += [to_dev(x["log_alpha"]), to_dev(x["lam"]), to_dev(upstream_grad(w), dtype)]
+    outs = []
+    for _ in range(2):
+        ws = ll.ll_mamba2_bwd_workspace(args[0], args[2], C)
+        ws.fill_(255)
+        grads = tuple(torch.full_like(t, float("nan")) for t in (args[0], args[1], args[2], args[3], args[4]))
+        ll.ll_mamba2_bwd(*args, C, grads=grads, workspace=ws)
+        torch.cuda.synchronize()
+        for n, g in zip(NAMES, grads):
+            assert not torch.isnan(g).any(), n
+        outs.append([g.clone() for g in grads])
+    for n, a, b in zip(NAMES, *outs):
+        assert torch.equal(a, b), n
