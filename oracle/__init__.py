@@ -13,9 +13,11 @@ mamba2    log-linear Mamba-2: quadratic masked form, per-level recurrent form,
 mamba2_grad  gradients of log-linear Mamba-2 with respect to q, k, v, log alpha and lambda,
           from the quadratic form by the chain rule (full and sampled rows/columns)
 gdn       log-linear Gated DeltaNet: the same three forms              (Sec. 2 delta rule, Sec. 3.4)
+matrix_lambda  log-linear Mamba-2 with matrix-valued level weights Lambda_t^(l) (the 4D-tensor
+          view of App. A): quadratic, recurrent and brute-force forms
 
 Every function works on arrays laid out as [B, T, H, ...] (batch, time, head, feature),
 the layout of the paper's own PyTorch listing (App. C), and returns float64.
 """
 
-from . import fenwick, mamba2, mamba2_grad, gdn  # noqa: F401
+from . import fenwick, mamba2, mamba2_grad, gdn, matrix_lambda  # noqa: F401
