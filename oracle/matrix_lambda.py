@@ -38,28 +38,39 @@ def as_full(lam_diag):
     return lam_diag[..., :, None] * np.eye(d)
 
 
+def _is_diag(Lam, dk):
+    if Lam.ndim == 5 and Lam.shape[-1] == dk:
+        return True
+    if Lam.ndim == 6 and Lam.shape[-2:] == (dk, dk):
+        return False
+    raise ValueError("Lam must be [B, T, H, L, d_k] (diagonal) or [B, T, H, L, d_k, d_k] (full)")
+
+
 def _full(Lam, dk):
     Lam = np.asarray(Lam, dtype=np.float64)
-    if Lam.ndim == 5 and Lam.shape[-1] == dk:
-        return as_full(Lam)
-    if Lam.ndim == 6 and Lam.shape[-2:] == (dk, dk):
-        return Lam
-    raise ValueError("Lam must be [B, T, H, L, d_k] (diagonal) or [B, T, H, L, d_k, d_k] (full)")
+    return as_full(Lam) if _is_diag(Lam, dk) else Lam
+
+
+def _times_lambda(qv, lam, diag):
+    """q Lambda for row vectors qv [..., d_k] and matching weights lam ([..., d_k] diagonals, applied
+    as the elementwise product that q diag(lam) is, or [..., d_k, d_k] matrices)."""
+    lam = np.asarray(lam, dtype=np.float64)
+    return qv * lam if diag else np.einsum('...a,...ac->...c', qv, lam)
 
 
 def level_queries(q, Lam):
     """q_t Lambda_t^(l) for every (b, t, h, l): [B, T, H, L, d_k]."""
     q = np.asarray(q, dtype=np.float64)
-    F = _full(Lam, q.shape[-1])
-    return np.einsum('btha,bthlac->bthlc', q, F)
+    return _times_lambda(q[:, :, :, None, :], Lam, _is_diag(np.asarray(Lam), q.shape[-1]))
 
 
 def quadratic(q, k, v, log_alpha, Lam, rows=None):
     """The definition, level by level; with `rows` only those output rows ([B, len(rows), H, d_v])."""
     q, k, v, log_alpha = (np.asarray(x, dtype=np.float64) for x in (q, k, v, log_alpha))
     B, T, H, dk = q.shape
-    F = _full(Lam, dk)
-    if F.shape[3] < fenwick.num_levels(T):
+    Lam = np.asarray(Lam)
+    diag = _is_diag(Lam, dk)
+    if Lam.shape[3] < fenwick.num_levels(T):
         raise ValueError("Lam has fewer levels than the sequence needs")
     rows = np.arange(T) if rows is None else np.asarray(rows)
     lev = np.full((len(rows), T), -1, dtype=np.int64)        # l(t, s), -1 above the diagonal
@@ -76,7 +87,7 @@ def quadratic(q, k, v, log_alpha, Lam, rows=None):
                 sel = lev == l
                 if not sel.any():
                     continue
-                ql = np.einsum('ta,tac->tc', q[b, rows, h], F[b, rows, h, l])   # q_t Lambda_t^(l)
+                ql = _times_lambda(q[b, rows, h], Lam[b, rows, h, l], diag)   # q_t Lambda_t^(l)
                 scores = (ql @ k[b, :, h].T) * decay * sel
                 out[b, :, h] += scores @ v[b, :, h]
     return out
@@ -88,8 +99,9 @@ def recurrent(q, k, v, log_alpha, Lam):
     transformed query."""
     q, k, v, log_alpha = (np.asarray(x, dtype=np.float64) for x in (q, k, v, log_alpha))
     B, T, H, dk = q.shape
-    F = _full(Lam, dk)
-    L = F.shape[3]
+    Lam = np.asarray(Lam)
+    diag = _is_diag(Lam, dk)
+    L = Lam.shape[3]
     if L < fenwick.num_levels(T):
         raise ValueError("Lam has fewer levels than the sequence needs")
     S = np.zeros((B, H, L, v.shape[-1], dk))
@@ -102,7 +114,7 @@ def recurrent(q, k, v, log_alpha, Lam):
             S[:, :, p + 1] = merged
             S *= np.exp(log_alpha[:, t, :])[:, :, None, None, None]
         S[:, :, 0] = v[:, t, :, :, None] * k[:, t, :, None, :]
-        ql = np.einsum('bha,bhlac->bhlc', q[:, t], F[:, t])    # [B, H, L, d_k]
+        ql = _times_lambda(q[:, t, :, None, :], Lam[:, t], diag)    # [B, H, L, d_k]
         out[:, t] = np.einsum('bhlpc,bhlc->bhp', S, ql)
     return out
 
