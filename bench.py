@@ -221,6 +221,8 @@ def main():
         return main_decode(args, w, torch, ll)
     if w.variant == "mamba2_bwd":
         return main_bwd(args, w, torch, ll)
+    if w.variant == "mamba2_diag_lambda":
+        return main_mlambda(args, w, torch, ll)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
@@ -745,6 +747,116 @@ def main_gdn(args, w, torch, ll):
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+def lq_level_rows(T, R):
+    """Level-query rows the tile kernel needs with matrix-valued weights, summed over a sequence:
+    row t (tile u = t // R, tile-local index i) scores its pairs at level 0, at level b + 1 for
+    every set bit b of i, and at one inter-tile level per set bit of u."""
+    t = np.arange(T)
+    pc = lambda x: np.array([bin(int(y)).count("1") for y in x])
+    return int(np.sum(1 + pc(t % R) + pc(t // R)))
+
+
+def main_mlambda(args, w, torch, ll):
+    """Log-linear Mamba-2 with diagonal matrix-valued level weights (ll_mamba2_fwd_matrix_lambda).
+    One step = the level queries, the tile states, the scan and the tile outputs."""
+    from synthetic import level_weight_matrices
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    es = 2 if w.dtype == "bf16" else 4
+    x = generate(w)
+    d = {n: torch.from_numpy(x[n]).to(dev).to(dt).contiguous() for n in ("q", "k", "v")}
+    la = torch.from_numpy(x["log_alpha"]).to(dev)
+    Lam = torch.from_numpy(level_weight_matrices(w, "diag")).to(dev)
+    out = torch.empty((w.B, w.T, w.H, w.dv), dtype=dt, device=dev)
+    ws = ll.ll_mamba2_matrix_lambda_workspace(d["q"], d["v"], w.C)
+    stream = torch.cuda.current_stream()
+    names = ["level_queries", "block_state", "scan", "tile_out"]
+    K, W = args.steps, args.warmup
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(max(K, 1))]
+    print(f"[bench] {w.name}: warmup {W}, steps {K}", file=sys.stderr, flush=True)
+    for i in range(W):
+        ll.ll_mamba2_fwd_matrix_lambda_staged(d["q"], d["k"], d["v"], la, Lam, w.C, evs[i % K], out=out,
+                                              workspace=ws, stream=stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(K):
+        ll.ll_mamba2_fwd_matrix_lambda_staged(d["q"], d["k"], d["v"], la, Lam, w.C, evs[i], out=out,
+                                              workspace=ws, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    stage_ms = np.array([[e[s].elapsed_time(e[s + 1]) for s in range(4)] for e in evs[:K]]).mean(axis=0)
+    print(f"[bench] {ms:.3f} ms/step (stages {', '.join(f'{x:.3f}' for x in stage_ms)})", file=sys.stderr,
+          flush=True)
+
+    BHT, L = w.B * w.H * w.T, w.levels
+    R = max(2 * w.C, 64)
+    base = stage_figures(w)
+    lq_rows = w.B * w.H * lq_level_rows(w.T, R)
+    figs = {
+        # no kernel for diagonal weights
+        "level_queries": (0.0, 0.0),
+        "block_state": base["block_state"],
+        "scan": base["scan"],
+        # q, k, v and the log-gates read, the diagonals of the levels each row scores with read,
+        # o written; forming the level queries costs L d_k multiplies per row
+        "tile_out": (base["tile_out"][0] + BHT * L * w.dk,
+                     lq_rows * w.dk * 4 + BHT * ((2 * w.dk + 2 * w.dv) * es + 4)),
+    }
+    dom = int(np.argmax(stage_ms))
+    roof = roofline(w, *figs[names[dom]], stage_ms[dom])
+    F = flops_loglinear(w) + BHT * L * w.dk
+    tflops = F / (ms * 1e-3) / 1e12
+    alg_bytes = BHT * ((2 * w.dk + w.dv) * es + 4 + L * w.dk * 4 + w.dv * es)
+    res = {
+        "metric": "fwd tokens/sec, log-linear Mamba-2 with diagonal matrix-valued level weights",
+        "value": w.B * w.T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "variant": "log-linear Mamba-2, Lambda_t^(l) = diag(lambda_t^(l)) in R^d_k",
+                   "B": w.B, "H": w.H, "T": w.T, "d_k": w.dk, "d_v": w.dv, "C": w.C, "levels": L,
+                   "inputs": "bf16 q/k/v, fp32 log-gates and diagonal weights [B, T, H, L, d_k], seeded synthetic"},
+        "tflops": tflops,
+        "mfma_peak_frac": tflops / (PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS),
+        "flop_convention": "B*H*T*[2C(dk+dv) + 2dk*dv + dk*dv*log2(T/C)] + B*H*T*L*dk (level queries)",
+        "hbm_GBps_algorithmic": alg_bytes / (ms * 1e-3) / 1e9,
+        "stages_ms": dict(zip(names, [float(x) for x in stage_ms])),
+        "roofline": {"kernel": names[dom], **roof, "traffic": None,
+                     "traffic_note": "no counter record for this workload"},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import matrix_lambda
+        print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
+        xs = generate(w.with_(T=min(w.T, 4096)))
+        lam_h = level_weight_matrices(w.with_(T=min(w.T, 4096)), "diag")
+        T = 32
+        while True:
+            sl = slice(0, T)
+            t0, c0 = time.perf_counter(), time.process_time()
+            matrix_lambda.recurrent(xs["q"][:, sl], xs["k"][:, sl], xs["v"][:, sl], xs["log_alpha"][:, sl],
+                                    lam_h[:, sl])
+            wall, cpu = time.perf_counter() - t0, time.process_time() - c0
+            if wall >= args.cpu_budget / 2 or T >= xs["q"].shape[1]:
+                break
+            T *= 2
+        res["cpu_baseline"] = {
+            "value": w.B * T / wall, "unit": "tokens/s", "cores": max(1, round(cpu / wall)),
+            "host_cores_available": len(os.sched_getaffinity(0)), "kind": "oracle",
+            "sample": f"float64 per-level recurrent form with diagonal level weights, first {T} tokens of "
+                      f"all {w.H} heads, B={w.B}; {wall:.2f} s wall, {cpu:.2f} s CPU"}
     print(json.dumps(res), flush=True)
 
 

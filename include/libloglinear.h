@@ -111,6 +111,48 @@ ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, cons
                                void* workspace, size_t workspace_bytes, void* stream,
                                void* const* events);
 
+/* ---- Matrix-valued level weights (the 4D-tensor view of App. A) ------------------------------
+ *
+ * App. A writes a pair's score as q_t M[t,s] k_s^T with a d_k x d_k matrix per pair; log-linear
+ * Mamba-2 with matrix-valued weights takes M[t,s] = Lambda_t^(l(t,s)) prod_{r=s+1..t} alpha_r, so
+ *     O_t = sum_{s <= t} prod(alpha) (q_t Lambda_t^(l(t,s)) . k_s) v_s
+ * (q_t a row vector).  lambda_t^(l) I gives ll_mamba2_fwd.  Computed as ll_mamba2_fwd is, with the
+ * level queries q_t Lambda_t^(l), rounded once to the storage dtype, in place of q: each score tile
+ * uses the queries of its level.  Full matrices: the level queries are formed first, into the
+ * workspace; diagonal ones: the tile kernel scales its query fragments as it needs them.
+ *
+ * Lambda is float32, 16-byte aligned, in one of two layouts (lambda_form):
+ *   LL_LAMBDA_DIAG  [B, T, H, L, d_k]        Lambda_t^(l) = diag(Lambda[b, t, h, l, :]);
+ *   LL_LAMBDA_FULL  [B, T, H, L, d_k, d_k]   (Lambda_t^(l))_{a c} = Lambda[b, t, h, l, a, c].
+ * L = ll_num_levels(T).  Every (dtype, C, d_k, d_v) of ll_mamba2_fwd is supported; the query and
+ * key heads are not shared (H_qk = H).  The workspace is
+ * ll_mamba2_matrix_lambda_workspace_size(lambda_form, ...) bytes: the forward's summaries (the
+ * size ll_workspace_size gives with lambda), plus B * T * H * L * d_k level queries for full
+ * matrices; 0 for invalid arguments.  An unknown lambda_form or a misaligned Lambda gives
+ * LL_ERR_BAD_SHAPE; B * T * H * L >= 2^33 gives LL_ERR_UNSUPPORTED; otherwise as ll_mamba2_fwd. */
+typedef enum { LL_LAMBDA_DIAG = 0, LL_LAMBDA_FULL = 1 } ll_lambda_form;
+
+size_t ll_mamba2_matrix_lambda_workspace_size(int32_t lambda_form, int32_t dtype, int64_t B,
+                                              int64_t T, int64_t H, int64_t d_k, int64_t d_v,
+                                              int64_t C);
+
+ll_status ll_mamba2_fwd_matrix_lambda(const void* q, const void* k, const void* v,
+                                      const float* log_alpha, const float* Lambda,
+                                      int32_t lambda_form, void* o, int64_t B, int64_t T, int64_t H,
+                                      int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* As ll_mamba2_fwd_matrix_lambda, recording five caller-owned HIP events on `stream`: before the
+ * level queries (no kernel for diagonal weights), the tile states, the scan and the tile outputs,
+ * and after the tile outputs.
+ * events == NULL or any events[i] == NULL gives LL_ERR_NULL_ARG. */
+ll_status ll_mamba2_fwd_matrix_lambda_staged(const void* q, const void* k, const void* v,
+                                             const float* log_alpha, const float* Lambda,
+                                             int32_t lambda_form, void* o, int64_t B, int64_t T,
+                                             int64_t H, int64_t d_k, int64_t d_v, int64_t C,
+                                             int32_t dtype, void* workspace, size_t workspace_bytes,
+                                             void* stream, void* const* events);
+
 /* ---- Backward pass of log-linear Mamba-2 -----------------------------------------------------
  *
  * Gradients of the scalar sum(O (.) dO) for O = (Q K^T (.) M^S (.) M^H) V (Sec. 3.4), with respect

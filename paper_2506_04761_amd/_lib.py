@@ -21,6 +21,7 @@ LIB_PATH = os.environ.get("LIBLOGLINEAR_PATH") or os.path.join(HERE, "liblogline
 LL_OK, LL_ERR_NULL_ARG, LL_ERR_BAD_SHAPE, LL_ERR_UNSUPPORTED, LL_ERR_WORKSPACE, LL_ERR_HIP = range(6)
 LL_F32, LL_BF16 = 0, 1
 LL_MAMBA2, LL_GDN, LL_MAMBA2_BWD = 0, 1, 2
+LL_LAMBDA_DIAG, LL_LAMBDA_FULL = 0, 1
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(
@@ -57,6 +58,14 @@ lib.ll_gdn_decode_step.restype = _i32
 lib.ll_mamba2_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i32,
                                       _vp, _sz, _vp, ctypes.POINTER(_vp)]
 lib.ll_mamba2_fwd_staged.restype = _i32
+lib.ll_mamba2_matrix_lambda_workspace_size.argtypes = [_i32, _i32, _i64, _i64, _i64, _i64, _i64, _i64]
+lib.ll_mamba2_matrix_lambda_workspace_size.restype = _sz
+lib.ll_mamba2_fwd_matrix_lambda.argtypes = [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _i64, _i64, _i64, _i64, _i64, _i64,
+                                            _i32, _vp, _sz, _vp]
+lib.ll_mamba2_fwd_matrix_lambda.restype = _i32
+lib.ll_mamba2_fwd_matrix_lambda_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _i64, _i64, _i64, _i64, _i64,
+                                                   _i64, _i32, _vp, _sz, _vp, ctypes.POINTER(_vp)]
+lib.ll_mamba2_fwd_matrix_lambda_staged.restype = _i32
 lib.ll_gdn_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _sz, _vp]
 lib.ll_gdn_fwd.restype = _i32
 lib.ll_gdn_fwd_staged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _sz,
@@ -173,6 +182,62 @@ def ll_mamba2_fwd(q, k, v, log_alpha, lam, C, out=None, workspace=None, stream=N
     if st != LL_OK:
         raise LLError(st)
     return out
+
+
+def _ml_call(q, k, v, log_alpha, Lam, C, out, workspace, stream, handles):
+    torch = _torch()
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    _check(q, "q")
+    _check(k, "k", q.dtype, (B, T, H, dk))
+    _check(v, "v", q.dtype, (B, T, H, dv))
+    _check(log_alpha, "log_alpha", torch.float32, (B, T, H))
+    L = ll_num_levels(T)
+    if Lam.dim() == 5:
+        form = LL_LAMBDA_DIAG
+        _check(Lam, "Lambda", torch.float32, (B, T, H, L, dk))
+    else:
+        form = LL_LAMBDA_FULL
+        _check(Lam, "Lambda", torch.float32, (B, T, H, L, dk, dk))
+    code = _dtype_code(q)
+    if out is None:
+        out = torch.empty((B, T, H, dv), dtype=q.dtype, device=q.device)
+    _check(out, "out", q.dtype, (B, T, H, dv))
+    if workspace is None:
+        workspace = ll_mamba2_matrix_lambda_workspace(q, v, C, full=form == LL_LAMBDA_FULL)
+    _check(workspace, "workspace", torch.uint8)
+    args = [_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(Lam), form, _ptr(out), B, T, H, dk, dv, C, code,
+            _ptr(workspace), workspace.numel(), _stream(stream)]
+    st = (lib.ll_mamba2_fwd_matrix_lambda(*args) if handles is None
+          else lib.ll_mamba2_fwd_matrix_lambda_staged(*args, handles))
+    if st != LL_OK:
+        raise LLError(st)
+    return out
+
+
+def ll_mamba2_matrix_lambda_workspace(q, v, C, full=True):
+    """A workspace for ll_mamba2_fwd_matrix_lambda shaped for q [B, T, H, d_k] and v [B, T, H, d_v]
+    (full=True: for full matrices, which also serves diagonal ones)."""
+    torch = _torch()
+    B, T, H, dk = q.shape
+    form = LL_LAMBDA_FULL if full else LL_LAMBDA_DIAG
+    need = lib.ll_mamba2_matrix_lambda_workspace_size(form, _dtype_code(q), B, T, H, dk, v.shape[-1], C)
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+
+
+def ll_mamba2_fwd_matrix_lambda(q, k, v, log_alpha, Lam, C, out=None, workspace=None, stream=None):
+    """Log-linear Mamba-2 with matrix-valued level weights (the 4D-tensor view of App. A):
+    O_t = sum_{s<=t} prod(alpha) (q_t Lambda_t^(l(t,s)) . k_s) v_s.  `Lam` is float32, either
+    [B, T, H, L, d_k] (diagonal matrices) or [B, T, H, L, d_k, d_k] (full matrices).  Returns `out`;
+    enqueued on `stream` (default: torch's current stream), not synchronised."""
+    return _ml_call(q, k, v, log_alpha, Lam, C, out, workspace, stream, None)
+
+
+def ll_mamba2_fwd_matrix_lambda_staged(q, k, v, log_alpha, Lam, C, events, out=None, workspace=None, stream=None):
+    """As ll_mamba2_fwd_matrix_lambda, and records the five torch.cuda.Event objects in `events` around
+    the four stages (level queries, tile states, scan, tile outputs)."""
+    handles, s = _event_handles(events, 5, stream)
+    return _ml_call(q, k, v, log_alpha, Lam, C, out, workspace, s, handles)
 
 
 def ll_mamba2_fwd_grouped(q, k, v, log_alpha, lam, C, out=None, workspace=None, stream=None):

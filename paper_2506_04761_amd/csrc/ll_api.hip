@@ -72,6 +72,15 @@ size_t ll_workspace_size(int32_t variant, int32_t dtype, int64_t B, int64_t T, i
   return 0;
 }
 
+size_t ll_mamba2_matrix_lambda_workspace_size(int32_t lambda_form, int32_t dtype, int64_t B, int64_t T, int64_t H,
+                                              int64_t d_k, int64_t d_v, int64_t C) {
+  if (check_shape(B, T, H, d_k, d_v, C) != LL_OK) return 0;
+  if (dtype != LL_F32 && dtype != LL_BF16) return 0;
+  if (lambda_form != LL_LAMBDA_DIAG && lambda_form != LL_LAMBDA_FULL) return 0;
+  return (size_t)ll::mamba2_ml_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), levels_of(T),
+                                         lambda_form == LL_LAMBDA_FULL, nullptr);
+}
+
 size_t ll_mamba2_bwd_workspace_size(int32_t dtype, int64_t B, int64_t T, int64_t H, int64_t H_qk, int64_t d_k,
                                     int64_t d_v, int64_t C) {
   if (check_shape(B, T, H, d_k, d_v, C) != LL_OK) return 0;
@@ -125,6 +134,41 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   if (events)
     for (int i = 0; i <= ll::kMamba2Stages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);
   const hipError_t err = e->launch(a, hs, events ? ev : nullptr);
+  return err == hipSuccess ? LL_OK : LL_ERR_HIP;
+}
+ll_status mamba2_ml_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* Lambda,
+                         int32_t form, void* o, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C,
+                         int32_t dtype, void* workspace, size_t workspace_bytes, void* stream, void* const* events) {
+  if (!q || !k || !v || !log_alpha || !Lambda || !o) return LL_ERR_NULL_ARG;
+  ll_status st = check_shape(B, T, H, d_k, d_v, C);
+  if (st != LL_OK) return st;
+  if (form != LL_LAMBDA_DIAG && form != LL_LAMBDA_FULL) return LL_ERR_BAD_SHAPE;
+  if (reinterpret_cast<uintptr_t>(Lambda) & 15) return LL_ERR_BAD_SHAPE;
+  if (dtype != LL_F32 && dtype != LL_BF16) return LL_ERR_UNSUPPORTED;
+  const ll::KernelEntry* e = find_mamba2(dtype, C, d_k, d_v);
+  if (!e) return LL_ERR_UNSUPPORTED;
+  const int L = levels_of(T);
+  const int64_t tiles = ll::tiles_of(T, C);
+  // the tile grid and the scan grid as in the forward; one wave per (row, level) for full matrices
+  if (L > kMaxL || tiles > kMaxTiles || B * H > 65535 || tiles * 2 * H * B >= (int64_t(1) << 31) ||
+      B * T * H * L / 4 >= (int64_t(1) << 31))
+    return LL_ERR_UNSUPPORTED;
+  const int64_t need =
+      ll::mamba2_ml_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), L, form == LL_LAMBDA_FULL, nullptr);
+  if (!workspace) return LL_ERR_NULL_ARG;
+  if ((int64_t)workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
+  ll::Mamba2Args a;
+  a.q = q; a.k = k; a.v = v; a.log_alpha = log_alpha; a.lambda = nullptr; a.o = o;
+  a.B = B; a.T = T; a.H = H; a.dk = d_k; a.dv = d_v; a.C = C;
+  a.Hqk = H;
+  a.L = L;
+  a.workspace = workspace;
+  a.lambda_matrix = Lambda;
+  a.lambda_full = form == LL_LAMBDA_FULL;
+  hipEvent_t ev[ll::kMamba2MlStages + 1];
+  if (events)
+    for (int i = 0; i <= ll::kMamba2MlStages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);
+  const hipError_t err = e->launch_ml(a, static_cast<hipStream_t>(stream), events ? ev : nullptr);
   return err == hipSuccess ? LL_OK : LL_ERR_HIP;
 }
 ll_status mamba2_bwd_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
@@ -218,6 +262,26 @@ ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, cons
     if (!events[i]) return LL_ERR_NULL_ARG;
   return mamba2_impl(q, k, v, log_alpha, lambda, o, B, T, H, H_qk, d_k, d_v, C, dtype, workspace, workspace_bytes,
                      stream, events);
+}
+
+ll_status ll_mamba2_fwd_matrix_lambda(const void* q, const void* k, const void* v, const float* log_alpha,
+                                      const float* Lambda, int32_t lambda_form, void* o, int64_t B, int64_t T,
+                                      int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  return mamba2_ml_impl(q, k, v, log_alpha, Lambda, lambda_form, o, B, T, H, d_k, d_v, C, dtype, workspace,
+                        workspace_bytes, stream, nullptr);
+}
+
+ll_status ll_mamba2_fwd_matrix_lambda_staged(const void* q, const void* k, const void* v, const float* log_alpha,
+                                             const float* Lambda, int32_t lambda_form, void* o, int64_t B, int64_t T,
+                                             int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
+                                             void* workspace, size_t workspace_bytes, void* stream,
+                                             void* const* events) {
+  if (!events) return LL_ERR_NULL_ARG;
+  for (int i = 0; i <= ll::kMamba2MlStages; ++i)
+    if (!events[i]) return LL_ERR_NULL_ARG;
+  return mamba2_ml_impl(q, k, v, log_alpha, Lambda, lambda_form, o, B, T, H, d_k, d_v, C, dtype, workspace,
+                        workspace_bytes, stream, events);
 }
 
 ll_status ll_mamba2_bwd(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,

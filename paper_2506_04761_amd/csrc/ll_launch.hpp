@@ -36,16 +36,27 @@ struct Mamba2Args {
   int64_t Hqk;          // query/key heads (H % Hqk == 0; head h uses query/key head h / (H / Hqk))
   int L;                // Fenwick levels of T
   void* workspace;      // at least mamba2_workspace(...) bytes, 256-byte aligned
+  // matrix-valued level weights (launch_ml only): [B, T, H, L, dk] diagonals or, with
+  // lambda_full, [B, T, H, L, dk, dk] matrices; the workspace is mamba2_ml_workspace(...) bytes
+  const float* lambda_matrix = nullptr;
+  bool lambda_full = false;
 };
 
 typedef hipError_t (*Mamba2Launch)(const Mamba2Args&, hipStream_t, hipEvent_t* /* null or 4 events */);
 constexpr int kMamba2Stages = 3;
+constexpr int kMamba2MlStages = 4;  // level queries, block_state, level scan, tile_out
 
 struct KernelEntry {
   int dtype;  // 0 = fp32, 1 = bf16
   int C, dk, dv;
   Mamba2Launch launch;
+  Mamba2Launch launch_ml;  // matrix-valued level weights (null or 5 events)
 };
+
+// Workspace of the matrix-valued-weight forward: the Fenwick summaries' layout, then (full
+// matrices only) the level queries [B, T, H, L, dk] at *qlev_offset; returns the total byte count.
+int64_t mamba2_ml_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, int64_t esize,
+                            int L, bool full, int64_t* qlev_offset);
 
 const KernelEntry* mamba2_table(int* n);
 

@@ -24,6 +24,7 @@
 // Decays are kept in the log2 domain (gates pre-multiplied by log2 e) and every exp2 argument
 // is <= 0: tile-local cumulative sums and exact range sums of tile totals, never differences of
 // sequence-long prefix sums.
+#include <algorithm>
 #include <type_traits>
 
 #include "ll_mamba2_common.hpp"
@@ -431,8 +432,17 @@ struct RowMap {
   }
 };
 
-template <typename T, int C, int DK, int DV, bool HAS_LAMBDA>
-__global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
+// Matrix-valued level weights (the 4D-tensor view of App. A), LQ != 0: every 16 x 16 score tile
+// is formed with the queries q_t Lambda_t^(l) of its own level -- one level for an off-diagonal
+// key tile, levels 0-4 (selected per element) on the diagonal one, level log2 R + j for
+// inter-tile level j -- and the scalar weights are 1.
+//   LQ = 1: `q` holds those level queries, laid out [B, T, H, L, DK] (formed beforehand);
+//   LQ = 2: diagonal Lambda: `q` is the plain query and `lam` the diagonals [B, T, H, L, DK]; the
+//           level's query fragment is q (.) diag, rounded to T, formed in registers.
+// Both read the Fenwick summaries (HAS_LAMBDA) and need H_qk = H.
+// (the level-query forms hold a second query fragment set: two waves per SIMD, 256 registers)
+template <typename T, int C, int DK, int DV, bool HAS_LAMBDA, int LQ = 0>
+__global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, LQ ? 2 : 4) void k_tile_out(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ log_alpha,
     const float* __restrict__ lam, Nodes<T> nodes, const T* __restrict__ running, T* __restrict__ o, int64_t Tlen,
     int H, int Hqk, int L, int J) {
@@ -454,7 +464,9 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
   __shared__ T buf_s[KV_ELEMS > U_ELEMS ? KV_ELEMS : U_ELEMS];
   __shared__ float cl_s[R];
   __shared__ float wsum_s[4];
-  __shared__ float lam_s[HAS_LAMBDA ? ROWS * kMaxLevels : 1];  // row 16 * wave + r16 of this workgroup
+  static_assert(LQ == 0 || HAS_LAMBDA, "level queries read the Fenwick summaries");
+  constexpr bool STAGE_LAMBDA = HAS_LAMBDA && LQ == 0;
+  __shared__ float lam_s[STAGE_LAMBDA ? ROWS * kMaxLevels : 1];  // row 16 * wave + r16 of this workgroup
   __shared__ float kdec_s[R];
   T* k_s = buf_s;
   T* v_s = buf_s + kKB * LDK;
@@ -481,14 +493,46 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
   vr.load(v, row0, 0, nrow, H, h);
   const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);  // issued with the other loads
 
-  // Q^T fragments (B operand) of this lane's row, kept in registers.
-  typename M::frag qf[KS];
+  // Q^T fragments (B operand) of this lane's row, kept in registers (LQ: of one level at a time,
+  // qlev naming it; LQ = 2 keeps the plain query in qbase).
+  typename M::frag qf[KS], qbase[LQ == 2 ? KS : 1];
+  int qlev = 0;
+  auto load_q = [&](int l) {
+    if constexpr (LQ == 2) {
+      const float* wsrc = lam + (((row0 + i) * H + h) * L + l) * DK + g * M::KPL;
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    if (i < nrow) qf[ks] = M::load(q + ((row0 + i) * Hqk + hq) * DK + ks * M::KSTEP + g * M::KPL);
-    else qf[ks] = typename M::frag{};
+      for (int ks = 0; ks < KS; ++ks) {
+        typename M::frag f{};
+        if (i < nrow) {
+          if constexpr (M::KPL == 8) {
+            const f32x4 w0 = *reinterpret_cast<const f32x4*>(wsrc + ks * M::KSTEP);
+            const f32x4 w1 = *reinterpret_cast<const f32x4*>(wsrc + ks * M::KSTEP + 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              f[e] = from_f32<T>(to_f32(qbase[ks][e]) * w0[e]);
+              f[4 + e] = from_f32<T>(to_f32(qbase[ks][4 + e]) * w1[e]);
+            }
+          } else {
+            f = from_f32<T>(to_f32(qbase[ks]) * wsrc[ks * M::KSTEP]);
+          }
+        }
+        qf[ks] = f;
+      }
+    } else {
+      const T* src = LQ == 1 ? q + (((row0 + i) * H + h) * L + l) * DK : q + ((row0 + i) * Hqk + hq) * DK;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        qf[ks] = i < nrow ? M::load(src + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
+    }
+    qlev = l;
+  };
+  if constexpr (LQ == 2) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qbase[ks] = i < nrow ? M::load(q + ((row0 + i) * H + h) * DK + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
   }
-  if constexpr (HAS_LAMBDA) {
+  load_q(0);
+  if constexpr (STAGE_LAMBDA) {
     // one row of lambda per thread of the first ROWS threads, loads issued before the stores
     if (tid < ROWS) {
       const int row = 16 * RM::group(c, tid >> 4) + (tid & 15);
@@ -510,7 +554,7 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
   tile_cumsum_of<R>(la, nrow, cl_s, wsum_s);
   // key-side decay to the end of each 16-key tile: kdec[j] = exp2(cl[j | 15] - cl[j])
   for (int r = tid; r < R; r += NT) kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
-  const float* lrow = &lam_s[(16 * wave + r16) * L];  // this lane's lambda row
+  const float* lrow = STAGE_LAMBDA ? &lam_s[(16 * wave + r16) * L] : lam_s;  // this lane's lambda row
 
   // ---- summaries of the inter-tile levels (set bits of u); the first one is prefetched while
   //      the last key block is being used, each next one while the current level is
@@ -576,14 +620,44 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
         p[hh] = f32x4{0.f, 0.f, 0.f, 0.f};
         if (KT > gi) continue;
         f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+        auto scores = [&]() {
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          sacc = M::mma(M::load(&k_s[(kt * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]), qf[ks], sacc);
+          for (int ks = 0; ks < KS; ++ks)
+            acc = M::mma(M::load(&k_s[(kt * 16 + r16) * LDK + ks * M::KSTEP + g * M::KPL]), qf[ks], acc);
+          return acc;
+        };
+        if constexpr (LQ != 0) {
+          if (KT < gi) {
+            const int lv = level_local(16 * gi, 16 * KT);
+            if (lv != qlev) load_q(lv);
+            sacc = scores();
+          } else {
+            // diagonal 16 x 16 tile: pairs at levels 0-4, each scored with its level's queries
+            f32x4 sl[5];
+#pragma unroll
+            for (int l = 0; l < 5; ++l) {
+              load_q(l);
+              sl[l] = scores();
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int j = 16 * KT + 4 * g + r, lv = level_local(i, j);
+              float x = 0.f;
+#pragma unroll
+              for (int l = 0; l < 5; ++l) x = lv == l ? sl[l][r] : x;
+              p[hh][r] = j <= i ? x * fast_exp2(cli - cl_s[j]) : 0.f;
+            }
+            continue;
+          }
+        } else {
+          sacc = scores();
+        }
         if (KT < gi) {
           // off-diagonal 16x16 tile: one level for the whole tile (4 + bitlen(gi ^ KT)) and the
           // decay split at the tile's last key: exp2(cl_i - cl_end) * exp2(cl_end - cl_j)
           float qs = fast_exp2(cli - cl_s[16 * KT + 15]);
-          if constexpr (HAS_LAMBDA) qs *= lrow[level_local(16 * gi, 16 * KT)];
+          if constexpr (STAGE_LAMBDA) qs *= lrow[level_local(16 * gi, 16 * KT)];
           const f32x4 kd = *reinterpret_cast<const f32x4*>(&kdec_s[16 * KT + 4 * g]);
 #pragma unroll
           for (int r = 0; r < 4; ++r) p[hh][r] = sacc[r] * qs * kd[r];
@@ -594,7 +668,7 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
             float w = 0.f;
             if (j <= i) {
               w = fast_exp2(cli - cl_s[j]);
-              if constexpr (HAS_LAMBDA) w *= lrow[level_local(i, j)];
+              if constexpr (STAGE_LAMBDA) w *= lrow[level_local(i, j)];
             }
             p[hh][r] = sacc[r] * w;
           }
@@ -638,7 +712,8 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, 4) void k_tile_out(
     float gap_n = 0.f;
     if (jn) load_u(level_src(jn, &gap_n));
     float w = fast_exp2(cl_s[i] + gap);
-    if constexpr (HAS_LAMBDA) w *= (i < nrow) ? lrow[LOG2R + j] : 0.f;
+    if constexpr (STAGE_LAMBDA) w *= (i < nrow) ? lrow[LOG2R + j] : 0.f;
+    if constexpr (LQ != 0) load_q(LOG2R + j);  // rows past the end load zeros
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
@@ -976,6 +1051,54 @@ __global__ void k_debug_level_map(int64_t Tlen, int R, int log2R, int J, int8_t*
 }
 
 // ---------------------------------------------------------------------------------------------
+// Level queries for full matrix-valued level weights (App. A): qlev[row, l, :] = q[row, :] Lambda
+// with Lambda = lam[row, l] (laid out [rows, L, DK, DK], (q Lambda)_c = sum_a q_a lam[row, l, a, c])
+// for every row (b, t, h) and level l < L, rounded once to the storage type.  One wave per
+// (row, level): lane c accumulates columns c and c + 64, each step a reading one coalesced row of
+// Lambda, with q_a broadcast from the lane that loaded it.  (Diagonal weights need no such pass:
+// the tile kernel scales its query fragments in registers.)
+// ---------------------------------------------------------------------------------------------
+constexpr int kLevelQueryThreads = 256;
+
+template <typename T, int DK>
+__global__ __launch_bounds__(kLevelQueryThreads) void k_level_queries_full(const T* __restrict__ q,
+                                                                           const float* __restrict__ lam,
+                                                                           T* __restrict__ qlev, int64_t rows, int L) {
+  constexpr int CPL = (DK + 63) / 64;  // columns (and q entries) per lane
+  const int lane = threadIdx.x & 63;
+  const int64_t rl = blockIdx.x * (int64_t)(kLevelQueryThreads / 64) + (threadIdx.x >> 6);
+  if (rl >= rows * L) return;  // whole waves leave together
+  const int64_t row = rl / L;
+  float qa[CPL], acc[CPL];
+#pragma unroll
+  for (int e = 0; e < CPL; ++e) {
+    const int a = lane + 64 * e;
+    qa[e] = a < DK ? to_f32(q[row * DK + a]) : 0.f;
+    acc[e] = 0.f;
+  }
+  const float* m = lam + rl * DK * DK;
+  constexpr int AN = DK < 64 ? DK : 64;  // q entries held per lane slot
+#pragma unroll
+  for (int ea = 0; ea < CPL; ++ea) {
+#pragma unroll 4
+    for (int a0 = 0; a0 < AN; ++a0) {
+      const int a = 64 * ea + a0;
+      const float qv = __shfl(qa[ea], a0, 64);
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) {
+        const int c = lane + 64 * e;
+        if (c < DK) acc[e] += qv * m[a * DK + c];
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < CPL; ++e) {
+    const int c = lane + 64 * e;
+    if (c < DK) qlev[rl * DK + c] = from_f32<T>(acc[e]);
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------------------------
 static int bitlen_h(uint64_t x) { return x ? 64 - __builtin_clzll(x) : 0; }
@@ -1102,6 +1225,51 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
   return hipGetLastError();
 }
 
+int64_t mamba2_ml_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, int64_t esize,
+                            int L, bool full, int64_t* qlev_offset) {
+  const int64_t fwd = mamba2_workspace(B, T, H, dk, dv, C, esize, true, nullptr);
+  if (!full) return fwd;
+  const int64_t base = (fwd + 255) & ~int64_t(255);
+  if (qlev_offset) *qlev_offset = base;
+  return base + B * T * H * L * dk * esize;
+}
+
+// Matrix-valued level weights: for full matrices the level queries go into the workspace (after
+// the Fenwick summaries' regions) first; then the summaries and the tile outputs with per-level
+// queries.  Events (optional, 5): before the level queries (an empty stage for diagonal weights),
+// block_state, the level scan and tile_out, and after tile_out.
+template <typename T, int C, int DK, int DV>
+hipError_t launch_mamba2_ml(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
+  WsLayout w;
+  mamba2_workspace(a.B, a.T, a.H, DK, DV, C, sizeof(T), true, &w);
+  int64_t qoff = 0;
+  mamba2_ml_workspace(a.B, a.T, a.H, DK, DV, C, sizeof(T), a.L, a.lambda_full, &qoff);
+  const Nodes<T> nodes = mamba2_nodes<T>(w, a.workspace, true);
+  T* qlev = reinterpret_cast<T*>(static_cast<char*>(a.workspace) + qoff);
+  const int64_t rows = a.B * a.T * a.H;
+  if (ev) (void)hipEventRecord(ev[0], st);
+  if (a.lambda_full) {
+    const int64_t nblk = (rows * a.L + kLevelQueryThreads / 64 - 1) / (kLevelQueryThreads / 64);
+    hipLaunchKernelGGL((k_level_queries_full<T, DK>), dim3((unsigned)nblk), dim3(kLevelQueryThreads), 0, st,
+                       (const T*)a.q, a.lambda_matrix, qlev, rows, a.L);
+  }
+  if (ev) (void)hipEventRecord(ev[1], st);
+  hipError_t e = launch_mamba2_summaries<T, C, DK, DV>(a, w, nodes, st, ev ? ev[2] : nullptr);
+  if (e != hipSuccess) return e;
+  if (ev) (void)hipEventRecord(ev[3], st);
+  const dim3 gtile((unsigned)(w.N * RowMap<tile_rows(C)>::RS * a.H * a.B));
+  if (a.lambda_full)
+    hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, true, 1>), gtile, dim3(RowMap<tile_rows(C)>::NT), 0, st,
+                       (const T*)qlev, (const T*)a.k, (const T*)a.v, a.log_alpha, (const float*)nullptr, nodes,
+                       (const T*)nullptr, (T*)a.o, a.T, (int)a.H, (int)a.H, a.L, w.J);
+  else
+    hipLaunchKernelGGL((k_tile_out<T, C, DK, DV, true, 2>), gtile, dim3(RowMap<tile_rows(C)>::NT), 0, st,
+                       (const T*)a.q, (const T*)a.k, (const T*)a.v, a.log_alpha, a.lambda_matrix, nodes,
+                       (const T*)nullptr, (T*)a.o, a.T, (int)a.H, (int)a.H, a.L, w.J);
+  if (ev) (void)hipEventRecord(ev[4], st);
+  return hipGetLastError();
+}
+
 hipError_t launch_debug_level_map(int64_t T, int64_t C, int8_t* out, hipStream_t st) {
   const int R = tile_rows((int)C);
   hipLaunchKernelGGL(k_debug_level_map, dim3((unsigned)T), dim3(256), 0, st, T, R, bitlen_h(uint64_t(R)) - 1,
@@ -1116,7 +1284,8 @@ LL_MAMBA2_SHAPES(LL_SUMMARIES_INST)
 #undef LL_SUMMARIES_INST
 
 const KernelEntry* mamba2_table(int* n) {
-#define LL_ENTRY(T, C, DK, DV) {std::is_same<T, float>::value ? 0 : 1, C, DK, DV, &launch_mamba2<T, C, DK, DV>},
+#define LL_ENTRY(T, C, DK, DV) \
+  {std::is_same<T, float>::value ? 0 : 1, C, DK, DV, &launch_mamba2<T, C, DK, DV>, &launch_mamba2_ml<T, C, DK, DV>},
   static const KernelEntry table[] = {LL_MAMBA2_SHAPES(LL_ENTRY)};
 #undef LL_ENTRY
   *n = sizeof(table) / sizeof(table[0]);

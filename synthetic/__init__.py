@@ -5,4 +5,5 @@ standard normals in a fixed order, applies the input transforms of each workload
 Both the float64 oracle and the GPU library receive exactly the arrays returned here.
 """
 
-from .gen import WORKLOADS, Workload, generate, shared_qk, to_storage, upstream_grad  # noqa: F401
+from .gen import (WORKLOADS, Workload, generate, level_weight_matrices, shared_qk, to_storage,  # noqa: F401
+                  upstream_grad)

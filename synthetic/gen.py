@@ -27,7 +27,8 @@ import numpy as np
 @dataclass(frozen=True)
 class Workload:
     name: str
-    variant: str      # "mamba2", "gdn", "mamba2_bwd" (backward pass), "decode" or "gdn_decode" (decoding)
+    variant: str      # "mamba2", "gdn", "mamba2_bwd" (backward pass), "decode" or "gdn_decode" (decoding),
+                      # "mamba2_diag_lambda" (matrix-valued level weights, diagonal)
     dtype: str        # "f32" or "bf16": storage dtype of q, k, v and o
     B: int
     H: int
@@ -66,6 +67,9 @@ WORKLOADS = {
         Workload("ll_mamba2_bwd_bf16_T65536", "mamba2_bwd", "bf16", 1, 16, 65536, 128, 128, 64, 4, "unit"),
         Workload("ll_gdn_decode_bf16_T8192", "gdn_decode", "bf16", 64, 16, 8192, 128, 128, 64, 8, "gdn"),
         Workload("ll_mamba2_decode_bf16_T8192", "decode", "bf16", 64, 16, 8192, 128, 128, 64, 7, "unit"),
+        # matrix-valued level weights (diagonal Lambda_t^(l), see level_weight_matrices)
+        Workload("ll_mamba2_diag_lambda_bf16_T8192", "mamba2_diag_lambda", "bf16", 1, 16, 8192, 128, 128, 64, 9,
+                 "unit"),
     ]
 }
 
@@ -147,3 +151,32 @@ def upstream_grad(w: Workload, T: int = None, heads=None):
     if T is not None or heads is not None:
         do = np.ascontiguousarray(do[:, :w.T if T is None else T][:, :, slice(None) if heads is None else heads])
     return do
+
+
+def level_weight_matrices(w: Workload, form: str, T: int = None, heads=None) -> np.ndarray:
+    """Matrix-valued level weights Lambda_t^(l) for workload w, float32.  Drawn from their own
+    stream, torch's CPU generator seeded w.seed + 2000 (these arrays are large; the other inputs
+    do not change), standard normals in row-major order, then:
+      "diag"  [B, T, H, L, d_k]        softplus(x), the distribution of the scalar weights;
+      "full"  [B, T, H, L, d_k, d_k]   x / sqrt(d_k), plus softplus(y) on the diagonal from a
+                                       second draw y [B, T, H, L, d_k] (a perturbed positive
+                                       diagonal).
+    `T` and `heads` select a prefix and a subset of heads of the full draw, as in generate()."""
+    import torch
+    g = torch.Generator().manual_seed(w.seed + 2000)
+    B, TT, H, dk, L = w.B, w.T, w.H, w.dk, w.levels
+    zero = torch.zeros((), dtype=torch.float32)
+    if form == "diag":
+        lam = torch.logaddexp(zero, torch.randn((B, TT, H, L, dk), generator=g, dtype=torch.float32))
+    elif form == "full":
+        lam = torch.randn((B, TT, H, L, dk, dk), generator=g, dtype=torch.float32) / math.sqrt(dk)
+        d = torch.logaddexp(zero, torch.randn((B, TT, H, L, dk), generator=g, dtype=torch.float32))
+        lam.diagonal(dim1=-2, dim2=-1).add_(d)
+    else:
+        raise ValueError(form)
+    lam = lam.numpy()
+    if T is not None or heads is not None:
+        T = TT if T is None else T
+        Lt = 1 if T == 1 else (T - 1).bit_length() + 1
+        lam = lam[:, :T][:, :, slice(None) if heads is None else heads][:, :, :, :Lt]
+    return np.ascontiguousarray(lam)

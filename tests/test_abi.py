@@ -213,3 +213,41 @@ def test_debug_level_map_checks():
 def test_status_strings():
     for s in range(6):
         assert ll.ll_status_string(s).startswith("LL_")
+
+
+def _ml(lam=FAKE, form=0, T=128, dk=64, dv=64, C=64, dtype=1, ws=FAKE, wsb=1 << 40, staged=False, ev=None, B=1, H=2):
+    args = [FAKE, FAKE, FAKE, FAKE, lam, form, FAKE, B, T, H, dk, dv, C, dtype, ws, wsb, None]
+    if staged:
+        return lib.ll_mamba2_fwd_matrix_lambda_staged(*args, ev)
+    return lib.ll_mamba2_fwd_matrix_lambda(*args)
+
+
+def test_matrix_lambda_argument_checks_return_before_launch():
+    assert _ml(lam=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _ml(ws=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _ml(form=2) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _ml(lam=ctypes.c_void_p(4096 + 4)) == ll._lib.LL_ERR_BAD_SHAPE   # Lambda must be 16-byte aligned
+    assert _ml(T=100) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _ml(dk=96) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _ml(dtype=7) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _ml(B=300, H=300) == ll._lib.LL_ERR_UNSUPPORTED
+    assert _ml(wsb=1000) == ll._lib.LL_ERR_WORKSPACE
+    assert _ml(ws=ctypes.c_void_p(4096 + 8)) == ll._lib.LL_ERR_WORKSPACE
+    assert _ml(staged=True, ev=None) == ll._lib.LL_ERR_NULL_ARG
+    five_nulls = (ctypes.c_void_p * 5)()
+    assert _ml(staged=True, ev=five_nulls) == ll._lib.LL_ERR_NULL_ARG
+
+
+def test_matrix_lambda_workspace_size():
+    ws = lib.ll_mamba2_matrix_lambda_workspace_size
+    for dtype, esize, C, dk, dv in ((ll.LL_F32, 4, 16, 16, 16), (ll.LL_BF16, 2, 64, 128, 128)):
+        B, T, H = 2, 4096, 3
+        L = ll.ll_num_levels(T)
+        fwd = ll.ll_workspace_size(ll.LL_MAMBA2, dtype, B, T, H, dk, dv, C, 1)
+        # full matrices: the forward's summaries (rounded up to 256 bytes), then the level queries;
+        # diagonal ones: the forward's summaries only
+        assert ws(ll.LL_LAMBDA_FULL, dtype, B, T, H, dk, dv, C) == (fwd + 255) // 256 * 256 + B * T * H * L * dk * esize
+        assert ws(ll.LL_LAMBDA_DIAG, dtype, B, T, H, dk, dv, C) == fwd
+    assert ws(ll.LL_LAMBDA_FULL, ll.LL_BF16, 1, 100, 1, 64, 64, 64) == 0
+    assert ws(ll.LL_LAMBDA_FULL, 9, 1, 128, 1, 64, 64, 64) == 0
+    assert ws(2, ll.LL_BF16, 1, 128, 1, 64, 64, 64) == 0
