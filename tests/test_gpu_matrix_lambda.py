@@ -45,7 +45,7 @@ def _case(dtype, C, dk, dv, T, H, seed, dist="unit"):
 
 @pytest.mark.parametrize("form", ["diag", "full"])
 @pytest.mark.parametrize("dtype,C,dk,dv,T", [
-    ("f32", 16, 16, 16, 16 * 13),      # tiles of 32 rows: 6 full tiles and a half one
+    ("f32", 16, 16, 16, 16 * 13),      # tiles of 64 rows: 3 full tiles and a quarter of one
     ("f32", 64, 64, 64, 64 * 5),       # tiles of 128 rows, ragged last tile
     ("bf16", 64, 64, 64, 64 * 7),
     ("bf16", 64, 128, 64, 64 * 5),
