@@ -494,44 +494,81 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, LQ ? 2 : 4) void k_tile_o
   const float la = tile_gate<R>(log_alpha, row0, nrow, H, h);  // issued with the other loads
 
   // Q^T fragments (B operand) of this lane's row, kept in registers (LQ: of one level at a time,
-  // qlev naming it; LQ = 2 keeps the plain query in qbase).
-  typename M::frag qf[KS], qbase[LQ == 2 ? KS : 1];
+  // qlev naming it; LQ = 2 keeps the plain query in qbase).  With LQ, a level's data is fetched
+  // (fetch_q: LQ = 1 the level-query fragments, LQ = 2 the diagonal's entries of this lane's k
+  // slots, zeros for rows past the end) and then turned into qf (form_q), so that the inter-tile
+  // loop can fetch the next level while the current one runs.
+  typename M::frag qf[KS], qbase[LQ == 2 ? KS : 1], qraw[LQ == 1 ? KS : 1];
+  float wraw[LQ == 2 ? KS * M::KPL : 1];
   int qlev = 0;
-  auto load_q = [&](int l) {
+  auto fetch_q = [&](int l) {
     if constexpr (LQ == 2) {
       const float* wsrc = lam + (((row0 + i) * H + h) * L + l) * DK + g * M::KPL;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        typename M::frag f{};
-        if (i < nrow) {
-          if constexpr (M::KPL == 8) {
-            const f32x4 w0 = *reinterpret_cast<const f32x4*>(wsrc + ks * M::KSTEP);
-            const f32x4 w1 = *reinterpret_cast<const f32x4*>(wsrc + ks * M::KSTEP + 4);
+        if constexpr (M::KPL == 8) {
+          const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
+          const f32x4 w0 = i < nrow ? *reinterpret_cast<const f32x4*>(wsrc + ks * M::KSTEP) : z4;
+          const f32x4 w1 = i < nrow ? *reinterpret_cast<const f32x4*>(wsrc + ks * M::KSTEP + 4) : z4;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              f[e] = from_f32<T>(to_f32(qbase[ks][e]) * w0[e]);
-              f[4 + e] = from_f32<T>(to_f32(qbase[ks][4 + e]) * w1[e]);
-            }
-          } else {
-            f = from_f32<T>(to_f32(qbase[ks]) * wsrc[ks * M::KSTEP]);
+          for (int e = 0; e < 4; ++e) {
+            wraw[ks * 8 + e] = w0[e];
+            wraw[ks * 8 + 4 + e] = w1[e];
           }
+        } else {
+          wraw[ks] = i < nrow ? wsrc[ks * M::KSTEP] : 0.f;
         }
-        qf[ks] = f;
       }
+    } else if constexpr (LQ == 1) {
+      const T* src = q + (((row0 + i) * H + h) * L + l) * DK;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        qraw[ks] = i < nrow ? M::load(src + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
+    }
+  };
+  auto form_q = [&](int l) {
+    if constexpr (LQ == 2) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if constexpr (M::KPL == 8) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) qf[ks][e] = from_f32<T>(to_f32(qbase[ks][e]) * wraw[ks * 8 + e]);
+        } else {
+          qf[ks] = from_f32<T>(to_f32(qbase[ks]) * wraw[ks]);
+        }
+      }
+    } else if constexpr (LQ == 1) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qf[ks] = qraw[ks];
+    }
+    qlev = l;
+  };
+  auto load_q = [&](int l) {
+    if constexpr (LQ != 0) {
+      fetch_q(l);
+      form_q(l);
     } else {
-      const T* src = LQ == 1 ? q + (((row0 + i) * H + h) * L + l) * DK : q + ((row0 + i) * Hqk + hq) * DK;
+      const T* src = q + ((row0 + i) * Hqk + hq) * DK;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
         qf[ks] = i < nrow ? M::load(src + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
+      qlev = l;
     }
-    qlev = l;
   };
   if constexpr (LQ == 2) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       qbase[ks] = i < nrow ? M::load(q + ((row0 + i) * H + h) * DK + ks * M::KSTEP + g * M::KPL) : typename M::frag{};
   }
-  load_q(0);
+  // LQ: the level of this wave's first key tile is fetched now, formed when the tile comes
+  int pre = -1;
+  if constexpr (LQ != 0) {
+    qlev = -1;
+    pre = gi > 0 ? level_local(16 * gi, 0) : 0;
+    fetch_q(pre);
+  } else {
+    load_q(0);
+  }
   if constexpr (STAGE_LAMBDA) {
     // one row of lambda per thread of the first ROWS threads, loads issued before the stores
     if (tid < ROWS) {
@@ -630,16 +667,29 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, LQ ? 2 : 4) void k_tile_o
         if constexpr (LQ != 0) {
           if (KT < gi) {
             const int lv = level_local(16 * gi, 16 * KT);
-            if (lv != qlev) load_q(lv);
+            if (lv != qlev) {
+              if (pre == lv) form_q(lv);
+              else load_q(lv);
+              // fetch the next level this wave's key tiles reach: as KT grows the highest bit in
+              // which KT differs from gi (level 5 + that bit) steps down the set bits of gi, and
+              // after the last one comes the diagonal tile (level 0)
+              const int below = gi & ((1 << (lv - 5)) - 1);
+              pre = below ? 4 + bitlen(uint32_t(below)) : 0;
+              fetch_q(pre);
+            }
             sacc = scores();
           } else {
-            // diagonal 16 x 16 tile: pairs at levels 0-4, each scored with its level's queries
+            // diagonal 16 x 16 tile: pairs at levels 0-4, each scored with its level's queries,
+            // the next level fetched while the current one is scored
+            if (pre != 0) fetch_q(0);
             f32x4 sl[5];
 #pragma unroll
             for (int l = 0; l < 5; ++l) {
-              load_q(l);
+              form_q(l);
+              if (l + 1 < 5) fetch_q(l + 1);
               sl[l] = scores();
             }
+            pre = -1;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int j = 16 * KT + 4 * g + r, lv = level_local(i, j);
@@ -697,6 +747,9 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, LQ ? 2 : 4) void k_tile_o
   }
 
   if (!HAS_LAMBDA && j) load_u(level_src(j, &gap));
+  if constexpr (LQ != 0) {
+    if (j) fetch_q(LOG2R + j);
+  }
   while (j) {
     __syncthreads();  // LDS buffer free
 #pragma unroll
@@ -713,7 +766,10 @@ __global__ __launch_bounds__(RowMap<tile_rows(C)>::NT, LQ ? 2 : 4) void k_tile_o
     if (jn) load_u(level_src(jn, &gap_n));
     float w = fast_exp2(cl_s[i] + gap);
     if constexpr (STAGE_LAMBDA) w *= (i < nrow) ? lrow[LOG2R + j] : 0.f;
-    if constexpr (LQ != 0) load_q(LOG2R + j);  // rows past the end load zeros
+    if constexpr (LQ != 0) {
+      form_q(LOG2R + j);                   // fetched one level ahead
+      if (jn) fetch_q(LOG2R + jn);
+    }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
