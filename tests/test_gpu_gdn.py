@@ -33,6 +33,7 @@ BASE = WORKLOADS["ll_gdn_bf16_T8192"]
 def test_parity_chunk_counts(d, chunks):
     x = generate(BASE.with_(B=1, H=2, T=64 * chunks, dk=d, dv=d, seed=50 + chunks))
     err = rel_err(run_gdn(x, 64), _ref(x))
+    print(f"GDN d={d} chunks={chunks}: rel err {err:.3e}")
     assert err <= TOL, err
 
 
@@ -40,6 +41,7 @@ def test_parity_chunk_counts(d, chunks):
 def test_parity_stress_gates(dist):
     x = generate(BASE.with_(B=1, H=2, T=1024, dist=dist, seed=61))
     err = rel_err(run_gdn(x, 64), _ref(x))
+    print(f"GDN gates {dist}: rel err {err:.3e}")
     assert err <= TOL, err
 
 
@@ -80,6 +82,21 @@ def test_parity_full_size_sampled():
         worst = max(worst, rel_err(got[b:b + 1, rows, h:h + 1], _ref(xs, rows)))
     print(f"GDN T=8192 sampled rel err {worst:.3e}")
     assert worst <= TOL
+
+
+def test_parity_upper_level_slots():
+    """600 chunks (chunk levels up to J = 10): the scan's second level slot of each wave (levels
+    9-16) runs.  Every output row of one head against the oracle's per-level recurrent form (the
+    quadratic form's T x T solve is too large at this length); slow decay keeps the high levels
+    large."""
+    w = BASE.with_(B=1, H=2, T=64 * 600, dk=64, dv=64, dist="gdn_slow", seed=67)
+    x = generate(w)
+    got = run_gdn(x, 64)
+    xs = {n: x[n][:, :, 1:2] for n in ("q", "k", "v", "log_alpha", "beta", "lam")}
+    ref = gdn.recurrent(xs["q"], xs["k"], xs["v"], xs["log_alpha"], xs["beta"], xs["lam"])
+    err = rel_err(got[:, :, 1:2], ref)
+    print(f"GDN T={w.T} (J = 10) rel err {err:.3e}", flush=True)
+    assert err <= TOL, err
 
 
 def test_deterministic():

@@ -57,6 +57,7 @@ def test_parity_ragged_chunk_counts(chunks, dk, dv):
     w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=2, H=2, T=64 * chunks, dk=dk, dv=dv, seed=40 + chunks)
     x = generate(w)
     err = rel_err(run_mamba2(x, "bf16", 64), _oracle_full(x))
+    print(f"bf16 {dk}x{dv} chunks={chunks}: rel err {err:.3e}")
     assert err <= TOL["bf16"], err
 
 
@@ -79,6 +80,7 @@ def test_parity_fp32_small_chunk(T):
     w = WORKLOADS["ll_mamba2_f32_T64"].with_(B=2, H=3, T=T, seed=T)
     x = generate(w)
     err = rel_err(run_mamba2(x, "f32", 16), _oracle_full(x))
+    print(f"f32 C=16 T={T}: rel err {err:.3e}")
     assert err <= TOL["f32"], err
 
 
@@ -87,6 +89,7 @@ def test_parity_fp32_c64(T):
     w = WORKLOADS["ll_mamba2_f32_T64"].with_(B=1, H=2, T=T, dk=64, dv=64, C=64, seed=7 + T)
     x = generate(w)
     err = rel_err(run_mamba2(x, "f32", 64), _oracle_full(x))
+    print(f"f32 C=64 T={T}: rel err {err:.3e}")
     assert err <= TOL["f32"], err
 
 
@@ -96,6 +99,7 @@ def test_parity_stress_gates(dist):
     w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=1, H=2, T=2048, dist=dist, seed=11)
     x = generate(w)
     err = rel_err(run_mamba2(x, "bf16", 64), _oracle_full(x))
+    print(f"bf16 gates {dist}: rel err {err:.3e}")
     assert err <= TOL["bf16"], err
 
 
