@@ -303,14 +303,22 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
 
 // ---------------------------------------------------------------------------------------------
 // Kernel 2: level scan.  One workgroup (8 waves) per (b, h, 16 d_v columns), sequential over
-// the chunks.  Wave w owns levels w+1 and w+9; each level state R_j (d_k x 16, fp32)
-// lives in registers in the MFMA result layout (lane: column = lane & 15, rows 16 mt + 4g + r).
-// lambda == NULL: one state, read by every chunk, absorbing every chunk (wave 0).
-// Everything a chunk step reads (P_z, Q~, this slice of H_z and of the intra output, the level
-// weights) is copied into LDS by direct global->LDS loads one chunk ahead, into the other half of
-// double buffers.
+// the chunks.  Each level state R_j (d_k x 16) is split over the waves by rows and levels: wave w
+// owns rows 32 (w % 4) .. 32 (w % 4) + 31 (DK = 128; 16 rows for DK = 64) of the levels
+// j = 1 + (w / 4) + 2 m, in fp32 registers in the MFMA result layout, and reads out chunk row
+// tile w % 4 for those levels.  Every wave therefore does the same work.  The propagation
+// P_z R_j needs all of R_j's rows as the B operand, so the states of the chunk's start are kept
+// in LDS too (bf16, transposed, 16-byte chunks XOR-swizzled by column), rewritten by their owners
+// after each step.
+// Per step: barrier A (chunk z and the start states are in LDS), propagation and read-out, barrier
+// B, then the owners write the new states, P_z and Q~ of chunk z + 1 (loaded into registers during
+// the step) go into their single LDS buffers, and the two level groups' partial outputs are added
+// to the intra-chunk output.  The H_z and intra-output slices and the level weights come by direct
+// global->LDS loads into double buffers, one chunk ahead.
+// lambda == NULL: one state (level slot 0 of the first level group), read by every chunk.
+// SLOTS: level slots per wave (levels up to 2 SLOTS; 1 for lambda == NULL).
 // ---------------------------------------------------------------------------------------------
-template <int C, int DK, int DV, bool HAS_LAMBDA>
+template <int C, int DK, int DV, bool HAS_LAMBDA, int SLOTS>
 __global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __restrict__ lam, const bf* __restrict__ qc_in,
                                                   const bf* __restrict__ pz_in, const bf* __restrict__ hz_in,
                                                   const float* __restrict__ oin_in, bf* __restrict__ o,
@@ -318,18 +326,24 @@ __global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __res
   using MF = Mfma<bf>;
   constexpr int LOG2C = (C == 16) ? 4 : (C == 32) ? 5 : 6;
   constexpr int MTD = DK / 16;          // 16-row tiles of a state
-  constexpr int MTC = C / 16;           // 16-row tiles of a chunk
+  constexpr int MPW = MTD / 4;          // of them owned by a wave
   constexpr int KS = DK / 32;           // k steps over d_k
   constexpr int NSL = DV / kSlice;
-  constexpr int LPW = HAS_LAMBDA ? kMaxJ / kScanWaves : 1;  // level slots per wave
+  constexpr int LPW = SLOTS;                       // level slots per wave
+  static_assert(HAS_LAMBDA ? 2 * SLOTS <= kMaxJ : SLOTS == 1, "level slots");
+  constexpr int NLV = HAS_LAMBDA ? kMaxJ : 1;      // level states kept in LDS
   constexpr int NT = 64 * kScanWaves;
-  static_assert(kSlice == 16, "one 16-column slice: 2 bf16 / 4 fp32 chunks per row");
-  __shared__ bf pz_s[2][DK * DK];                    // swizzled
-  __shared__ bf qc_s[2][C * DK];                     // swizzled
+  constexpr int CPR = DK / 8;           // 16-byte chunks per state column / per P_z or Q~ row
+  constexpr int PZC = DK * CPR / NT, QCC = C * CPR / NT;  // chunks per thread of P_z, Q~
+  static_assert(kSlice == 16 && kScanWaves == 8 && C == 64, "4 row groups x 2 level groups, 4 chunk row tiles");
+  static_assert(MTD % 4 == 0 && PZC >= 1 && QCC >= 1 && DK * CPR % NT == 0 && C * CPR % NT == 0, "tile split");
+  __shared__ bf pz_s[DK * DK];                       // swizzled rows
+  __shared__ bf qc_s[C * DK];                        // swizzled rows
+  __shared__ bf rs_s[NLV * kSlice * DK];             // [level][column][row], swizzled chunks
   __shared__ bf hz_s[2][DK * kSlice];                // [row][16]
   __shared__ float oin_s[2][C * kSlice];             // [t][16]
   __shared__ float lw_s[2][HAS_LAMBDA ? C * kMaxJ : 1];
-  __shared__ float part_s[kScanWaves * C * kSlice];
+  __shared__ float part_s[2 * C * kSlice];           // [level group][t][16]
 
   const int64_t N = Tlen / C;
   const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // (b, h, slice)
@@ -338,14 +352,17 @@ __global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __res
   const int h = (int)(bh % H), b = (int)(bh / H);
   const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rg = wave & 3, lgp = wave >> 2;  // row group, level group
   const int p0 = sl * kSlice;
 
-  // copies of chunk z into buffer half `buf`
+  // state entry (level slot l, column c, row) in rs_s
+  auto rs_off = [](int l, int c, int row) {
+    return (l * kSlice + c) * DK + ((((row >> 3) ^ c) & (CPR - 1)) << 3) + (row & 7);
+  };
+  // the small per-chunk inputs into buffer half `buf`
   auto fetch = [&](int64_t z, int buf) {
     const int64_t cidx = bh * N + z;
     const int64_t tok0 = (int64_t)b * Tlen + z * C;
-    lds_copy_rows<DK, DK, NT>(pz_s[buf], pz_in + cidx * (DK * DK), DK, DK);
-    lds_copy_rows<DK, C, NT>(qc_s[buf], qc_in + cidx * (C * DK), DK, C);
     const bf* hs = hz_in + cidx * (DK * DV) + p0;
     lds_gather16<NT>(hz_s[buf], DK * 2, [&](int q) { return hs + (q >> 1) * DV + (q & 1) * 8; });
     const float* os = oin_in + cidx * (C * DV) + p0;
@@ -360,106 +377,132 @@ __global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __res
       }
     }
   };
+  // P_z and Q~ of chunk z into registers, then (once the step's readers are done) into LDS
+  bf16x8 pzr[PZC], qcr[QCC];
+  auto load_big = [&](int64_t z) {
+    const int64_t cidx = bh * N + z;
+#pragma unroll
+    for (int e = 0; e < PZC; ++e) {
+      const int x = e * NT + tid;
+      pzr[e] = *reinterpret_cast<const bf16x8*>(pz_in + cidx * (DK * DK) + (x / CPR) * DK + (x % CPR) * 8);
+    }
+#pragma unroll
+    for (int e = 0; e < QCC; ++e) {
+      const int x = e * NT + tid;
+      qcr[e] = *reinterpret_cast<const bf16x8*>(qc_in + cidx * (C * DK) + (x / CPR) * DK + (x % CPR) * 8);
+    }
+  };
+  auto store_big = [&]() {
+#pragma unroll
+    for (int e = 0; e < PZC; ++e) {
+      const int x = e * NT + tid;
+      *reinterpret_cast<bf16x8*>(pz_s + swz<DK>(x / CPR, x % CPR)) = pzr[e];
+    }
+#pragma unroll
+    for (int e = 0; e < QCC; ++e) {
+      const int x = e * NT + tid;
+      *reinterpret_cast<bf16x8*>(qc_s + swz<DK>(x / CPR, x % CPR)) = qcr[e];
+    }
+  };
 
-  f32x4 R[LPW][MTD];
+  f32x4 R[LPW][MPW];
 #pragma unroll
   for (int m = 0; m < LPW; ++m)
 #pragma unroll
-    for (int mt = 0; mt < MTD; ++mt) R[m][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
+    for (int i = 0; i < MPW; ++i) R[m][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int x = tid; x < NLV * kSlice * DK / 8; x += NT) reinterpret_cast<bf16x8*>(rs_s)[x] = bf16x8{};
+  load_big(0);
+  store_big();
   fetch(0, 0);
   for (int64_t z = 0; z < N; ++z) {
     const int buf = (int)(z & 1);
     const int64_t tok0 = (int64_t)b * Tlen + z * C;
     wait_vmem();
-    __syncthreads();  // chunk z in LDS; every wave is done with the other half
-    if (z + 1 < N) fetch(z + 1, buf ^ 1);
-    const bf* pzb = pz_s[buf];
-    const bf* qcb = qc_s[buf];
-    // A-operand fragment of a swizzled [rows][DK] tile: row, k slots 0-3 <- columns ks*32 + 4g..,
-    // slots 4-7 <- columns ks*32 + 16 + 4g.. (the layout of the R_j fragments below)
-    auto afrag = [&](const bf* m, int row, int ks) {
-      const int c0 = ks * 32 + 4 * g;
-      const bf16x4 lo = *reinterpret_cast<const bf16x4*>(m + swz<DK>(row, c0 >> 3) + (c0 & 7));
-      const bf16x4 hi = *reinterpret_cast<const bf16x4*>(m + swz<DK>(row, (c0 + 16) >> 3) + (c0 & 7));
-      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-    };
+    __syncthreads();  // A: chunk z and the start states in LDS; every wave is done with the other half
+    if (z + 1 < N) {
+      fetch(z + 1, buf ^ 1);
+      load_big(z + 1);
+    }
 
-    f32x4 out[MTC];
+    f32x4 out = {0.f, 0.f, 0.f, 0.f};  // chunk rows 16 rg + 4g + r, column p0 + r16
+    // this lane's entries of H_z (rows 16 (MPW rg + i) + 4g + r, column p0 + r16)
+    f32x4 hzv[MPW];
 #pragma unroll
-    for (int mt = 0; mt < MTC; ++mt) out[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // this lane's entries of H_z (rows 16 mt + 4g + r, column p0 + r16)
-    f32x4 hzv[MTD];
+    for (int i = 0; i < MPW; ++i)
 #pragma unroll
-    for (int mt = 0; mt < MTD; ++mt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) hzv[mt][r] = static_cast<float>(hz_s[buf][(mt * 16 + 4 * g + r) * kSlice + r16]);
+      for (int r = 0; r < 4; ++r)
+        hzv[i][r] = static_cast<float>(hz_s[buf][(16 * (MPW * rg + i) + 4 * g + r) * kSlice + r16]);
 
 #pragma unroll
     for (int m = 0; m < LPW; ++m) {
       int j;
       bool reader, source, restart;
       if constexpr (HAS_LAMBDA) {
-        j = wave + 1 + kScanWaves * m;
+        j = 1 + lgp + 2 * m;
         if (j > J) continue;
         reader = (z >> (j - 1)) & 1;
         source = !reader;
         restart = (z & ((int64_t(1) << j) - 1)) == 0;
       } else {
-        if (wave != 0) continue;
+        if (lgp != 0) continue;
         j = 0;
         reader = z > 0;
         source = true;
         restart = z == 0;
       }
-      // B fragments of R_j (k slots: rows 4g..4g+3 of tiles 2ks and 2ks+1)
+      const int slot = HAS_LAMBDA ? j - 1 : 0;
+      // B fragments of R_j at the chunk's start: column r16, rows 32 ks + 8 g .. + 7
       bf16x8 rb[KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
+        rb[ks] = *reinterpret_cast<const bf16x8*>(rs_s + rs_off(slot, r16, 32 * ks + 8 * g));
+      if (reader) {
+        f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) tmp = MF::mma(frag_along_row_swz<DK>(qc_s, 16 * rg, 4 * ks), rb[ks], tmp);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          rb[ks][r] = static_cast<bf>(R[m][2 * ks][r]);
-          rb[ks][4 + r] = static_cast<bf>(R[m][2 * ks + 1][r]);
-        }
-      if (reader) {
-#pragma unroll
-        for (int mt = 0; mt < MTC; ++mt) {
-          f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) tmp = MF::mma(afrag(qcb, mt * 16 + r16, ks), rb[ks], tmp);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int t = mt * 16 + 4 * g + r;
-            const float wgt = HAS_LAMBDA ? lw_s[buf][t * kMaxJ + (j - 1)] : 1.f;
-            out[mt][r] += wgt * tmp[r];
-          }
+          const int t = 16 * rg + 4 * g + r;
+          const float wgt = HAS_LAMBDA ? lw_s[buf][t * kMaxJ + (j - 1)] : 1.f;
+          out[r] += wgt * tmp[r];
         }
       }
-      if (restart) {
 #pragma unroll
-        for (int mt = 0; mt < MTD; ++mt) R[m][mt] = hzv[mt];
-      } else {
+      for (int i = 0; i < MPW; ++i) {
+        if (restart) {
+          R[m][i] = hzv[i];
+        } else {
+          f32x4 acc = source ? hzv[i] : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int mt = 0; mt < MTD; ++mt) {
-          f32x4 acc = source ? hzv[mt] : f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) acc = MF::mma(afrag(pzb, mt * 16 + r16, ks), rb[ks], acc);
-          R[m][mt] = acc;
+          for (int ks = 0; ks < KS; ++ks)
+            acc = MF::mma(frag_along_row_swz<DK>(pz_s, 16 * (MPW * rg + i), 4 * ks), rb[ks], acc);
+          R[m][i] = acc;
         }
       }
     }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) part_s[(lgp * C + 16 * rg + 4 * g + r) * kSlice + r16] = out[r];
+    __syncthreads();  // B: every read of the start states, P_z and Q~ is done; partial outputs complete
 
-    // combine the waves' contributions with the intra-chunk output
+    // the new states (rows 16 (MPW rg + i) + 4g .. + 3 of column r16: 8 bytes each)
 #pragma unroll
-    for (int mt = 0; mt < MTC; ++mt)
+    for (int m = 0; m < LPW; ++m) {
+      const int j = HAS_LAMBDA ? 1 + lgp + 2 * m : 0;
+      if (HAS_LAMBDA ? j > J : lgp != 0) continue;
+      const int slot = HAS_LAMBDA ? j - 1 : 0;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) part_s[(wave * C + mt * 16 + 4 * g + r) * kSlice + r16] = out[mt][r];
-    __syncthreads();
+      for (int i = 0; i < MPW; ++i) {
+        bf16x4 v4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v4[r] = static_cast<bf>(R[m][i][r]);
+        *reinterpret_cast<bf16x4*>(rs_s + rs_off(slot, r16, 16 * (MPW * rg + i) + 4 * g)) = v4;
+      }
+    }
+    if (z + 1 < N) store_big();
     for (int idx = tid; idx < C * kSlice; idx += NT) {
       const int t = idx / kSlice, p = idx % kSlice;
-      float acc = oin_s[buf][idx];
-#pragma unroll
-      for (int w = 0; w < kScanWaves; ++w) acc += part_s[(w * C + t) * kSlice + p];
+      float acc = oin_s[buf][idx] + part_s[idx];
+      if constexpr (HAS_LAMBDA) acc += part_s[C * kSlice + idx];
       o[((tok0 + t) * H + h) * DV + p0 + p] = static_cast<bf>(acc);
     }
   }
@@ -510,11 +553,14 @@ hipError_t launch_gdn(const GdnArgs& a, hipStream_t st, hipEvent_t* ev) {
     hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, false>), g1, dim3(64 * gdn::kChunkWaves), 0, st, q, k, v, a.log_alpha, a.beta,
                        a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L);
   if (ev) (void)hipEventRecord(ev[1], st);
-  if (a.lambda)
-    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, true>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz, hz,
-                       oin, o, a.T, (int)a.H, a.L, J);
+  if (a.lambda && J <= 8)
+    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, true, 4>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz,
+                       hz, oin, o, a.T, (int)a.H, a.L, J);
+  else if (a.lambda)
+    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, true, gdn::kMaxJ / 2>), g2, dim3(64 * gdn::kScanWaves), 0, st,
+                       a.lambda, qc, pz, hz, oin, o, a.T, (int)a.H, a.L, J);
   else
-    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, false>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz,
+    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, false, 1>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz,
                        hz, oin, o, a.T, (int)a.H, a.L, J);
   if (ev) (void)hipEventRecord(ev[2], st);
   return hipGetLastError();
