@@ -104,7 +104,25 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   const int64_t tok0 = (int64_t)b * Tlen + z * C;
   const int64_t cidx = bh * N + z;
 
-  // ---- phase A: gates, staging, K K^T and Q K^T
+  // ---- phase A: gates, staging, K K^T and Q K^T.  The chunk's K, Q and V rows are loaded into
+  //      registers first, so that their latency overlaps the gate scan and lambda staging.  The 64
+  //      lanes of a wave take 64 consecutive tokens of one 8-column piece, so that the transposed
+  //      (column-major) LDS copies below are written as contiguous runs.
+  constexpr int NTH = 64 * kChunkWaves;
+  constexpr int NKQ = C * DK / VEC / NTH, NVV = C * DV / VEC / NTH;  // 16-byte pieces per thread
+  static_assert(C * DK / VEC % NTH == 0 && C * DV / VEC % NTH == 0, "whole passes of the workgroup");
+  bf16x8 kpre[NKQ], qpre[NKQ], vpre[NVV];
+#pragma unroll
+  for (int e = 0; e < NKQ; ++e) {
+    const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
+    kpre[e] = *reinterpret_cast<const bf16x8*>(k + ((tok0 + t) * H + h) * DK + d0);
+    qpre[e] = *reinterpret_cast<const bf16x8*>(q + ((tok0 + t) * H + h) * DK + d0);
+  }
+#pragma unroll
+  for (int e = 0; e < NVV; ++e) {
+    const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
+    vpre[e] = *reinterpret_cast<const bf16x8*>(v + ((tok0 + t) * H + h) * DV + d0);
+  }
   if (wave == 0) {
     const float la = lane < C ? log_alpha[(tok0 + lane) * H + h] * kLog2e : 0.f;
     const float cl = wave_inclusive_scan(la);
@@ -123,10 +141,10 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
     }
   }
   __syncthreads();
-  for (int idx = tid; idx < C * DK / VEC; idx += 64 * kChunkWaves) {
-    const int t = idx / (DK / VEC), d0 = (idx % (DK / VEC)) * VEC;
-    const bf16x8 kv = *reinterpret_cast<const bf16x8*>(k + ((tok0 + t) * H + h) * DK + d0);
-    const bf16x8 qv = *reinterpret_cast<const bf16x8*>(q + ((tok0 + t) * H + h) * DK + d0);
+#pragma unroll
+  for (int e = 0; e < NKQ; ++e) {
+    const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
+    const bf16x8 kv = kpre[e], qv = qpre[e];
     *reinterpret_cast<bf16x8*>(&k_s[t * LDD + d0]) = kv;
     *reinterpret_cast<bf16x8*>(&q_s[t * LDD + d0]) = qv;
     const float gt = gm_s[t], dt = dc_s[t];
@@ -137,9 +155,10 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
       kdt_s[(d0 + e) * LDC + t] = static_cast<bf>(x * dt);
     }
   }
-  for (int idx = tid; idx < C * DV / VEC; idx += 64 * kChunkWaves) {
-    const int t = idx / (DV / VEC), d0 = (idx % (DV / VEC)) * VEC;
-    const bf16x8 vv = *reinterpret_cast<const bf16x8*>(v + ((tok0 + t) * H + h) * DV + d0);
+#pragma unroll
+  for (int e = 0; e < NVV; ++e) {
+    const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
+    const bf16x8 vv = vpre[e];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) vt_s[(d0 + e) * LDC + t] = vv[e];
   }
