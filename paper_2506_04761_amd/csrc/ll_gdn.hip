@@ -66,7 +66,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
                                                    const float* __restrict__ beta, const float* __restrict__ lam,
                                                    bf* __restrict__ qc_out, bf* __restrict__ pz_out,
                                                    bf* __restrict__ hz_out, float* __restrict__ oin_out,
-                                                   int64_t Tlen, int H, int L) {
+                                                   int64_t Tlen, int H, int L, int64_t nchunks) {
   static_assert(C == 64, "the inversion works on 4 x 4 blocks of 16 x 16 (one lane per column of wave 0)");
   constexpr int LOG2C = 6;
   constexpr int PD = 8;                 // row padding (elements)
@@ -96,48 +96,75 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   bf* ph_s = ut_s + DV * LDC;
 
   const int64_t N = Tlen / C;
-  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // (b, h, z)
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
+
+  // A persistent grid: the workgroup takes chunks blockIdx.x, blockIdx.x + gridDim.x, ... (logical
+  // order (b, h, z) through the XCD mapping), and loads the next chunk's inputs (K, Q, V rows, gates,
+  // beta, lambda) into registers as soon as the current chunk has staged its own, so that their
+  // memory latency overlaps the current chunk's work.  The 64 lanes of a wave take 64 consecutive
+  // tokens of one 8-column piece, so that the transposed (column-major) LDS copies below are
+  // written as contiguous runs.
+  constexpr int NTH = 64 * kChunkWaves;
+  constexpr int NKQ = C * DK / VEC / NTH, NVV = C * DV / VEC / NTH;  // 16-byte pieces per thread
+  constexpr int NLW = HAS_LAMBDA ? (C * (LOG2C + 1) + NTH - 1) / NTH : 1;  // lambda values per thread
+  static_assert(C * DK / VEC % NTH == 0 && C * DV / VEC % NTH == 0, "whole passes of the workgroup");
+  bf16x8 kpre[NKQ], qpre[NKQ], vpre[NVV];
+  float la_r = 0.f, bt_r = 0.f, lam_r[NLW];
+  auto load_inputs = [&](int64_t it) {
+    const int64_t wk = xcd_remap(it, nchunks);
+    const int64_t zz = wk % N, bhh = wk / N;
+    const int hh = (int)(bhh % H), bb = (int)(bhh / H);
+    const int64_t t0 = (int64_t)bb * Tlen + zz * C;
+#pragma unroll
+    for (int e = 0; e < NKQ; ++e) {
+      const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
+      kpre[e] = *reinterpret_cast<const bf16x8*>(k + ((t0 + t) * H + hh) * DK + d0);
+      qpre[e] = *reinterpret_cast<const bf16x8*>(q + ((t0 + t) * H + hh) * DK + d0);
+    }
+#pragma unroll
+    for (int e = 0; e < NVV; ++e) {
+      const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
+      vpre[e] = *reinterpret_cast<const bf16x8*>(v + ((t0 + t) * H + hh) * DV + d0);
+    }
+    if (wave == 0 && lane < C) {
+      la_r = log_alpha[(t0 + lane) * H + hh] * kLog2e;
+      bt_r = beta[(t0 + lane) * H + hh];
+    }
+    if constexpr (HAS_LAMBDA) {
+#pragma unroll
+      for (int e = 0; e < NLW; ++e) {
+        const int idx = tid + e * NTH, t = idx / (LOG2C + 1), l = idx % (LOG2C + 1);
+        if (idx < C * (LOG2C + 1)) lam_r[e] = lam[((t0 + t) * H + hh) * L + l];
+      }
+    }
+  };
+  if (blockIdx.x < nchunks) load_inputs(blockIdx.x);
+  for (int64_t it = blockIdx.x; it < nchunks; it += gridDim.x) {
+  const int64_t work = xcd_remap(it, nchunks);  // (b, h, z)
   const int64_t z = work % N;
   const int64_t bh = work / N;
   const int h = (int)(bh % H), b = (int)(bh / H);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
   const int64_t tok0 = (int64_t)b * Tlen + z * C;
   const int64_t cidx = bh * N + z;
+  __syncthreads();  // the previous chunk's readers of LDS are done
 
-  // ---- phase A: gates, staging, K K^T and Q K^T.  The chunk's K, Q and V rows are loaded into
-  //      registers first, so that their latency overlaps the gate scan and lambda staging.  The 64
-  //      lanes of a wave take 64 consecutive tokens of one 8-column piece, so that the transposed
-  //      (column-major) LDS copies below are written as contiguous runs.
-  constexpr int NTH = 64 * kChunkWaves;
-  constexpr int NKQ = C * DK / VEC / NTH, NVV = C * DV / VEC / NTH;  // 16-byte pieces per thread
-  static_assert(C * DK / VEC % NTH == 0 && C * DV / VEC % NTH == 0, "whole passes of the workgroup");
-  bf16x8 kpre[NKQ], qpre[NKQ], vpre[NVV];
-#pragma unroll
-  for (int e = 0; e < NKQ; ++e) {
-    const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
-    kpre[e] = *reinterpret_cast<const bf16x8*>(k + ((tok0 + t) * H + h) * DK + d0);
-    qpre[e] = *reinterpret_cast<const bf16x8*>(q + ((tok0 + t) * H + h) * DK + d0);
-  }
-#pragma unroll
-  for (int e = 0; e < NVV; ++e) {
-    const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
-    vpre[e] = *reinterpret_cast<const bf16x8*>(v + ((tok0 + t) * H + h) * DV + d0);
-  }
+  // ---- phase A: gates, staging, K K^T and Q K^T
   if (wave == 0) {
-    const float la = lane < C ? log_alpha[(tok0 + lane) * H + h] * kLog2e : 0.f;
+    const float la = lane < C ? la_r : 0.f;
     const float cl = wave_inclusive_scan(la);
     const float tot = __shfl(cl, C - 1, 64);
     if (lane < C) {
       cl_s[lane] = cl;
       gm_s[lane] = fast_exp2(cl);
       dc_s[lane] = fast_exp2(tot - cl);
-      bt_s[lane] = beta[(tok0 + lane) * H + h];
+      bt_s[lane] = bt_r;
     }
   }
   if constexpr (HAS_LAMBDA) {
-    for (int idx = tid; idx < C * (LOG2C + 1); idx += 64 * kChunkWaves) {
-      const int t = idx / (LOG2C + 1), l = idx % (LOG2C + 1);
-      lam_s[idx] = lam[((tok0 + t) * H + h) * L + l];
+#pragma unroll
+    for (int e = 0; e < NLW; ++e) {
+      const int idx = tid + e * NTH;
+      if (idx < C * (LOG2C + 1)) lam_s[idx] = lam_r[e];
     }
   }
   __syncthreads();
@@ -162,6 +189,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
 #pragma unroll
     for (int e = 0; e < VEC; ++e) vt_s[(d0 + e) * LDC + t] = vv[e];
   }
+  if (it + gridDim.x < nchunks) load_inputs(it + gridDim.x);  // the next chunk's, while this one runs
   __syncthreads();
   // L[t][s] = beta_t (k_t . k_s) Gamma[t,s] for s < t (fp32);  P_G[t][s] = (q_t . k_s) Gamma[t,s], s <= t
   gemm_lds<C, C, DK>(k_s, LDD, k_s, LDD, [&](int mt, int nt, f32x4 acc) {
@@ -318,6 +346,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
 #pragma unroll
     for (int r = 0; r < 4; ++r) hz[(mt * 16 + 4 * g + r) * DV + nt * 16 + r16] = static_cast<bf>(acc[r]);
   });
+  }  // chunk loop
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -559,7 +588,12 @@ hipError_t launch_gdn(const GdnArgs& a, hipStream_t st, hipEvent_t* ev) {
   float* oin = reinterpret_cast<float*>(base + w.oin);
   const int64_t N = a.T / C;
   const int J = N <= 1 ? 0 : 64 - __builtin_clzll(uint64_t(N - 1));
-  const dim3 g1((unsigned)(a.B * a.H * N)), g2((unsigned)(a.B * a.H * (DV / gdn::kSlice)));
+  // the chunk kernel runs one persistent workgroup per compute unit (its LDS allows no more)
+  const int64_t nchunks = a.B * a.H * N;
+  int dev = 0, ncu = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu < 1)
+    ncu = 256;
+  const dim3 g1((unsigned)(nchunks < ncu ? nchunks : ncu)), g2((unsigned)(a.B * a.H * (DV / gdn::kSlice)));
   const __bf16* q = static_cast<const __bf16*>(a.q);
   const __bf16* k = static_cast<const __bf16*>(a.k);
   const __bf16* v = static_cast<const __bf16*>(a.v);
@@ -567,10 +601,10 @@ hipError_t launch_gdn(const GdnArgs& a, hipStream_t st, hipEvent_t* ev) {
   if (ev) (void)hipEventRecord(ev[0], st);
   if (a.lambda)
     hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, true>), g1, dim3(64 * gdn::kChunkWaves), 0, st, q, k, v, a.log_alpha, a.beta,
-                       a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L);
+                       a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L, nchunks);
   else
     hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, false>), g1, dim3(64 * gdn::kChunkWaves), 0, st, q, k, v, a.log_alpha, a.beta,
-                       a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L);
+                       a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L, nchunks);
   if (ev) (void)hipEventRecord(ev[1], st);
   if (a.lambda && J <= 8)
     hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, true, 4>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz,
