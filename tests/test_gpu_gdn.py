@@ -84,18 +84,19 @@ def test_parity_full_size_sampled():
     assert worst <= TOL
 
 
-def test_parity_upper_level_slots():
-    """600 chunks (chunk levels up to J = 10): the scan's second level slot of each wave (levels
-    9-16) runs.  Every output row of one head against the oracle's per-level recurrent form (the
-    quadratic form's T x T solve is too large at this length); slow decay keeps the high levels
-    large."""
-    w = BASE.with_(B=1, H=2, T=64 * 600, dk=64, dv=64, dist="gdn_slow", seed=67)
+@pytest.mark.parametrize("d,chunks", [(64, 600), (128, 300)])
+def test_parity_upper_level_slots(d, chunks):
+    """More than 256 chunks (chunk levels above 8): the scan instance with eight level slots per
+    wave runs (600 chunks: levels up to 10; 300 chunks: up to 9).  Every output row of one head
+    against the oracle's per-level recurrent form (the quadratic form's T x T solve is too large at
+    this length); slow decay keeps the high levels large."""
+    w = BASE.with_(B=1, H=2, T=64 * chunks, dk=d, dv=d, dist="gdn_slow", seed=67 + d)
     x = generate(w)
     got = run_gdn(x, 64)
     xs = {n: x[n][:, :, 1:2] for n in ("q", "k", "v", "log_alpha", "beta", "lam")}
     ref = gdn.recurrent(xs["q"], xs["k"], xs["v"], xs["log_alpha"], xs["beta"], xs["lam"])
     err = rel_err(got[:, :, 1:2], ref)
-    print(f"GDN T={w.T} (J = 10) rel err {err:.3e}", flush=True)
+    print(f"GDN d={d} T={w.T} rel err {err:.3e}", flush=True)
     assert err <= TOL, err
 
 
