@@ -147,6 +147,35 @@ def recorded_traffic(workload):
         return None
 
 
+def measured_gemm_tflops(torch, dev, n=8192, reps=10):
+    """bf16 TFLOP/s of a large plain matrix product (n x n x n through torch, i.e. the vendor BLAS)
+    on this GPU: a measured second denominator for the MFMA fraction."""
+    a = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(n, n, device=dev, dtype=torch.bfloat16)
+    for _ in range(3):
+        torch.matmul(a, b)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        torch.matmul(a, b)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    return 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+
+
+def blas_threads():
+    """Threads of the BLAS library NumPy uses (the oracle's matrix products), if it can be read."""
+    try:
+        import threadpoolctl
+        info = [i for i in threadpoolctl.threadpool_info() if i.get("user_api") == "blas"]
+        return max(i["num_threads"] for i in info) if info else None
+    except Exception:
+        return None
+
+
 def qk_share(w):
     """Query/key heads per head: 1, or H_qk / H when heads share them in groups."""
     return (w.qk_heads or w.H) / w.H
@@ -187,7 +216,7 @@ def cpu_baseline(w, budget_s):
         "value": w.B * T / wall,
         "unit": "tokens/s",
         "cores": max(1, round(cpu / wall)),
-        "host_cores_available": len(os.sched_getaffinity(0)),
+        "host_cores_available": len(os.sched_getaffinity(0)), "blas_threads": blas_threads(),
         "kind": "oracle",
         "sample": f"float64 per-level recurrent form (Sec. 3.2 states, Eq. 3 output, "
                   f"{'gated delta rule' if w.variant == 'gdn' else 'scalar decay'}), first {T} tokens of "
@@ -318,6 +347,9 @@ def main():
                      "traffic_note": "HBM bytes per launch from rocprofv3 FETCH_SIZE x 2 + WRITE_SIZE x 1 "
                                      "(factors from a 1 GiB copy), null if the kernel changed since"},
     }
+    # a measured second denominator: a large bf16 matrix product through the vendor BLAS
+    res["measured_bf16_gemm_tflops"] = measured_gemm_tflops(torch, dev)
+    res["mfma_frac_of_measured_gemm"] = tflops / res["measured_bf16_gemm_tflops"]
     if args.copy_mib:
         # A plain copy kernel of known size: its FETCH_SIZE / WRITE_SIZE counters calibrate the
         # HBM traffic that the same counters report for the kernels above.
@@ -400,7 +432,7 @@ def cpu_baseline_bwd(w, budget_s):
         T *= 2
     return {
         "value": w.B * T / wall, "unit": "tokens/s", "cores": max(1, round(cpu / wall)),
-        "host_cores_available": len(os.sched_getaffinity(0)), "kind": "oracle",
+        "host_cores_available": len(os.sched_getaffinity(0)), "blas_threads": blas_threads(), "kind": "oracle",
         "sample": f"float64 gradients of the quadratic form (chain rule, every input), first {T} tokens "
                   f"of all {w.H} heads, B={w.B}; {wall:.2f} s wall, {cpu:.2f} s CPU (the quadratic form's "
                   f"cost grows with T, so longer prefixes run slower per token)",
@@ -854,7 +886,7 @@ def main_mlambda(args, w, torch, ll):
             T *= 2
         res["cpu_baseline"] = {
             "value": w.B * T / wall, "unit": "tokens/s", "cores": max(1, round(cpu / wall)),
-            "host_cores_available": len(os.sched_getaffinity(0)), "kind": "oracle",
+            "host_cores_available": len(os.sched_getaffinity(0)), "blas_threads": blas_threads(), "kind": "oracle",
             "sample": f"float64 per-level recurrent form with diagonal level weights, first {T} tokens of "
                       f"all {w.H} heads, B={w.B}; {wall:.2f} s wall, {cpu:.2f} s CPU"}
     print(json.dumps(res), flush=True)
