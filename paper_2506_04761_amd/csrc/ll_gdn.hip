@@ -17,9 +17,11 @@
 // (bit j-1 of z clear) and propagates through P_z everywhere; a chunk with bit j-1 set adds
 // lambda_t^(log2 C + j) q~_t^T R_j to its rows, with R_j taken at the chunk's start.
 //
-// Kernels: gdn_chunk (per chunk: the WY solve in fp32, a blocked inversion, and all chunk-local products on MFMA,
-// bf16 operands with fp32 accumulation) and gdn_scan (per (b, h, 16 d_v columns): every level's
-// state slice in registers, P_z / Q~ streamed through LDS once per chunk).
+// Kernels: gdn_chunk (one persistent workgroup per compute unit walking its chunks; per chunk the WY
+// solve in fp32 by a blocked inversion and all chunk-local products on MFMA, bf16 operands with fp32
+// accumulation) and gdn_scan (per (b, h, 16 d_v columns), sequential over the chunks: the level
+// states split over the waves by rows and by levels, shared through LDS, P_z / Q~ read once per
+// chunk).
 #include <type_traits>
 
 #include "ll_device.hpp"
