@@ -64,8 +64,11 @@ size_t ll_workspace_size(int32_t variant, int32_t dtype, int64_t B, int64_t T, i
                          int64_t C, int32_t has_lambda) {
   if (check_shape(B, T, H, d_k, d_v, C) != LL_OK) return 0;
   if (dtype != LL_F32 && dtype != LL_BF16) return 0;
-  if (variant == LL_MAMBA2)
+  if (variant == LL_MAMBA2) {
+    if (ll::mamba2_fused_supported(dtype, C, d_k, d_v, has_lambda != 0))
+      return (size_t)ll::mamba2_fused_workspace(B, T, H, d_k, d_v, nullptr);
     return (size_t)ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), has_lambda != 0, nullptr);
+  }
   if (variant == LL_GDN) return (size_t)ll::gdn_workspace(B, T, H, d_k, d_v, C, nullptr);
   if (variant == LL_MAMBA2_BWD && has_lambda)
     return (size_t)ll::mamba2_bwd_workspace(B, T, H, H, d_k, d_v, C, elem_size(dtype), nullptr);
@@ -119,7 +122,9 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   // B * H indexes the second grid dimension of the scan kernels (at most 65535)
   if (L > kMaxL || tiles > kMaxTiles || B * H > 65535 || tiles * 2 * H * B >= (int64_t(1) << 31))
     return LL_ERR_UNSUPPORTED;
-  const int64_t need = ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), lambda != nullptr, nullptr);
+  const bool fused = ll::mamba2_fused_supported(dtype, C, d_k, d_v, lambda != nullptr);
+  const int64_t need = fused ? ll::mamba2_fused_workspace(B, T, H, d_k, d_v, nullptr)
+                             : ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), lambda != nullptr, nullptr);
   if (!workspace) return LL_ERR_NULL_ARG;
   if ((int64_t)workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
 
@@ -133,7 +138,7 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   hipEvent_t ev[ll::kMamba2Stages + 1];
   if (events)
     for (int i = 0; i <= ll::kMamba2Stages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);
-  const hipError_t err = e->launch(a, hs, events ? ev : nullptr);
+  const hipError_t err = fused ? ll::launch_mamba2_fused(a, hs, events ? ev : nullptr) : e->launch(a, hs, events ? ev : nullptr);
   return err == hipSuccess ? LL_OK : LL_ERR_HIP;
 }
 ll_status mamba2_ml_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* Lambda,
@@ -200,7 +205,8 @@ ll_status mamba2_bwd_impl(const void* q, const void* k, const void* v, const flo
   a.Hqk = Hqk;
   a.L = L;
   a.workspace = workspace;
-  a.reuse_summaries = reuse;
+  // the single-pass forward leaves no three-kernel summaries behind: recompute them
+  a.reuse_summaries = reuse && !ll::mamba2_fused_supported(dtype, C, d_k, d_v, true);
   hipEvent_t ev[ll::kMamba2BwdStages + 1];
   if (events)
     for (int i = 0; i <= ll::kMamba2BwdStages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);

@@ -60,6 +60,20 @@ int64_t mamba2_ml_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t
 
 const KernelEntry* mamba2_table(int* n);
 
+// Single-pass forward (ll_mamba2_fused.hip): byte offsets of its workspace regions.
+struct FusedLayout {
+  int64_t N = 0;       // tiles of 128 tokens per sequence
+  int J = 0;           // inter-tile levels
+  int64_t stride = 0;  // floats per (b, h) row of the block sums
+  int64_t ctr = 0, flag = 0, bsum = 0, node = 0, total = 0;
+};
+int64_t mamba2_fused_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, FusedLayout* lay);
+// Whether ll_mamba2_fwd takes the single-pass kernels for these arguments (dtype 1 = bf16).
+bool mamba2_fused_supported(int dtype, int64_t C, int64_t dk, int64_t dv, bool has_lambda);
+// Enqueues the single-pass forward; with `ev` non-null, ev[0..3] are recorded before the tile
+// totals, before the block sums, before the tile kernel and after it.
+hipError_t launch_mamba2_fused(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev);
+
 // Log-linear Mamba-2 backward: the forward's summary workspace followed by the key-side level
 // summaries (byte offsets).
 struct BwdLayout {

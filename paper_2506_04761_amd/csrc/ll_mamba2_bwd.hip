@@ -1393,6 +1393,9 @@ int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t Hqk, int64
     w.dqh = cur; cur += al(B * T * H * dk * esize);
     w.dkh = cur; cur += al(B * T * H * dk * esize);
   }
+  // the forward run in this workspace may be the single-pass one
+  const int64_t fused = mamba2_fused_workspace(B, T, H, dk, dv, nullptr);
+  if (cur < fused) cur = fused;
   w.total = cur;
   if (lay) *lay = w;
   return cur;
