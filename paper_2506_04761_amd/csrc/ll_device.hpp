@@ -121,7 +121,8 @@ __device__ inline int swz(int r, int c) {
 // `dst` by direct global->LDS loads, one 1 KiB span per wave instruction, spans dealt to the NT/64
 // waves in turn.  Rows at or beyond `nrow` are filled from row nrow - 1 (callers never read
 // them).  The copy is complete once the issuing wave has waited for its vector-memory operations.
-template <int D, int ROWS, int NT>
+// AUX: cache-policy bits of the loads (0 by default; 2, non-temporal, for data read once).
+template <int D, int ROWS, int NT, int AUX = 0>
 __device__ inline void lds_copy_rows(__bf16* dst, const __bf16* __restrict__ src, int64_t stride, int nrow) {
   constexpr int CH = D / 8;      // chunks per row
   constexpr int RPI = NT / CH;   // rows per pass of all waves
@@ -136,7 +137,7 @@ __device__ inline void lds_copy_rows(__bf16* dst, const __bf16* __restrict__ src
     const int rs = r < nrow ? r : nrow - 1;
     __builtin_amdgcn_global_load_lds(src + rs * stride + c * 8,
                                      (__attribute__((address_space(3))) void*)(dst + (it * NT + wave * 64) * 8), 16, 0,
-                                     0);
+                                     AUX);
   }
 }
 

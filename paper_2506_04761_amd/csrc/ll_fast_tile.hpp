@@ -18,15 +18,18 @@ constexpr int kFastThreads = 256;
 // its K and V (swizzled LDS tiles), 32 keys per step, no barrier.  The body is instantiated per
 // wave (groups GA = wave, GB = 7 - wave known at compile time), so that every skipped key tile
 // and every mask case is resolved statically.  Accumulates into oA, oB (O^T fragments).
-template <int DK, int DV, bool HAS_LAMBDA>
+//
+// MTW d_v tiles starting at tile mt0 are accumulated (all DV / 16 of them by default); a wave
+// that covers only part of d_v still forms the full score tiles of its rows.
+template <int DK, int DV, bool HAS_LAMBDA, int MTW = DV / 16>
 __device__ __attribute__((always_inline)) inline void fast_intra(
     int wave, const __bf16* k_s, const __bf16* v_s, const float* cl_s, const float* kdec_s,
     const bf16x8 (&qA)[DK / 32], const bf16x8 (&qB)[DK / 32], float cliA, float cliB, const float* lrowA,
-    const float* lrowB, f32x4 (&oA)[DV / 16], f32x4 (&oB)[DV / 16]) {
+    const float* lrowB, f32x4 (&oA)[MTW], f32x4 (&oB)[MTW], int mt0 = 0) {
   using M = Mfma<__bf16>;
   typedef __bf16 bf;
   typedef typename M::frag frag;
-  constexpr int MT = DV / 16, KS = DK / M::KSTEP, KC = M::KSTEP / 8;
+  constexpr int KS = DK / M::KSTEP, KC = M::KSTEP / 8;
   const int lane = threadIdx.x & 63, r16 = lane & 15, g = lane >> 4;
   // weights of the diagonal 16 x 16 tile (keys 16 gi + 4g + r): decay and lambda of the level
   // bitlen(r16 ^ (4g + r)); zero above the diagonal
@@ -102,8 +105,8 @@ __device__ __attribute__((always_inline)) inline void fast_intra(
           }
         }
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const frag vf = frag_down_rows_swz<DV>(v_s, ST * 32, mt * 16);
+        for (int mt = 0; mt < MTW; ++mt) {
+          const frag vf = frag_down_rows_swz<DV>(v_s, ST * 32, (mt0 + mt) * 16);
           oB[mt] = M::mma(vf, pB, oB[mt]);
           if constexpr (A0) oA[mt] = M::mma(vf, pA, oA[mt]);
         }

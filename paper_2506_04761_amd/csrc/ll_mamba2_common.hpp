@@ -166,7 +166,7 @@ struct RowBlock {
 
 // Copies lambda of the tile's rows into dst[r * kMaxLevels + l] (l < L; the other slots receive
 // copies of valid entries and are never read) by direct global->LDS loads of one float per lane.
-template <int ROWS, int NT>
+template <int ROWS, int NT, int AUX = 0>
 __device__ inline void lds_copy_lambda(float* dst, const float* __restrict__ lam, int64_t row0, int H, int h, int L,
                                        int nrow) {
   constexpr int TOTAL = ROWS * kMaxLevels;
@@ -179,7 +179,7 @@ __device__ inline void lds_copy_lambda(float* dst, const float* __restrict__ lam
     const int r = pos / kMaxLevels, l = pos % kMaxLevels;
     const int rs = r < nrow ? r : nrow - 1, ls = l < L ? l : L - 1;
     __builtin_amdgcn_global_load_lds(lam + ((row0 + rs) * H + h) * L + ls,
-                                     (__attribute__((address_space(3))) void*)(dst + it * NT + wave * 64), 4, 0, 0);
+                                     (__attribute__((address_space(3))) void*)(dst + it * NT + wave * 64), 4, 0, AUX);
   }
 }
 

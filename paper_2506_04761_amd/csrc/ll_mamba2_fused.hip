@@ -21,13 +21,15 @@
 //                  and the lambda-weighted terms of every inter-tile level from the published nodes
 //
 // Work order and visibility.  Workgroups take tickets from the queue of the XCD they run on (the
-// hardware register XCC_ID); queue x holds the tiles of heads x, x + 8, ... in time order, so a
-// head's nodes are written and read within one L2.  A workgroup whose queue is empty takes tickets
-// from the other queues.  A tile only waits for nodes of earlier tickets of its own queue, held by
-// workgroups that are already running, so the waits always end; each wait is also bounded in time
-// (a timed-out tile writes NaN rows and counts the event).  Nodes are stored write-through (sc1) and
-// their flag is raised after the stores are acknowledged; readers poll the flag at device scope and
-// then load the node with ordinary loads: no cache holds a node slot before it is published, since
+// hardware register XCC_ID) and only from it; queue x holds the tiles of heads x, x + 8, ... in time
+// order, so a head's nodes are written and read through one L2.  The grid gives every XCD as many
+// workgroups as the longest queue has tiles (the hardware deals workgroups to the 8 XCDs in turn);
+// a workgroup that finds its queue drained exits.  A tile only waits for nodes of earlier tickets of
+// its own queue, held by workgroups that are already running, so the waits always end; each wait is
+// also bounded in time (a timed-out tile writes NaN rows and counts the event).  Nodes are written
+// with ordinary stores into the XCD's L2 and their flag is raised (device scope) after the stores are
+// acknowledged; readers poll the flag through the scalar cache, forced to miss it, and then load the
+// node with ordinary loads from the same L2.  No cache holds a node slot before it is published:
 // every slot is written once per launch and never read before its flag.
 #include "ll_fast_tile.hpp"
 #include "ll_launch.hpp"
@@ -36,7 +38,6 @@ namespace ll {
 
 namespace {
 
-constexpr int kSc1 = 16;                 // cache-policy bits of a buffer store: write through to memory
 constexpr uint64_t kSpinTicks = 500000;  // 5 ms of the 100 MHz real-time counter
 constexpr int kQueues = 8;               // XCDs of an MI355X
 
@@ -189,15 +190,13 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
   const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // ---- ticket: own XCD's queue first, then the others
+  // ---- ticket from this XCD's queue
   if (tid == 0) {
-    const int x0 = xcc_id();
+    const int x = xcc_id();
+    const int nh = x < BH ? (BH - 1 - x) / kQueues + 1 : 0;
     int got = -1;
     int64_t gu = 0;
-    for (int i = 0; i < kQueues && got < 0; ++i) {
-      const int x = (x0 + i) & (kQueues - 1);
-      const int nh = x < BH ? (BH - 1 - x) / kQueues + 1 : 0;
-      if (!nh) continue;
+    if (nh) {
       const unsigned t = __hip_atomic_fetch_add(&ws.ctr[x], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if ((int64_t)t < (int64_t)nh * N) {
         got = x + kQueues * (int)(t % nh);
@@ -209,9 +208,9 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
     tk_s[2] = 0;  // set when a wait timed out
   }
   __syncthreads();
-  const int bhi = tk_s[0];
+  const int bhi = __builtin_amdgcn_readfirstlane(tk_s[0]);
   if (bhi < 0) return;
-  const int u = tk_s[1];
+  const int u = __builtin_amdgcn_readfirstlane(tk_s[1]);
   const int64_t bh = bhi;
   const int h = (int)(bh % H), b = (int)(bh / H);
   const int hq = h / (H / Hqk);
@@ -295,14 +294,12 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
   }
   // node(u) pieces of this wave: write-through stores, then (after every wave's) the flag
   auto publish = [&]() {
-    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-    const auto rs = __builtin_amdgcn_make_buffer_rsrc(node_bh + (int64_t)u * SZ, (short)0, SZ * 2, 0x00020000);
+    bf* dst = node_bh + (int64_t)u * SZ;
 #pragma unroll
     for (int mt = 0; mt < DKT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NTW; ++nt)
-        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, sbf[mt][nt]), rs,
-                                              ((mt * MT + wave * NTW + nt) * 64 + lane) * 8, 0, kSc1);
+        *reinterpret_cast<bf16x4*>(dst + ((mt * MT + wave * NTW + nt) * 64 + lane) * 4) = sbf[mt][nt];
     wait_vmem();
     __syncthreads();
     if (tid == 0) __hip_atomic_store(ws.flag + bh * N + u, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -479,7 +476,9 @@ static hipError_t launch_fused(const Mamba2Args& a, hipStream_t st, hipEvent_t* 
     hipLaunchKernelGGL(k_fused_tree, dim3((unsigned)BH), dim3(256), (size_t)n1 * 2 * sizeof(float), st, ws, w.N, w.J);
   }
   if (ev) (void)hipEventRecord(ev[2], st);
-  hipLaunchKernelGGL((k_fused_fwd<DK, DV, true>), dim3((unsigned)(BH * w.N)), dim3(kFastThreads), 0, st,
+  // every XCD receives (workgroups round-robin) as many workgroups as its queue has tiles
+  const int64_t grid = (int64_t)kQueues * ((BH + kQueues - 1) / kQueues) * w.N;
+  hipLaunchKernelGGL((k_fused_fwd<DK, DV, true>), dim3((unsigned)grid), dim3(kFastThreads), 0, st,
                      (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v, a.log_alpha, a.lambda, ws,
                      (__bf16*)a.o, a.T, (int)a.H, (int)a.Hqk, a.L, w.J, w.N, BH);
   if (ev) (void)hipEventRecord(ev[3], st);
