@@ -1,19 +1,21 @@
 """Benchmark: log-linear Mamba-2 chunkwise forward on one MI355X.
 
-One step = one ll_mamba2_fwd call over the whole workload (all three kernel stages: tile
-states, the scan -- the block tree of summaries, or the running state when lambda == NULL -- and
-tile outputs), inputs already resident in HBM.  Default workload:
-B=1, H=16, T=65536, d_k=d_v=128, C=64, bf16 q/k/v with fp32 gates and lambda (17 levels).
+One step = one ll_mamba2_fwd call over the whole workload, inputs already resident in HBM.  For
+bf16 with C = 64 that is the single-pass path (tile totals, block sums of the totals, the tile
+kernel that forms and consumes the Fenwick nodes); otherwise the three-kernel path (tile states,
+the level scan, tile outputs).  Default workload (the headline): B=1, H=16, T=65536,
+d_k=d_v=128, C=64, bf16 q/k/v with fp32 gates and lambda (17 levels).
 
-Prints ONE JSON line with throughput (tokens/s), TFLOP/s against the bf16 MFMA peak, the
-lambda == NULL (Mamba-2) run of the same library, per-stage durations read from HIP events
-recorded between the stages of every timed step, the roofline of the dominant kernel and the
-float64 oracle timed on the host cores.
+Prints ONE JSON line with throughput (tokens/s), TFLOP/s against the bf16 MFMA peak, the same
+kernels with lambda = 1 and the lambda == NULL Mamba-2 path, per-stage durations read from HIP
+events recorded between the stages of every timed step, the roofline of the dominant kernel, the
+float64 oracle timed on the host cores, and (default run) the other workloads of the scope table
+(T = 2048, T = 8192 with its lambda = 1 run, and the Gated DeltaNet forward) as sub-objects.
 
 FLOP convention (counted, not issued): log-linear Mamba-2
     F = B*H*T*[2C(d_k+d_v) + 2 d_k d_v + d_k d_v log2(T/C)]
 (dense C x C intra-chunk blocks, chunk states, one inter-chunk product per (chunk, set bit)),
-and for the lambda == NULL Mamba-2 run  F = B*H*T*[2C(d_k+d_v) + 4 d_k d_v].
+and for Mamba-2 (lambda == NULL)  F = B*H*T*[2C(d_k+d_v) + 4 d_k d_v].
 Algorithmic bytes: q, k, v, log alpha, lambda read once and o written once.
 """
 
@@ -47,9 +49,29 @@ def flops_mamba2(w):
 
 
 STAGES = ["block_state", "scan", "tile_out"]
-KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_mamba2.hip", "paper_2506_04761_amd/csrc/ll_mamba2_common.hpp",
-                  "paper_2506_04761_amd/csrc/ll_device.hpp"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tile_out_ll_mamba2_bf16_T65536_hbm_traffic.md")
+FUSED_STAGES = ["tile_totals", "block_sums", "fused_tile"]
+KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_mamba2_fused.hip", "paper_2506_04761_amd/csrc/ll_fast_tile.hpp",
+                  "paper_2506_04761_amd/csrc/ll_mamba2_common.hpp", "paper_2506_04761_amd/csrc/ll_device.hpp"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fused_tile_ll_mamba2_bf16_T65536_hbm_traffic.md")
+
+
+def fused_path(w, has_lambda=True):
+    """Whether ll_mamba2_fwd takes the single-pass kernels for this workload."""
+    return w.dtype == "bf16" and w.C == 64 and has_lambda and w.dk in (64, 128) and w.dv in (64, 128)
+
+
+def fused_stage_figures(w):
+    """Algorithmic work of one launch of each single-pass stage: {stage: (flops, bytes)}.
+    tile_totals reads the log-gates and writes one total per tile; block_sums reads and writes the
+    block sums of those totals; fused_tile reads q, k, v, the log-gates and lambda and writes o --
+    the path's algorithmic bytes -- and does all of the path's FLOPs.  The Fenwick nodes the tiles
+    write and read are implementation traffic (see the rocprofv3 counters)."""
+    N = -(-w.T // 128)
+    BH = w.B * w.H
+    b_tot = w.B * w.T * w.H * 4 + BH * N * 4
+    b_sum = BH * 2 * N * 4
+    return {"tile_totals": (0.0, b_tot), "block_sums": (0.0, b_sum),
+            "fused_tile": (flops_loglinear(w), algorithmic_bytes(w))}
 
 
 def tree_nodes_read(N):
@@ -187,10 +209,40 @@ def algorithmic_bytes(w):
     return BTH * ((w.dk * 2 * qk_share(w) + w.dv) * es + 4 + w.levels * 4 + w.dv * es)
 
 
-def cpu_baseline(w, budget_s):
-    """Time the float64 oracle's per-level recurrent form on a prefix of the workload (all heads),
-    growing the prefix until one run takes at least `budget_s` / 2; report tokens/s."""
+def _pool_init():
+    """Worker set-up: one BLAS thread per worker process (the workers are the parallelism)."""
+    try:
+        import threadpoolctl
+        threadpoolctl.threadpool_limits(1)
+    except Exception:
+        pass
+    import oracle  # noqa: F401  (imported before the timed calls)
+
+
+def _pool_ready(_):
+    return os.getpid()
+
+
+def _oracle_part(job):
+    """One worker's share of the CPU baseline: the recurrent oracle on a group of heads; returns
+    its compute seconds."""
+    variant, arrs = job
     from oracle import gdn, mamba2
+    t0 = time.perf_counter()
+    if variant == "gdn":
+        gdn.recurrent(*arrs)
+    else:
+        mamba2.recurrent(*arrs)
+    return time.perf_counter() - t0, os.getpid()
+
+
+def cpu_baseline(w, budget_s):
+    """Time the float64 oracle's per-level recurrent form on a prefix of the workload, all heads:
+    the heads are dealt to a pool of worker processes, one per host core (at most 16, the CPU share
+    of one GPU), each with one BLAS thread.  The prefix doubles until one run takes at least
+    `budget_s` / 2; the time is that of the slowest worker (all run at once)."""
+    import concurrent.futures
+    import multiprocessing
     x = generate(w.with_(T=min(w.T, 16384)))
     if w.qk_heads:  # the shared q, k repeated to every head of its group: the same computation
         G = w.H // w.qk_heads
@@ -199,59 +251,44 @@ def cpu_baseline(w, budget_s):
     L = w.levels
     lam_full = np.zeros(x["lam"].shape[:-1] + (L,), np.float32)
     lam_full[..., :x["lam"].shape[-1]] = x["lam"]
-    T = 32
-    while True:
-        sl = slice(0, T)
-        t0, c0 = time.perf_counter(), time.process_time()
-        if w.variant == "gdn":
-            gdn.recurrent(x["q"][:, sl], x["k"][:, sl], x["v"][:, sl], x["log_alpha"][:, sl], x["beta"][:, sl],
-                          lam_full[:, sl])
-        else:
-            mamba2.recurrent(x["q"][:, sl], x["k"][:, sl], x["v"][:, sl], x["log_alpha"][:, sl], lam_full[:, sl])
-        wall, cpu = time.perf_counter() - t0, time.process_time() - c0
-        if wall >= budget_s / 2 or T >= x["q"].shape[1]:
-            break
-        T *= 2
+    names = ["q", "k", "v", "log_alpha"] + (["beta"] if w.variant == "gdn" else [])
+    arrays = [x[n] for n in names] + [lam_full]
+    cores = max(1, min(len(os.sched_getaffinity(0)), 16))
+    groups = [g for g in np.array_split(np.arange(w.H), min(cores, w.H)) if len(g)]
+    ctx = multiprocessing.get_context("spawn")  # fresh interpreters: nothing of this process's GPU state
+    with concurrent.futures.ProcessPoolExecutor(max_workers=len(groups), mp_context=ctx,
+                                                initializer=_pool_init) as pool:
+        list(pool.map(_pool_ready, range(4 * len(groups))))
+        T = 32
+        while True:
+            jobs = [(w.variant, [a[:, :T, g[0]:g[-1] + 1] for a in arrays]) for g in groups]
+            t0 = time.perf_counter()
+            parts = list(pool.map(_oracle_part, jobs))
+            wall = time.perf_counter() - t0
+            compute = max(p[0] for p in parts)
+            pids = {p[1] for p in parts}
+            if compute >= budget_s / 2 or T >= x["q"].shape[1]:
+                break
+            T *= 2
     return {
-        "value": w.B * T / wall,
+        "value": w.B * T / compute,
         "unit": "tokens/s",
-        "cores": max(1, round(cpu / wall)),
-        "host_cores_available": len(os.sched_getaffinity(0)), "blas_threads": blas_threads(),
+        "cores": len(groups),
+        "host_cores_available": len(os.sched_getaffinity(0)), "worker_processes": len(pids),
+        "blas_threads": 1,
         "kind": "oracle",
         "sample": f"float64 per-level recurrent form (Sec. 3.2 states, Eq. 3 output, "
                   f"{'gated delta rule' if w.variant == 'gdn' else 'scalar decay'}), first {T} tokens of "
-                  f"all {w.H} heads, B={w.B}, {L} level states; {wall:.2f} s wall, {cpu:.2f} s CPU",
+                  f"all {w.H} heads (B={w.B}, {L} level states), heads dealt to {len(groups)} worker "
+                  f"processes with one BLAS thread each; slowest worker {compute:.2f} s, "
+                  f"{wall:.2f} s wall with the transfers",
     }
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="ll_mamba2_bf16_T65536")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=20.0)
-    ap.add_argument("--copy-mib", type=int, default=0,
-                    help="also run a plain device-to-device copy of this many MiB (counter calibration)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the operator's "
-              "multi-GPU sharding is a design note, not built.", file=sys.stderr)
-        sys.exit(2)
-
-    import torch
-    import paper_2506_04761_amd as ll
-
-    w = WORKLOADS[args.workload]
-    if w.variant == "gdn":
-        return main_gdn(args, w, torch, ll)
-    if w.variant in ("decode", "gdn_decode"):
-        return main_decode(args, w, torch, ll)
-    if w.variant == "mamba2_bwd":
-        return main_bwd(args, w, torch, ll)
-    if w.variant == "mamba2_diag_lambda":
-        return main_mlambda(args, w, torch, ll)
+def measure_mamba2(w, K, W, torch, ll, with_gemm=False, copy_mib=0):
+    """Times the log-linear Mamba-2 forward on workload `w` (K timed steps after W warm-up steps,
+    HIP events between the kernel stages of every step), the same call with lambda = 1 and the
+    lambda == NULL Mamba-2 path; returns the bench line's fields."""
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
@@ -261,6 +298,7 @@ def main():
     d = {n: torch.from_numpy(x[n]).to(dev).to(dt).contiguous() for n in ("q", "k", "v")}
     la = torch.from_numpy(x["log_alpha"]).to(dev)
     lam = torch.from_numpy(x["lam"]).to(dev)
+    ones = torch.ones_like(lam)
     del x
     out = torch.empty((w.B, w.T, w.H, w.dv), dtype=dt, device=dev)
     code = ll.LL_BF16 if w.dtype == "bf16" else ll.LL_F32
@@ -268,13 +306,12 @@ def main():
                    for has_l in (0, 1))
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
-
     fwd = ll.ll_mamba2_fwd_grouped if w.qk_heads else ll.ll_mamba2_fwd
 
     def run(lmb):
         fwd(d["q"], d["k"], d["v"], la, lmb, w.C, out=out, workspace=ws, stream=stream)
 
-    def timed_plain(lmb, K, W):
+    def timed_plain(lmb):
         for _ in range(W):
             run(lmb)
         torch.cuda.synchronize()
@@ -286,7 +323,7 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / K
 
-    def timed_staged(K, W):
+    def timed_staged():
         """K timed steps, each recording HIP events between its kernel stages on the launch
         stream; returns (ms per step over the whole region, mean ms of each stage)."""
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(max(K, 1))]
@@ -304,61 +341,117 @@ def main():
         st = np.array([[e[s].elapsed_time(e[s + 1]) for s in range(3)] for e in evs[:K]]).mean(axis=0)
         return e0.elapsed_time(e1) / K, st
 
-    print(f"[bench] {w.name}: warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
-    ms, stage_ms = timed_staged(args.steps, args.warmup)
-    ms_m2 = timed_plain(None, args.steps, args.warmup)
-    print(f"[bench] log-linear {ms:.3f} ms/step (stages {', '.join(f'{x:.3f}' for x in stage_ms)}), "
-          f"lambda=NULL {ms_m2:.3f} ms/step", file=sys.stderr, flush=True)
+    print(f"[bench] {w.name}: warmup {W}, steps {K}", file=sys.stderr, flush=True)
+    ms, stage_ms = timed_staged()
+    ms_ones = timed_plain(ones)
+    ms_null = timed_plain(None)
+    print(f"[bench] {w.name} log-linear {ms:.3f} ms/step (stages {', '.join(f'{x:.3f}' for x in stage_ms)}), "
+          f"lambda=1 {ms_ones:.3f}, lambda=NULL {ms_null:.3f} ms/step", file=sys.stderr, flush=True)
 
-    figs = stage_figures(w)
+    fused = fused_path(w)
+    names = FUSED_STAGES if fused else STAGES
+    figs = fused_stage_figures(w) if fused else stage_figures(w)
     dom = int(np.argmax(stage_ms))
-    roof = roofline(w, *figs[STAGES[dom]], stage_ms[dom])
-    traffic = recorded_traffic(w.name) if STAGES[dom] == "tile_out" else None
-
+    roof = roofline(w, *figs[names[dom]], stage_ms[dom])
+    traffic = recorded_traffic(w.name) if names[dom] == "fused_tile" else None
     F = flops_loglinear(w)
     tflops = F / (ms * 1e-3) / 1e12
     F2 = flops_mamba2(w)
     res = {
-        "metric": METRIC,
         "value": w.B * w.T / (ms * 1e-3),
         "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": ms,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
         "dtype": w.dtype,
-        "data": "synthetic",
         "config": {"workload": w.name, "variant": "log-linear Mamba-2", "B": w.B, "H": w.H, "T": w.T,
                    "d_k": w.dk, "d_v": w.dv, "C": w.C, "levels": w.levels,
                    **({"qk_heads": w.qk_heads} if w.qk_heads else {}),
-                   "inputs": "bf16 q/k/v, fp32 log-gates and lambda, seeded synthetic (numpy PCG64)"},
+                   "path": "single-pass" if fused else "three-kernel",
+                   "inputs": f"{w.dtype} q/k/v, fp32 log-gates and lambda, seeded synthetic (numpy PCG64)"},
         "tflops": tflops,
         "mfma_peak_frac": tflops / (PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_MFMA_TFLOPS),
         "flop_convention": "B*H*T*[2C(dk+dv) + 2dk*dv + dk*dv*log2(T/C)]",
         "hbm_GBps_algorithmic": algorithmic_bytes(w) / (ms * 1e-3) / 1e9,
-        "mamba2_lambda_null": {"ms_per_step": ms_m2, "tokens_per_s": w.B * w.T / (ms_m2 * 1e-3),
-                               "tflops": F2 / (ms_m2 * 1e-3) / 1e12},
-        "log_factor_overhead": ms / ms_m2,
-        "stages_ms": dict(zip(STAGES, [float(x) for x in stage_ms])),
-        "roofline": {"kernel": STAGES[dom], **roof, "traffic": traffic,
+        "mamba2_lambda_ones": {"ms_per_step": ms_ones, "tokens_per_s": w.B * w.T / (ms_ones * 1e-3),
+                               "note": "the same kernels with every level weight 1 (the output is Mamba-2's)"},
+        "mamba2_lambda_null": {"ms_per_step": ms_null, "tokens_per_s": w.B * w.T / (ms_null * 1e-3),
+                               "tflops": F2 / (ms_null * 1e-3) / 1e12,
+                               "note": "lambda == NULL: one running state per tile (Mamba-2's own cost)"},
+        "log_factor_overhead": ms / ms_null,
+        "log_factor_overhead_note": "log-linear ms / lambda == NULL Mamba-2 ms",
+        "lambda_ones_ratio": ms / ms_ones,
+        "stages_ms": dict(zip(names, [float(v) for v in stage_ms])),
+        "roofline": {"kernel": names[dom], **roof, "traffic": traffic,
                      "traffic_note": "HBM bytes per launch from rocprofv3 FETCH_SIZE x 2 + WRITE_SIZE x 1 "
                                      "(factors from a 1 GiB copy), null if the kernel changed since"},
     }
-    # a measured second denominator: a large bf16 matrix product through the vendor BLAS
-    res["measured_bf16_gemm_tflops"] = measured_gemm_tflops(torch, dev)
-    res["mfma_frac_of_measured_gemm"] = tflops / res["measured_bf16_gemm_tflops"]
-    if args.copy_mib:
+    del d, la, lam, ones, out, ws
+    torch.cuda.empty_cache()
+    if with_gemm:
+        # a measured second denominator: a large bf16 matrix product through the vendor BLAS
+        res["measured_bf16_gemm_tflops"] = measured_gemm_tflops(torch, dev)
+        res["mfma_frac_of_measured_gemm"] = tflops / res["measured_bf16_gemm_tflops"]
+    if copy_mib:
         # A plain copy kernel of known size: its FETCH_SIZE / WRITE_SIZE counters calibrate the
         # HBM traffic that the same counters report for the kernels above.
-        src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        src = torch.empty(copy_mib << 20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    return res
+
+
+# The other workloads of the scope table, measured in the default run beside the headline.
+EXTRA_WORKLOADS = {"ll_mamba2_bf16_T2048": "mamba2", "ll_mamba2_bf16_T8192": "mamba2", "ll_gdn_bf16_T8192": "gdn"}
+HEADLINE = "ll_mamba2_bf16_T65536"
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=None, help=f"one workload only (default: {HEADLINE} plus the others)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="also run a plain device-to-device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the operator's "
+              "multi-GPU sharding is a design note, not built.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2506_04761_amd as ll
+
+    w = WORKLOADS[args.workload or HEADLINE]
+    if w.variant == "gdn":
+        res = main_gdn(args, w, torch, ll)
+        print(json.dumps(res), flush=True)
+        return
+    if w.variant in ("decode", "gdn_decode"):
+        return main_decode(args, w, torch, ll)
+    if w.variant == "mamba2_bwd":
+        return main_bwd(args, w, torch, ll)
+    if w.variant == "mamba2_diag_lambda":
+        return main_mlambda(args, w, torch, ll)
+    m = measure_mamba2(w, args.steps, args.warmup, torch, ll, with_gemm=True, copy_mib=args.copy_mib)
+    res = {"metric": METRIC, "value": m.pop("value"), "unit": m.pop("unit"), "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": m.pop("ms_per_step"), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": m.pop("dtype"), "data": "synthetic",
+           "config": m.pop("config"), **m}
+    if args.workload is None:
+        extra = {}
+        for name, kind in EXTRA_WORKLOADS.items():
+            we = WORKLOADS[name]
+            if kind == "gdn":
+                sub = main_gdn(args, we, torch, ll, cpu=False)
+            else:
+                sub = measure_mamba2(we, args.steps, args.warmup, torch, ll)
+            extra[name] = sub
+        res["other_workloads"] = extra
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
@@ -692,8 +785,9 @@ def main_decode(args, w, torch, ll):
     print(json.dumps(res), flush=True)
 
 
-def main_gdn(args, w, torch, ll):
-    """Log-linear Gated DeltaNet forward: same line format, issued-FLOP convention."""
+def main_gdn(args, w, torch, ll, cpu=True):
+    """Log-linear Gated DeltaNet forward: same line format, issued-FLOP convention; returns the
+    line's fields (with the CPU baseline when `cpu`)."""
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     x = generate(w)
@@ -776,10 +870,12 @@ def main_gdn(args, w, torch, ll):
         "stages_ms": dict(zip(names, [float(v) for v in stage_ms])),
         "roofline": {"kernel": names[dom], **roof, "traffic": None},
     }
-    if not args.no_cpu_baseline:
+    del d, la, beta, lam, out, ws
+    torch.cuda.empty_cache()
+    if cpu and not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
-    print(json.dumps(res), flush=True)
+    return res
 
 
 def lq_level_rows(T, R):

@@ -177,13 +177,17 @@ ll_status ll_mamba2_bwd(const void* q, const void* k, const void* v, const float
                         int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                         void* workspace, size_t workspace_bytes, void* stream);
 
-/* ll_mamba2_bwd without recomputing the forward's level summaries: for a backward that follows
- * ll_mamba2_fwd_grouped (ll_mamba2_fwd for H_qk = H) on the same q, k, v, log_alpha and lambda
- * (non-NULL) run with this same workspace (ll_mamba2_bwd_workspace_size(...) bytes: the forward
- * uses its leading part and leaves its summaries there), with nothing else writing the workspace
- * in between, on the same stream or ordered after it.  Any other use gives wrong gradients without
- * an error.  Saves the forward's first two stages (block_state and the level scan).  Arguments
- * and checks as ll_mamba2_bwd_grouped. */
+/* ll_mamba2_bwd reusing the forward's level summaries instead of recomputing them: for a backward
+ * that follows ll_mamba2_fwd_grouped (ll_mamba2_fwd for H_qk = H) with non-NULL lambda on the same
+ * inputs, run with this same workspace (ll_mamba2_bwd_workspace_size(...) bytes: the forward uses
+ * its leading part and leaves its summaries there), on the same stream or ordered after it.  The
+ * summaries depend on the shapes, k, v and log_alpha only; the forward records those (shapes and
+ * pointers) beside them, and the backward compares that record on the device with its own
+ * arguments: on a mismatch (another forward, another workspace user in between, other inputs) every
+ * gradient is written as NaN instead.  Inputs changed in place at the same addresses are not
+ * detected.  For the shapes whose forward is the single-pass kernel (bf16, C = 64: no summaries
+ * are left behind) the summaries are recomputed, exactly as ll_mamba2_bwd_grouped.  Arguments and
+ * checks as ll_mamba2_bwd_grouped. */
 ll_status ll_mamba2_bwd_after_fwd(const void* q, const void* k, const void* v, const float* log_alpha,
                                   const float* lambda, const void* d_o, void* dq, void* dk, void* dv,
                                   float* dlog_alpha, float* dlambda, int64_t B, int64_t T, int64_t H,
@@ -287,8 +291,11 @@ ll_status ll_gdn_fwd_staged(const void* q, const void* k, const void* v, const f
 /* Debug: writes out[t*T + s] = the Fenwick level l(t,s) that the forward kernels assign to the
  * pair (t, s) for chunk size C (Sec. 3.1; the intra/inter split of Eq. 5), and -1 for s > t.
  * `out` is device memory of T*T bytes.  Computed on the GPU by the same device functions the
- * forward kernels use to pick masks and source groups.  Requires T % C == 0, C a power of two,
- * 1 <= T <= 16384. */
+ * kernels use to pick masks and source groups, in every decomposition they use: inside a tile by
+ * the tile-local indices and, for 128-row tiles, by the 16 x 16 MFMA tiles of the fast and
+ * single-pass kernels; across tiles by the source-group start and by the group end.  A pair on
+ * which two decompositions disagree is written as -3, a pair no source group claims as -2.
+ * Requires T % C == 0, C a power of two, 1 <= T <= 16384. */
 ll_status ll_debug_level_map(int64_t T, int64_t C, int8_t* out, void* stream);
 
 /* Static, human-readable name of a status code. */

@@ -374,6 +374,8 @@ def _bwd_call(q, k, v, log_alpha, lam, d_o, C, grads, workspace, stream, handles
     _check(dla, "dlog_alpha", torch.float32, (B, T, H))
     _check(dlam, "dlambda", torch.float32, (B, T, H, L))
     if workspace is None:
+        if after_fwd:
+            raise ValueError("ll_mamba2_bwd_after_fwd needs the workspace its forward ran in")
         need = lib.ll_mamba2_bwd_workspace_size(code, B, T, H, Hqk, dk, dv, C)
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
     _check(workspace, "workspace", torch.uint8)
@@ -463,8 +465,9 @@ def _autograd_function():
     class LogLinearMamba2(torch.autograd.Function):
         """O = log-linear Mamba-2 attention of (q, k, v, log_alpha, lam) as a differentiable op: the
         forward runs ll_mamba2_fwd (ll_mamba2_fwd_grouped when q, k have fewer heads than v) in a
-        backward-sized workspace kept until the backward, which runs ll_mamba2_bwd_after_fwd on it
-        (the forward's level summaries are reused, not recomputed).  Memory held between the two:
+        backward-sized workspace kept with the graph, and the backward runs ll_mamba2_bwd_after_fwd
+        on it (the forward's level summaries are reused where the forward leaves them, and the
+        reuse is checked on the device).  Memory held until the graph is freed:
         ll_mamba2_bwd_workspace_size(...) bytes plus the saved inputs."""
 
         @staticmethod
@@ -480,8 +483,9 @@ def _autograd_function():
         @staticmethod
         def backward(ctx, d_o):
             q, k, v, log_alpha, lam = ctx.saved_tensors
+            # the workspace stays with ctx (freed with the graph): a second backward through the
+            # same graph (retain_graph=True) reuses it as well
             grads = ll_mamba2_bwd_after_fwd(q, k, v, log_alpha, lam, d_o.contiguous(), ctx.C, ctx.ws)
-            ctx.ws = None
             return (*grads, None)
 
     return LogLinearMamba2

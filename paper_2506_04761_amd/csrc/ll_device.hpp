@@ -97,12 +97,21 @@ __device__ __host__ inline int bitlen(uint32_t x) { return x ? 32 - __builtin_cl
 __device__ __host__ inline int level_local(int i, int j) { return bitlen(uint32_t(i ^ j)); }
 
 // Source group (Sec. 3.3, Eq. 5), for aligned blocks of P = 2^p tokens (chunks in the paper,
-// tiles of 4 chunks here): block z reads a term at block level j >= 1 (token level p + j) iff
+// tiles of two chunks here): block z reads a term at block level j >= 1 (token level p + j) iff
 // bit j-1 of z is set; the keys then come from the block range [first, first + 2^(j-1)) with
 // first = ((z >> (j-1)) - 1) << (j-1), the 2^(j-1) blocks immediately before z's own aligned
 // 2^(j-1)-block.
 __device__ __host__ inline bool reads_level(int64_t z, int j) { return (z >> (j - 1)) & 1; }
 __device__ __host__ inline int64_t source_first(int64_t z, int j) { return ((z >> (j - 1)) - 1) << (j - 1); }
+// The same group by its end: the level-j group of block z (bit j - 1 of z set) is the 2^(j-1)
+// blocks before group_end(z, j); group_end has exactly j - 1 trailing zeros.
+__device__ __host__ inline int64_t group_end(int64_t z, int j) { return (z >> (j - 1)) << (j - 1); }
+
+// level_local(i, j) of a 128-row tile as the 16 x 16 MFMA tiles see it (i = 16 gi + r,
+// j = 16 gj + c): inside one 16-row group the level is that of the in-group indices; across groups
+// (gj < gi) it is 4 + the level of the group indices, one level for the whole 16 x 16 tile.
+__device__ __host__ inline int level_in_group(int r, int c) { return bitlen(uint32_t(r ^ c)); }
+__device__ __host__ inline int level_across_groups(int gi, int gj) { return 4 + bitlen(uint32_t(gi ^ gj)); }
 
 // ------------------------------------------------------------------ direct global -> LDS tiles
 //

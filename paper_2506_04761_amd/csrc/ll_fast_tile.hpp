@@ -39,7 +39,7 @@ __device__ __attribute__((always_inline)) inline void fast_intra(
     for (int r = 0; r < 4; ++r) {
       const int jl = 4 * g + r;
       float x = fast_exp2(fminf(cli - cl_s[16 * gi + jl], 0.f));
-      if constexpr (HAS_LAMBDA) x *= lrow[bitlen(uint32_t(r16 ^ jl))];
+      if constexpr (HAS_LAMBDA) x *= lrow[level_in_group(r16, jl)];
       w[r] = jl <= r16 ? x : 0.f;
     }
     return w;
@@ -47,7 +47,7 @@ __device__ __attribute__((always_inline)) inline void fast_intra(
   // off-diagonal key tile KT < gi: one level for the whole tile, decay split at its last key
   auto offdiag = [&](f32x4 sacc, int KT, int gi, float cli, const float* lrow) {
     float qs = fast_exp2(cli - cl_s[16 * KT + 15]);
-    if constexpr (HAS_LAMBDA) qs *= lrow[4 + bitlen(uint32_t(gi ^ KT))];
+    if constexpr (HAS_LAMBDA) qs *= lrow[level_across_groups(gi, KT)];
     const f32x4 kd = *reinterpret_cast<const f32x4*>(&kdec_s[16 * KT + 4 * g]);
     f32x4 p;
 #pragma unroll

@@ -10,6 +10,7 @@ namespace ll {
 
 // Byte offsets of the workspace regions of one forward call (see mamba2_workspace).
 struct WsLayout {
+  int64_t tag = 0;     // 256 bytes: WsTag of the inputs the level summaries were formed from
   int64_t N = 0;       // tiles per sequence
   int J = 0;           // inter-tile levels
   int64_t n1 = 0, n2 = 0, nb = 0, nup = 0;  // per-(b,h) summary slots: levels 1, 2, 3 (blocks), >= 4
@@ -24,6 +25,14 @@ int64_t tiles_of(int64_t T, int64_t C);
 // Workspace layout of ll_mamba2_fwd; returns the total byte count.
 int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, int64_t esize,
                          bool has_lambda, WsLayout* lay);
+
+// Identity of the inputs a workspace's level summaries were formed from: kept in the workspace so
+// that the backward's reuse of them (ll_mamba2_bwd_after_fwd) can be checked on the device.  The
+// summaries depend on the shapes, k, v and the log-gates only.
+struct WsTag {
+  uint64_t v[12];
+};
+constexpr uint64_t kWsTagMagic = 0x314741545354534CULL;  // any other value marks a workspace without summaries
 
 struct Mamba2Args {
   const void* q;
@@ -60,6 +69,12 @@ int64_t mamba2_ml_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t
 
 const KernelEntry* mamba2_table(int* n);
 
+// The tag of the summaries formed from `a` (storage element size esize); magic = 0 gives a tag that
+// matches nothing.
+WsTag mamba2_tag(const Mamba2Args& a, int64_t esize, bool valid);
+// Enqueues the write of `tag` into the workspace's tag region.
+hipError_t launch_write_tag(void* workspace, const WsLayout& w, const WsTag& tag, hipStream_t st);
+
 // Single-pass forward (ll_mamba2_fused.hip): byte offsets of its workspace regions.
 struct FusedLayout {
   int64_t N = 0;       // tiles of 128 tokens per sequence
@@ -78,6 +93,7 @@ hipError_t launch_mamba2_fused(const Mamba2Args& a, hipStream_t st, hipEvent_t* 
 // summaries (byte offsets).
 struct BwdLayout {
   WsLayout fwd;
+  int64_t bad = 0;  // 256 bytes: set when the forward summaries to be reused belong to other inputs
   int64_t NR = 0, nd = 0, npart = 0;  // 8-tile regions; key-side summaries and partials per (b, h)
   int64_t d = 0, dtot = 0, part = 0, qdq = 0, tsum = 0, dqh = 0, dkh = 0, total = 0;
 };

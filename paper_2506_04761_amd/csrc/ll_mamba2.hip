@@ -1,5 +1,5 @@
 // Log-linear Mamba-2 forward: O = (Q K^T (.) M^S (.) M^H) V  (Sec. 3.4), computed with the
-// chunkwise algorithm of Sec. 3.3 (Eq. 5), organised for gfx950 in tiles of R = 4C tokens.
+// chunkwise algorithm of Sec. 3.3 (Eq. 5), organised for gfx950 in tiles of R = 2C tokens (at least 64).
 //
 // The hierarchical mask splits at the tile boundary exactly as Eq. 5 splits it at the chunk
 // boundary: pairs (t, s) inside one aligned tile have levels 0..log2 R and are computed densely
@@ -975,6 +975,11 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_tile_out_fast(
 // ---------------------------------------------------------------------------------------------
 // Debug level map: the level each (t, s) pair receives from the device functions the kernels use.
 // ---------------------------------------------------------------------------------------------
+// Inside a tile the level is evaluated both as the generic tile kernels pick it (level_local) and, for
+// tiles of 128 rows, as the 16 x 16 MFMA tiles of the fast and single-pass kernels pick it; across
+// tiles both by the source-group start (three-kernel forward, backward) and by the group end (the
+// single-pass forward walks the set bits of the tile index from the highest).  A pair the two
+// decompositions disagree on is written as -3, a pair no group claims as -2.
 __global__ void k_debug_level_map(int64_t Tlen, int R, int log2R, int J, int8_t* out) {
   const int64_t t = blockIdx.x;
   for (int64_t s = threadIdx.x; s < Tlen; s += blockDim.x) {
@@ -982,12 +987,22 @@ __global__ void k_debug_level_map(int64_t Tlen, int R, int log2R, int J, int8_t*
     if (s <= t) {
       const int64_t ut = t / R, us = s / R;
       if (ut == us) {
-        lev = level_local(int(t % R), int(s % R));
+        const int i = int(t % R), j = int(s % R);
+        lev = level_local(i, j);
+        if (R == 128) {
+          const int fast = (i >> 4) == (j >> 4) ? level_in_group(i & 15, j & 15) : level_across_groups(i >> 4, j >> 4);
+          if (fast != lev) lev = -3;
+        }
       } else {
         lev = -2;  // no source group claims the pair: a bug
         for (int j = 1; j <= J; ++j)
           if (reads_level(ut, j) && us >= source_first(ut, j) && us < source_first(ut, j) + (int64_t(1) << (j - 1)))
             lev = log2R + j;
+        int byend = -2;
+        for (int j = ut ? bitlen(uint32_t(ut)) : 0; j >= 1; --j)
+          if (((ut >> (j - 1)) & 1) && us < group_end(ut, j) && us >= group_end(ut, j) - (int64_t(1) << (j - 1)))
+            byend = log2R + j;
+        if (byend != lev) lev = -3;
       }
     }
     out[t * Tlen + s] = (int8_t)lev;
@@ -1070,6 +1085,7 @@ int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv
   for (int l = 1; l <= J - 3; ++l) w.nup += (w.nb + (int64_t(1) << l) - 1) >> l;  // block-tree levels
   const int64_t nup1 = w.nup > 0 ? w.nup : 1;
   int64_t cur = 0;
+  w.tag = cur; cur += al(sizeof(WsTag));
   w.tot2 = cur; cur += al(BH * N * 4);
   w.cl = cur; cur += al(BH * N * tile_rows((int)C) * 4);
   if (has_lambda) {
@@ -1089,6 +1105,34 @@ int64_t mamba2_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv
   return cur;
 }
 
+__global__ void k_write_tag(uint64_t* dst, WsTag tag) {
+  if (threadIdx.x < 12) dst[threadIdx.x] = tag.v[threadIdx.x];
+}
+
+WsTag mamba2_tag(const Mamba2Args& a, int64_t esize, bool valid) {
+  WsTag t{};
+  t.v[0] = valid ? kWsTagMagic : 0;
+  t.v[1] = (uint64_t)a.B;
+  t.v[2] = (uint64_t)a.T;
+  t.v[3] = (uint64_t)a.H;
+  t.v[4] = (uint64_t)a.Hqk;
+  t.v[5] = (uint64_t)a.dk;
+  t.v[6] = (uint64_t)a.dv;
+  t.v[7] = (uint64_t)a.C;
+  t.v[8] = (uint64_t)esize;
+  t.v[9] = (uint64_t)(uintptr_t)a.k;
+  t.v[10] = (uint64_t)(uintptr_t)a.v;
+  t.v[11] = (uint64_t)(uintptr_t)a.log_alpha;
+  return t;
+}
+
+hipError_t launch_write_tag(void* workspace, const WsLayout& w, const WsTag& tag, hipStream_t st) {
+  hipLaunchKernelGGL(k_write_tag, dim3(1), dim3(64), 0, st,
+                     reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + w.tag), tag);
+  return hipGetLastError();
+}
+
+// Also records, once the summaries are complete, the tag of the inputs they were formed from.
 template <typename T, int C, int DK, int DV>
 hipError_t launch_mamba2_summaries(const Mamba2Args& a, const WsLayout& w, const Nodes<T>& nodes, hipStream_t st,
                                    hipEvent_t ev_mid) {
@@ -1111,7 +1155,7 @@ hipError_t launch_mamba2_summaries(const Mamba2Args& a, const WsLayout& w, const
       hipLaunchKernelGGL((k_level_scan<T, kMaxLevels>), glev, dim3(kScanThreads), tt * sizeof(float), st, nodes, w.N,
                          w.J, SZ);
   }
-  return hipGetLastError();
+  return launch_write_tag(a.workspace, w, mamba2_tag(a, sizeof(T), true), st);
 }
 
 // Enqueues the stages on `st`.  With `ev` non-null, ev[i] is recorded before stage i and ev[3]
@@ -1137,6 +1181,9 @@ hipError_t launch_mamba2(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
     const hipError_t e = launch_mamba2_summaries<T, C, DK, DV>(a, w, nodes, st, ev ? ev[1] : nullptr);
     if (e != hipSuccess) return e;
   } else {
+    // the workspace no longer holds level summaries
+    const hipError_t e = launch_write_tag(a.workspace, w, mamba2_tag(a, sizeof(T), false), st);
+    if (e != hipSuccess) return e;
     const dim3 gblk((unsigned)(w.nb * a.H * a.B));
     const dim3 gscan((unsigned)((SZ / 2 + 255) / 256), (unsigned)(a.B * a.H));
     hipLaunchKernelGGL((k_block_state<T, C, DK, DV, false>), gblk, dim3(kStateThreads), 0, st, (const T*)a.k, (const T*)a.v,

@@ -1384,6 +1384,7 @@ int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t Hqk, int64
   w.npart = 0;
   for (int j = 5; j <= J; ++j) w.npart += RevNodes<float>::parts(w.NR, j);
   const int64_t nd1 = w.nd > 0 ? w.nd : 1, np1 = w.npart > 0 ? w.npart : 1;
+  w.bad = cur; cur += al(4);
   w.d = cur; cur += al(BH * nd1 * SZ * esize);
   w.dtot = cur; cur += al(BH * nd1 * 4);
   w.part = cur; cur += al(BH * np1 * SZ * 4);
@@ -1399,6 +1400,28 @@ int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t Hqk, int64
   w.total = cur;
   if (lay) *lay = w;
   return cur;
+}
+
+// Compares the workspace's summary tag with the tag of this call's inputs: *bad = 1 on a mismatch.
+__global__ void k_check_tag(const uint64_t* tag, WsTag want, int* bad) {
+  const int i = threadIdx.x;
+  const bool diff = i < 12 && tag[i] != want.v[i];
+  const bool any = __any(diff);
+  if (i == 0) *bad = any ? 1 : 0;
+}
+
+// NaN-fills every gradient when *bad is set (the reused summaries belonged to other inputs).
+template <typename T>
+__global__ void k_poison_grads(const int* bad, T* dq, int64_t nq, T* dk, T* dv, int64_t nv, float* dla, int64_t na,
+                               float* dlam, int64_t nl) {
+  if (*bad == 0) return;
+  const T tn = from_f32<T>(__builtin_nanf(""));
+  const float fn = __builtin_nanf("");
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nq; i += stride) dq[i] = dk[i] = tn;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nv; i += stride) dv[i] = tn;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < na; i += stride) dla[i] = fn;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nl; i += stride) dlam[i] = fn;
 }
 
 // Stages (ev[i] recorded before stage i, ev[4] after the last): 0 the forward summaries (skipped
@@ -1432,10 +1455,14 @@ hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t*
   fa.q = a.q; fa.k = a.k; fa.v = a.v; fa.log_alpha = a.log_alpha; fa.lambda = a.lambda; fa.o = nullptr;
   fa.B = a.B; fa.T = a.T; fa.H = a.H; fa.dk = DK; fa.dv = DV; fa.C = C; fa.Hqk = a.Hqk; fa.L = a.L;
   fa.workspace = a.workspace;
+  int* bad = reinterpret_cast<int*>(base + w.bad);
   if (ev) (void)hipEventRecord(ev[0], st);
   if (!a.reuse_summaries) {
     const hipError_t e = launch_mamba2_summaries<T, C, DK, DV>(fa, w.fwd, nodes, st, nullptr);
     if (e != hipSuccess) return e;
+  } else {
+    hipLaunchKernelGGL(k_check_tag, dim3(1), dim3(64), 0, st,
+                       reinterpret_cast<const uint64_t*>(base + w.fwd.tag), mamba2_tag(fa, sizeof(T), true), bad);
   }
   if (ev) (void)hipEventRecord(ev[1], st);
   if (J >= 1) {
@@ -1478,6 +1505,11 @@ hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t*
                        a.B * a.T, (int)a.H, (int)a.Hqk, DK);
     hipLaunchKernelGGL((k_group_sum<T>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, (const T*)dkh, (T*)a.dk,
                        a.B * a.T, (int)a.H, (int)a.Hqk, DK);
+  }
+  if (a.reuse_summaries) {
+    const int64_t nq = a.B * a.T * a.Hqk * DK, nv = a.B * a.T * a.H * DV, na = a.B * a.T * a.H;
+    hipLaunchKernelGGL((k_poison_grads<T>), dim3(512), dim3(256), 0, st, (const int*)bad, (T*)a.dq, nq, (T*)a.dk,
+                       (T*)a.dv, nv, a.dlog_alpha, na, a.dlambda, na * a.L);
   }
   if (ev) (void)hipEventRecord(ev[4], st);
   return hipGetLastError();

@@ -315,7 +315,7 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
   for (int mt = 0; mt < MT; ++mt) oA[mt] = oB[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
   fast_intra<DK, DV, HAS_LAMBDA>(wave, k_s, v_s, cl_s, kdec_s, qA, qB, cliA, cliB, lrowA, lrowB, oA, oB);
 
-  auto slot_of = [&](int j) -> int64_t { return ((int64_t)(u >> (j - 1)) << (j - 1)) - 1; };
+  auto slot_of = [&](int j) -> int64_t { return group_end(u, j) - 1; };  // node(e - 1) covers the group ending at e
 
   // ---- odd tiles: node(u) = S_u + the tile's low-level groups, decayed to the end of the tile
   if (u & 1) {

@@ -109,20 +109,54 @@ def test_bwd_full_size_sampled():
     assert np.all(np.isfinite(dq)) and np.all(np.isfinite(dk)) and np.all(np.isfinite(dv))
 
 
-@pytest.mark.parametrize("T,dk,dv", [(64 * 66, 128, 128), (64 * 19, 128, 64)])
-def test_bwd_after_fwd_reuses_the_forward_summaries(T, dk, dv):
-    """ll_mamba2_bwd_after_fwd on the workspace a forward just filled equals ll_mamba2_bwd bit for
-    bit (the same kernels on the same summaries), and so matches the oracle too."""
-    import torch
-    import paper_2506_04761_amd as ll
-    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=1, H=2, T=T, dk=dk, dv=dv, seed=97)
+def _bwd_case(dtype, C, T, dk, dv, seed=97):
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(dtype=dtype, C=C, B=1, H=2, T=T, dk=dk, dv=dv, seed=seed)
     x = generate(w)
     do = upstream_grad(w)
-    args = [to_dev(x[n], "bf16") for n in ("q", "k", "v")]
-    args += [to_dev(x["log_alpha"]), to_dev(x["lam"]), to_dev(do, "bf16")]
+    args = [to_dev(x[n], dtype) for n in ("q", "k", "v")]
+    args += [to_dev(x["log_alpha"]), to_dev(x["lam"]), to_dev(do, dtype)]
+    return w, args
+
+
+@pytest.mark.parametrize("dtype,C,T,dk,dv", [("bf16", 64, 64 * 66, 128, 128), ("bf16", 64, 64 * 19, 128, 64),
+                                             ("f32", 16, 16 * 70, 16, 16)])
+def test_bwd_after_fwd_reuses_the_forward_summaries(dtype, C, T, dk, dv):
+    """ll_mamba2_bwd_after_fwd on the workspace a forward just filled equals ll_mamba2_bwd bit for
+    bit (the same kernels on the same summaries: reused from the three-kernel forward, fp32 here;
+    recomputed after the single-pass forward, bf16 with C = 64), and so matches the oracle too."""
+    import torch
+    import paper_2506_04761_amd as ll
+    w, args = _bwd_case(dtype, C, T, dk, dv)
     ref = [g.clone() for g in ll.ll_mamba2_bwd(*args, w.C)]
     ws = ll.ll_mamba2_bwd_workspace(args[0], args[2], w.C)
     ws.fill_(255)  # stale bytes: everything the backward reads must come from the forward
+    ll.ll_mamba2_fwd(*args[:5], w.C, workspace=ws)
+    got = ll.ll_mamba2_bwd_after_fwd(*args, w.C, ws)
+    torch.cuda.synchronize()
+    for n, a, b in zip(NAMES, got, ref):
+        assert torch.equal(a, b), n
+
+
+def test_bwd_after_fwd_detects_a_workspace_of_other_inputs():
+    """The summaries in the workspace belong to the forward of other inputs (another k tensor), or a
+    lambda = NULL forward overwrote them: every gradient comes back NaN, not silently wrong; a
+    forward on the right inputs makes the reuse valid again."""
+    import torch
+    import paper_2506_04761_amd as ll
+    w, args = _bwd_case("f32", 16, 16 * 70, 16, 16, seed=5)
+    _, other = _bwd_case("f32", 16, 16 * 70, 16, 16, seed=6)
+    ws = ll.ll_mamba2_bwd_workspace(args[0], args[2], w.C)
+    ll.ll_mamba2_fwd(*other[:5], w.C, workspace=ws)
+    got = ll.ll_mamba2_bwd_after_fwd(*args, w.C, ws)
+    torch.cuda.synchronize()
+    for n, g in zip(NAMES, got):
+        assert torch.isnan(g).all(), n
+    ll.ll_mamba2_fwd(*args[:4], None, w.C, workspace=ws)  # lambda = NULL: no summaries left
+    got = ll.ll_mamba2_bwd_after_fwd(*args, w.C, ws)
+    torch.cuda.synchronize()
+    for n, g in zip(NAMES, got):
+        assert torch.isnan(g).all(), n
+    ref = [g.clone() for g in ll.ll_mamba2_bwd(*args, w.C)]
     ll.ll_mamba2_fwd(*args[:5], w.C, workspace=ws)
     got = ll.ll_mamba2_bwd_after_fwd(*args, w.C, ws)
     torch.cuda.synchronize()
@@ -208,6 +242,24 @@ def test_autograd_function_matches_the_entry_points(Hqk):
     torch.cuda.synchronize()
     for n, t, r in zip(NAMES, leaves, ref):
         assert torch.equal(t.grad, r), n
+
+
+@pytest.mark.parametrize("dtype,C", [("bf16", 64), ("f32", 16)])
+def test_autograd_backward_twice_with_retain_graph(dtype, C):
+    """Two backward passes through one graph (retain_graph=True): both give the entry point's
+    gradients (the forward's workspace stays with the graph)."""
+    import torch
+    import paper_2506_04761_amd as ll
+    w, args = _bwd_case(dtype, C, 16 * 72, 128 if dtype == "bf16" else 16, 64 if dtype == "bf16" else 16, seed=71)
+    leaves = [t.clone().requires_grad_() for t in args[:5]]
+    do = args[5]
+    o = ll.log_linear_mamba2(*leaves, w.C)
+    ref = ll.ll_mamba2_bwd(*args, w.C)
+    for rep in range(2):
+        grads = torch.autograd.grad(o, leaves, grad_outputs=do, retain_graph=True)
+        torch.cuda.synchronize()
+        for n, g, r in zip(NAMES, grads, ref):
+            assert torch.equal(g, r), (rep, n)
 
 
 @pytest.mark.parametrize("dtype,C,dk,dv,H,Hqk,T", [
