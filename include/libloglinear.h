@@ -28,15 +28,16 @@
  *           the compiled kernel shapes (ll_supported).  Size limits (LL_ERR_UNSUPPORTED beyond them):
  *           L <= 24 levels; for log-linear Mamba-2 at most 8192 tiles of max(2C, 64) tokens per
  *           sequence and B * H <= 65535.
- * Ownership. Every pointer is caller-owned device memory.  The library allocates nothing, keeps no
- *           pointer after the call returns, and enqueues all work on `stream` (a hipStream_t passed
- *           as void*, NULL = the default stream).  Calls return before the work finishes: the caller
- *           keeps all buffers alive and unmodified until the stream reaches this point.
+ * Ownership. Every pointer is caller-owned device memory.  The library allocates nothing (the one
+ *           static device array of ll_mamba2_fwd_noalloc aside), keeps no pointer after the call
+ *           returns, and enqueues all work on `stream` (a hipStream_t passed as void*, NULL = the
+ *           default stream).  Calls return before the work finishes: the caller keeps all buffers
+ *           alive and unmodified until the stream reaches this point.
  * Workspace. Device scratch of at least ll_workspace_size(...) bytes, 256-byte aligned, owned by the
  *           caller; its contents on entry are irrelevant.  Calls sharing a workspace must be ordered.
  * Errors.   Argument checks run on the host before any launch; on error nothing is enqueued.
- *           A failed launch returns LL_ERR_HIP.  No exceptions cross the ABI.  Thread-safe: no
- *           mutable global state.
+ *           A failed launch returns LL_ERR_HIP.  No exceptions cross the ABI.  Thread-safe: the
+ *           only mutable global state is ll_mamba2_fwd_noalloc's per-device scratch (see there).
  */
 #ifndef LIBLOGLINEAR_H
 #define LIBLOGLINEAR_H
@@ -55,8 +56,13 @@ typedef enum {
   LL_ERR_UNSUPPORTED = 3,  /* no compiled kernel for (dtype, C, d_k, d_v), an unknown dtype, or
                               sizes beyond the limits stated under Shapes                        */
   LL_ERR_WORKSPACE = 4,    /* workspace smaller than ll_workspace_size(...) or misaligned       */
-  LL_ERR_HIP = 5           /* the HIP runtime reported an error when launching                   */
+  LL_ERR_HIP = 5,          /* the HIP runtime reported an error when launching                   */
+  LL_ERR_SCRATCH = 6       /* ll_mamba2_fwd_noalloc: the call needs more device scratch than
+                              LL_NOALLOC_SCRATCH_BYTES                                          */
 } ll_status;
+
+/* Bytes of the static device scratch ll_mamba2_fwd_noalloc works in (one copy per GPU). */
+#define LL_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
 
 typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
 
@@ -84,6 +90,24 @@ ll_status ll_mamba2_fwd(const void* q, const void* k, const void* v, const float
                         const float* lambda, void* o, int64_t B, int64_t T, int64_t H,
                         int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,
                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* ll_mamba2_fwd for callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops, harnesses that forbid hipMalloc): the same kernels and the same result as
+ * ll_mamba2_fwd, with the workspace taken from a static device array of LL_NOALLOC_SCRATCH_BYTES
+ * (64 MiB) instead of an argument.  The caller still owns q, k, v, log_alpha, lambda and o.
+ * Each GPU holds its own copy of the array from the first call on that GPU (whose device address
+ * is looked up then, with the stream's device current) until the process ends.  Nothing is
+ * allocated, on the device or the host, by this call.
+ * Limits.   Arguments whose ll_workspace_size(LL_MAMBA2, ...) exceeds LL_NOALLOC_SCRATCH_BYTES
+ *           return LL_ERR_SCRATCH before anything is enqueued; e.g. bf16 with C = 64 and
+ *           d_k = d_v = 128 needs about 256 bytes per token and head (B * T * H up to about 2^18).
+ * Sharing.  Every call on one GPU works in that GPU's one array and leaves its contents behind
+ *           (the kernels clear what must start at zero): calls on one GPU must be ordered (one
+ *           stream, or streams joined by events); calls that overlap on one GPU race and give
+ *           wrong results.  Other errors as ll_mamba2_fwd. */
+ll_status ll_mamba2_fwd_noalloc(const void* q, const void* k, const void* v, const float* log_alpha,
+                                const float* lambda, void* o, int64_t B, int64_t T, int64_t H,
+                                int64_t d_k, int64_t d_v, int64_t C, int32_t dtype, void* stream);
 
 /* Log-linear Mamba-2 forward with query/key heads shared by groups of heads: q and k are
  * [B, T, H_qk, d_k] and head h (of H) uses query/key head h / (H / H_qk); v, o, log_alpha and

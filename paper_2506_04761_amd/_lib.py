@@ -18,7 +18,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # build.py --asan); by default the in-tree library is loaded.
 LIB_PATH = os.environ.get("LIBLOGLINEAR_PATH") or os.path.join(HERE, "libloglinear.so")
 
-LL_OK, LL_ERR_NULL_ARG, LL_ERR_BAD_SHAPE, LL_ERR_UNSUPPORTED, LL_ERR_WORKSPACE, LL_ERR_HIP = range(6)
+LL_OK, LL_ERR_NULL_ARG, LL_ERR_BAD_SHAPE, LL_ERR_UNSUPPORTED, LL_ERR_WORKSPACE, LL_ERR_HIP, LL_ERR_SCRATCH = range(7)
+LL_NOALLOC_SCRATCH_BYTES = 64 << 20
 LL_F32, LL_BF16 = 0, 1
 LL_MAMBA2, LL_GDN, LL_MAMBA2_BWD = 0, 1, 2
 LL_LAMBDA_DIAG, LL_LAMBDA_FULL = 0, 1
@@ -40,6 +41,8 @@ lib.ll_workspace_size.argtypes = [_i32, _i32, _i64, _i64, _i64, _i64, _i64, _i64
 lib.ll_workspace_size.restype = _sz
 lib.ll_mamba2_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp, _sz, _vp]
 lib.ll_mamba2_fwd.restype = _i32
+lib.ll_mamba2_fwd_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i32, _vp]
+lib.ll_mamba2_fwd_noalloc.restype = _i32
 lib.ll_mamba2_fwd_grouped.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i32,
                                        _vp, _sz, _vp]
 lib.ll_mamba2_fwd_grouped.restype = _i32
@@ -179,6 +182,27 @@ def ll_mamba2_fwd(q, k, v, log_alpha, lam, C, out=None, workspace=None, stream=N
     (B, T, H, dk, dv, code), out, ws = _prepare(LL_MAMBA2, q, k, v, log_alpha, None, lam, C, out, workspace)
     st = lib.ll_mamba2_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(lam), _ptr(out),
                            B, T, H, dk, dv, C, code, _ptr(ws), ws.numel(), _stream(stream))
+    if st != LL_OK:
+        raise LLError(st)
+    return out
+
+
+def ll_mamba2_fwd_noalloc(q, k, v, log_alpha, lam, C, out, stream=None):
+    """ll_mamba2_fwd through the entry point that allocates nothing: the library works in its
+    static per-GPU scratch, so calls on one GPU must be ordered.  `out` is caller-allocated.
+    Returns `out`; raises LLError (LL_ERR_SCRATCH beyond LL_NOALLOC_SCRATCH_BYTES)."""
+    torch = _torch()
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    _check(q, "q")
+    _check(k, "k", q.dtype, (B, T, H, dk))
+    _check(v, "v", q.dtype, (B, T, H, dv))
+    _check(log_alpha, "log_alpha", torch.float32, (B, T, H))
+    if lam is not None:
+        _check(lam, "lambda", torch.float32, (B, T, H, ll_num_levels(T)))
+    _check(out, "out", q.dtype, (B, T, H, dv))
+    st = lib.ll_mamba2_fwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(lam), _ptr(out),
+                                   B, T, H, dk, dv, C, _dtype_code(q), _stream(stream))
     if st != LL_OK:
         raise LLError(st)
     return out

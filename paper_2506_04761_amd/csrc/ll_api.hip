@@ -1,5 +1,7 @@
 // C ABI of libloglinear: argument validation, workspace carving and kernel dispatch.
 // All checks run on the host before anything is enqueued.
+#include <atomic>
+#include <mutex>
 #include <type_traits>
 
 #include "../../include/libloglinear.h"
@@ -100,6 +102,7 @@ const char* ll_status_string(ll_status s) {
     case LL_ERR_UNSUPPORTED: return "LL_ERR_UNSUPPORTED: no kernel for this dtype/C/d_k/d_v";
     case LL_ERR_WORKSPACE: return "LL_ERR_WORKSPACE: workspace too small or misaligned";
     case LL_ERR_HIP: return "LL_ERR_HIP: HIP launch error";
+    case LL_ERR_SCRATCH: return "LL_ERR_SCRATCH: the call needs more than the 64 MiB static device scratch";
   }
   return "unknown ll_status";
 }
@@ -107,39 +110,62 @@ const char* ll_status_string(ll_status s) {
 }  // extern "C"
 
 namespace {
-ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
+// What one log-linear Mamba-2 forward runs and the workspace it needs, from the host-side checks.
+struct Mamba2Plan {
+  const ll::KernelEntry* e = nullptr;
+  bool fused = false;
+  int L = 0;
+  int64_t need = 0;
+};
+
+ll_status mamba2_plan(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
                       void* o, int64_t B, int64_t T, int64_t H, int64_t Hqk, int64_t d_k, int64_t d_v, int64_t C,
-                      int32_t dtype, void* workspace, size_t workspace_bytes, void* stream, void* const* events) {
+                      int32_t dtype, Mamba2Plan* p) {
   if (!q || !k || !v || !log_alpha || !o) return LL_ERR_NULL_ARG;
   ll_status st = check_shape(B, T, H, d_k, d_v, C);
   if (st != LL_OK) return st;
   if (Hqk < 1 || Hqk > H || H % Hqk != 0) return LL_ERR_BAD_SHAPE;
   if (dtype != LL_F32 && dtype != LL_BF16) return LL_ERR_UNSUPPORTED;
-  const ll::KernelEntry* e = find_mamba2(dtype, C, d_k, d_v);
-  if (!e) return LL_ERR_UNSUPPORTED;
-  const int L = levels_of(T);
+  p->e = find_mamba2(dtype, C, d_k, d_v);
+  if (!p->e) return LL_ERR_UNSUPPORTED;
+  p->L = levels_of(T);
   const int64_t tiles = ll::tiles_of(T, C);
   // B * H indexes the second grid dimension of the scan kernels (at most 65535)
-  if (L > kMaxL || tiles > kMaxTiles || B * H > 65535 || tiles * 2 * H * B >= (int64_t(1) << 31))
+  if (p->L > kMaxL || tiles > kMaxTiles || B * H > 65535 || tiles * 2 * H * B >= (int64_t(1) << 31))
     return LL_ERR_UNSUPPORTED;
-  const bool fused = ll::mamba2_fused_supported(dtype, C, d_k, d_v, lambda != nullptr);
-  const int64_t need = fused ? ll::mamba2_fused_workspace(B, T, H, d_k, d_v, nullptr)
-                             : ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), lambda != nullptr, nullptr);
-  if (!workspace) return LL_ERR_NULL_ARG;
-  if ((int64_t)workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
+  p->fused = ll::mamba2_fused_supported(dtype, C, d_k, d_v, lambda != nullptr);
+  p->need = p->fused ? ll::mamba2_fused_workspace(B, T, H, d_k, d_v, nullptr)
+                     : ll::mamba2_workspace(B, T, H, d_k, d_v, C, elem_size(dtype), lambda != nullptr, nullptr);
+  return LL_OK;
+}
 
+ll_status mamba2_launch(const Mamba2Plan& p, const void* q, const void* k, const void* v, const float* log_alpha,
+                        const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t Hqk, int64_t d_k,
+                        int64_t d_v, int64_t C, void* workspace, void* stream, void* const* events) {
   ll::Mamba2Args a;
   a.q = q; a.k = k; a.v = v; a.log_alpha = log_alpha; a.lambda = lambda; a.o = o;
   a.B = B; a.T = T; a.H = H; a.dk = d_k; a.dv = d_v; a.C = C;
   a.Hqk = Hqk;
-  a.L = L;
+  a.L = p.L;
   a.workspace = workspace;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipEvent_t ev[ll::kMamba2Stages + 1];
   if (events)
     for (int i = 0; i <= ll::kMamba2Stages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);
-  const hipError_t err = fused ? ll::launch_mamba2_fused(a, hs, events ? ev : nullptr) : e->launch(a, hs, events ? ev : nullptr);
+  const hipError_t err =
+      p.fused ? ll::launch_mamba2_fused(a, hs, events ? ev : nullptr) : p.e->launch(a, hs, events ? ev : nullptr);
   return err == hipSuccess ? LL_OK : LL_ERR_HIP;
+}
+
+ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* lambda,
+                      void* o, int64_t B, int64_t T, int64_t H, int64_t Hqk, int64_t d_k, int64_t d_v, int64_t C,
+                      int32_t dtype, void* workspace, size_t workspace_bytes, void* stream, void* const* events) {
+  Mamba2Plan p;
+  const ll_status st = mamba2_plan(q, k, v, log_alpha, lambda, o, B, T, H, Hqk, d_k, d_v, C, dtype, &p);
+  if (st != LL_OK) return st;
+  if (!workspace) return LL_ERR_NULL_ARG;
+  if ((int64_t)workspace_bytes < p.need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
+  return mamba2_launch(p, q, k, v, log_alpha, lambda, o, B, T, H, Hqk, d_k, d_v, C, workspace, stream, events);
 }
 ll_status mamba2_ml_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* Lambda,
                          int32_t form, void* o, int64_t B, int64_t T, int64_t H, int64_t d_k, int64_t d_v, int64_t C,
@@ -343,6 +369,66 @@ ll_status ll_gdn_fwd_staged(const void* q, const void* k, const void* v, const f
     if (!events[i]) return LL_ERR_NULL_ARG;
   return gdn_impl(q, k, v, log_alpha, beta, lambda, o, B, T, H, d_k, d_v, C, dtype, workspace, workspace_bytes, stream,
                   events);
+}
+
+}  // extern "C"
+
+// ---- forward without allocation ----------------------------------------------------------------
+// The workspace of ll_mamba2_fwd_noalloc: each GPU the library runs on holds one copy of this
+// array until the process ends.  In host code the name stands for a host-side shadow, not a device
+// address: host code only ever uses the address scratch_ptr() looked up for the device.
+static __device__ __align__(256) unsigned char scratch[LL_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch[kMaxDevices];  // device address of `scratch`, per device
+std::mutex g_scratch_mu;                    // serialises the one look-up per device
+
+// The device address of `scratch` on the device that `stream` belongs to (the current device for
+// the NULL stream), looked up on that device's first call with the device current.
+ll_status scratch_ptr(void* stream, void** out) {
+  int dev = -1;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (hs) {
+    hipDevice_t d = -1;
+    if (hipStreamGetDevice(hs, &d) != hipSuccess) return LL_ERR_HIP;
+    dev = d;
+  } else if (hipGetDevice(&dev) != hipSuccess) {
+    return LL_ERR_HIP;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return LL_ERR_UNSUPPORTED;
+  void* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      int cur = -1;
+      if (hipGetDevice(&cur) != hipSuccess) return LL_ERR_HIP;
+      if (cur != dev && hipSetDevice(dev) != hipSuccess) return LL_ERR_HIP;
+      const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (cur != dev) (void)hipSetDevice(cur);
+      if (e != hipSuccess || !p) return LL_ERR_HIP;
+      g_scratch[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return LL_OK;
+}
+}  // namespace
+
+extern "C" {
+
+ll_status ll_mamba2_fwd_noalloc(const void* q, const void* k, const void* v, const float* log_alpha,
+                                const float* lambda, void* o, int64_t B, int64_t T, int64_t H, int64_t d_k,
+                                int64_t d_v, int64_t C, int32_t dtype, void* stream) {
+  Mamba2Plan p;
+  ll_status st = mamba2_plan(q, k, v, log_alpha, lambda, o, B, T, H, H, d_k, d_v, C, dtype, &p);
+  if (st != LL_OK) return st;
+  if (p.need > (int64_t)LL_NOALLOC_SCRATCH_BYTES) return LL_ERR_SCRATCH;
+  void* ws = nullptr;
+  st = scratch_ptr(stream, &ws);
+  if (st != LL_OK) return st;
+  return mamba2_launch(p, q, k, v, log_alpha, lambda, o, B, T, H, H, d_k, d_v, C, ws, stream, nullptr);
 }
 
 ll_status ll_debug_level_map(int64_t T, int64_t C, int8_t* out, void* stream) {

@@ -68,6 +68,27 @@ def _m2g(H=4, Hqk=2, q=FAKE, T=128, dk=64, dv=64, C=64):
     return lib.ll_mamba2_fwd_grouped(q, FAKE, FAKE, FAKE, FAKE, FAKE, 1, T, H, Hqk, dk, dv, C, 1, FAKE, 1 << 40, None)
 
 
+def _m2n(q=FAKE, la=FAKE, lam=FAKE, o=FAKE, B=1, T=128, H=2, dk=64, dv=64, C=64, dtype=1):
+    return lib.ll_mamba2_fwd_noalloc(q, FAKE, FAKE, la, lam, o, B, T, H, dk, dv, C, dtype, None)
+
+
+def test_noalloc_checks_and_scratch_limit_return_before_launch():
+    """The allocation-free forward runs the checks of ll_mamba2_fwd, then rejects arguments whose
+    workspace exceeds its static scratch, all before touching a device."""
+    assert _m2n(q=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _m2n(o=None) == ll._lib.LL_ERR_NULL_ARG
+    assert _m2n(T=100) == ll._lib.LL_ERR_BAD_SHAPE
+    assert _m2n(dk=96) == ll._lib.LL_ERR_UNSUPPORTED
+    cap = ll.LL_NOALLOC_SCRATCH_BYTES
+    # bf16, C = 64, d = 128 with lambda: the single-pass workspace, about 256 bytes per token and head
+    for lam, T in ((FAKE, 16384), (None, 65536)):
+        need = ll.ll_workspace_size(ll.LL_MAMBA2, ll.LL_BF16, 1, T, 16, 128, 128, 64, lam is not None)
+        assert need > cap
+        assert _m2n(lam=lam, T=T, H=16, dk=128, dv=128) == ll._lib.LL_ERR_SCRATCH
+    assert ll.ll_workspace_size(ll.LL_MAMBA2, ll.LL_BF16, 1, 8192, 16, 128, 128, 64, 1) <= cap
+    assert ll.ll_status_string(ll._lib.LL_ERR_SCRATCH).startswith("LL_ERR_SCRATCH")
+
+
 def test_mamba2_grouped_argument_checks_return_before_launch():
     assert _m2g(q=None) == ll._lib.LL_ERR_NULL_ARG
     assert _m2g(Hqk=0) == ll._lib.LL_ERR_BAD_SHAPE
@@ -211,7 +232,7 @@ def test_debug_level_map_checks():
 
 
 def test_status_strings():
-    for s in range(6):
+    for s in range(7):
         assert ll.ll_status_string(s).startswith("LL_")
 
 
