@@ -192,6 +192,14 @@ __device__ inline void lds_gather4(void* dst, int n, Src src) {
 // Waits for this wave's outstanding vector-memory operations (including direct-to-LDS loads).
 __device__ inline void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
 
+// Waits until at most N of this wave's vector-memory operations are outstanding (they complete in
+// issue order); memory accesses are not moved across it.
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 // ------------------------------------------------------------------------- dispatch order
 
 // MI355X has 8 XCDs, each with its own L2, and hands out workgroups round-robin over them.

@@ -28,9 +28,15 @@
 // its own queue, held by workgroups that are already running, so the waits always end; each wait is
 // also bounded in time (a timed-out tile writes NaN rows and counts the event).  Nodes are written
 // with ordinary stores into the XCD's L2 and their flag is raised (device scope) after the stores are
-// acknowledged; readers poll the flag through the scalar cache, forced to miss it, and then load the
-// node with ordinary loads from the same L2.  No cache holds a node slot before it is published:
-// every slot is written once per launch and never read before its flag.
+// acknowledged; readers poll the flag with device-scope loads and then load the node with ordinary
+// loads from the same L2.  No cache holds a node slot before it is published: every slot is written
+// once per launch and never read before its flag.
+//
+// Latency.  Chains of odd tiles carry the nodes of large groups (node(u) waits for node(u - 1),
+// node(u - 2), node(u - 4), ...), so the kernel keeps each link short: an odd tile awaits all its
+// source flags first and then streams the source nodes through LDS one node ahead; K, V and the
+// gates are loaded before Q so that the state, and an even tile's node, do not wait for Q; and in
+// the level loop a node whose flag is not yet up is awaited after the current level's products.
 #include "ll_fast_tile.hpp"
 #include "ll_launch.hpp"
 
@@ -222,21 +228,13 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
   __bf16* node_bh = ws.node + bh * N * SZ;
   const int* flag_bh = ws.flag + bh * N;
 
-  // ---- loads: the raw gates, Q into registers, K, V, lambda into LDS; the block sums of the
-  //      tile's source groups (lane b: level b + 1)
+  // ---- loads: the raw gates, lambda, K and V into LDS and the block sums of the tile's source
+  //      groups (lane b: level b + 1) first; Q (into registers) once they are in, so that the
+  //      state, and an even tile's node, do not wait for it
   const float la_raw = tile_gate<R>(log_alpha, row0, nrow, H, h);
-  frag qA[KS], qB[KS];
-  {
-    const int rA = iA < nrow ? iA : nrow - 1, rB = iB < nrow ? iB : nrow - 1;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      qA[ks] = M::load(q + ((row0 + rA) * Hqk + hq) * DK + ks * M::KSTEP + g * M::KPL);
-      qB[ks] = M::load(q + ((row0 + rB) * Hqk + hq) * DK + ks * M::KSTEP + g * M::KPL);
-    }
-  }
+  if constexpr (HAS_LAMBDA) lds_copy_lambda<R, NT>(lam_s, lam, row0, H, h, L, nrow);
   lds_copy_rows<DK, R, NT>(k_s, k + (row0 * Hqk + hq) * DK, (int64_t)Hqk * DK, nrow);
   lds_copy_rows<DV, R, NT>(v_s, v + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
-  if constexpr (HAS_LAMBDA) lds_copy_lambda<R, NT>(lam_s, lam, row0, H, h, L, nrow);
   float lb = 0.f;
   if (lane < J && ((u >> lane) & 1)) lb = ws.bsum[bh * ws.stride + bsum_offset(N, lane) + (u >> lane) - 1];
 
@@ -250,9 +248,14 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
   const float gapv = wave_inclusive_scan(lb) - lb;
   wait_vmem();
   __syncthreads();  // K, V, lambda, decays visible
-  if (!liveB) {
+  frag qA[KS], qB[KS];
+  {
+    const int rA = iA < nrow ? iA : nrow - 1, rB = iB < nrow ? iB : nrow - 1;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qB[ks] = frag{};
+    for (int ks = 0; ks < KS; ++ks) {
+      qA[ks] = M::load(q + ((row0 + rA) * Hqk + hq) * DK + ks * M::KSTEP + g * M::KPL);
+      qB[ks] = liveB ? M::load(q + ((row0 + rB) * Hqk + hq) * DK + ks * M::KSTEP + g * M::KPL) : frag{};
+    }
   }
 
   // ---- the tile's state S_u = K^T diag(tdec) V: d_k x (this wave's d_v tiles), K = R tokens
@@ -317,7 +320,9 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
 
   auto slot_of = [&](int j) -> int64_t { return group_end(u, j) - 1; };  // node(e - 1) covers the group ending at e
 
-  // ---- odd tiles: node(u) = S_u + the tile's low-level groups, decayed to the end of the tile
+  // ---- odd tiles: node(u) = S_u + the tile's low-level groups, decayed to the end of the tile.
+  //      Every source flag is awaited first; then each wave streams its own pieces of the source
+  //      nodes through two slots of its own in the (now free) K and V regions, one node ahead.
   if (u & 1) {
     const int t = __builtin_ctz(~(unsigned)u);  // levels 1..t: the low set bits of u
     const float tot_u = cl_s[R - 1];
@@ -328,23 +333,39 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
       for (int nt = 0; nt < NTW; ++nt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[mt][nt][r] = to_f32(sbf[mt][nt][r]);
+    for (int j = 1; j <= t; ++j)
+      if (!wait_flag(flag_bh + slot_of(j), ws.ctr + 8)) tk_s[2] = 1;
+    __syncthreads();  // every wave is done with K and V
+    // slot x of this wave: SLICE bf16 = its pieces (d_k tile mt, d_v tile nt) at (mt NTW + nt) 256
+    constexpr int SLICE = DKT * NTW * 256, PCS = SLICE / 8, NPW = PCS / 64;
+    bf* const slots = (wave < 2 ? k_s : v_s) + (wave & 1) * 2 * SLICE;
+    auto issue = [&](int jj, bf* dst) {
+      const bf* src = node_bh + slot_of(jj) * SZ + wave * NTW * 256;
+#pragma unroll
+      for (int i = 0; i < NPW; ++i) {
+        const int pq = i * 64 + lane, mt = pq / (NTW * 32), rem = pq % (NTW * 32);
+        __builtin_amdgcn_global_load_lds(src + mt * MT * 256 + rem * 8,
+                                         (__attribute__((address_space(3))) void*)(dst + i * 512), 16, 0, 0);
+      }
+    };
+    issue(1, slots);
     for (int j = 1; j <= t; ++j) {
-      const int64_t s = slot_of(j);
-      if (!wait_flag(flag_bh + s, ws.ctr + 8)) tk_s[2] = 1;
+      if (j < t) {
+        issue(j + 1, slots + (j & 1) * SLICE);
+        wait_vmcnt<NPW>();
+      } else {
+        wait_vmcnt<0>();
+      }
       const float w = fast_exp2(gap_of(gapv, j) + tot_u);
-      const bf* src = node_bh + s * SZ;
-      bf16x4 pc[DKT][NTW];
+      const bf* cur = slots + ((j - 1) & 1) * SLICE;
 #pragma unroll
       for (int mt = 0; mt < DKT; ++mt)
 #pragma unroll
-        for (int nt = 0; nt < NTW; ++nt)
-          pc[mt][nt] = *reinterpret_cast<const bf16x4*>(src + ((mt * MT + wave * NTW + nt) * 64 + lane) * 4);
+        for (int nt = 0; nt < NTW; ++nt) {
+          const bf16x4 pc = *reinterpret_cast<const bf16x4*>(cur + (mt * NTW + nt) * 256 + lane * 4);
 #pragma unroll
-      for (int mt = 0; mt < DKT; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < NTW; ++nt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) acc[mt][nt][r] += w * to_f32(pc[mt][nt][r]);
+          for (int r = 0; r < 4; ++r) acc[mt][nt][r] += w * to_f32(pc[r]);
+        }
     }
 #pragma unroll
     for (int mt = 0; mt < DKT; ++mt)
@@ -357,11 +378,13 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
 
   // ---- inter-tile levels: the set bits of u, highest (oldest node) first; the nodes alternate
   //      between the K and V regions, the next one copied in while the current one is used
-  auto copy_level = [&](int j, bf* dst) {
-    const int64_t s = slot_of(j);
-    if (!wait_flag(flag_bh + s, ws.ctr + 8)) tk_s[2] = 1;
-    const bf* src = node_bh + s * SZ;
+  auto copy_node = [&](int j, bf* dst) {
+    const bf* src = node_bh + slot_of(j) * SZ;
     lds_gather16<NT>(dst, SZ * 2 / 16, [&](int x) { return src + 8 * x; });
+  };
+  auto copy_level = [&](int j, bf* dst) {
+    if (!wait_flag(flag_bh + slot_of(j), ws.ctr + 8)) tk_s[2] = 1;
+    copy_node(j, dst);
   };
   auto next_level = [&](int j) {
     for (--j; j >= 1; --j)
@@ -372,7 +395,12 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
     wait_vmem();
     __syncthreads();  // `cur` complete and visible; every wave is done with `nxt`
     const int jn = next_level(j);
-    if (jn) copy_level(jn, nxt);
+    // a node not yet published is awaited after this level's products, not before them
+    const bool early = jn && flag_up(flag_bh + slot_of(jn));
+    if (early) {
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+      copy_node(jn, nxt);
+    }
     const float gap = gap_of(gapv, j);
     float wA = fast_exp2(cliA + gap), wB = fast_exp2(cliB + gap);
     if constexpr (HAS_LAMBDA) {
@@ -397,6 +425,7 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
       oA[mt] += wA * tA;
       oB[mt] += wB * tB;
     }
+    if (jn && !early) copy_level(jn, nxt);
     j = jn;
   };
   int j = u ? bitlen((uint32_t)u) : 0;
