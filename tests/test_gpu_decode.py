@@ -81,3 +81,23 @@ def test_decode_spare_levels_and_restart():
     state = torch.empty(ll.ll_decode_state_bytes(1, 2, 16, 16, L + 3), dtype=torch.uint8, device="cuda")
     for _ in range(2):  # the second pass runs on the state the first one left behind
         assert rel_err(decode_all(y, "f32", L + 3, state=state), ref) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("dist,T,L", [("slow", 8192, 14), ("nodecay", 8192, 14), ("slow", 8200, 15)])
+def test_decode_long_sampled(dist, T, L):
+    """T decode steps of a d = 128 bf16 head pair: 8192 steps with the L = 14 levels of the
+    benchmark's decode run (positions 7192 .. 8191 of a 14-level state), and 8200 steps, whose
+    last positions reach level 14 (L = 15); sampled positions (the last 64, the powers of two and
+    random ones) against the row-restricted quadratic form."""
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=1, H=2, T=T, C=8, dist=dist, seed=140)
+    x = generate(w)
+    assert fenwick.num_levels(T) == L
+    got = decode_all(x, "bf16", L)
+    rng = np.random.default_rng(141)
+    rows = np.unique(np.concatenate([np.arange(T - 64, T), 2 ** np.arange(14) - 1, 2 ** np.arange(13),
+                                     rng.integers(0, T, 32)]))
+    ref = mamba2.quadratic(x["q"], x["k"], x["v"], x["log_alpha"], x["lam"], rows=rows)
+    err = rel_err(got[:, rows], ref)
+    print(f"decode T={T} {dist}: sampled rel err {err:.3e}", flush=True)
+    assert err <= TOL["bf16"], err
+

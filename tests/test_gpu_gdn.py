@@ -100,6 +100,32 @@ def test_parity_upper_level_slots(d, chunks):
     assert err <= TOL, err
 
 
+def test_parity_full_size_every_row_two_heads():
+    """Every output row of two heads of the T = 8192, 2 x 16-head workload (the launch
+    configuration the benchmark times) against the oracle's per-level recurrent form."""
+    from tests.oracle_pool import recurrent_heads
+    x = generate(BASE)
+    got = run_gdn(x, BASE.C)
+    heads = [(0, 0), (1, 15)]
+    refs = recurrent_heads("gdn", x, heads, ("q", "k", "v", "log_alpha", "beta", "lam"))
+    for (b, h), ref in zip(heads, refs):
+        err = rel_err(got[b:b + 1, :, h:h + 1], ref)
+        print(f"GDN T=8192 (b, h) = ({b}, {h}): every row rel err {err:.3e}", flush=True)
+        assert err <= TOL, (b, h, err)
+
+
+@pytest.mark.parametrize("dist,chunks", [("gdn", 128), ("gdn_nodecay", 260)])
+def test_lambda_null_long(dist, chunks):
+    """lambda == NULL (Gated DeltaNet's single running state, carried across every chunk) over
+    128 chunks with the workload's gates and 260 chunks with alpha = 1, every row against the
+    oracle's plain gated delta-rule recurrence."""
+    x = generate(BASE.with_(B=1, H=2, T=64 * chunks, dist=dist, seed=68 + chunks))
+    ref = gdn.gdn_recurrent(x["q"], x["k"], x["v"], x["log_alpha"], x["beta"])
+    err = rel_err(run_gdn(x, 64, with_lambda=False), ref)
+    print(f"GDN lambda=NULL {dist} chunks={chunks}: rel err {err:.3e}", flush=True)
+    assert err <= TOL, err
+
+
 def test_deterministic():
     import torch
     import paper_2506_04761_amd as ll

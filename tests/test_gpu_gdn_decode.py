@@ -62,3 +62,21 @@ def test_gdn_decode_matches_quadratic(dtype, dk, dv, T, dist):
         err = rel_err(gdn_decode_all(x, dtype, L, with_lambda), ref)
         print(f"gdn decode {dtype} dk={dk} dv={dv} T={T} {dist} lambda={with_lambda}: rel err {err:.3e}")
         assert err <= TOL[dtype], err
+
+
+def test_gdn_decode_long():
+    """8200 decode steps of one d = 128 bf16 head (L = 15: the last positions reach level 14):
+    every position against the oracle's per-level recurrent form (the quadratic form's T x T
+    solve is too large here)."""
+    T = 8200
+    w = WORKLOADS["ll_gdn_bf16_T8192"].with_(B=1, H=1, T=T, C=8, dist="gdn_slow", seed=142)
+    x = generate(w)
+    L = fenwick.num_levels(T)
+    assert L == 15
+    got = gdn_decode_all(x, "bf16", L)
+    ref = gdn.recurrent(x["q"], x["k"], x["v"], x["log_alpha"], x["beta"], x["lam"])
+    err = rel_err(got, ref)
+    late = rel_err(got[:, 8000:], ref[:, 8000:])
+    print(f"GDN decode T={T}: rel err {err:.3e}, positions >= 8000 {late:.3e}", flush=True)
+    assert err <= TOL["bf16"] and late <= TOL["bf16"], (err, late)
+

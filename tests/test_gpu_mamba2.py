@@ -187,6 +187,44 @@ def test_parity_T65536_full_size_sampled():
     assert _sampled_parity("ll_mamba2_bf16_T65536", heads=((0, 0), (0, 15))) <= TOL["bf16"]
 
 
+def test_parity_T65536_every_row_four_heads():
+    """Every output row of four of the 16 heads (the first and the last among them) of the
+    T = 65536 workload, in the launch configuration the benchmark times, against the oracle's
+    per-level recurrent form (one worker process per head)."""
+    from tests.oracle_pool import recurrent_heads
+    w = WORKLOADS["ll_mamba2_bf16_T65536"]
+    x = generate(w)
+    got = run_mamba2(x, w.dtype, w.C)
+    heads = [(0, 0), (0, 5), (0, 10), (0, 15)]
+    refs = recurrent_heads("mamba2", x, heads, ("q", "k", "v", "log_alpha", "lam"))
+    for (b, h), ref in zip(heads, refs):
+        err = rel_err(got[b:b + 1, :, h:h + 1], ref)
+        print(f"T=65536 head {h}: every row rel err {err:.3e}", flush=True)
+        assert err <= TOL["bf16"], (h, err)
+
+
+@pytest.mark.parametrize("lv", [12, 13, 14, 15, 16])
+def test_each_top_level_alone_T65536(lv):
+    """One-hot lambda at one of the top token levels 12..16 of T = 65536 (inter-tile levels 5..9
+    of the tiles of 128 tokens), with alpha = 1 so that the far levels carry full weight; sampled
+    rows (half of them with bit lv - 1 set, i.e. with keys at that level) against the
+    row-restricted quadratic form."""
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=1, H=2, dist="nodecay", seed=130 + lv)
+    x = generate(w)
+    lam = np.zeros_like(x["lam"])
+    lam[..., lv] = x["lam"][..., lv]
+    y = dict(x, lam=lam)
+    got = run_mamba2(y, w.dtype, w.C)
+    rng = np.random.default_rng(lv)
+    r = rng.integers(0, w.T, 24)
+    rows = np.unique(np.concatenate([r | (1 << (lv - 1)), r & ~(1 << (lv - 1)), [w.T - 1, (1 << (lv - 1))]]))
+    ref = mamba2.quadratic(y["q"], y["k"], y["v"], y["log_alpha"], y["lam"], rows=rows)
+    assert np.max(np.abs(ref)) > 0
+    err = rel_err(got[:, rows], ref)
+    print(f"level {lv} alone at T=65536: rel err {err:.3e}", flush=True)
+    assert err <= TOL["bf16"], err
+
+
 def test_parity_T8192_other_reading_of_distribution():
     # The large workloads say "same distributions as config 1"; the other possible reading
     # (the second workload's gates and unscaled values) must pass too.

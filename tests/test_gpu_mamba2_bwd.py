@@ -106,6 +106,18 @@ def test_bwd_full_size_sampled():
         assert e <= TOL["bf16"], (n, e)
     # the first gate only shifts every cumulative sum: its gradient vanishes
     assert np.max(np.abs(dla[:, 0])) <= TOL["bf16"] * np.max(np.abs(dla))
+    # Every position: dlog_alpha_t - dlog_alpha_{t+1} = q_t . dq_t - k_t . dk_t (dlog_alpha_T = 0), so
+    # these T differences pin the kernels' reverse cumulative sum (tile sums included) at full
+    # length.  The right side is formed in float64 from the returned bf16 dq and dk, whose rounding
+    # (at most 2^-8 of each element) bounds the gap by 2^-8 a_t, a_t = sum_d |q dq| + |k dk|; the
+    # test allows twice that plus a float32 margin.  (A reverse cumulative sum of the right side
+    # itself would add up T of those rounding errors.)
+    qf, kf = (x[n].astype(np.float64) for n in ("q", "k"))
+    per_pos = np.einsum("bthd,bthd->bth", qf, dq) - np.einsum("bthd,bthd->bth", kf, dk)
+    a_t = np.einsum("bthd,bthd->bth", np.abs(qf), np.abs(dq)) + np.einsum("bthd,bthd->bth", np.abs(kf), np.abs(dk))
+    gap = np.abs((dla - nxt) - per_pos) / (2.0 ** -7 * a_t + 1e-6 * np.max(np.abs(dla)))
+    print(f"T=65536 dlog_alpha differences at every position: worst gap / bound {gap.max():.3f}", flush=True)
+    assert gap.max() <= 1.0, (np.unravel_index(np.argmax(gap), gap.shape), gap.max())
     assert np.all(np.isfinite(dq)) and np.all(np.isfinite(dk)) and np.all(np.isfinite(dv))
 
 
