@@ -17,11 +17,20 @@
 // (bit j-1 of z clear) and propagates through P_z everywhere; a chunk with bit j-1 set adds
 // lambda_t^(log2 C + j) q~_t^T R_j to its rows, with R_j taken at the chunk's start.
 //
+// Block tree instead of a sequential scan.  For a block of chunks [a, c) let T = P_{c-1} ... P_a
+// (its transition) and A = sum over s in [a, c) of P_{c-1} ... P_{s+1} H_s (its accumulated state);
+// the block [a, c) = [a, b) then [b, c) has T = T_hi T_lo and A = T_hi A_lo + A_hi.  The level-j
+// state read by chunk z (bit j-1 set) is R_j = T(G_1) ... T(G_{j-1}) A(G_j), with G_j the aligned
+// source group of 2^(j-1) chunks ending at ((z >> (j-1)) << (j-1)) and G_1, .. the lower source
+// groups of z (its set bits below j-1), the most recent first.  So a chunk reads its levels from
+// the lowest set bit up, carrying q~^T through each group's transition: out += lambda^(j) q~^T A(G_j),
+// then q~^T <- q~^T T(G_j).  Every source group is the aligned block (level j-1, index
+// (z >> (j-1)) - 1) of a binary block tree built level by level.
+//
 // Kernels: gdn_chunk (one persistent workgroup per compute unit walking its chunks; per chunk the WY
 // solve in fp32 by a blocked inversion and all chunk-local products on MFMA, bf16 operands with fp32
-// accumulation) and gdn_scan (per (b, h, 16 d_v columns), sequential over the chunks: the level
-// states split over the waves by rows and by levels, shared through LDS, P_z / Q~ read once per
-// chunk).
+// accumulation), gdn_combine (one launch per tree level, one workgroup per block) and gdn_read (one
+// workgroup per chunk: the level read-out and the final output).
 #include <type_traits>
 
 #include "ll_device.hpp"
@@ -31,10 +40,8 @@ namespace ll {
 
 namespace gdn {
 
-constexpr int kMaxJ = 16;      // inter-chunk levels handled by the scan (T <= C * 2^16)
+constexpr int kMaxJ = 16;      // inter-chunk levels handled by the read-out (T <= C * 2^16)
 constexpr int kChunkWaves = 8; // waves per gdn_chunk workgroup
-constexpr int kSlice = 16;     // d_v columns per scan workgroup
-constexpr int kScanWaves = 8;  // waves per scan workgroup
 typedef __bf16 bf;
 
 // C = A B over 16x16 output tiles, A [M][K] row-major (lda), Bt = B^T [N][K] row-major (ldb), both
@@ -57,10 +64,21 @@ __device__ inline void gemm_lds(const bf* A, int lda, const bf* Bt, int ldb, Epi
   }
 }
 
+// "kfrag" layout of a K x N bf16 matrix X (KR = K rows), in which X is read as the B operand of a
+// product Y X: the operand fragment of column tile nt and k step ks (32 rows) is 64 lanes x 8
+// elements, lane (n % 16) + 16 ((k % 32) / 8) holding rows k with k % 8 = 0..7 in order.  The same
+// bytes are the A-operand fragments of X^T (row tile nt of X^T, k step ks).  Four consecutive rows
+// 4i .. 4i + 3 of one column are four consecutive elements.
+template <int KR>
+__device__ inline int kfrag_idx(int k, int n) {
+  return (((n >> 4) * (KR / 32) + (k >> 5)) * 64 + (n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7);
+}
+
 // ---------------------------------------------------------------------------------------------
 // Kernel 1: per-chunk WY solve and chunk-local products.  One workgroup (kChunkWaves waves) per chunk.
-// Outputs (workspace, per chunk): Qc [C][DK] bf16, P_z [DK][DK] bf16, H_z [DK][DV] bf16,
-// intra-chunk output [C][DV] fp32.
+// Outputs (workspace, per chunk): Qc [C][DK] bf16 row-major, P_z [DK][DK] bf16 (kfrag layout for
+// even chunks z, row-major for odd ones: the two sides of a tree combination), H_z [DK][DV] bf16
+// (kfrag), intra-chunk output [C][DV] fp32 row-major.
 // ---------------------------------------------------------------------------------------------
 template <int C, int DK, int DV, bool HAS_LAMBDA>
 __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __restrict__ q, const bf* __restrict__ k,
@@ -340,221 +358,259 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int d = mt * 16 + 4 * g + r, e = nt * 16 + r16;
-      pz[d * DK + e] = static_cast<bf>((d == e ? gC : 0.f) - acc[r]);
+      pz[(z & 1) ? d * DK + e : kfrag_idx<DK>(d, e)] = static_cast<bf>((d == e ? gC : 0.f) - acc[r]);
     }
   });
   bf* hz = hz_out + cidx * (DK * DV);
   gemm_lds<DK, DV, C>(kdt_s, LDC, ut_s, LDC, [&](int mt, int nt, f32x4 acc) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) hz[(mt * 16 + 4 * g + r) * DV + nt * 16 + r16] = static_cast<bf>(acc[r]);
+    for (int r = 0; r < 4; ++r) hz[kfrag_idx<DK>(mt * 16 + 4 * g + r, nt * 16 + r16)] = static_cast<bf>(acc[r]);
   });
   }  // chunk loop
 }
 
 // ---------------------------------------------------------------------------------------------
-// Kernel 2: level scan.  One workgroup (8 waves) per (b, h, 16 d_v columns), sequential over
-// the chunks.  Each level state R_j (d_k x 16) is split over the waves by rows and levels: wave w
-// owns rows 32 (w % 4) .. 32 (w % 4) + 31 (DK = 128; 16 rows for DK = 64) of the levels
-// j = 1 + (w / 4) + 2 m, in fp32 registers in the MFMA result layout, and reads out chunk row
-// tile w % 4 for those levels.  Every wave therefore does the same work.  The propagation
-// P_z R_j needs all of R_j's rows as the B operand, so the states of the chunk's start are kept
-// in LDS too (bf16, transposed, 16-byte chunks XOR-swizzled by column), rewritten by their owners
-// after each step.
-// Per step: barrier A (chunk z and the start states are in LDS), propagation and read-out, barrier
-// B, then the owners write the new states, P_z and Q~ of chunk z + 1 (loaded into registers during
-// the step) go into their single LDS buffers, and the two level groups' partial outputs are added
-// to the intra-chunk output.  The H_z and intra-output slices and the level weights come by direct
-// global->LDS loads into double buffers, one chunk ahead.
-// lambda == NULL: one state (level slot 0 of the first level group), read by every chunk.
-// SLOTS: level slots per wave (levels up to 2 SLOTS; 1 for lambda == NULL).
+// Kernel 2: one level m >= 1 of the block tree.  Block (m, k) of a sequence covers chunks
+// [k 2^m, (k + 1) 2^m).  It is formed from blocks lo = 2k and hi = 2k + 1 of level m - 1:
+// T = T_hi T_lo, A = T_hi A_lo + A_hi, fp32 accumulation, one RNE cast.  Storage of a block:
+// T (DK x DK) then A (DK x DV), A in the kfrag layout, T in the kfrag layout when k is even (the
+// source groups that chunks read, and the lo side of the next level) and row-major when k is odd
+// (the hi side).  Level 0 is the chunk kernel's P_z and H_z (same layout rule, by chunk parity).
+// The (DK + DV) / 16 column tiles of [T | A] are split over kCombineSplit-column-tile workgroups,
+// which the dispatch-order remap keeps on one XCD; wave w forms rows 16 (RT w + i) + 0..15 of its
+// workgroup's tiles (RT = DK / 64).  An odd block's T is formed transposed (T^T = T_lo^T T_hi^T)
+// so that its rows are stored whole.  Every operand fragment of a workgroup is loaded up front.
 // ---------------------------------------------------------------------------------------------
-template <int C, int DK, int DV, bool HAS_LAMBDA, int SLOTS>
-__global__ __launch_bounds__(64 * kScanWaves) void k_gdn_scan(const float* __restrict__ lam, const bf* __restrict__ qc_in,
-                                                  const bf* __restrict__ pz_in, const bf* __restrict__ hz_in,
-                                                  const float* __restrict__ oin_in, bf* __restrict__ o,
-                                                  int64_t Tlen, int H, int L, int J) {
+constexpr int kCombineTiles = 4;  // column tiles per workgroup
+
+template <int DK, int DV>
+__global__ __launch_bounds__(256) void k_gdn_combine(const bf* __restrict__ t_in, const bf* __restrict__ a_in,
+                                                     int64_t t_stride, int64_t a_stride, int64_t n_in,
+                                                     bf* __restrict__ out, int64_t n_out) {
   using MF = Mfma<bf>;
+  typedef MF::frag frag;
+  constexpr int KS = DK / 32, RT = DK / 64;  // k steps; row tiles per wave
+  constexpr int TT = DK / 16, AT = DV / 16;  // column tiles of T and A
+  constexpr int CT = kCombineTiles, S = (TT + AT) / CT;
+  static_assert(TT % CT == 0 && AT % CT == 0, "a workgroup's tiles lie in T or in A");
+  constexpr int BS = DK * (DK + DV);
+  const int64_t id = xcd_remap(blockIdx.x, (int64_t)gridDim.x);
+  const int64_t kb = id / S, bh = blockIdx.y;
+  const int c0 = (int)(id % S) * CT;  // first column tile of [T | A]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
+  const bf* tlo = t_in + (bh * n_in + 2 * kb) * t_stride;
+  const bf* thi = tlo + t_stride;
+  const bf* alo = a_in + (bh * n_in + 2 * kb) * a_stride;
+  const bf* ahi = alo + a_stride;
+  bf* tout = out + (bh * n_out + kb) * BS;
+  bf* aout = tout + DK * DK;
+  const bool t_part = c0 < TT, transposed = t_part && (kb & 1);
+
+  // A operand: rows of T_hi (row-major), or for a transposed T the rows of T_lo^T (kfrag of T_lo);
+  // rows 16 (RT wave + i) + r16, k = 32 ks + 8 g + 0..7
+  frag fa[RT][KS];
+  // B operand of column tile c0 + c: A_lo or T_lo (kfrag), or for a transposed T the rows of T_hi
+  frag fb[CT][KS];
+#pragma unroll
+  for (int i = 0; i < RT; ++i)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      fa[i][ks] = transposed ? MF::load(tlo + (((RT * wave + i) * KS + ks) * 64 + lane) * 8)
+                             : MF::load(thi + (16 * (RT * wave + i) + r16) * DK + 32 * ks + 8 * g);
+#pragma unroll
+  for (int c = 0; c < CT; ++c)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int nt = t_part ? c0 + c : c0 - TT + c;
+      fb[c][ks] = transposed ? MF::load(thi + (16 * nt + r16) * DK + 32 * ks + 8 * g)
+                             : MF::load((t_part ? tlo : alo) + ((nt * KS + ks) * 64 + lane) * 8);
+    }
+#pragma unroll
+  for (int c = 0; c < CT; ++c) {
+    const int nt = t_part ? c0 + c : c0 - TT + c;
+    f32x4 acc[RT];
+#pragma unroll
+    for (int i = 0; i < RT; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int i = 0; i < RT; ++i) acc[i] = MF::mma(fa[i][ks], fb[c][ks], acc[i]);
+#pragma unroll
+    for (int i = 0; i < RT; ++i) {
+      const int row0 = 16 * (RT * wave + i) + 4 * g;
+      bf16x4 res;
+      if (!t_part) {  // A = T_hi A_lo + A_hi; the lane's four rows are four consecutive kfrag elements
+        const int idx = kfrag_idx<DK>(row0, 16 * nt + r16);
+        const bf16x4 add = *reinterpret_cast<const bf16x4*>(ahi + idx);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) res[r] = static_cast<bf>(acc[i][r] + static_cast<float>(add[r]));
+        *reinterpret_cast<bf16x4*>(aout + idx) = res;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) res[r] = static_cast<bf>(acc[i][r]);
+        if (!transposed)  // T = T_hi T_lo, kfrag
+          *reinterpret_cast<bf16x4*>(tout + kfrag_idx<DK>(row0, 16 * nt + r16)) = res;
+        else  // lane value r is T[16 nt + r16][row0 + r]: row-major T
+          *reinterpret_cast<bf16x4*>(tout + (16 * nt + r16) * DK + row0) = res;
+      }
+    }
+  }
+}
+
+// Element offset of tree level m >= 1 in the tree region (levels 1 .. m-1 before it).
+__device__ __host__ inline int64_t tree_level_offset(int64_t BH, int64_t N, int m, int64_t block_size) {
+  int64_t off = 0;
+  for (int x = 1; x < m; ++x) off += BH * (N >> x) * block_size;
+  return off;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Kernel 3: read-out.  One workgroup (4 waves) per chunk z.  The chunk's Q~ rows are carried
+// through its source groups from the lowest set bit of z up: at level j (bit j - 1 set) the rows
+// add lambda_t^(log2 C + j) q~_t^T A(G_j) and, if a higher bit follows, become q~^T T(G_j).  The
+// node fragments come straight from global memory in the kfrag layout; Q~ lives in LDS (double
+// buffered, bf16); wave w owns the output columns DV/4 w .. and the Q~ columns DK/4 w .. .  The
+// chunk's intra-chunk output is added at the end and the rows are stored through LDS.
+// lambda == NULL: every level weight is 1 (Gated DeltaNet: the whole prefix state).
+// ---------------------------------------------------------------------------------------------
+template <int C, int DK, int DV, bool HAS_LAMBDA>
+__global__ __launch_bounds__(256) void k_gdn_read(const float* __restrict__ lam, const bf* __restrict__ qc_in,
+                                                  const bf* __restrict__ pz, const bf* __restrict__ hz,
+                                                  const bf* __restrict__ tree, const float* __restrict__ oin_in,
+                                                  bf* __restrict__ o, int64_t Tlen, int H, int L, int BH) {
+  using MF = Mfma<bf>;
+  typedef MF::frag frag;
   constexpr int LOG2C = (C == 16) ? 4 : (C == 32) ? 5 : 6;
-  constexpr int MTD = DK / 16;          // 16-row tiles of a state
-  constexpr int MPW = MTD / 4;          // of them owned by a wave
-  constexpr int KS = DK / 32;           // k steps over d_k
-  constexpr int NSL = DV / kSlice;
-  constexpr int LPW = SLOTS;                       // level slots per wave
-  static_assert(HAS_LAMBDA ? 2 * SLOTS <= kMaxJ : SLOTS == 1, "level slots");
-  constexpr int NLV = HAS_LAMBDA ? kMaxJ : 1;      // level states kept in LDS
-  constexpr int NT = 64 * kScanWaves;
-  constexpr int CPR = DK / 8;           // 16-byte chunks per state column / per P_z or Q~ row
-  constexpr int PZC = DK * CPR / NT, QCC = C * CPR / NT;  // chunks per thread of P_z, Q~
-  static_assert(kSlice == 16 && kScanWaves == 8 && C == 64, "4 row groups x 2 level groups, 4 chunk row tiles");
-  static_assert(MTD % 4 == 0 && PZC >= 1 && QCC >= 1 && DK * CPR % NT == 0 && C * CPR % NT == 0, "tile split");
-  __shared__ bf pz_s[DK * DK];                       // swizzled rows
-  __shared__ bf qc_s[C * DK];                        // swizzled rows
-  __shared__ bf rs_s[NLV * kSlice * DK];             // [level][column][row], swizzled chunks
-  __shared__ bf hz_s[2][DK * kSlice];                // [row][16]
-  __shared__ float oin_s[2][C * kSlice];             // [t][16]
-  __shared__ float lw_s[2][HAS_LAMBDA ? C * kMaxJ : 1];
-  __shared__ float part_s[2 * C * kSlice];           // [level group][t][16]
+  constexpr int KS = DK / 32, RT = C / 16;  // k steps; row tiles (all of them, every wave)
+  constexpr int VT = DV / 64, KT = DK / 64; // column tiles of this wave: output, carried Q~
+  constexpr int LDQ = DK + 8;
+  constexpr int BS = DK * (DK + DV);
+  static_assert(C == 64 && VT >= 1 && KT >= 1, "four row tiles, whole column tiles per wave");
+  static_assert(2 * C * LDQ * 2 >= C * DV * 4, "the output staging fits the Q~ buffers");
+  __shared__ __attribute__((aligned(16))) bf q_s[2][C * LDQ];
+  __shared__ float lw_s[HAS_LAMBDA ? C * kMaxJ : 1];
 
   const int64_t N = Tlen / C;
-  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // (b, h, slice)
-  const int sl = (int)(work % NSL);
-  const int64_t bh = work / NSL;
+  const int64_t work = xcd_remap(blockIdx.x, (int64_t)gridDim.x);  // (b h, z): a sequence's chunks on one XCD
+  const int64_t z = work % N, bh = work / N;
   const int h = (int)(bh % H), b = (int)(bh / H);
+  const int64_t cidx = bh * N + z;
+  const int64_t tok0 = (int64_t)b * Tlen + z * C;
   const int tid = threadIdx.x, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int rg = wave & 3, lgp = wave >> 2;  // row group, level group
-  const int p0 = sl * kSlice;
+  const int J = N <= 1 ? 0 : 32 - __builtin_clz((unsigned)(N - 1));
 
-  // state entry (level slot l, column c, row) in rs_s
-  auto rs_off = [](int l, int c, int row) {
-    return (l * kSlice + c) * DK + ((((row >> 3) ^ c) & (CPR - 1)) << 3) + (row & 7);
-  };
-  // the small per-chunk inputs into buffer half `buf`
-  auto fetch = [&](int64_t z, int buf) {
-    const int64_t cidx = bh * N + z;
-    const int64_t tok0 = (int64_t)b * Tlen + z * C;
-    const bf* hs = hz_in + cidx * (DK * DV) + p0;
-    lds_gather16<NT>(hz_s[buf], DK * 2, [&](int q) { return hs + (q >> 1) * DV + (q & 1) * 8; });
-    const float* os = oin_in + cidx * (C * DV) + p0;
-    lds_gather16<NT>(oin_s[buf], C * 4, [&](int q) { return os + (q >> 2) * DV + (q & 3) * 4; });
-    if constexpr (HAS_LAMBDA) {
-      if (J > 0) {  // weights of levels LOG2C + 1 .. LOG2C + J (slots jj >= J repeat level J)
-        const float* ls = lam + (tok0 * H + h) * L + LOG2C + 1;
-        lds_gather4<NT>(lw_s[buf], C * kMaxJ, [&](int q) {
-          const int t = q / kMaxJ, jj = q % kMaxJ;
-          return ls + (int64_t)t * H * L + (jj < J ? jj : J - 1);
-        });
-      }
+  for (int x = tid; x < C * DK / 8; x += 256) {
+    const int t = x / (DK / 8), c = x % (DK / 8);
+    *reinterpret_cast<bf16x8*>(&q_s[0][t * LDQ + 8 * c]) =
+        *reinterpret_cast<const bf16x8*>(qc_in + cidx * (C * DK) + t * DK + 8 * c);
+  }
+  if constexpr (HAS_LAMBDA) {
+    for (int x = tid; x < C * J; x += 256) {
+      const int t = x / J, jj = x % J;
+      lw_s[t * kMaxJ + jj] = lam[((tok0 + t) * H + h) * L + LOG2C + 1 + jj];
     }
-  };
-  // P_z and Q~ of chunk z into registers, then (once the step's readers are done) into LDS
-  bf16x8 pzr[PZC], qcr[QCC];
-  auto load_big = [&](int64_t z) {
-    const int64_t cidx = bh * N + z;
-#pragma unroll
-    for (int e = 0; e < PZC; ++e) {
-      const int x = e * NT + tid;
-      pzr[e] = *reinterpret_cast<const bf16x8*>(pz_in + cidx * (DK * DK) + (x / CPR) * DK + (x % CPR) * 8);
-    }
-#pragma unroll
-    for (int e = 0; e < QCC; ++e) {
-      const int x = e * NT + tid;
-      qcr[e] = *reinterpret_cast<const bf16x8*>(qc_in + cidx * (C * DK) + (x / CPR) * DK + (x % CPR) * 8);
-    }
-  };
-  auto store_big = [&]() {
-#pragma unroll
-    for (int e = 0; e < PZC; ++e) {
-      const int x = e * NT + tid;
-      *reinterpret_cast<bf16x8*>(pz_s + swz<DK>(x / CPR, x % CPR)) = pzr[e];
-    }
-#pragma unroll
-    for (int e = 0; e < QCC; ++e) {
-      const int x = e * NT + tid;
-      *reinterpret_cast<bf16x8*>(qc_s + swz<DK>(x / CPR, x % CPR)) = qcr[e];
-    }
-  };
+  }
+  __syncthreads();
 
-  f32x4 R[LPW][MPW];
+  f32x4 acc[RT][VT];
 #pragma unroll
-  for (int m = 0; m < LPW; ++m)
+  for (int mt = 0; mt < RT; ++mt)
 #pragma unroll
-    for (int i = 0; i < MPW; ++i) R[m][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int x = tid; x < NLV * kSlice * DK / 8; x += NT) reinterpret_cast<bf16x8*>(rs_s)[x] = bf16x8{};
-  load_big(0);
-  store_big();
-  fetch(0, 0);
-  for (int64_t z = 0; z < N; ++z) {
-    const int buf = (int)(z & 1);
-    const int64_t tok0 = (int64_t)b * Tlen + z * C;
-    wait_vmem();
-    __syncthreads();  // A: chunk z and the start states in LDS; every wave is done with the other half
-    if (z + 1 < N) {
-      fetch(z + 1, buf ^ 1);
-      load_big(z + 1);
+    for (int v = 0; v < VT; ++v) acc[mt][v] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int cur = 0;
+  unsigned bits = (unsigned)z;
+  while (bits) {
+    const int m = __builtin_ctz(bits);  // tree level of the source group; token level log2 C + m + 1
+    bits &= bits - 1;
+    const int64_t kblk = (z >> m) - 1;
+    const bf *tn, *an;
+    if (m == 0) {
+      tn = pz + (bh * N + kblk) * (DK * DK);
+      an = hz + (bh * N + kblk) * (DK * DV);
+    } else {
+      tn = tree + tree_level_offset(BH, N, m, BS) + (bh * (N >> m) + kblk) * BS;
+      an = tn + DK * DK;
     }
-
-    f32x4 out = {0.f, 0.f, 0.f, 0.f};  // chunk rows 16 rg + 4g + r, column p0 + r16
-    // this lane's entries of H_z (rows 16 (MPW rg + i) + 4g + r, column p0 + r16)
-    f32x4 hzv[MPW];
+    frag ba[VT][KS], bt[KT][KS];
 #pragma unroll
-    for (int i = 0; i < MPW; ++i)
+    for (int v = 0; v < VT; ++v)
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        hzv[i][r] = static_cast<float>(hz_s[buf][(16 * (MPW * rg + i) + 4 * g + r) * kSlice + r16]);
-
+      for (int ks = 0; ks < KS; ++ks) ba[v][ks] = MF::load(an + (((VT * wave + v) * KS + ks) * 64 + lane) * 8);
+    if (bits) {
 #pragma unroll
-    for (int m = 0; m < LPW; ++m) {
-      int j;
-      bool reader, source, restart;
-      if constexpr (HAS_LAMBDA) {
-        j = 1 + lgp + 2 * m;
-        if (j > J) continue;
-        reader = (z >> (j - 1)) & 1;
-        source = !reader;
-        restart = (z & ((int64_t(1) << j) - 1)) == 0;
-      } else {
-        if (lgp != 0) continue;
-        j = 0;
-        reader = z > 0;
-        source = true;
-        restart = z == 0;
-      }
-      const int slot = HAS_LAMBDA ? j - 1 : 0;
-      // B fragments of R_j at the chunk's start: column r16, rows 32 ks + 8 g .. + 7
-      bf16x8 rb[KS];
+      for (int v = 0; v < KT; ++v)
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        rb[ks] = *reinterpret_cast<const bf16x8*>(rs_s + rs_off(slot, r16, 32 * ks + 8 * g));
-      if (reader) {
-        f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
+        for (int ks = 0; ks < KS; ++ks) bt[v][ks] = MF::load(tn + (((KT * wave + v) * KS + ks) * 64 + lane) * 8);
+    }
+    // q~ A(G) for this wave's output columns and, when a higher level follows, q~ T(G) for its
+    // q~ columns, from one read of each q~ fragment
+    const bf* qs = q_s[cur];
+    f32x4 part[RT][VT], qn[RT][KT];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) tmp = MF::mma(frag_along_row_swz<DK>(qc_s, 16 * rg, 4 * ks), rb[ks], tmp);
+    for (int mt = 0; mt < RT; ++mt) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = 16 * rg + 4 * g + r;
-          const float wgt = HAS_LAMBDA ? lw_s[buf][t * kMaxJ + (j - 1)] : 1.f;
-          out[r] += wgt * tmp[r];
+      for (int v = 0; v < VT; ++v) part[mt][v] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int v = 0; v < KT; ++v) qn[mt][v] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int mt = 0; mt < RT; ++mt) {
+        const frag a = *reinterpret_cast<const bf16x8*>(&qs[(16 * mt + r16) * LDQ + 32 * ks + 8 * g]);
+#pragma unroll
+        for (int v = 0; v < VT; ++v) part[mt][v] = MF::mma(a, ba[v][ks], part[mt][v]);
+        if (bits) {
+#pragma unroll
+          for (int v = 0; v < KT; ++v) qn[mt][v] = MF::mma(a, bt[v][ks], qn[mt][v]);
         }
       }
 #pragma unroll
-      for (int i = 0; i < MPW; ++i) {
-        if (restart) {
-          R[m][i] = hzv[i];
-        } else {
-          f32x4 acc = source ? hzv[i] : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int mt = 0; mt < RT; ++mt)
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks)
-            acc = MF::mma(frag_along_row_swz<DK>(pz_s, 16 * (MPW * rg + i), 4 * ks), rb[ks], acc);
-          R[m][i] = acc;
-        }
+      for (int r = 0; r < 4; ++r) {
+        const float w = HAS_LAMBDA ? lw_s[(16 * mt + 4 * g + r) * kMaxJ + m] : 1.f;
+#pragma unroll
+        for (int v = 0; v < VT; ++v) acc[mt][v][r] += w * part[mt][v][r];
       }
-    }
+    if (bits) {
+      bf* qd = q_s[cur ^ 1];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) part_s[(lgp * C + 16 * rg + 4 * g + r) * kSlice + r16] = out[r];
-    __syncthreads();  // B: every read of the start states, P_z and Q~ is done; partial outputs complete
+      for (int mt = 0; mt < RT; ++mt)
+#pragma unroll
+        for (int v = 0; v < KT; ++v)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) qd[(16 * mt + 4 * g + r) * LDQ + 16 * (KT * wave + v) + r16] = static_cast<bf>(qn[mt][v][r]);
+      __syncthreads();  // the carried rows complete; every wave is done with the old ones
+      cur ^= 1;
+    }
+  }
 
-    // the new states (rows 16 (MPW rg + i) + 4g .. + 3 of column r16: 8 bytes each)
+  // o = intra-chunk output + the levels, rows staged through LDS (over the Q~ buffers)
+  __syncthreads();
+  float* o_s = reinterpret_cast<float*>(&q_s[0][0]);
 #pragma unroll
-    for (int m = 0; m < LPW; ++m) {
-      const int j = HAS_LAMBDA ? 1 + lgp + 2 * m : 0;
-      if (HAS_LAMBDA ? j > J : lgp != 0) continue;
-      const int slot = HAS_LAMBDA ? j - 1 : 0;
+  for (int mt = 0; mt < RT; ++mt)
 #pragma unroll
-      for (int i = 0; i < MPW; ++i) {
-        bf16x4 v4;
+    for (int v = 0; v < VT; ++v)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v4[r] = static_cast<bf>(R[m][i][r]);
-        *reinterpret_cast<bf16x4*>(rs_s + rs_off(slot, r16, 16 * (MPW * rg + i) + 4 * g)) = v4;
-      }
+      for (int r = 0; r < 4; ++r) o_s[(16 * mt + 4 * g + r) * DV + 16 * (VT * wave + v) + r16] = acc[mt][v][r];
+  __syncthreads();
+  const float* oin = oin_in + cidx * (C * DV);
+  for (int x = tid; x < C * DV / 8; x += 256) {
+    const int t = x / (DV / 8), c = 8 * (x % (DV / 8));
+    const f32x4 a0 = *reinterpret_cast<const f32x4*>(oin + t * DV + c);
+    const f32x4 a1 = *reinterpret_cast<const f32x4*>(oin + t * DV + c + 4);
+    const f32x4 s0 = *reinterpret_cast<const f32x4*>(o_s + t * DV + c);
+    const f32x4 s1 = *reinterpret_cast<const f32x4*>(o_s + t * DV + c + 4);
+    bf16x8 res;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      res[e] = static_cast<bf>(a0[e] + s0[e]);
+      res[4 + e] = static_cast<bf>(a1[e] + s1[e]);
     }
-    if (z + 1 < N) store_big();
-    for (int idx = tid; idx < C * kSlice; idx += NT) {
-      const int t = idx / kSlice, p = idx % kSlice;
-      float acc = oin_s[buf][idx] + part_s[idx];
-      if constexpr (HAS_LAMBDA) acc += part_s[C * kSlice + idx];
-      o[((tok0 + t) * H + h) * DV + p0 + p] = static_cast<bf>(acc);
-    }
+    *reinterpret_cast<bf16x8*>(o + ((tok0 + t) * H + h) * DV + c) = res;
   }
 }
 
@@ -572,13 +628,17 @@ int64_t gdn_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, i
   w.pz = cur; cur += al(BHN * dk * dk * 2);
   w.hz = cur; cur += al(BHN * dk * dv * 2);
   w.oin = cur; cur += al(BHN * C * dv * 4);
+  int64_t blocks = 0;  // tree levels 1 .. J-1 (the source groups of 2 .. 2^(J-1) chunks)
+  for (int64_t m = 1; (int64_t(1) << m) < N; ++m) blocks += N >> m;
+  w.tree = cur; cur += al(B * H * blocks * dk * (dk + dv) * 2);
   w.total = cur;
   if (lay) *lay = w;
   return cur;
 }
 
 // Enqueues the two stages on `st`.  With `ev` non-null, ev[0] is recorded before the chunk
-// kernel, ev[1] between the kernels and ev[2] after the scan (used by the staged entry point).
+// kernel, ev[1] after it and ev[2] after the tree and read-out kernels (used by the staged entry
+// point).
 template <int C, int DK, int DV>
 hipError_t launch_gdn(const GdnArgs& a, hipStream_t st, hipEvent_t* ev) {
   GdnLayout w;
@@ -595,7 +655,7 @@ hipError_t launch_gdn(const GdnArgs& a, hipStream_t st, hipEvent_t* ev) {
   int dev = 0, ncu = 0;
   if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu < 1)
     ncu = 256;
-  const dim3 g1((unsigned)(nchunks < ncu ? nchunks : ncu)), g2((unsigned)(a.B * a.H * (DV / gdn::kSlice)));
+  const dim3 g1((unsigned)(nchunks < ncu ? nchunks : ncu));
   const __bf16* q = static_cast<const __bf16*>(a.q);
   const __bf16* k = static_cast<const __bf16*>(a.k);
   const __bf16* v = static_cast<const __bf16*>(a.v);
@@ -608,15 +668,25 @@ hipError_t launch_gdn(const GdnArgs& a, hipStream_t st, hipEvent_t* ev) {
     hipLaunchKernelGGL((gdn::k_gdn_chunk<C, DK, DV, false>), g1, dim3(64 * gdn::kChunkWaves), 0, st, q, k, v, a.log_alpha, a.beta,
                        a.lambda, qc, pz, hz, oin, a.T, (int)a.H, a.L, nchunks);
   if (ev) (void)hipEventRecord(ev[1], st);
-  if (a.lambda && J <= 8)
-    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, true, 4>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz,
-                       hz, oin, o, a.T, (int)a.H, a.L, J);
-  else if (a.lambda)
-    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, true, gdn::kMaxJ / 2>), g2, dim3(64 * gdn::kScanWaves), 0, st,
-                       a.lambda, qc, pz, hz, oin, o, a.T, (int)a.H, a.L, J);
+  // the block tree, one level per launch (level m from level m - 1; level 0 = P_z, H_z)
+  __bf16* tree = reinterpret_cast<__bf16*>(base + w.tree);
+  const int64_t BH = a.B * a.H, BS = (int64_t)DK * (DK + DV);
+  for (int m = 1; m < J; ++m) {
+    const __bf16* tin = m == 1 ? pz : tree + gdn::tree_level_offset(BH, N, m - 1, BS);
+    const __bf16* ain = m == 1 ? hz : tin + DK * DK;
+    const int64_t ts = m == 1 ? DK * DK : BS, as = m == 1 ? DK * DV : BS;
+    const int64_t nin = m == 1 ? N : (N >> (m - 1));
+    constexpr int split = (DK + DV) / 16 / gdn::kCombineTiles;
+    hipLaunchKernelGGL((gdn::k_gdn_combine<DK, DV>), dim3((unsigned)((N >> m) * split), (unsigned)BH), dim3(256), 0, st,
+                       tin, ain, ts, as, nin, tree + gdn::tree_level_offset(BH, N, m, BS), N >> m);
+  }
+  const dim3 g2((unsigned)nchunks);
+  if (a.lambda)
+    hipLaunchKernelGGL((gdn::k_gdn_read<C, DK, DV, true>), g2, dim3(256), 0, st, a.lambda, qc, pz, hz, tree, oin, o,
+                       a.T, (int)a.H, a.L, (int)BH);
   else
-    hipLaunchKernelGGL((gdn::k_gdn_scan<C, DK, DV, false, 1>), g2, dim3(64 * gdn::kScanWaves), 0, st, a.lambda, qc, pz,
-                       hz, oin, o, a.T, (int)a.H, a.L, J);
+    hipLaunchKernelGGL((gdn::k_gdn_read<C, DK, DV, false>), g2, dim3(256), 0, st, a.lambda, qc, pz, hz, tree, oin, o,
+                       a.T, (int)a.H, a.L, (int)BH);
   if (ev) (void)hipEventRecord(ev[2], st);
   return hipGetLastError();
 }

@@ -130,7 +130,7 @@ const BwdEntry* mamba2_bwd_table(int* n);
 
 // Gated DeltaNet: per-chunk buffers carved from the workspace (byte offsets).
 struct GdnLayout {
-  int64_t qc = 0, pz = 0, hz = 0, oin = 0, total = 0;
+  int64_t qc = 0, pz = 0, hz = 0, oin = 0, tree = 0, total = 0;
 };
 int64_t gdn_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, int64_t C, GdnLayout* lay);
 
