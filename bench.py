@@ -55,9 +55,10 @@ KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_mamba2_fused.hip", "paper_2506_0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fused_tile_ll_mamba2_bf16_T65536_hbm_traffic.md")
 
 
-def fused_path(w, has_lambda=True):
-    """Whether ll_mamba2_fwd takes the single-pass kernels for this workload."""
-    return w.dtype == "bf16" and w.C == 64 and has_lambda and w.dk in (64, 128) and w.dv in (64, 128)
+def fused_path(w):
+    """Whether ll_mamba2_fwd takes the single-pass kernels for this workload (with or without
+    lambda)."""
+    return w.dtype == "bf16" and w.C == 64 and w.dk in (64, 128) and w.dv in (64, 128)
 
 
 def fused_stage_figures(w):
@@ -394,7 +395,8 @@ def measure_mamba2(w, K, W, torch, ll, with_gemm=False, copy_mib=0):
                                "note": "the same kernels with every level weight 1 (the output is Mamba-2's)"},
         "mamba2_lambda_null": {"ms_per_step": ms_null, "tokens_per_s": w.B * w.T / (ms_null * 1e-3),
                                "tflops": F2 / (ms_null * 1e-3) / 1e12,
-                               "note": "lambda == NULL: one running state per tile (Mamba-2's own cost)"},
+                               "note": ("lambda == NULL: Mamba-2 itself (every level weight 1; the single-pass "
+                                        "kernels for bf16 at C = 64, else one running state per tile)")},
         "log_factor_overhead": ms / ms_null,
         "log_factor_overhead_note": "log-linear ms / lambda == NULL Mamba-2 ms",
         "lambda_ones_ratio": ms / ms_ones,

@@ -83,9 +83,10 @@ size_t ll_workspace_size(int32_t variant, int32_t dtype, int64_t B, int64_t T, i
                          int64_t d_k, int64_t d_v, int64_t C, int32_t has_lambda);
 
 /* Log-linear Mamba-2 forward, O = (Q K^T (.) M^S (.) M^H) V (Sec. 3.4; chunkwise algorithm
- * Sec. 3.3, Eq. 5).  lambda == NULL runs the same kernels with all level weights equal to 1,
- * which is exactly Mamba-2 / gated linear attention (Eq. 2) with a single running state
- * between chunks.  Arguments as in the conventions above; o is written in full. */
+ * Sec. 3.3, Eq. 5).  lambda == NULL sets all level weights to 1, which is exactly Mamba-2 /
+ * gated linear attention (Eq. 2): bf16 with C = 64 runs the same single-pass kernels with unit
+ * weights, the other shapes one running state between chunks.  Arguments as in the conventions
+ * above; o is written in full. */
 ll_status ll_mamba2_fwd(const void* q, const void* k, const void* v, const float* log_alpha,
                         const float* lambda, void* o, int64_t B, int64_t T, int64_t H,
                         int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,

@@ -22,8 +22,9 @@ TOL = {"f32": 1e-4, "bf16": 2e-2}
 CASES = [
     ("bf16", 64, 128, 128, True, (1, 8192, 4), (1, 2176, 2)),   # single-pass kernels
     ("bf16", 64, 128, 64, True, (2, 4096, 4), (1, 1216, 3)),    # single-pass kernels, d_v = 64
-    ("bf16", 64, 128, 128, False, (1, 8192, 4), (2, 704, 2)),   # lambda = NULL: running-scan path
+    ("bf16", 64, 128, 128, False, (1, 8192, 4), (2, 704, 2)),   # lambda = NULL: single pass, unit weights
     ("f32", 16, 16, 16, True, (2, 1024, 3), (1, 80, 1)),        # fp32 three-kernel path
+    ("f32", 16, 16, 16, False, (2, 1024, 3), (1, 80, 1)),       # fp32 lambda = NULL: running-scan path
 ]
 
 
