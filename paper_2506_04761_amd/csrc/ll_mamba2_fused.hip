@@ -238,6 +238,11 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
   lds_copy_rows<DV, R, NT>(v_s, v + (row0 * H + h) * DV, (int64_t)H * DV, nrow);
   float lb = 0.f;
   if (lane < J && ((u >> lane) & 1)) lb = ws.bsum[bh * ws.stride + bsum_offset(N, lane) + (u >> lane) - 1];
+  auto slot_of = [&](int j) -> int64_t { return group_end(u, j) - 1; };  // node(e - 1) covers the group ending at e
+  // the flags of all the tile's source groups in one poll (lane j - 1: level j); polled again after
+  // the intra-tile phase, so that most levels need no poll of their own
+  const bool src_lane = lane < J && ((u >> lane) & 1);
+  bool fup = src_lane && flag_up(flag_bh + slot_of(lane + 1));
 
   // ---- gates: tile-local cumulative log2-gates, decays to the group and tile ends
   tile_cumsum_of<R>(la_raw, nrow, cl_s, wsum_s);
@@ -318,8 +323,12 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) oA[mt] = oB[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
   fast_intra<DK, DV, HAS_LAMBDA>(wave, k_s, v_s, cl_s, kdec_s, qA, qB, cliA, cliB, lrowA, lrowB, oA, oB);
-
-  auto slot_of = [&](int j) -> int64_t { return group_end(u, j) - 1; };  // node(e - 1) covers the group ending at e
+  if (src_lane && !fup) fup = flag_up(flag_bh + slot_of(lane + 1));
+  const uint64_t seen = __ballot(fup);  // bit j - 1: node of level j known to be published
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");  // node loads stay below the polls
+  auto await_level = [&](int j) {
+    if (!((seen >> (j - 1)) & 1) && !wait_flag(flag_bh + slot_of(j), ws.ctr + 8)) tk_s[2] = 1;
+  };
 
   // ---- odd tiles: node(u) = S_u + the tile's low-level groups, decayed to the end of the tile.
   //      Every source flag is awaited first; then each wave streams its own pieces of the source
@@ -334,8 +343,7 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
       for (int nt = 0; nt < NTW; ++nt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[mt][nt][r] = to_f32(sbf[mt][nt][r]);
-    for (int j = 1; j <= t; ++j)
-      if (!wait_flag(flag_bh + slot_of(j), ws.ctr + 8)) tk_s[2] = 1;
+    for (int j = 1; j <= t; ++j) await_level(j);
     __syncthreads();  // every wave is done with K and V
     // slot x of this wave: SLICE bf16 = its pieces (d_k tile mt, d_v tile nt) at (mt NTW + nt) 256
     constexpr int SLICE = DKT * NTW * 256, PCS = SLICE / 8, NPW = PCS / 64;
@@ -384,7 +392,7 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
     lds_gather16<NT>(dst, SZ * 2 / 16, [&](int x) { return src + 8 * x; });
   };
   auto copy_level = [&](int j, bf* dst) {
-    if (!wait_flag(flag_bh + slot_of(j), ws.ctr + 8)) tk_s[2] = 1;
+    await_level(j);
     copy_node(j, dst);
   };
   auto next_level = [&](int j) {
@@ -397,7 +405,7 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
     __syncthreads();  // `cur` complete and visible; every wave is done with `nxt`
     const int jn = next_level(j);
     // a node not yet published is awaited after this level's products, not before them
-    const bool early = jn && flag_up(flag_bh + slot_of(jn));
+    const bool early = jn && (((seen >> (jn - 1)) & 1) || flag_up(flag_bh + slot_of(jn)));
     if (early) {
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
       copy_node(jn, nxt);
