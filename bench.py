@@ -662,28 +662,27 @@ def main_bwd(args, w, torch, ll):
 # ------------------------------------------------------------------------- Gated DeltaNet
 
 def gdn_issued(w, has_lambda=True):
-    """MFMA FLOPs the two GDN kernels issue, counted from their loop structure, and the
-    algorithmic bytes of the whole call.
+    """MFMA FLOPs the GDN kernels issue, counted from their loop structure, and the algorithmic
+    bytes of the whole call.
     gdn_chunk, per chunk: K K^T, Q K^T (C x C x d_k), W = T_G (gamma K), Q~ correction (C x d_k x C),
     U = T_G V, intra output (C x d_v x C), P_G T_G (C x C x C), P_z (d_k x d_k x C), H_z (d_k x d_v x C).
-    gdn_scan, per chunk and level j: propagation R_j <- P_z R_j (d_k x d_k x d_v) unless the level
-    restarts at this chunk, and the read-out q~^T R_j (C x d_k x d_v) if the chunk reads level j."""
+    Block tree, per block of levels 1 .. J-1: T_hi T_lo (d_k x d_k x d_k) and T_hi A_lo
+    (d_k x d_v x d_k).  Read-out, per chunk and set bit of its index: q~ A (C x d_v x d_k) and, when
+    a higher set bit follows, q~ T (C x d_k x d_k).  lambda == NULL issues the same work."""
     C, dk, dv = w.C, w.dk, w.dv
     N = w.T // C
     J = (N - 1).bit_length() if N > 1 else 0
     f_chunk = 2.0 * (3 * C * C * dk + C * C * dk + 2 * C * C * dv + C ** 3 + dk * dk * C + dk * dv * C)
-    f_scan = 0.0
+    f_tree = sum((N >> m) * 2.0 * dk * dk * (dk + dv) for m in range(1, J))
+    f_read = 0.0
     for z in range(N):
-        levels = range(1, J + 1) if has_lambda else [0]
-        for j in levels:
-            reader = ((z >> (j - 1)) & 1) if j else z > 0
-            restart = (z & ((1 << j) - 1)) == 0 if j else z == 0
-            f_scan += (2.0 * C * dk * dv if reader else 0.0) + (0.0 if restart else 2.0 * dk * dk * dv)
+        nb = bin(z).count("1")
+        f_read += nb * 2.0 * C * dk * dv + max(nb - 1, 0) * 2.0 * C * dk * dk
     BH = w.B * w.H
     es = 2 if w.dtype == "bf16" else 4
     L = w.levels if has_lambda else 0
     nbytes = w.B * w.T * w.H * ((2 * dk + 2 * dv) * es + 8 + 4 * L)
-    return BH * N * f_chunk, BH * f_scan, nbytes
+    return BH * N * f_chunk, BH * (f_tree + f_read), nbytes
 
 
 def decode_level_reads(T):
@@ -862,18 +861,18 @@ def main_gdn(args, w, torch, ll, cpu=True):
           f"lambda=NULL {ms_null:.3f} ms/step", file=sys.stderr, flush=True)
 
     f_chunk, f_scan, nbytes = gdn_issued(w)
-    names = ["gdn_chunk", "gdn_scan"]
+    names = ["gdn_chunk", "gdn_tree_read"]
     dom = int(np.argmax(stage_ms))
     # per-stage algorithmic bytes: the chunk kernel reads q, k, v, gates, beta and writes the
-    # per-chunk products (Q~, P_z, H_z bf16, intra output fp32); the scan reads those and lambda
-    # and writes o.
+    # per-chunk products (Q~, P_z, H_z bf16, intra output fp32); the block tree and the read-out
+    # read those and lambda and write o (the tree's own blocks are not counted).
     N = w.T // w.C
     BHN = w.B * w.H * N
     prod = BHN * (w.C * w.dk * 2 + w.dk * w.dk * 2 + w.dk * w.dv * 2 + w.C * w.dv * 4)
     BTH = w.B * w.T * w.H
     b_chunk = BTH * ((2 * w.dk + w.dv) * 2 + 8) + prod
     b_scan = prod + BTH * (4 * w.levels + w.dv * 2)
-    figs = {"gdn_chunk": (f_chunk, b_chunk), "gdn_scan": (f_scan, b_scan)}
+    figs = {"gdn_chunk": (f_chunk, b_chunk), "gdn_tree_read": (f_scan, b_scan)}
     roof = roofline(w, *figs[names[dom]], stage_ms[dom])
     F = f_chunk + f_scan
     f_n, s_n, _ = gdn_issued(w, has_lambda=False)
@@ -889,7 +888,7 @@ def main_gdn(args, w, torch, ll, cpu=True):
                    "inputs": "bf16 q/k/v (k L2-normalised), fp32 log-gates, beta and lambda, seeded synthetic"},
         "tflops_issued": F / (ms * 1e-3) / 1e12,
         "mfma_peak_frac": F / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
-        "flop_convention": "MFMA FLOPs issued by gdn_chunk and gdn_scan (see gdn_issued)",
+        "flop_convention": "MFMA FLOPs issued by gdn_chunk, the block tree and the read-out (see gdn_issued)",
         "hbm_GBps_algorithmic": nbytes / (ms * 1e-3) / 1e9,
         "gdn_lambda_null": {"ms_per_step": ms_null, "tokens_per_s": w.B * w.T / (ms_null * 1e-3),
                             "tflops_issued": (f_n + s_n) / (ms_null * 1e-3) / 1e12},
