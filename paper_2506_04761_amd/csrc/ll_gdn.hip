@@ -44,12 +44,23 @@ constexpr int kMaxJ = 16;      // inter-chunk levels handled by the read-out (T 
 constexpr int kChunkWaves = 8; // waves per gdn_chunk workgroup
 typedef __bf16 bf;
 
+// Element offset of entry (r, k) of a staged bf16 matrix with rows of ld elements whose 8-element
+// chunks are XOR-swizzled by row group when SW: chunk k / 8 of row r sits at position
+// (k / 8) ^ ((r / 8) % 8).  Used for the transposed (d-major) copies of the chunk's K and V, whose
+// rows of C = 64 tokens are written eight rows at a time (see the staging in k_gdn_chunk).
+template <bool SW>
+__device__ inline int stg(int r, int ld, int k) {
+  return r * ld + (SW ? ((((k >> 3) ^ (r >> 3)) & 7) << 3) + (k & 7) : k);
+}
+
 // C = A B over 16x16 output tiles, A [M][K] row-major (lda), Bt = B^T [N][K] row-major (ldb), both
-// bf16 in LDS; tiles dealt round-robin to the kChunkWaves waves; epi(mt, nt, acc) consumes each tile
-// (lane holds column 16 nt + (lane & 15), rows 16 mt + 4 (lane >> 4) + r).
-template <int M, int N, int K, typename Epi>
+// bf16 in LDS (SWA / SWB: the operand's chunks are swizzled as by stg, K = 64); tiles dealt
+// round-robin to the kChunkWaves waves; epi(mt, nt, acc) consumes each tile (lane holds column
+// 16 nt + (lane & 15), rows 16 mt + 4 (lane >> 4) + r).
+template <int M, int N, int K, bool SWA = false, bool SWB = false, typename Epi>
 __device__ inline void gemm_lds(const bf* A, int lda, const bf* Bt, int ldb, Epi epi) {
   using MF = Mfma<bf>;
+  static_assert(!(SWA || SWB) || K == 64, "swizzled operands have rows of 64 elements");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
   constexpr int MT = M / 16, NT = N / 16;
   for (int tile = wave; tile < MT * NT; tile += kChunkWaves) {
@@ -58,9 +69,30 @@ __device__ inline void gemm_lds(const bf* A, int lda, const bf* Bt, int ldb, Epi
 #pragma unroll
     for (int ks = 0; ks < K / MF::KSTEP; ++ks) {
       const int k0 = ks * MF::KSTEP + g * MF::KPL;
-      acc = MF::mma(MF::load(&A[(mt * 16 + r16) * lda + k0]), MF::load(&Bt[(nt * 16 + r16) * ldb + k0]), acc);
+      acc = MF::mma(MF::load(&A[stg<SWA>(mt * 16 + r16, lda, k0)]), MF::load(&Bt[stg<SWB>(nt * 16 + r16, ldb, k0)]), acc);
     }
     epi(mt, nt, acc);
+  }
+}
+
+// As gemm_lds with the wave's tiles unrolled: epi(i, mt, nt, acc) for the wave's i-th tile
+// (tile wave + kChunkWaves i), so that the epilogue can index registers by i.
+template <int M, int N, int K, typename Epi>
+__device__ inline void gemm_lds_unrolled(const bf* A, int lda, const bf* Bt, int ldb, Epi epi) {
+  using MF = Mfma<bf>;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, r16 = lane & 15, g = lane >> 4;
+  constexpr int MT = M / 16, NT = N / 16;
+  static_assert(MT * NT % kChunkWaves == 0, "whole rounds of tiles");
+#pragma unroll
+  for (int i = 0; i < MT * NT / kChunkWaves; ++i) {
+    const int tile = wave + i * kChunkWaves, mt = tile / NT, nt = tile % NT;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < K / MF::KSTEP; ++ks) {
+      const int k0 = ks * MF::KSTEP + g * MF::KPL;
+      acc = MF::mma(MF::load(&A[(mt * 16 + r16) * lda + k0]), MF::load(&Bt[(nt * 16 + r16) * ldb + k0]), acc);
+    }
+    epi(i, mt, nt, acc);
   }
 }
 
@@ -78,7 +110,8 @@ __device__ inline int kfrag_idx(int k, int n) {
 // Kernel 1: per-chunk WY solve and chunk-local products.  One workgroup (kChunkWaves waves) per chunk.
 // Outputs (workspace, per chunk): Qc [C][DK] bf16 row-major, P_z [DK][DK] bf16 (kfrag layout for
 // even chunks z, row-major for odd ones: the two sides of a tree combination), H_z [DK][DV] bf16
-// (kfrag), intra-chunk output [C][DV] fp32 row-major.
+// (kfrag), intra-chunk output [C][DV] fp32 in the MFMA result layout (16 x 16 tiles, row tile
+// major; lane l of a tile holds rows 4 (l / 16) + 0..3 of column l % 16).
 // ---------------------------------------------------------------------------------------------
 template <int C, int DK, int DV, bool HAS_LAMBDA>
 __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __restrict__ q, const bf* __restrict__ k,
@@ -99,9 +132,9 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   constexpr int R1B = (DK * LDC + DV * LDC + C * LDC) * 2;
   constexpr int R1 = R1A > R1B ? R1A : R1B;
   __shared__ __attribute__((aligned(16))) char r1[R1];
-  __shared__ bf kgt_s[DK * LDC];   // (gamma K)^T
-  __shared__ bf kdt_s[DK * LDC];   // (decay-to-end K)^T
-  __shared__ bf vt_s[DV * LDC];    // V^T
+  __shared__ bf kgt_s[DK * LDC];   // (gamma K)^T, chunks swizzled (stg)
+  __shared__ bf kdt_s[DK * LDC];   // (decay-to-end K)^T, chunks swizzled
+  __shared__ bf vt_s[DV * LDC];    // V^T, chunks swizzled
   __shared__ bf pg_s[C * LDC];     // P_G
   __shared__ bf z_s[C * LDC];      // T_G
   __shared__ bf zt_s[C * LDC];     // T_G^T
@@ -121,11 +154,15 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   // A persistent grid: the workgroup takes chunks blockIdx.x, blockIdx.x + gridDim.x, ... (logical
   // order (b, h, z) through the XCD mapping), and loads the next chunk's inputs (K, Q, V rows, gates,
   // beta, lambda) into registers as soon as the current chunk has staged its own, so that their
-  // memory latency overlaps the current chunk's work.  The 64 lanes of a wave take 64 consecutive
-  // tokens of one 8-column piece, so that the transposed (column-major) LDS copies below are
-  // written as contiguous runs.
+  // memory latency overlaps the current chunk's work.  A wave instruction loads 16-byte pieces of
+  // 8 tokens x 8 consecutive pieces (piece p of the tensor: token 8 (b % 8) + (l % 8), columns
+  // 8 (8 (b / 8) + l / 8) .. + 7, with b = p / 64 and l = p % 64): whole 128-byte lines, and in the
+  // transposed LDS copies eight rows 8 apart whose swizzled chunks fall in distinct banks.
   constexpr int NTH = 64 * kChunkWaves;
   constexpr int NKQ = C * DK / VEC / NTH, NVV = C * DV / VEC / NTH;  // 16-byte pieces per thread
+  static_assert(C == 64, "pieces of 8 tokens x 8 column pieces");
+  auto piece_t = [&](int p) { return ((p >> 6) & 7) * 8 + (p & 7); };        // token of piece p
+  auto piece_d = [&](int p) { return (((p >> 6) >> 3) * 8 + ((p & 63) >> 3)) * VEC; };  // first column
   constexpr int NLW = HAS_LAMBDA ? (C * (LOG2C + 1) + NTH - 1) / NTH : 1;  // lambda values per thread
   static_assert(C * DK / VEC % NTH == 0 && C * DV / VEC % NTH == 0, "whole passes of the workgroup");
   bf16x8 kpre[NKQ], qpre[NKQ], vpre[NVV];
@@ -135,30 +172,34 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
     const int64_t zz = wk % N, bhh = wk / N;
     const int hh = (int)(bhh % H), bb = (int)(bhh / H);
     const int64_t t0 = (int64_t)bb * Tlen + zz * C;
+    // the small loads first and unconditionally (every wave, clamped indices; only wave 0 and the
+    // in-range entries are used), so that no wave waits on them where their registers are reused
+    la_r = log_alpha[(t0 + lane) * H + hh];  // scaled at its use: nothing waits for the load here
+    bt_r = beta[(t0 + lane) * H + hh];
+    if constexpr (HAS_LAMBDA) {
+#pragma unroll
+      for (int e = 0; e < NLW; ++e) {
+        const int idx = tid + e * NTH, ic = idx < C * (LOG2C + 1) ? idx : C * (LOG2C + 1) - 1;
+        lam_r[e] = lam[((t0 + ic / (LOG2C + 1)) * H + hh) * L + ic % (LOG2C + 1)];
+      }
+    }
 #pragma unroll
     for (int e = 0; e < NKQ; ++e) {
-      const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
+      const int idx = tid + e * NTH, t = piece_t(idx), d0 = piece_d(idx);
       kpre[e] = *reinterpret_cast<const bf16x8*>(k + ((t0 + t) * H + hh) * DK + d0);
       qpre[e] = *reinterpret_cast<const bf16x8*>(q + ((t0 + t) * H + hh) * DK + d0);
     }
 #pragma unroll
     for (int e = 0; e < NVV; ++e) {
-      const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
+      const int idx = tid + e * NTH, t = piece_t(idx), d0 = piece_d(idx);
       vpre[e] = *reinterpret_cast<const bf16x8*>(v + ((t0 + t) * H + hh) * DV + d0);
-    }
-    if (wave == 0 && lane < C) {
-      la_r = log_alpha[(t0 + lane) * H + hh] * kLog2e;
-      bt_r = beta[(t0 + lane) * H + hh];
-    }
-    if constexpr (HAS_LAMBDA) {
-#pragma unroll
-      for (int e = 0; e < NLW; ++e) {
-        const int idx = tid + e * NTH, t = idx / (LOG2C + 1), l = idx % (LOG2C + 1);
-        if (idx < C * (LOG2C + 1)) lam_r[e] = lam[((t0 + t) * H + hh) * L + l];
-      }
     }
   };
   if (blockIdx.x < nchunks) load_inputs(blockIdx.x);
+  // The first chunk's inputs are awaited here, once: the compiler's counter waits at the loop head
+  // then see, on every path into it, the epilogue stores issued after the prefetch, and no longer
+  // wait for those stores to drain before each chunk's first use of its prefetched inputs.
+  wait_vmem();
   for (int64_t it = blockIdx.x; it < nchunks; it += gridDim.x) {
   const int64_t work = xcd_remap(it, nchunks);  // (b, h, z)
   const int64_t z = work % N;
@@ -170,7 +211,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
 
   // ---- phase A: gates, staging, K K^T and Q K^T
   if (wave == 0) {
-    const float la = lane < C ? la_r : 0.f;
+    const float la = lane < C ? la_r * kLog2e : 0.f;
     const float cl = wave_inclusive_scan(la);
     const float tot = __shfl(cl, C - 1, 64);
     if (lane < C) {
@@ -190,7 +231,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   __syncthreads();
 #pragma unroll
   for (int e = 0; e < NKQ; ++e) {
-    const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
+    const int idx = tid + e * NTH, t = piece_t(idx), d0 = piece_d(idx);
     const bf16x8 kv = kpre[e], qv = qpre[e];
     *reinterpret_cast<bf16x8*>(&k_s[t * LDD + d0]) = kv;
     *reinterpret_cast<bf16x8*>(&q_s[t * LDD + d0]) = qv;
@@ -198,19 +239,29 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
 #pragma unroll
     for (int e = 0; e < VEC; ++e) {
       const float x = static_cast<float>(kv[e]);
-      kgt_s[(d0 + e) * LDC + t] = static_cast<bf>(x * gt);
-      kdt_s[(d0 + e) * LDC + t] = static_cast<bf>(x * dt);
+      kgt_s[stg<true>(d0 + e, LDC, t)] = static_cast<bf>(x * gt);
+      kdt_s[stg<true>(d0 + e, LDC, t)] = static_cast<bf>(x * dt);
     }
   }
 #pragma unroll
   for (int e = 0; e < NVV; ++e) {
-    const int idx = tid + e * NTH, t = idx % C, d0 = (idx / C) * VEC;
+    const int idx = tid + e * NTH, t = piece_t(idx), d0 = piece_d(idx);
     const bf16x8 vv = vpre[e];
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) vt_s[(d0 + e) * LDC + t] = vv[e];
+    for (int e = 0; e < VEC; ++e) vt_s[stg<true>(d0 + e, LDC, t)] = vv[e];
   }
   if (it + gridDim.x < nchunks) load_inputs(it + gridDim.x);  // the next chunk's, while this one runs
   __syncthreads();
+  // the Q entries of this lane's tiles of the corrected-query product (formed transposed: tile
+  // (mt, nt) holds columns d = 16 mt + 4 g + 0..3 of row t = 16 nt + (lane & 15)), read while Q is
+  // staged (its LDS region is reused by phase C), so that the product's epilogue issues no loads
+  constexpr int QCT = (DK / 16) * (C / 16) / kChunkWaves;
+  bf16x4 qreg[QCT];
+#pragma unroll
+  for (int i = 0; i < QCT; ++i) {
+    const int tile = wave + i * kChunkWaves, mt = tile / (C / 16), nt = tile % (C / 16);
+    qreg[i] = *reinterpret_cast<const bf16x4*>(&q_s[(nt * 16 + r16) * LDD + mt * 16 + 4 * g]);
+  }
   // L[t][s] = beta_t (k_t . k_s) Gamma[t,s] for s < t (fp32);  P_G[t][s] = (q_t . k_s) Gamma[t,s], s <= t
   gemm_lds<C, C, DK>(k_s, LDD, k_s, LDD, [&](int mt, int nt, f32x4 acc) {
 #pragma unroll
@@ -314,13 +365,13 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   __syncthreads();
 
   // ---- phase C: W = T_G (gamma K), U = T_G V (stored transposed), A_c = P_G T_G masked by M^H
-  gemm_lds<C, DK, C>(z_s, LDC, kgt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+  gemm_lds<C, DK, C, false, true>(z_s, LDC, kgt_s, LDC, [&](int mt, int nt, f32x4 acc) {
     bf16x4 w4;
 #pragma unroll
     for (int r = 0; r < 4; ++r) w4[r] = static_cast<bf>(acc[r]);
     *reinterpret_cast<bf16x4*>(&wt_s[(nt * 16 + r16) * LDC + mt * 16 + 4 * g]) = w4;
   });
-  gemm_lds<C, DV, C>(z_s, LDC, vt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+  gemm_lds<C, DV, C, false, true>(z_s, LDC, vt_s, LDC, [&](int mt, int nt, f32x4 acc) {
     bf16x4 u4;
 #pragma unroll
     for (int r = 0; r < 4; ++r) u4[r] = static_cast<bf>(acc[r]);
@@ -338,33 +389,51 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   __syncthreads();
 
   // ---- phase D: intra output, corrected queries, transition and chunk state
+  // the intra output in the MFMA result layout, tile by tile (one 1 KB store per tile; the
+  // read-out kernel adds it to accumulators of the same layout)
   float* oin = oin_out + cidx * (C * DV);
-  gemm_lds<C, DV, C>(ph_s, LDC, vt_s, LDC, [&](int mt, int nt, f32x4 acc) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) oin[(mt * 16 + 4 * g + r) * DV + nt * 16 + r16] = acc[r];
+  gemm_lds<C, DV, C, false, true>(ph_s, LDC, vt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+    *reinterpret_cast<f32x4*>(oin + ((mt * (DV / 16) + nt) * 64 + lane) * 4) = acc;
   });
   bf* qc = qc_out + cidx * (C * DK);
-  gemm_lds<C, DK, C>(pg_s, LDC, wt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+  // Qc^T = gamma Q^T - W^T P_G^T: four consecutive columns of one row of Qc per lane, one 8-byte
+  // store each
+  gemm_lds_unrolled<DK, C, C>(wt_s, LDC, pg_s, LDC, [&](int i, int mt, int nt, f32x4 acc) {
+    const int d0 = mt * 16 + 4 * g, t = nt * 16 + r16;
+    const float gt = gm_s[t];
+    bf16x4 q4;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int t = mt * 16 + 4 * g + r, d = nt * 16 + r16;
-      const float qv = static_cast<float>(q[((tok0 + t) * H + h) * DK + d]);
-      qc[t * DK + d] = static_cast<bf>(gm_s[t] * qv - acc[r]);
-    }
+    for (int r = 0; r < 4; ++r) q4[r] = static_cast<bf>(gt * static_cast<float>(qreg[i][r]) - acc[r]);
+    *reinterpret_cast<bf16x4*>(qc + t * DK + d0) = q4;
   });
   bf* pz = pz_out + cidx * (DK * DK);
   const float gC = gm_s[C - 1];
-  gemm_lds<DK, DK, C>(kdt_s, LDC, wt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+  // P_z = gamma_C I - K~^T W, stored four consecutive elements per lane: an even chunk's in the
+  // kfrag layout (rows d .. d + 3 of column e), an odd chunk's row-major from the transposed
+  // product (columns e .. e + 3 of row d)
+  if (!(z & 1)) {
+    gemm_lds<DK, DK, C, true, false>(kdt_s, LDC, wt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+      const int d0 = mt * 16 + 4 * g, e = nt * 16 + r16;
+      bf16x4 p4;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int d = mt * 16 + 4 * g + r, e = nt * 16 + r16;
-      pz[(z & 1) ? d * DK + e : kfrag_idx<DK>(d, e)] = static_cast<bf>((d == e ? gC : 0.f) - acc[r]);
-    }
-  });
+      for (int r = 0; r < 4; ++r) p4[r] = static_cast<bf>((d0 + r == e ? gC : 0.f) - acc[r]);
+      *reinterpret_cast<bf16x4*>(pz + kfrag_idx<DK>(d0, e)) = p4;
+    });
+  } else {
+    gemm_lds<DK, DK, C, false, true>(wt_s, LDC, kdt_s, LDC, [&](int mt, int nt, f32x4 acc) {
+      const int e0 = mt * 16 + 4 * g, d = nt * 16 + r16;
+      bf16x4 p4;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) p4[r] = static_cast<bf>((d == e0 + r ? gC : 0.f) - acc[r]);
+      *reinterpret_cast<bf16x4*>(pz + d * DK + e0) = p4;
+    });
+  }
   bf* hz = hz_out + cidx * (DK * DV);
-  gemm_lds<DK, DV, C>(kdt_s, LDC, ut_s, LDC, [&](int mt, int nt, f32x4 acc) {
+  gemm_lds<DK, DV, C, true, false>(kdt_s, LDC, ut_s, LDC, [&](int mt, int nt, f32x4 acc) {
+    bf16x4 h4;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) hz[kfrag_idx<DK>(mt * 16 + 4 * g + r, nt * 16 + r16)] = static_cast<bf>(acc[r]);
+    for (int r = 0; r < 4; ++r) h4[r] = static_cast<bf>(acc[r]);
+    *reinterpret_cast<bf16x4*>(hz + kfrag_idx<DK>(mt * 16 + 4 * g, nt * 16 + r16)) = h4;
   });
   }  // chunk loop
 }
@@ -587,7 +656,15 @@ __global__ __launch_bounds__(256) void k_gdn_read(const float* __restrict__ lam,
     }
   }
 
-  // o = intra-chunk output + the levels, rows staged through LDS (over the Q~ buffers)
+  // o = intra-chunk output (stored by the chunk kernel in this accumulator layout) + the levels,
+  // rows staged through LDS (over the Q~ buffers)
+  const float* oin = oin_in + cidx * (C * DV);
+  f32x4 oi[RT][VT];
+#pragma unroll
+  for (int mt = 0; mt < RT; ++mt)
+#pragma unroll
+    for (int v = 0; v < VT; ++v)
+      oi[mt][v] = *reinterpret_cast<const f32x4*>(oin + ((mt * (DV / 16) + VT * wave + v) * 64 + lane) * 4);
   __syncthreads();
   float* o_s = reinterpret_cast<float*>(&q_s[0][0]);
 #pragma unroll
@@ -595,20 +672,18 @@ __global__ __launch_bounds__(256) void k_gdn_read(const float* __restrict__ lam,
 #pragma unroll
     for (int v = 0; v < VT; ++v)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) o_s[(16 * mt + 4 * g + r) * DV + 16 * (VT * wave + v) + r16] = acc[mt][v][r];
+      for (int r = 0; r < 4; ++r)
+        o_s[(16 * mt + 4 * g + r) * DV + 16 * (VT * wave + v) + r16] = oi[mt][v][r] + acc[mt][v][r];
   __syncthreads();
-  const float* oin = oin_in + cidx * (C * DV);
   for (int x = tid; x < C * DV / 8; x += 256) {
     const int t = x / (DV / 8), c = 8 * (x % (DV / 8));
-    const f32x4 a0 = *reinterpret_cast<const f32x4*>(oin + t * DV + c);
-    const f32x4 a1 = *reinterpret_cast<const f32x4*>(oin + t * DV + c + 4);
     const f32x4 s0 = *reinterpret_cast<const f32x4*>(o_s + t * DV + c);
     const f32x4 s1 = *reinterpret_cast<const f32x4*>(o_s + t * DV + c + 4);
     bf16x8 res;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      res[e] = static_cast<bf>(a0[e] + s0[e]);
-      res[4 + e] = static_cast<bf>(a1[e] + s1[e]);
+      res[e] = static_cast<bf>(s0[e]);
+      res[4 + e] = static_cast<bf>(s1[e]);
     }
     *reinterpret_cast<bf16x8*>(o + ((tok0 + t) * H + h) * DV + c) = res;
   }
