@@ -189,13 +189,24 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
       kpre[e] = *reinterpret_cast<const bf16x8*>(k + ((t0 + t) * H + hh) * DK + d0);
       qpre[e] = *reinterpret_cast<const bf16x8*>(q + ((t0 + t) * H + hh) * DK + d0);
     }
+  };
+  // V is prefetched separately, later in the chunk (phase B), so that no wave issues the whole
+  // burst at once
+  auto load_v = [&](int64_t it) {
+    const int64_t wk = xcd_remap(it, nchunks);
+    const int64_t zz = wk % N, bhh = wk / N;
+    const int hh = (int)(bhh % H), bb = (int)(bhh / H);
+    const int64_t t0 = (int64_t)bb * Tlen + zz * C;
 #pragma unroll
     for (int e = 0; e < NVV; ++e) {
       const int idx = tid + e * NTH, t = piece_t(idx), d0 = piece_d(idx);
       vpre[e] = *reinterpret_cast<const bf16x8*>(v + ((t0 + t) * H + hh) * DV + d0);
     }
   };
-  if (blockIdx.x < nchunks) load_inputs(blockIdx.x);
+  if (blockIdx.x < nchunks) {
+    load_inputs(blockIdx.x);
+    load_v(blockIdx.x);
+  }
   // The first chunk's inputs are awaited here, once: the compiler's counter waits at the loop head
   // then see, on every path into it, the epilogue stores issued after the prefetch, and no longer
   // wait for those stores to drain before each chunk's first use of its prefetched inputs.
@@ -283,7 +294,9 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
     z_s[t * LDC + c] = zv;
     zt_s[c * LDC + t] = zv;
   };
+  const bool more = it + gridDim.x < nchunks;
   if (wave != 0) {
+    if (more) load_v(it + gridDim.x);
     // P_G[t][s] = (q_t . k_s) Gamma[t,s], s <= t, 16 x 16 tiles dealt to the other waves
     using MF = Mfma<bf>;
     constexpr int MT = C / 16;
@@ -335,6 +348,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
       xs_s[blk(bb, bb) + i * 16 + c] = x[i];
       put_t(16 * bb + i, 16 * bb + c, x[i]);
     }
+    if (more) load_v(it + gridDim.x);
   }
   for (int i = 1; i < C / 16; ++i) {
     __syncthreads();  // blocks of rows < i (and the diagonal ones) are in xs_s
@@ -494,6 +508,15 @@ __global__ __launch_bounds__(256) void k_gdn_combine(const bf* __restrict__ t_in
       fb[c][ks] = transposed ? MF::load(thi + (16 * nt + r16) * DK + 32 * ks + 8 * g)
                              : MF::load((t_part ? tlo : alo) + ((nt * KS + ks) * 64 + lane) * 8);
     }
+  // A_hi (added to the A tiles) with the operands, not after the products
+  bf16x4 ahv[CT][RT];
+  if (!t_part) {
+#pragma unroll
+    for (int c = 0; c < CT; ++c)
+#pragma unroll
+      for (int i = 0; i < RT; ++i)
+        ahv[c][i] = *reinterpret_cast<const bf16x4*>(ahi + kfrag_idx<DK>(16 * (RT * wave + i) + 4 * g, 16 * (c0 - TT + c) + r16));
+  }
 #pragma unroll
   for (int c = 0; c < CT; ++c) {
     const int nt = t_part ? c0 + c : c0 - TT + c;
@@ -510,7 +533,7 @@ __global__ __launch_bounds__(256) void k_gdn_combine(const bf* __restrict__ t_in
       bf16x4 res;
       if (!t_part) {  // A = T_hi A_lo + A_hi; the lane's four rows are four consecutive kfrag elements
         const int idx = kfrag_idx<DK>(row0, 16 * nt + r16);
-        const bf16x4 add = *reinterpret_cast<const bf16x4*>(ahi + idx);
+        const bf16x4 add = ahv[c][i];
 #pragma unroll
         for (int r = 0; r < 4; ++r) res[r] = static_cast<bf>(acc[i][r] + static_cast<float>(add[r]));
         *reinterpret_cast<bf16x4*>(aout + idx) = res;
