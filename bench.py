@@ -53,6 +53,10 @@ FUSED_STAGES = ["tile_totals", "block_sums", "fused_tile"]
 KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_mamba2_fused.hip", "paper_2506_04761_amd/csrc/ll_fast_tile.hpp",
                   "paper_2506_04761_amd/csrc/ll_mamba2_common.hpp", "paper_2506_04761_amd/csrc/ll_device.hpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fused_tile_ll_mamba2_bf16_T65536_hbm_traffic.md")
+# the GDN forward's counter record (block tree + read-out stage) and the sources it depends on
+GDN_KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_gdn.hip", "paper_2506_04761_amd/csrc/ll_device.hpp",
+                      "paper_2506_04761_amd/csrc/ll_launch.hpp"]
+GDN_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ll_gdn_bf16_T8192_hbm_traffic.md")
 
 
 def fused_path(w):
@@ -136,12 +140,12 @@ def roofline(w, flops, nbytes, ms):
     return r
 
 
-def kernel_source_hash():
-    """Hash of the kernel sources with comments and blank lines removed (comment edits do not
-    change the kernel)."""
+def kernel_source_hash(sources=None):
+    """Hash of the kernel sources (default: the single-pass forward's) with comments and blank
+    lines removed (comment edits do not change the kernel)."""
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in sources or KERNEL_SOURCES:
         with open(os.path.join(ROOT, f)) as fh:
             for line in fh:
                 code = line.split("//", 1)[0].strip()
@@ -150,19 +154,19 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(workload):
-    """HBM bytes per tile_out launch from the committed counter summary (FETCH_SIZE and
-    WRITE_SIZE, calibrated against a plain copy), or None when there is none for this workload
-    or the kernel sources changed since the counters were taken."""
-    if not os.path.exists(TRAFFIC_FILE):
+def recorded_traffic(workload, traffic_file=TRAFFIC_FILE, sources=None):
+    """HBM bytes per launch (per stage for a multi-kernel stage) from a committed counter summary
+    (FETCH_SIZE and WRITE_SIZE, calibrated against a plain copy), or None when there is none for
+    this workload or the kernel sources changed since the counters were taken."""
+    if not os.path.exists(traffic_file):
         return None
     rec = {}
-    with open(TRAFFIC_FILE) as fh:
+    with open(traffic_file) as fh:
         for line in fh:
             if line.startswith("- ") and ": " in line:
                 key, val = line[2:].split(": ", 1)
                 rec[key.strip()] = val.strip().strip("`")
-    if rec.get("workload") != workload or rec.get("kernel_source_sha256") != kernel_source_hash():
+    if rec.get("workload") != workload or rec.get("kernel_source_sha256") != kernel_source_hash(sources):
         return None
     try:
         return float(rec["hbm_bytes_per_launch"])
@@ -895,7 +899,9 @@ def main_gdn(args, w, torch, ll, cpu=True):
         "log_factor_overhead": ms / ms_null,
         "clock_settle_s": CLOCK_SETTLE_S, "clock_settle_note": CLOCK_SETTLE_NOTE,
         "stages_ms": dict(zip(names, [float(v) for v in stage_ms])),
-        "roofline": {"kernel": names[dom], **roof, "traffic": None},
+        "roofline": {"kernel": names[dom], **roof,
+                     "traffic": recorded_traffic(w.name, GDN_TRAFFIC_FILE, GDN_KERNEL_SOURCES)
+                     if names[dom] == "gdn_tree_read" else None},
     }
     del d, la, beta, lam, out, ws
     torch.cuda.empty_cache()
