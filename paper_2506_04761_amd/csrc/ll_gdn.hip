@@ -187,6 +187,17 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
     for (int e = 0; e < NKQ; ++e) {
       const int idx = tid + e * NTH, t = piece_t(idx), d0 = piece_d(idx);
       kpre[e] = *reinterpret_cast<const bf16x8*>(k + ((t0 + t) * H + hh) * DK + d0);
+    }
+  };
+  // Q is prefetched in phase C
+  auto load_q = [&](int64_t it) {
+    const int64_t wk = xcd_remap(it, nchunks);
+    const int64_t zz = wk % N, bhh = wk / N;
+    const int hh = (int)(bhh % H), bb = (int)(bhh / H);
+    const int64_t t0 = (int64_t)bb * Tlen + zz * C;
+#pragma unroll
+    for (int e = 0; e < NKQ; ++e) {
+      const int idx = tid + e * NTH, t = piece_t(idx), d0 = piece_d(idx);
       qpre[e] = *reinterpret_cast<const bf16x8*>(q + ((t0 + t) * H + hh) * DK + d0);
     }
   };
@@ -206,6 +217,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   if (blockIdx.x < nchunks) {
     load_inputs(blockIdx.x);
     load_v(blockIdx.x);
+    load_q(blockIdx.x);
   }
   // The first chunk's inputs are awaited here, once: the compiler's counter waits at the loop head
   // then see, on every path into it, the epilogue stores issued after the prefetch, and no longer
@@ -379,6 +391,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
   __syncthreads();
 
   // ---- phase C: W = T_G (gamma K), U = T_G V (stored transposed), A_c = P_G T_G masked by M^H
+  if (more) load_q(it + gridDim.x);
   gemm_lds<C, DK, C, false, true>(z_s, LDC, kgt_s, LDC, [&](int mt, int nt, f32x4 acc) {
     bf16x4 w4;
 #pragma unroll
