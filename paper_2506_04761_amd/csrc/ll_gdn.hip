@@ -489,6 +489,7 @@ __global__ __launch_bounds__(256) void k_gdn_combine(const bf* __restrict__ t_in
   constexpr int TT = DK / 16, AT = DV / 16;  // column tiles of T and A
   constexpr int CT = kCombineTiles, S = (TT + AT) / CT;
   static_assert(TT % CT == 0 && AT % CT == 0, "a workgroup's tiles lie in T or in A");
+  static_assert(CT * KS % 4 == 0, "the B fragments split evenly over the four waves");
   constexpr int BS = DK * (DK + DV);
   const int64_t id = xcd_remap(blockIdx.x, (int64_t)gridDim.x);
   const int64_t kb = id / S, bh = blockIdx.y;
@@ -505,22 +506,24 @@ __global__ __launch_bounds__(256) void k_gdn_combine(const bf* __restrict__ t_in
   // A operand: rows of T_hi (row-major), or for a transposed T the rows of T_lo^T (kfrag of T_lo);
   // rows 16 (RT wave + i) + r16, k = 32 ks + 8 g + 0..7
   frag fa[RT][KS];
-  // B operand of column tile c0 + c: A_lo or T_lo (kfrag), or for a transposed T the rows of T_hi
-  frag fb[CT][KS];
+  // B operand of column tile c0 + c: A_lo or T_lo (kfrag), or for a transposed T the rows of T_hi.
+  // The same for every wave: each wave loads a quarter of them into LDS and reads all back.
+  __shared__ frag fb_s[CT * KS][64];
+  constexpr int FPW = CT * KS / 4;  // B fragments loaded per wave
+  frag fbw[FPW];
+#pragma unroll
+  for (int x = 0; x < FPW; ++x) {
+    const int f = wave + 4 * x, c = f / KS, ks = f % KS;
+    const int nt = t_part ? c0 + c : c0 - TT + c;
+    fbw[x] = transposed ? MF::load(thi + (16 * nt + r16) * DK + 32 * ks + 8 * g)
+                        : MF::load((t_part ? tlo : alo) + ((nt * KS + ks) * 64 + lane) * 8);
+  }
 #pragma unroll
   for (int i = 0; i < RT; ++i)
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       fa[i][ks] = transposed ? MF::load(tlo + (((RT * wave + i) * KS + ks) * 64 + lane) * 8)
                              : MF::load(thi + (16 * (RT * wave + i) + r16) * DK + 32 * ks + 8 * g);
-#pragma unroll
-  for (int c = 0; c < CT; ++c)
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int nt = t_part ? c0 + c : c0 - TT + c;
-      fb[c][ks] = transposed ? MF::load(thi + (16 * nt + r16) * DK + 32 * ks + 8 * g)
-                             : MF::load((t_part ? tlo : alo) + ((nt * KS + ks) * 64 + lane) * 8);
-    }
   // A_hi (added to the A tiles) with the operands, not after the products
   bf16x4 ahv[CT][RT];
   if (!t_part) {
@@ -531,6 +534,9 @@ __global__ __launch_bounds__(256) void k_gdn_combine(const bf* __restrict__ t_in
         ahv[c][i] = *reinterpret_cast<const bf16x4*>(ahi + kfrag_idx<DK>(16 * (RT * wave + i) + 4 * g, 16 * (c0 - TT + c) + r16));
   }
 #pragma unroll
+  for (int x = 0; x < FPW; ++x) fb_s[wave + 4 * x][lane] = fbw[x];
+  __syncthreads();
+#pragma unroll
   for (int c = 0; c < CT; ++c) {
     const int nt = t_part ? c0 + c : c0 - TT + c;
     f32x4 acc[RT];
@@ -539,7 +545,7 @@ __global__ __launch_bounds__(256) void k_gdn_combine(const bf* __restrict__ t_in
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int i = 0; i < RT; ++i) acc[i] = MF::mma(fa[i][ks], fb[c][ks], acc[i]);
+      for (int i = 0; i < RT; ++i) acc[i] = MF::mma(fa[i][ks], fb_s[c * KS + ks][lane], acc[i]);
 #pragma unroll
     for (int i = 0; i < RT; ++i) {
       const int row0 = 16 * (RT * wave + i) + 4 * g;
