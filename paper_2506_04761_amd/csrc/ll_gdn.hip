@@ -472,10 +472,11 @@ __global__ __launch_bounds__(64 * kChunkWaves) void k_gdn_chunk(const bf* __rest
 // T (DK x DK) then A (DK x DV), A in the kfrag layout, T in the kfrag layout when k is even (the
 // source groups that chunks read, and the lo side of the next level) and row-major when k is odd
 // (the hi side).  Level 0 is the chunk kernel's P_z and H_z (same layout rule, by chunk parity).
-// The (DK + DV) / 16 column tiles of [T | A] are split over kCombineSplit-column-tile workgroups,
-// which the dispatch-order remap keeps on one XCD; wave w forms rows 16 (RT w + i) + 0..15 of its
-// workgroup's tiles (RT = DK / 64).  An odd block's T is formed transposed (T^T = T_lo^T T_hi^T)
-// so that its rows are stored whole.  Every operand fragment of a workgroup is loaded up front.
+// The (DK + DV) / 16 column tiles of [T | A] are split over workgroups of kCombineTiles column
+// tiles, which the dispatch-order remap keeps on one XCD; wave w forms rows 16 (RT w + i) + 0..15
+// of its workgroup's tiles (RT = DK / 64).  An odd block's T is formed transposed
+// (T^T = T_lo^T T_hi^T) so that its rows are stored whole.  Every operand fragment of a workgroup
+// is loaded up front; the B-operand fragments, the same for every wave, go through LDS.
 // ---------------------------------------------------------------------------------------------
 constexpr int kCombineTiles = 4;  // column tiles per workgroup
 
