@@ -586,7 +586,7 @@ __device__ __host__ inline int64_t tree_level_offset(int64_t BH, int64_t N, int 
 // lambda == NULL: every level weight is 1 (Gated DeltaNet: the whole prefix state).
 // ---------------------------------------------------------------------------------------------
 template <int C, int DK, int DV, bool HAS_LAMBDA>
-__global__ __launch_bounds__(256) void k_gdn_read(const float* __restrict__ lam, const bf* __restrict__ qc_in,
+__global__ __launch_bounds__(256, 2) void k_gdn_read(const float* __restrict__ lam, const bf* __restrict__ qc_in,
                                                   const bf* __restrict__ pz, const bf* __restrict__ hz,
                                                   const bf* __restrict__ tree, const float* __restrict__ oin_in,
                                                   bf* __restrict__ o, int64_t Tlen, int H, int L, int BH) {
@@ -612,6 +612,33 @@ __global__ __launch_bounds__(256) void k_gdn_read(const float* __restrict__ lam,
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int J = N <= 1 ? 0 : 32 - __builtin_clz((unsigned)(N - 1));
 
+  // node fragments of the level at bit m: A(G) for this wave's output columns, and T(G) for its
+  // q~ columns when a higher level follows.  The first level's are loaded before Q~ is staged.
+  frag ba[VT][KS], bt[KT][KS];
+  auto load_level = [&](int m, bool with_t) {
+    const int64_t kblk = (z >> m) - 1;
+    const bf *tn, *an;
+    if (m == 0) {
+      tn = pz + (bh * N + kblk) * (DK * DK);
+      an = hz + (bh * N + kblk) * (DK * DV);
+    } else {
+      tn = tree + tree_level_offset(BH, N, m, BS) + (bh * (N >> m) + kblk) * BS;
+      an = tn + DK * DK;
+    }
+#pragma unroll
+    for (int v = 0; v < VT; ++v)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) ba[v][ks] = MF::load(an + (((VT * wave + v) * KS + ks) * 64 + lane) * 8);
+    if (with_t) {
+#pragma unroll
+      for (int v = 0; v < KT; ++v)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) bt[v][ks] = MF::load(tn + (((KT * wave + v) * KS + ks) * 64 + lane) * 8);
+    }
+  };
+  unsigned bits = (unsigned)z;
+  if (bits) load_level(__builtin_ctz(bits), (bits & (bits - 1)) != 0);
+
   for (int x = tid; x < C * DK / 8; x += 256) {
     const int t = x / (DK / 8), c = x % (DK / 8);
     *reinterpret_cast<bf16x8*>(&q_s[0][t * LDQ + 8 * c]) =
@@ -631,30 +658,12 @@ __global__ __launch_bounds__(256) void k_gdn_read(const float* __restrict__ lam,
 #pragma unroll
     for (int v = 0; v < VT; ++v) acc[mt][v] = f32x4{0.f, 0.f, 0.f, 0.f};
   int cur = 0;
-  unsigned bits = (unsigned)z;
+  bool first = true;
   while (bits) {
     const int m = __builtin_ctz(bits);  // tree level of the source group; token level log2 C + m + 1
     bits &= bits - 1;
-    const int64_t kblk = (z >> m) - 1;
-    const bf *tn, *an;
-    if (m == 0) {
-      tn = pz + (bh * N + kblk) * (DK * DK);
-      an = hz + (bh * N + kblk) * (DK * DV);
-    } else {
-      tn = tree + tree_level_offset(BH, N, m, BS) + (bh * (N >> m) + kblk) * BS;
-      an = tn + DK * DK;
-    }
-    frag ba[VT][KS], bt[KT][KS];
-#pragma unroll
-    for (int v = 0; v < VT; ++v)
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) ba[v][ks] = MF::load(an + (((VT * wave + v) * KS + ks) * 64 + lane) * 8);
-    if (bits) {
-#pragma unroll
-      for (int v = 0; v < KT; ++v)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) bt[v][ks] = MF::load(tn + (((KT * wave + v) * KS + ks) * 64 + lane) * 8);
-    }
+    if (!first) load_level(m, bits != 0);
+    first = false;
     // q~ A(G) for this wave's output columns and, when a higher level follows, q~ T(G) for its
     // q~ columns, from one read of each q~ fragment
     const bf* qs = q_s[cur];
