@@ -305,8 +305,9 @@ ll_status ll_gdn_fwd(const void* q, const void* k, const void* v, const float* l
 
 /* Same computation as ll_gdn_fwd, for measurement: also records the caller's HIP events (as in
  * ll_mamba2_fwd_staged) on `stream`: events[0] before the per-chunk kernel, events[1] between
- * it and the level scan, events[2] after the scan.  Asynchronous.  events == NULL or any
- * events[i] == NULL returns LL_ERR_NULL_ARG. */
+ * it and the level stage (the block tree of chunk transitions and states, then the per-chunk
+ * read-out), events[2] after that stage.  Asynchronous.  events == NULL or any events[i] == NULL
+ * returns LL_ERR_NULL_ARG. */
 ll_status ll_gdn_fwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
                             const float* beta, const float* lambda, void* o, int64_t B, int64_t T,
                             int64_t H, int64_t d_k, int64_t d_v, int64_t C, int32_t dtype,

@@ -461,7 +461,7 @@ def ll_gdn_fwd(q, k, v, log_alpha, beta, lam, C, out=None, workspace=None, strea
 
 def ll_gdn_fwd_staged(q, k, v, log_alpha, beta, lam, C, events, out=None, workspace=None, stream=None):
     """As ll_gdn_fwd, recording three torch.cuda.Event objects around its two kernel stages
-    (per-chunk WY kernel, level scan); see ll_mamba2_fwd_staged."""
+    (per-chunk WY kernel; block tree and read-out); see ll_mamba2_fwd_staged."""
     handles, s = _event_handles(events, 3, stream)
     (B, T, H, dk, dv, code), out, ws = _prepare(LL_GDN, q, k, v, log_alpha, beta, lam, C, out, workspace)
     st = lib.ll_gdn_fwd_staged(_ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(beta), _ptr(lam), _ptr(out),
