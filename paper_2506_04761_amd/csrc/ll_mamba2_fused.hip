@@ -400,6 +400,16 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
       if ((u >> (j - 1)) & 1) return j;
     return 0;
   };
+  // lambda == NULL (every level weight 1): the row factor exp2(c_t) comes out of the level sum, so
+  // the tile sums its source nodes, each weighted by exp2(gap_j), into this wave's pieces of one
+  // fp32 state and multiplies Q by that state once after the loop, instead of once per level
+  f32x4 pre[DKT][NTW];
+  if constexpr (!HAS_LAMBDA) {
+#pragma unroll
+    for (int mt = 0; mt < DKT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NTW; ++nt) pre[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
   auto level_step = [&](int& j, const bf* cur, bf* nxt) {
     wait_vmem();
     __syncthreads();  // `cur` complete and visible; every wave is done with `nxt`
@@ -411,28 +421,36 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
       copy_node(jn, nxt);
     }
     const float gap = gap_of(gapv, j);
-    float wA = fast_exp2(cliA + gap), wB = fast_exp2(cliB + gap);
     if constexpr (HAS_LAMBDA) {
-      wA *= lrowA[LOG2R + j];
-      wB *= lrowB[LOG2R + j];
-    }
-    frag uf[2][KS];
+      const float wA = fast_exp2(cliA + gap) * lrowA[LOG2R + j], wB = fast_exp2(cliB + gap) * lrowB[LOG2R + j];
+      frag uf[2][KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) uf[0][ks] = node_frag<MT>(cur, 0, ks);
+      for (int ks = 0; ks < KS; ++ks) uf[0][ks] = node_frag<MT>(cur, 0, ks);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      if (mt + 1 < MT) {
+      for (int mt = 0; mt < MT; ++mt) {
+        if (mt + 1 < MT) {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) uf[(mt + 1) & 1][ks] = node_frag<MT>(cur, mt + 1, ks);
+          for (int ks = 0; ks < KS; ++ks) uf[(mt + 1) & 1][ks] = node_frag<MT>(cur, mt + 1, ks);
+        }
+        f32x4 tA = {0.f, 0.f, 0.f, 0.f}, tB = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          tA = M::mma(uf[mt & 1][ks], qA[ks], tA);
+          tB = M::mma(uf[mt & 1][ks], qB[ks], tB);
+        }
+        oA[mt] += wA * tA;
+        oB[mt] += wB * tB;
       }
-      f32x4 tA = {0.f, 0.f, 0.f, 0.f}, tB = {0.f, 0.f, 0.f, 0.f};
+    } else {
+      const float w = fast_exp2(gap);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        tA = M::mma(uf[mt & 1][ks], qA[ks], tA);
-        tB = M::mma(uf[mt & 1][ks], qB[ks], tB);
-      }
-      oA[mt] += wA * tA;
-      oB[mt] += wB * tB;
+      for (int mt = 0; mt < DKT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NTW; ++nt) {
+          const bf16x4 pc = *reinterpret_cast<const bf16x4*>(cur + ((mt * MT + wave * NTW + nt) * 64 + lane) * 4);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) pre[mt][nt][r] += w * to_f32(pc[r]);
+        }
     }
     if (jn && !early) copy_level(jn, nxt);
     j = jn;
@@ -444,6 +462,40 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
     level_step(j, k_s, v_s);
     if (!j) break;
     level_step(j, v_s, k_s);
+  }
+  if constexpr (!HAS_LAMBDA) {
+    if (u) {  // the combined state (bf16, node layout) into the K region, then one product pass
+      __syncthreads();  // every wave is done with the last node
+#pragma unroll
+      for (int mt = 0; mt < DKT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NTW; ++nt) {
+          bf16x4 v4;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v4[r] = from_f32<bf>(pre[mt][nt][r]);
+          *reinterpret_cast<bf16x4*>(k_s + ((mt * MT + wave * NTW + nt) * 64 + lane) * 4) = v4;
+        }
+      __syncthreads();
+      const float wA = fast_exp2(cliA), wB = fast_exp2(cliB);
+      frag uf[2][KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) uf[0][ks] = node_frag<MT>(k_s, 0, ks);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        if (mt + 1 < MT) {
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) uf[(mt + 1) & 1][ks] = node_frag<MT>(k_s, mt + 1, ks);
+        }
+        f32x4 tA = {0.f, 0.f, 0.f, 0.f}, tB = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          tA = M::mma(uf[mt & 1][ks], qA[ks], tA);
+          tB = M::mma(uf[mt & 1][ks], qB[ks], tB);
+        }
+        oA[mt] += wA * tA;
+        oB[mt] += wB * tB;
+      }
+    }
   }
 
   // ---- store O through LDS (rows iA, iB staged into a swizzled row-major tile in the V region)
