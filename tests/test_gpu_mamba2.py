@@ -161,6 +161,20 @@ def test_lambda_null_is_mamba2(dtype, C, dk, dv, T):
     assert rel_err(got_ones, ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("dist", ["slow", "nodecay"])
+@pytest.mark.parametrize("dk,dv,T", [(128, 128, 64 * 37), (128, 64, 64 * 52), (64, 64, 64 * 21)])
+def test_lambda_null_slow_decay_many_tiles(dist, dk, dv, T):
+    """lambda == NULL sums a tile's source nodes into one state before its product pass; with slow or
+    no decay every source group carries a sizeable share of |O|, so a wrong weight or node shows."""
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=1, H=2, T=T, dk=dk, dv=dv, dist=dist, seed=43)
+    x = generate(w)
+    ref = mamba2.gla_recurrent(x["q"], x["k"], x["v"], x["log_alpha"])
+    got = run_mamba2(x, "bf16", 64, with_lambda=False)
+    err = rel_err(got, ref)
+    print(f"lambda=NULL {dist} {dk}x{dv} T={T}: rel err {err:.3e}")
+    assert err <= TOL["bf16"], err
+
+
 # ------------------------------------------------------------------ full-size workloads, sampled rows
 
 def _sampled_parity(name, rows_per_head=24, heads=((0, 0), (0, 5))):
