@@ -125,10 +125,12 @@ ll_status ll_mamba2_fwd_grouped(const void* q, const void* k, const void* v, con
  * also records the caller's HIP events
  * (hipEvent_t handles passed as void*) on `stream`, events[i] right before kernel stage i and
  * events[3] after the last stage, so that the caller can read each stage's duration with
- * hipEventElapsedTime once the stream has passed them.  Stages: 0 tile states and the
- * summaries of the lowest three tile levels, 1 scan (the block tree of summaries above them;
- * with lambda == NULL the running state of every tile), 2 tile outputs (intra-tile and
- * inter-tile terms).  Asynchronous like ll_mamba2_fwd.  events
+ * hipEventElapsedTime once the stream has passed them.  Stages of the single-pass path (bf16,
+ * C = 64): 0 tile totals of the log-gates, 1 aligned block sums of those totals, 2 the tile
+ * kernel (states, Fenwick nodes, intra-tile and inter-tile terms).  Stages of the three-kernel
+ * path: 0 tile states and the summaries of the lowest three tile levels, 1 scan (the block tree
+ * of summaries above them; with lambda == NULL the running state of every tile), 2 tile outputs
+ * (intra-tile and inter-tile terms).  Asynchronous like ll_mamba2_fwd.  events
  * == NULL or any events[i] == NULL returns LL_ERR_NULL_ARG; the events stay owned by the caller. */
 ll_status ll_mamba2_fwd_staged(const void* q, const void* k, const void* v, const float* log_alpha,
                                const float* lambda, void* o, int64_t B, int64_t T, int64_t H,

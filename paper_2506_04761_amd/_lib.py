@@ -360,8 +360,10 @@ def _event_handles(events, n, stream):
 def ll_mamba2_fwd_staged(q, k, v, log_alpha, lam, C, events, out=None, workspace=None, stream=None):
     """As ll_mamba2_fwd (ll_mamba2_fwd_grouped when q, k have fewer heads than v), and records
     the four torch.cuda.Event objects in `events` (created with enable_timing=True) on the stream
-    around the three kernel stages: events[i] before stage i (tile states, scan -- summary tree,
-    or running states for lam=None -- and tile outputs) and events[3] after the last.
+    around the three kernel stages: events[i] before stage i and events[3] after the last.  The
+    stages are the tile totals, their block sums and the tile kernel on the single-pass path (bf16,
+    C = 64), and the tile states, the scan (summary tree, or running states for lam=None) and the
+    tile outputs on the three-kernel path.
     Asynchronous; read the durations with events[i].elapsed_time(events[i + 1]) after
     synchronising."""
     handles, s = _event_handles(events, 4, stream)
