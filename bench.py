@@ -53,6 +53,11 @@ FUSED_STAGES = ["tile_totals", "block_sums", "fused_tile"]
 KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_mamba2_fused.hip", "paper_2506_04761_amd/csrc/ll_fast_tile.hpp",
                   "paper_2506_04761_amd/csrc/ll_mamba2_common.hpp", "paper_2506_04761_amd/csrc/ll_device.hpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fused_tile_ll_mamba2_bf16_T65536_hbm_traffic.md")
+
+
+def fused_traffic_file(workload):
+    """The committed counter summary of the single-pass tile kernel for one workload."""
+    return os.path.join(ROOT, "profiles", f"fused_tile_{workload}_hbm_traffic.md")
 # the GDN forward's counter record (block tree + read-out stage) and the sources it depends on
 GDN_KERNEL_SOURCES = ["paper_2506_04761_amd/csrc/ll_gdn.hip", "paper_2506_04761_amd/csrc/ll_device.hpp",
                       "paper_2506_04761_amd/csrc/ll_launch.hpp"]
@@ -377,7 +382,7 @@ def measure_mamba2(w, K, W, torch, ll, with_gemm=False, copy_mib=0):
     figs = fused_stage_figures(w) if fused else stage_figures(w)
     dom = int(np.argmax(stage_ms))
     roof = roofline(w, *figs[names[dom]], stage_ms[dom])
-    traffic = recorded_traffic(w.name) if names[dom] == "fused_tile" else None
+    traffic = recorded_traffic(w.name, fused_traffic_file(w.name)) if names[dom] == "fused_tile" else None
     F = flops_loglinear(w)
     tflops = F / (ms * 1e-3) / 1e12
     F2 = flops_mamba2(w)
