@@ -614,8 +614,8 @@ def main_bwd(args, w, torch, ll):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / K
     stage_ms = np.array([[e[s].elapsed_time(e[s + 1]) for s in range(4)] for e in evs]).mean(axis=0)
-    # forward + backward, as one training step of the operator would run them (the backward
-    # reusing the forward's level summaries where the three-kernel forward leaves them)
+    # forward + backward, as one training step of the operator would run them (the forward in the
+    # backward-sized workspace leaves the level summaries that the backward reuses)
     for _ in range(W):
         fwd()
         bwd_after_fwd()
@@ -656,9 +656,7 @@ def main_bwd(args, w, torch, ll):
         "flop_convention": "B*H*T*[2C(3dk+2dv) + 2dk*dv + 5dk*dv*log2(T/C)]",
         "hbm_GBps_algorithmic": nbytes / (ms * 1e-3) / 1e9,
         "forward_plus_backward": {"ms": ms_fb, "tokens_per_s": w.B * w.T / (ms_fb * 1e-3),
-                                  "backward_entry": ("ll_mamba2_bwd_after_fwd (recomputes the level summaries: the "
-                                                     "single-pass forward leaves none)" if fused_path(w) else
-                                                     "ll_mamba2_bwd_after_fwd (level summaries from the forward)"),
+                                  "backward_entry": "ll_mamba2_bwd_after_fwd (level summaries from the forward)",
                                   "tflops": (F + Ff) / (ms_fb * 1e-3) / 1e12},
         "stages_ms": dict(zip(BWD_STAGES, [float(x) for x in stage_ms])),
         "roofline": {"kernel": BWD_STAGES[dom], **roof, "traffic": None,

@@ -212,9 +212,11 @@ ll_status ll_mamba2_bwd(const void* q, const void* k, const void* v, const float
  * pointers) beside them, and the backward compares that record on the device with its own
  * arguments: on a mismatch (another forward, another workspace user in between, other inputs) every
  * gradient is written as NaN instead.  Inputs changed in place at the same addresses are not
- * detected.  For the shapes whose forward is the single-pass kernel (bf16, C = 64: no summaries
- * are left behind) the summaries are recomputed, exactly as ll_mamba2_bwd_grouped.  Arguments and
- * checks as ll_mamba2_bwd_grouped. */
+ * detected.  For the shapes whose forward is the single-pass kernel (bf16, C = 64), a forward
+ * given this workspace also stores every Fenwick node it publishes in the backward's order, with
+ * the tiles' cumulative gates (any other forward in the buffer, lambda == NULL or with a smaller
+ * workspace_bytes, clears the record); the gradients then differ from ll_mamba2_bwd's by the
+ * rounding of those bf16 summaries.  Arguments and checks as ll_mamba2_bwd_grouped. */
 ll_status ll_mamba2_bwd_after_fwd(const void* q, const void* k, const void* v, const float* log_alpha,
                                   const float* lambda, const void* d_o, void* dq, void* dk, void* dv,
                                   float* dlog_alpha, float* dlambda, int64_t B, int64_t T, int64_t H,

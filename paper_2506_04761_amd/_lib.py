@@ -431,8 +431,7 @@ def ll_mamba2_bwd(q, k, v, log_alpha, lam, d_o, C, grads=None, workspace=None, s
 
 def ll_mamba2_bwd_workspace(q, v, C):
     """A workspace for the backward shaped for q [B, T, H_qk, d_k] and v [B, T, H, d_v] (also usable
-    by the forward; ll_mamba2_bwd_after_fwd reuses the summaries the three-kernel forward leaves
-    there)."""
+    by the forward, which then leaves there the level summaries ll_mamba2_bwd_after_fwd reuses)."""
     torch = _torch()
     B, T, Hqk, dk = q.shape
     need = lib.ll_mamba2_bwd_workspace_size(_dtype_code(q), B, T, v.shape[2], Hqk, dk, v.shape[-1], C)

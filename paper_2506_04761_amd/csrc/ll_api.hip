@@ -114,6 +114,7 @@ namespace {
 struct Mamba2Plan {
   const ll::KernelEntry* e = nullptr;
   bool fused = false;
+  bool bwd_out = false;  // single-pass forward in a backward-sized workspace: leave the backward's summaries
   int L = 0;
   int64_t need = 0;
 };
@@ -148,6 +149,7 @@ ll_status mamba2_launch(const Mamba2Plan& p, const void* q, const void* k, const
   a.Hqk = Hqk;
   a.L = p.L;
   a.workspace = workspace;
+  a.bwd_out = p.bwd_out;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipEvent_t ev[ll::kMamba2Stages + 1];
   if (events)
@@ -165,6 +167,10 @@ ll_status mamba2_impl(const void* q, const void* k, const void* v, const float* 
   if (st != LL_OK) return st;
   if (!workspace) return LL_ERR_NULL_ARG;
   if ((int64_t)workspace_bytes < p.need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LL_ERR_WORKSPACE;
+  // a workspace sized for the backward: the single-pass forward also leaves the summaries that
+  // ll_mamba2_bwd_after_fwd reuses
+  p.bwd_out = p.fused && lambda && find_mamba2_bwd(dtype, C, d_k, d_v) &&
+              (int64_t)workspace_bytes >= ll::mamba2_bwd_workspace(B, T, H, Hqk, d_k, d_v, C, elem_size(dtype), nullptr);
   return mamba2_launch(p, q, k, v, log_alpha, lambda, o, B, T, H, Hqk, d_k, d_v, C, workspace, stream, events);
 }
 ll_status mamba2_ml_impl(const void* q, const void* k, const void* v, const float* log_alpha, const float* Lambda,
@@ -231,8 +237,8 @@ ll_status mamba2_bwd_impl(const void* q, const void* k, const void* v, const flo
   a.Hqk = Hqk;
   a.L = L;
   a.workspace = workspace;
-  // the single-pass forward leaves no three-kernel summaries behind: recompute them
-  a.reuse_summaries = reuse && !ll::mamba2_fused_supported(dtype, C, d_k, d_v, true);
+  a.reuse_summaries = reuse;
+  a.fused_fwd = ll::mamba2_fused_supported(dtype, C, d_k, d_v, true);
   hipEvent_t ev[ll::kMamba2BwdStages + 1];
   if (events)
     for (int i = 0; i <= ll::kMamba2BwdStages; ++i) ev[i] = static_cast<hipEvent_t>(events[i]);

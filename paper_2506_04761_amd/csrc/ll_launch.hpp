@@ -49,6 +49,9 @@ struct Mamba2Args {
   // lambda_full, [B, T, H, L, dk, dk] matrices; the workspace is mamba2_ml_workspace(...) bytes
   const float* lambda_matrix = nullptr;
   bool lambda_full = false;
+  // single-pass path with lambda given: also leave the level summaries the backward reuses (the
+  // workspace is at least mamba2_bwd_workspace(...) bytes)
+  bool bwd_out = false;
 };
 
 typedef hipError_t (*Mamba2Launch)(const Mamba2Args&, hipStream_t, hipEvent_t* /* null or 4 events */);
@@ -74,15 +77,24 @@ const KernelEntry* mamba2_table(int* n);
 WsTag mamba2_tag(const Mamba2Args& a, int64_t esize, bool valid);
 // Enqueues the write of `tag` into the workspace's tag region.
 hipError_t launch_write_tag(void* workspace, const WsLayout& w, const WsTag& tag, hipStream_t st);
+// Enqueues the write of `tag` at `dst` (a workspace's tag region).
+hipError_t launch_write_tag_at(void* dst, const WsTag& tag, hipStream_t st);
 
 // Single-pass forward (ll_mamba2_fused.hip): byte offsets of its workspace regions.
 struct FusedLayout {
   int64_t N = 0;       // tiles of 128 tokens per sequence
   int J = 0;           // inter-tile levels
   int64_t stride = 0;  // floats per (b, h) row of the block sums
-  int64_t ctr = 0, flag = 0, bsum = 0, node = 0, total = 0;
+  // tag (at offset 0, where the three-kernel layout keeps its tag too), ticket counters, node flags,
+  // block sums of the tile totals, nodes (fragment-major)
+  int64_t tag = 0, ctr = 0, flag = 0, bsum = 0, node = 0;
+  // with the backward's summaries: every node again in the backward's [d_v][d_k] order ([BH][N]
+  // slots), the tiles' cumulative log2-gates [BH][N][128] and their totals [BH][N]
+  int64_t ubwd = 0, cl = 0, t1 = 0;
+  int64_t total = 0;
 };
-int64_t mamba2_fused_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, FusedLayout* lay);
+int64_t mamba2_fused_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, FusedLayout* lay,
+                               bool bwd_out = false);
 // Whether ll_mamba2_fwd takes the single-pass kernels for these arguments (dtype 1 = bf16).
 bool mamba2_fused_supported(int dtype, int64_t C, int64_t dk, int64_t dv, bool has_lambda);
 // Enqueues the single-pass forward; with `ev` non-null, ev[0..3] are recorded before the tile
@@ -118,6 +130,7 @@ struct Mamba2BwdArgs {
   int L;
   void* workspace;
   bool reuse_summaries;  // the workspace already holds the forward's summaries of these inputs
+  bool fused_fwd;        // ... left by the single-pass forward (FusedLayout with the backward's summaries)
 };
 typedef hipError_t (*Mamba2BwdLaunch)(const Mamba2BwdArgs&, hipStream_t, hipEvent_t* /* null or 5 events */);
 constexpr int kMamba2BwdStages = 4;

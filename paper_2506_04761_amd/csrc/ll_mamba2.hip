@@ -1126,10 +1126,13 @@ WsTag mamba2_tag(const Mamba2Args& a, int64_t esize, bool valid) {
   return t;
 }
 
-hipError_t launch_write_tag(void* workspace, const WsLayout& w, const WsTag& tag, hipStream_t st) {
-  hipLaunchKernelGGL(k_write_tag, dim3(1), dim3(64), 0, st,
-                     reinterpret_cast<uint64_t*>(static_cast<char*>(workspace) + w.tag), tag);
+hipError_t launch_write_tag_at(void* dst, const WsTag& tag, hipStream_t st) {
+  hipLaunchKernelGGL(k_write_tag, dim3(1), dim3(64), 0, st, static_cast<uint64_t*>(dst), tag);
   return hipGetLastError();
+}
+
+hipError_t launch_write_tag(void* workspace, const WsLayout& w, const WsTag& tag, hipStream_t st) {
+  return launch_write_tag_at(static_cast<char*>(workspace) + w.tag, tag, st);
 }
 
 // Also records, once the summaries are complete, the tag of the inputs they were formed from.

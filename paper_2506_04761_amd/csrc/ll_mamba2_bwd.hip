@@ -1375,6 +1375,12 @@ int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t Hqk, int64
                              int64_t esize, BwdLayout* lay) {
   BwdLayout w{};
   int64_t cur = mamba2_workspace(B, T, H, dk, dv, C, esize, true, &w.fwd);
+  // the forward run in this workspace may be the single-pass one, which leaves its summaries in
+  // its own layout: the backward's regions start after both
+  if (esize == 2 && mamba2_fused_supported(1, C, dk, dv, true)) {
+    const int64_t fused = mamba2_fused_workspace(B, T, H, dk, dv, nullptr, true);
+    if (cur < fused) cur = fused;
+  }
   auto al = [](int64_t x) { return (x + 255) & ~int64_t(255); };
   const int64_t N = w.fwd.N, BH = B * H, SZ = dk * dv;
   const int J = w.fwd.J;
@@ -1394,9 +1400,6 @@ int64_t mamba2_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t Hqk, int64
     w.dqh = cur; cur += al(B * T * H * dk * esize);
     w.dkh = cur; cur += al(B * T * H * dk * esize);
   }
-  // the forward run in this workspace may be the single-pass one
-  const int64_t fused = mamba2_fused_workspace(B, T, H, dk, dv, nullptr);
-  if (cur < fused) cur = fused;
   w.total = cur;
   if (lay) *lay = w;
   return cur;
@@ -1432,8 +1435,17 @@ hipError_t launch_mamba2_bwd(const Mamba2BwdArgs& a, hipStream_t st, hipEvent_t*
   constexpr int R = tile_rows(C), SZ = DK * DV;
   BwdLayout w;
   mamba2_bwd_workspace(a.B, a.T, a.H, a.Hqk, DK, DV, C, sizeof(T), &w);
-  const Nodes<T> nodes = mamba2_nodes<T>(w.fwd, a.workspace, true);
+  Nodes<T> nodes = mamba2_nodes<T>(w.fwd, a.workspace, true);
   char* base = static_cast<char*>(a.workspace);
+  if (a.reuse_summaries && a.fused_fwd) {  // the single-pass forward's summaries, by tile
+    FusedLayout fl;
+    mamba2_fused_workspace(a.B, a.T, a.H, DK, DV, &fl, true);
+    nodes.by_u = reinterpret_cast<T*>(base + fl.ubwd);
+    nodes.bsum = reinterpret_cast<const float*>(base + fl.bsum);
+    nodes.bstride = fl.stride;
+    nodes.t1 = reinterpret_cast<const float*>(base + fl.t1);
+    nodes.cl = reinterpret_cast<float*>(base + fl.cl);
+  }
   RevNodes<T> rev;
   rev.d = reinterpret_cast<T*>(base + w.d);
   rev.dtot = reinterpret_cast<float*>(base + w.dtot);

@@ -18,6 +18,14 @@ constexpr int kMaxLevels = 24;    // Fenwick levels handled (T <= 2^23)
 // Device view of the summaries (all in the storage dtype, layout [p][n] = d_v x d_k) and of their
 // summed log2-gates.  Above the blocks, node (l, k) of the block tree (l >= 1) covers blocks
 // [k 2^l, (k + 1) 2^l), i.e. the tiles of the level-(l + 3) source group with index k.
+// Offset of level b in a (b, h) row of the single-pass forward's block sums (level b: the sums of
+// the aligned blocks of 2^b tiles' log2-gates).
+__device__ __host__ inline int64_t bsum_offset(int64_t N, int b) {
+  int64_t off = 0;
+  for (int x = 0; x < b; ++x) off += (N + (int64_t(1) << x) - 1) >> x;
+  return off;
+}
+
 template <typename T>
 struct Nodes {
   T* lvl1;         // [BH][ceil(N/2)]  tile states of even tiles
@@ -30,6 +38,12 @@ struct Nodes {
   float* tup;      // [BH][nup]        totals of the upper nodes
   float* cl;       // [BH][N][R]       tile-local inclusive cumulative log2-gates (rows past T repeat the last)
   int64_t n1, n2, nb, nup;  // per-(b,h) slot counts
+  // Left by the single-pass forward instead (by_u non-null): the summary of the aligned group of
+  // tiles ending at tile u in slot [b h][u] of by_u (d_v x d_k), the groups' totals in the block
+  // sums `bsum` (rows of `bstride` floats).
+  T* by_u;
+  const float* bsum;
+  int64_t bstride;
   // Slot of block-tree node (l >= 1, k): tree levels 1 .. l-1 come first, ceil(nb / 2^l') slots each.
   __device__ __host__ int64_t up_slot(int64_t bh, int l, int64_t k) const {
     int64_t off = 0;
@@ -38,6 +52,7 @@ struct Nodes {
   }
   // Summary of the level-j source group that starts at tile f (f a multiple of 2^(j-1)).
   __device__ __host__ T* at(int64_t bh, int64_t N, int j, int64_t f, int SZ) const {
+    if (by_u) return by_u + (bh * N + f + (int64_t(1) << (j - 1)) - 1) * SZ;
     if (j == 1) return lvl1 + (bh * n1 + (f >> 1)) * SZ;
     if (j == 2) return lvl2 + (bh * n2 + (f >> 2)) * SZ;
     if (j == 3) return blocks + (bh * nb + (f >> 2)) * SZ;
@@ -45,6 +60,7 @@ struct Nodes {
   }
   // Summed log2-gate of the same group.
   __device__ __host__ float tot(int64_t bh, int64_t N, int j, int64_t f) const {
+    if (by_u) return bsum[bh * bstride + bsum_offset(N, j - 1) + (f >> (j - 1))];
     if (j == 1) return t1[bh * N + f];
     if (j == 2) return t2[bh * n2 + (f >> 2)];
     if (j == 3) return t3[bh * nb + (f >> 2)];

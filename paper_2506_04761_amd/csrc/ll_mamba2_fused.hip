@@ -53,6 +53,10 @@ struct FusedWs {
   float* bsum;     // [BH][stride] aligned block sums of tile totals; level b at sum_{b'<b} ceil(N / 2^b')
   int* flag;       // [BH][N] 1 once node(u) is published
   unsigned* ctr;   // [0..7] ticket counters of the XCD queues, [8] waits that timed out
+  uint64_t* tag;   // the workspace's summary tag (word 0 cleared: the backward finds no summaries)
+  __bf16* ubwd;    // with the backward's summaries: [BH][N] node slots in [d_v][d_k] order
+  float* cl;       //   [BH][N][R] tile-local cumulative log2-gates
+  float* t1;       //   [BH][N] tile totals
   int64_t stride;
 };
 
@@ -83,12 +87,6 @@ __device__ inline bool wait_flag(const int* f, unsigned* err) {
   return ok;
 }
 
-// Offset of level b in a (b, h) row of the block sums.
-__device__ __host__ inline int64_t bsum_offset(int64_t N, int b) {
-  int64_t off = 0;
-  for (int x = 0; x < b; ++x) off += (N + (int64_t(1) << x) - 1) >> x;
-  return off;
-}
 
 // U^T operand fragment (d_v tile dvt, d_k step ks of 32) from a node image in the fragment-major
 // result layout: piece (d_k tile mk, d_v tile dv, lane l) holds rows d_k = 16 mk + 4 (l / 16) + r,
@@ -133,6 +131,7 @@ __global__ __launch_bounds__(256) void k_fused_tiles(const float* __restrict__ l
     __syncthreads();
   }
   if (u == 0 && b == 0 && tid < 16) ws.ctr[tid] = 0;
+  if (u == 0 && b == 0 && tid == 0) ws.tag[0] = 0;  // re-tagged after the tile kernel when the backward's summaries are left
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -171,7 +170,7 @@ __global__ __launch_bounds__(256) void k_fused_tree(FusedWs ws, int64_t N, int J
 // with the query index as the MFMA column), and the d_v tiles w MT/4 .. (w + 1) MT/4 - 1 of the
 // tile's state and node.
 // ---------------------------------------------------------------------------------------------
-template <int DK, int DV, bool HAS_LAMBDA>
+template <int DK, int DV, bool HAS_LAMBDA, bool BWD_OUT>
 __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const float* __restrict__ log_alpha, const float* __restrict__ lam, FusedWs ws, __bf16* __restrict__ o,
@@ -249,6 +248,10 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
   for (int r = tid; r < R; r += NT) {
     kdec_s[r] = fast_exp2(cl_s[r | 15] - cl_s[r]);
     tdec_s[r] = r < nrow ? fast_exp2(cl_s[R - 1] - cl_s[r]) : 0.f;
+    if constexpr (BWD_OUT) {
+      ws.cl[(bh * N + u) * R + r] = cl_s[r];
+      if (r == 0) ws.t1[bh * N + u] = cl_s[R - 1];
+    }
   }
   // gap_j (lane j - 1): summed totals of the tile's lower-level source groups
   const float gapv = wave_inclusive_scan(lb) - lb;
@@ -312,6 +315,14 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
     wait_vmem();
     __syncthreads();
     if (tid == 0) __hip_atomic_store(ws.flag + bh * N + u, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if constexpr (BWD_OUT) {  // the same pieces in the backward's order (row d_v, four consecutive d_k)
+      bf* ub = ws.ubwd + (bh * N + u) * SZ;
+#pragma unroll
+      for (int mt = 0; mt < DKT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NTW; ++nt)
+          *reinterpret_cast<bf16x4*>(ub + (16 * (wave * NTW + nt) + r16) * DK + 16 * mt + 4 * g) = sbf[mt][nt];
+    }
   };
   if (!(u & 1)) publish();
 
@@ -524,7 +535,8 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
 
 }  // namespace
 
-int64_t mamba2_fused_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, FusedLayout* lay) {
+int64_t mamba2_fused_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int64_t dv, FusedLayout* lay,
+                               bool bwd_out) {
   auto al = [](int64_t x) { return (x + 255) & ~int64_t(255); };
   FusedLayout w;
   w.N = tiles_of(T, 64);
@@ -532,10 +544,16 @@ int64_t mamba2_fused_workspace(int64_t B, int64_t T, int64_t H, int64_t dk, int6
   w.stride = bsum_offset(w.N, w.J > 1 ? w.J : 1);
   const int64_t BH = B * H;
   int64_t cur = 0;
+  w.tag = cur; cur += al(sizeof(WsTag));
   w.ctr = cur; cur += al(16 * 4);
   w.flag = cur; cur += al(BH * w.N * 4);
   w.bsum = cur; cur += al(BH * w.stride * 4);
   w.node = cur; cur += al(BH * w.N * dk * dv * 2);
+  if (bwd_out) {
+    w.ubwd = cur; cur += al(BH * w.N * dk * dv * 2);
+    w.cl = cur; cur += al(BH * w.N * kFastRows * 4);
+    w.t1 = cur; cur += al(BH * w.N * 4);
+  }
   w.total = cur;
   if (lay) *lay = w;
   return cur;
@@ -548,14 +566,19 @@ bool mamba2_fused_supported(int dtype, int64_t C, int64_t dk, int64_t dv, bool h
 
 template <int DK, int DV>
 static hipError_t launch_fused(const Mamba2Args& a, hipStream_t st, hipEvent_t* ev) {
+  const bool bwd_out = a.bwd_out && a.lambda;
   FusedLayout w;
-  mamba2_fused_workspace(a.B, a.T, a.H, DK, DV, &w);
+  mamba2_fused_workspace(a.B, a.T, a.H, DK, DV, &w, bwd_out);
   char* base = static_cast<char*>(a.workspace);
   FusedWs ws;
   ws.node = reinterpret_cast<__bf16*>(base + w.node);
   ws.bsum = reinterpret_cast<float*>(base + w.bsum);
   ws.flag = reinterpret_cast<int*>(base + w.flag);
   ws.ctr = reinterpret_cast<unsigned*>(base + w.ctr);
+  ws.tag = reinterpret_cast<uint64_t*>(base + w.tag);
+  ws.ubwd = reinterpret_cast<__bf16*>(base + w.ubwd);
+  ws.cl = reinterpret_cast<float*>(base + w.cl);
+  ws.t1 = reinterpret_cast<float*>(base + w.t1);
   ws.stride = w.stride;
   const int BH = (int)(a.B * a.H);
   if (ev) (void)hipEventRecord(ev[0], st);
@@ -569,14 +592,23 @@ static hipError_t launch_fused(const Mamba2Args& a, hipStream_t st, hipEvent_t* 
   if (ev) (void)hipEventRecord(ev[2], st);
   // every XCD receives (workgroups round-robin) as many workgroups as its queue has tiles
   const int64_t grid = (int64_t)kQueues * ((BH + kQueues - 1) / kQueues) * w.N;
-  if (a.lambda)
-    hipLaunchKernelGGL((k_fused_fwd<DK, DV, true>), dim3((unsigned)grid), dim3(kFastThreads), 0, st,
+  if (bwd_out)
+    hipLaunchKernelGGL((k_fused_fwd<DK, DV, true, true>), dim3((unsigned)grid), dim3(kFastThreads), 0, st,
+                       (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v, a.log_alpha, a.lambda, ws,
+                       (__bf16*)a.o, a.T, (int)a.H, (int)a.Hqk, a.L, w.J, w.N, BH);
+  else if (a.lambda)
+    hipLaunchKernelGGL((k_fused_fwd<DK, DV, true, false>), dim3((unsigned)grid), dim3(kFastThreads), 0, st,
                        (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v, a.log_alpha, a.lambda, ws,
                        (__bf16*)a.o, a.T, (int)a.H, (int)a.Hqk, a.L, w.J, w.N, BH);
   else
-    hipLaunchKernelGGL((k_fused_fwd<DK, DV, false>), dim3((unsigned)grid), dim3(kFastThreads), 0, st,
+    hipLaunchKernelGGL((k_fused_fwd<DK, DV, false, false>), dim3((unsigned)grid), dim3(kFastThreads), 0, st,
                        (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v, a.log_alpha, a.lambda, ws,
                        (__bf16*)a.o, a.T, (int)a.H, (int)a.Hqk, a.L, w.J, w.N, BH);
+  // the summaries the backward reuses are complete: tag them with the inputs they came from
+  if (bwd_out) {
+    const hipError_t e = launch_write_tag_at(ws.tag, mamba2_tag(a, 2, true), st);
+    if (e != hipSuccess) return e;
+  }
   if (ev) (void)hipEventRecord(ev[3], st);
   return hipGetLastError();
 }
