@@ -322,14 +322,26 @@ __global__ __launch_bounds__(256) void k_rev_reduce(Nodes<T> nodes, RevNodes<T> 
   const int e0 = (blockIdx.x * 256 + threadIdx.x) * 4;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float base = 0.f;
-  for (int64_t r = 0; r < nreg; ++r) {
-    const int64_t rgn = rg0 + r;
-    if (e0 < SZ) {
-      const f32x4 x = *reinterpret_cast<const f32x4*>(rev.part + rev.pslot(bh, j, rgn) * SZ + e0);
-      acc += fast_exp2(base) * x;
+  // four regions per step: their partials are loaded together, then added in region order
+  constexpr int U = 4;
+  for (int64_t r = 0; r < nreg; r += U) {
+    f32x4 xs[U];
+    float wq[U];
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+      const int64_t rgn = rg0 + r + q;
+      const bool live = r + q < nreg;
+      xs[q] = live && e0 < SZ ? *reinterpret_cast<const f32x4*>(rev.part + rev.pslot(bh, j, rgn) * SZ + e0)
+                              : f32x4{0.f, 0.f, 0.f, 0.f};
+      wq[q] = fast_exp2(base);
+      if (live) {
+        const int64_t x1 = (rgn + 1) * kRegionTiles < N ? (rgn + 1) * kRegionTiles : N;
+        for (int64_t x = rgn * kRegionTiles; x < x1; ++x) base += nodes.t1[bh * N + x];
+      }
     }
-    const int64_t x1 = (rgn + 1) * kRegionTiles < N ? (rgn + 1) * kRegionTiles : N;
-    for (int64_t x = rgn * kRegionTiles; x < x1; ++x) base += nodes.t1[bh * N + x];
+#pragma unroll
+    for (int q = 0; q < U; ++q)
+      if (r + q < nreg) acc += wq[q] * xs[q];
   }
   const int64_t sl = rev.slot(bh, j, y);
   if (e0 < SZ)
