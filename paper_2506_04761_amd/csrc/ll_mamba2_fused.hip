@@ -116,9 +116,19 @@ __global__ __launch_bounds__(256) void k_fused_tiles(const float* __restrict__ l
   const int nrow = (int)((Tlen - u * R) < R ? (Tlen - u * R) : R);
   for (int h0 = 0; h0 < H; h0 += 16) {
     const int h = h0 + (tid & 15);
+    // the R / 16 rows of this thread loaded together (clamped addresses, no branch), then summed in
+    // row order (rows past the tile, and heads past H, add zero)
+    float g[R / 16];
+#pragma unroll
+    for (int i = 0; i < R / 16; ++i) {
+      const int r = (tid >> 4) + 16 * i;
+      const bool ok = h < H && r < nrow;
+      const float x = log_alpha[(row0 + (ok ? r : 0)) * H + (h < H ? h : 0)];
+      g[i] = ok ? x : 0.f;
+    }
     float s = 0.f;
-    if (h < H)
-      for (int r = tid >> 4; r < nrow; r += 16) s += log_alpha[(row0 + r) * H + h] * kLog2e;
+#pragma unroll
+    for (int i = 0; i < R / 16; ++i) s += g[i] * kLog2e;
     s += __shfl_xor(s, 16, 64);
     s += __shfl_xor(s, 32, 64);
     if (lane < 16) part_s[wave][lane] = s;
