@@ -1115,18 +1115,24 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dkv_fast(
       if (key_level(u, j, N)) return j;
     return 0;
   };
-  float gapr;
-  {
-    const int jl = lane + 1;
-    float t = 0.f;
-    if (jl <= J && key_level(u, jl, N)) t = rev.dtot[rev.slot(bh, jl, (int64_t)u >> jl)];
-    gapr = wave_inclusive_scan(t) - t;
-  }
+  // q . dq of this lane's key rows, for the tile's tail (loaded now, unconditionally: a load under a
+  // lane condition is waited for where the branch ends)
+  const float qdqA = qdq[growA], qdqB = qdq[growB];
+  // the first key-side summary (or the tile) is requested before the gaps are summed: their sum
+  // waits for every load issued before it
   int j = next_level(0);
   if (j) lds_copy_rows<DK, DV, NT>(q_s, rev.d + rev.slot(bh, j, (int64_t)u >> j) * SZ, DK, DV);
   else {
     copy_tile(q_s);
     copy_tile(o_s);
+  }
+  float gapr;
+  {
+    const int jl = lane + 1;
+    const bool use = jl <= J && key_level(u, jl, N);
+    const float tr = rev.dtot[rev.slot(bh, use ? jl : 1, use ? (int64_t)u >> jl : 0)];
+    const float t = use ? tr : 0.f;
+    gapr = wave_inclusive_scan(t) - t;
   }
   if (!liveB) {
 #pragma unroll
@@ -1277,8 +1283,8 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dkv_fast(
   kdA = sum_over_groups(kdA);
   kdB = sum_over_groups(kdB);
   if (g == 0) {
-    dc_s[jA] = qdq[growA] - kdA;
-    dc_s[jB] = liveB ? qdq[growB] - kdB : 0.f;
+    dc_s[jA] = qdqA - kdA;
+    dc_s[jB] = liveB ? qdqB - kdB : 0.f;
   }
   __syncthreads();  // every wave is done with Q and dO; dc visible
   // ---- dk and dv through LDS as whole rows
