@@ -839,13 +839,15 @@ __global__ __launch_bounds__(kBwdFastThreads, 2) void k_bwd_dq_fast(
       if (reads_level(u, j)) return j;
     return 0;
   };
-  const float gapv = level_gaps(nodes, bh, N, u, J);
+  // the first summary (or the tile) is requested before the gaps are summed: their sum waits for
+  // every load issued before it
   int j = next_level(0);
   if (j) lds_copy_rows<DK, DV, NT>(k_s, nodes.at(bh, N, j, source_first(u, j), SZ), DK, DV);
   else {
     copy_tile(k_s);
     copy_tile(v_s);
   }
+  const float gapv = level_gaps(nodes, bh, N, u, J);
   if (!liveB) {
 #pragma unroll
     for (int ks = 0; ks < KSK; ++ks) qB[ks] = frag{};
