@@ -88,17 +88,19 @@ __device__ inline bool wait_flag(const int* f, unsigned* err) {
 }
 
 
-// U^T operand fragment (d_v tile dvt, d_k step ks of 32) from a node image in the fragment-major
-// result layout: piece (d_k tile mk, d_v tile dv, lane l) holds rows d_k = 16 mk + 4 (l / 16) + r,
-// r = 0..3, of column d_v = 16 dv + l % 16.  Slots 0-3 and 4-7 of the fragment (d_k 32 ks + 8 g + s)
-// are the pieces of lanes 32 (g % 2) + i and 32 (g % 2) + 16 + i of d_k tile 2 ks + g / 2.
+// Node image layout: piece (d_k tile mk, d_v tile dv) is the 16 x 16 result block of the state
+// product, 64 lanes x 4 bf16; result lane l (rows d_k = 16 mk + 4 (l / 16) + r, r = 0..3, column
+// d_v = 16 dv + l % 16) is stored at slot piece_slot(l) of the piece, which puts lanes l and l + 16
+// side by side, so that the 8 d_k values an operand lane needs are 16 contiguous bytes.
+__device__ inline int piece_slot(int l) { return (l & 32) | ((l & 15) << 1) | ((l >> 4) & 1); }
+
+// U^T operand fragment (d_v tile dvt, d_k step ks of 32) from a node image: slots 0-3 and 4-7 of
+// the fragment (d_k 32 ks + 8 g + s) are result lanes 32 (g % 2) + i and 32 (g % 2) + 16 + i of d_k
+// tile 2 ks + g / 2, i.e. slots 32 (g % 2) + 2 i and + 1: one 16-byte read.
 template <int MT>
 __device__ inline bf16x8 node_frag(const __bf16* img, int dvt, int ks) {
   const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
-  const __bf16* p = img + (((2 * ks + (g >> 1)) * MT + dvt) * 64 + 32 * (g & 1) + i) * 4;
-  const bf16x4 lo = *reinterpret_cast<const bf16x4*>(p);
-  const bf16x4 hi = *reinterpret_cast<const bf16x4*>(p + 64);
-  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return *reinterpret_cast<const bf16x8*>(img + (((2 * ks + (g >> 1)) * MT + dvt) * 64 + 32 * (g & 1) + 2 * i) * 4);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -321,7 +323,7 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
     for (int mt = 0; mt < DKT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NTW; ++nt)
-        *reinterpret_cast<bf16x4*>(dst + ((mt * MT + wave * NTW + nt) * 64 + lane) * 4) = sbf[mt][nt];
+        *reinterpret_cast<bf16x4*>(dst + ((mt * MT + wave * NTW + nt) * 64 + piece_slot(lane)) * 4) = sbf[mt][nt];
     wait_vmem();
     __syncthreads();
     if (tid == 0) __hip_atomic_store(ws.flag + bh * N + u, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -392,7 +394,7 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
       for (int mt = 0; mt < DKT; ++mt)
 #pragma unroll
         for (int nt = 0; nt < NTW; ++nt) {
-          const bf16x4 pc = *reinterpret_cast<const bf16x4*>(cur + (mt * NTW + nt) * 256 + lane * 4);
+          const bf16x4 pc = *reinterpret_cast<const bf16x4*>(cur + (mt * NTW + nt) * 256 + piece_slot(lane) * 4);
 #pragma unroll
           for (int r = 0; r < 4; ++r) acc[mt][nt][r] += w * to_f32(pc[r]);
         }
@@ -423,7 +425,9 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
   };
   // lambda == NULL (every level weight 1): the row factor exp2(c_t) comes out of the level sum, so
   // the tile sums its source nodes, each weighted by exp2(gap_j), into this wave's pieces of one
-  // fp32 state and multiplies Q by that state once after the loop, instead of once per level
+  // fp32 state and multiplies Q by that state once after the loop, instead of once per level.  The
+  // sum is elementwise, so lane l sums slot l of each piece (consecutive 8-byte reads) and writes
+  // the result back to slot l
   f32x4 pre[DKT][NTW];
   if constexpr (!HAS_LAMBDA) {
 #pragma unroll
