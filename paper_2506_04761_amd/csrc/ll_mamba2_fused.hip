@@ -22,8 +22,11 @@
 //                  and the lambda-weighted terms of every inter-tile level from the published nodes
 //
 // Work order and visibility.  Workgroups take tickets from the queue of the XCD they run on (the
-// hardware register XCC_ID) and only from it; queue x holds the tiles of heads x, x + 8, ... in time
-// order, so a head's nodes are written and read through one L2.  The grid gives every XCD as many
+// hardware register XCC_ID) and only from it; queue x holds the tiles of some (batch, head) pairs in
+// time order (their tiles of one time step in turn), so a head's nodes are written and read through
+// one L2.  With at least 64 pairs a queue holds a block of consecutive pairs, whose rows of q, k, v,
+// o, lambda and the gates lie side by side in memory and share cache lines; with fewer it holds
+// pairs x, x + 8, ... (measured faster there).  The grid gives every XCD as many
 // workgroups as the longest queue has tiles (the hardware deals workgroups to the 8 XCDs in turn);
 // a workgroup that finds its queue drained exits.  A tile only waits for nodes of earlier tickets of
 // its own queue, held by workgroups that are already running, so the waits always end; each wait is
@@ -211,13 +214,17 @@ __global__ __launch_bounds__(kFastThreads, 2) void k_fused_fwd(
   // ---- ticket from this XCD's queue
   if (tid == 0) {
     const int x = xcc_id();
-    const int nh = x < BH ? (BH - 1 - x) / kQueues + 1 : 0;
+    // nh pairs in queue x: first .. first + nh - 1 (BH split into 8 blocks whose sizes differ by at
+    // most 1) or x, x + 8, ...
+    const int base = BH / kQueues, extra = BH % kQueues;
+    const int nh = base + (x < extra ? 1 : 0), first = x * base + (x < extra ? x : extra);
+    const bool blocks = BH >= 8 * kQueues;
     int got = -1;
     int64_t gu = 0;
     if (nh) {
       const unsigned t = __hip_atomic_fetch_add(&ws.ctr[x], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if ((int64_t)t < (int64_t)nh * N) {
-        got = x + kQueues * (int)(t % nh);
+        got = blocks ? first + (int)(t % nh) : x + kQueues * (int)(t % nh);
         gu = t / nh;
       }
     }
