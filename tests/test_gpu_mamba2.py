@@ -75,6 +75,20 @@ def test_parity_many_heads_short_blocks(chunks):
         assert err <= TOL["bf16"], err
 
 
+@pytest.mark.parametrize("dk,dv", [(128, 128), (128, 64)])
+def test_parity_uneven_head_blocks(dk, dv):
+    # 69 (batch, head) pairs: the single-pass kernel's eight XCD queues take blocks of 9 and 8
+    # consecutive pairs (blocks from 64 pairs on); 9 chunks give 5 tiles, the last one half full
+    w = WORKLOADS["ll_mamba2_bf16_T65536"].with_(B=3, H=23, T=64 * 9, dk=dk, dv=dv, seed=77 + dv)
+    x = generate(w)
+    for with_lambda in (True, False):
+        lam = x["lam"] if with_lambda else np.ones_like(x["lam"])
+        ref = mamba2.quadratic(x["q"], x["k"], x["v"], x["log_alpha"], lam)
+        err = rel_err(run_mamba2(x, "bf16", 64, with_lambda=with_lambda), ref)
+        print(f"B=3 H=23 {dk}x{dv} T={w.T} lambda={with_lambda}: rel err {err:.3e}")
+        assert err <= TOL["bf16"], err
+
+
 @pytest.mark.parametrize("T", [16, 48, 256, 1024])
 def test_parity_fp32_small_chunk(T):
     w = WORKLOADS["ll_mamba2_f32_T64"].with_(B=2, H=3, T=T, seed=T)
