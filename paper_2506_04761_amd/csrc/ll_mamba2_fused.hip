@@ -79,7 +79,9 @@ __device__ inline bool wait_flag(const int* f, unsigned* err) {
   if (!ok) {
     const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
     while (!(ok = flag_up(f))) {
-      __builtin_amdgcn_s_sleep(2);
+      // about 0.5 us between polls: each poll is a device-scope load that goes to memory, and
+      // denser polling (or two polls in flight) slows the publications being waited for
+      __builtin_amdgcn_s_sleep(20);
       if (__builtin_amdgcn_s_memrealtime() - t0 > kSpinTicks) {
         if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;
